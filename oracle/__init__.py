@@ -1,0 +1,151 @@
+"""TEST INFRASTRUCTURE ONLY: the fp64 CPU oracle for FSA-based one-symbol-per-frame
+transducer beam search (Sec. 2.2-2.5, Algorithm 1 of Kang et al., arXiv 2211.00484).
+
+Only the tests, ``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline`` leg may
+import this package.  It wraps ``tbs_oracle.cpp`` (plain C++17, double precision, built
+with g++ by :func:`build`) through ctypes and shares no code with the HIP library.
+
+Parity status: the decoder/joiner/log-softmax is pinned against library layers; the
+unpruned search against exhaustive enumeration and a Viterbi recursion; Ns = Nc = 1 on the
+trivial graph against per-frame argmax greedy search.  The exact tie-breaking of the
+finite beam / max-states / max-contexts selection is this implementation's reading of
+Sec. 2.5 and is pinned only by invariants ("parity unpinned" for those tie rules).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tbs_oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_I = ctypes.c_int
+_D = ctypes.c_double
+_P = ctypes.c_void_p
+
+
+def build(force: bool = True) -> str:
+    """Compiles the oracle with g++ (no GPU code involved)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-pthread",
+               "-ffp-contract=off", "-fno-fast-math", _SRC, "-o", tmp]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        lib.oracle_logp.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _I, _P]
+        lib.oracle_logp.restype = _I
+        lib.oracle_decode.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I,
+                                       _I, _I, _P, _P, _P, _P, _P, _D, _I, _I, _I] + [_P] * 7)
+        lib.oracle_decode.restype = _I
+        lib.oracle_rescore.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I,
+                                       _P, _P, _P, _P, _P, _P]
+        lib.oracle_rescore.restype = _I
+        _lib = lib
+    return _lib
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def logp(model, enc_rows: np.ndarray, ctx_a: np.ndarray, ctx_b: np.ndarray,
+         bf16: bool = False) -> np.ndarray:
+    """Joiner log-probabilities [R, V] (fp64) for R (encoder row, (a, b) context) pairs."""
+    lib = _load()
+    enc_rows = _f32(enc_rows)
+    R = int(enc_rows.shape[0])
+    a, b = _i32(ctx_a), _i32(ctx_b)
+    E, conv, W = _f32(model.embed), _f32(model.conv), _f32(model.w_out)
+    bias = None if model.b_out is None else _f32(model.b_out)
+    out = np.empty((R, model.vocab_size), dtype=np.float64)
+    lib.oracle_logp(model.dim, model.vocab_size, R, _ptr(enc_rows), _ptr(a), _ptr(b),
+                    _ptr(E), _ptr(conv), _ptr(W), _ptr(bias), int(bf16), _ptr(out))
+    return out
+
+
+class OracleResult:
+    def __init__(self, tokens, ntok, scores, status, arcs, trace, margins):
+        self.tokens, self.ntok, self.scores, self.status = tokens, ntok, scores, status
+        self.arcs, self.trace, self.margins = arcs, trace, margins
+
+    def token_lists(self):
+        return [list(self.tokens[b, : self.ntok[b]]) for b in range(self.tokens.shape[0])]
+
+
+def decode(model, graph, encoder_out: np.ndarray, lengths: np.ndarray, beam: float,
+           max_states: int, max_contexts: int, bf16: bool = False, nthreads: int = 0,
+           want_trace: bool = True, want_arcs: bool = True, streams=None) -> OracleResult:
+    """Decodes every stream (or the listed ``streams``) of a batch; see tbs_oracle.cpp."""
+    lib = _load()
+    enc = _f32(encoder_out)
+    lens = _i32(lengths)
+    if streams is not None:
+        idx = np.asarray(streams, dtype=np.int64)
+        enc = np.ascontiguousarray(enc[idx])
+        lens = np.ascontiguousarray(lens[idx])
+    B, T, C = enc.shape
+    V = model.vocab_size
+    if max_states < 1 or max_contexts < 1:
+        raise ValueError("max_states and max_contexts must be >= 1")
+    E, conv, W = _f32(model.embed), _f32(model.conv), _f32(model.w_out)
+    bias = None if model.b_out is None else _f32(model.b_out)
+    rp, dest, lab, q = _i32(graph.row_ptr), _i32(graph.dest), _i32(graph.label), _f32(graph.score)
+    fin = None if graph.final is None else _f32(graph.final)
+    tokens = np.empty((B, T), dtype=np.int32)
+    ntok = np.empty(B, dtype=np.int32)
+    scores = np.empty(B, dtype=np.float64)
+    status = np.empty(B, dtype=np.int32)
+    arcs = np.empty((B, T), dtype=np.int32) if want_arcs else None
+    trace = np.empty((T + 1, B, max_states, 4), dtype=np.int32) if want_trace else None
+    margins = np.empty(B, dtype=np.float64)
+    beam_v = float(beam) if beam is not None else math.inf
+    lib.oracle_decode(B, T, C, V, _ptr(enc), _ptr(lens), _ptr(E), _ptr(conv), _ptr(W),
+                      _ptr(bias), int(bf16), graph.num_states, graph.start, _ptr(rp), _ptr(dest),
+                      _ptr(lab), _ptr(q), _ptr(fin), beam_v, int(max_states), int(max_contexts),
+                      int(nthreads), _ptr(tokens), _ptr(ntok), _ptr(scores), _ptr(status),
+                      _ptr(arcs), _ptr(trace), _ptr(margins))
+    return OracleResult(tokens, ntok, scores, status, arcs, trace, margins)
+
+
+def rescore(model, graph, enc_stream: np.ndarray, arcs: np.ndarray, bf16: bool = False):
+    """Path score (fp64) of one stream's alignment (arc id per frame, -1 = blank).
+
+    Returns (code, score): code 0 = valid path ending in a final state, 1 = valid path
+    ending in a non-final state (score then excludes any final weight), -1 = not a path."""
+    lib = _load()
+    enc = _f32(enc_stream)
+    arcs = _i32(arcs)
+    E, conv, W = _f32(model.embed), _f32(model.conv), _f32(model.w_out)
+    bias = None if model.b_out is None else _f32(model.b_out)
+    rp, dest, lab, q = _i32(graph.row_ptr), _i32(graph.dest), _i32(graph.label), _f32(graph.score)
+    fin = None if graph.final is None else _f32(graph.final)
+    out = ctypes.c_double(0.0)
+    code = lib.oracle_rescore(model.dim, model.vocab_size, int(arcs.shape[0]), _ptr(enc),
+                              _ptr(arcs), _ptr(E), _ptr(conv), _ptr(W), _ptr(bias), int(bf16),
+                              graph.num_states, graph.start, _ptr(rp), _ptr(dest), _ptr(lab),
+                              _ptr(q), _ptr(fin), ctypes.byref(out))
+    return int(code), float(out.value)
