@@ -1,0 +1,182 @@
+/*
+ * tbs.h -- C ABI of the MI355X (gfx950) library for batched FSA-based
+ * one-symbol-per-frame transducer beam search.
+ *
+ * The method is the "FSA-based parallel beam search" of Kang et al., "Fast and
+ * parallel decoding for transducer" (arXiv 2211.00484): Sec. 2.2 (stateless
+ * transducer, two-label context), Sec. 2.3 (max-symbols decoding with S = 1),
+ * Sec. 2.4 (on-the-fly composition with an epsilon-free decoding graph),
+ * Sec. 2.5 (beam, max-states and max-contexts pruning) and Algorithm 1.
+ *
+ * Conventions shared by every entry point:
+ *  - Every function returns a tbs_status; 0 is success, negative values are
+ *    errors.  tbs_last_error() returns a message describing the last error of
+ *    the calling thread.
+ *  - All arguments are validated on the host before any device work is
+ *    enqueued; a call that returns an error has written nothing.
+ *  - Device pointers are plain HIP device addresses on the current device.
+ *    Host pointers are ordinary CPU memory.  Each argument states which.
+ *  - hip_stream is a hipStream_t (NULL = the null stream).  Device work is
+ *    enqueued on it; calls return after enqueueing (stream-ordered), except
+ *    where stated.
+ *  - Graph and model handles are immutable after creation and may be shared
+ *    between threads.  The decode workspace is cached in the model handle;
+ *    decodes that share a model are serialised on it (host side by a mutex,
+ *    device side by an event the next decode's stream waits on).
+ *  - Blank is label 0.  Contexts are packed as ctx = a * V + b, where b is the
+ *    most recent label (Sec. 2.4 footnote: the history fits one integer).
+ */
+#ifndef TBS_H
+#define TBS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TBS_OK = 0,
+  TBS_EINVAL = -1,        /* an argument is invalid; nothing was done            */
+  TBS_ENOMEM = -2,        /* device or pinned-host allocation failed             */
+  TBS_EDEVICE = -3,       /* a HIP call failed                                   */
+  TBS_ECAPACITY = -4,     /* a size exceeds a documented library limit           */
+  TBS_EUNSUPPORTED = -5   /* a valid but unsupported configuration               */
+} tbs_status;
+
+typedef struct tbs_graph tbs_graph;
+typedef struct tbs_model tbs_model;
+
+/*
+ * Decoding graph: an epsilon-free FSA (Sec. 2.4) given as CSR arcs sorted by
+ * source state.  All inputs are HOST arrays; the library copies them to the
+ * device and the caller may free them when the call returns.
+ *   num_states   S >= 1
+ *   start_state  in [0, S)
+ *   vocab_size   V in [2, 65535] (blank = 0 included)
+ *   row_ptr      host int32 [S+1]: row_ptr[0] = 0, non-decreasing; A = row_ptr[S]
+ *   dest         host int32 [A]: destination state of each arc, in [0, S)
+ *   label        host int32 [A]: label of each arc, in [1, V-1] (label 0 is
+ *                rejected: the graph must be epsilon-free)
+ *   score        host float [A]: finite log-domain arc weight (q in Sec. 2.4)
+ *   final_score  host float [S] or NULL.  NULL: every state is final with
+ *                weight 0.  Otherwise a finite value is the state's final
+ *                weight and -INFINITY marks a non-final state.
+ * Duplicate arcs are allowed; they merge by max during the search.
+ * Errors: TBS_EINVAL on any violation above (with the offending index in the
+ * message), TBS_ENOMEM / TBS_EDEVICE on allocation or copy failure.
+ */
+tbs_status tbs_graph_create(int32_t num_states, int32_t start_state, int32_t vocab_size,
+                            const int32_t *row_ptr, const int32_t *dest,
+                            const int32_t *label, const float *score,
+                            const float *final_score, tbs_graph **out);
+
+/*
+ * The "trivial graph" of Table 6: one state (start and final, weight 0) with a
+ * 0-weight self-loop for every non-blank label 1..V-1, in label order (so arc
+ * id = label - 1).  The search over it is plain one-symbol-per-frame beam
+ * search with (context) hypotheses.
+ */
+tbs_status tbs_graph_create_trivial(int32_t vocab_size, tbs_graph **out);
+void tbs_graph_destroy(tbs_graph *graph);
+
+typedef enum { TBS_JOINER_FP32 = 0, TBS_JOINER_BF16 = 1 } tbs_joiner_dtype;
+
+/*
+ * Transducer model pieces used by the search (Sec. 5.1 model; Algorithm 1
+ * decoder and joiner):
+ *   stateless decoder  dec(a, b) = ReLU(conv[:,0] * embed[a] + conv[:,1] * embed[b])
+ *                      (embedding followed by a depthwise kernel-2 convolution
+ *                      over the two most recent labels; tap 0 weights the older
+ *                      label a; no bias);
+ *   joiner             logits = w_out . tanh(enc + dec) + b_out, then log-softmax
+ *                      over all V outputs, blank included.
+ *   vocab_size V in [2, 65535]; dim C in [1, 4096]; context_size must be 2
+ *   (TBS_EUNSUPPORTED otherwise).
+ *   embed  DEVICE float [V][C];  conv DEVICE float [C][2];
+ *   w_out  DEVICE float [V][C] (torch Linear layout);  b_out DEVICE float [V] or NULL (= 0).
+ *   dtype  TBS_JOINER_FP32: fp32 operands; TBS_JOINER_BF16: tanh output and
+ *          w_out rounded to bfloat16 (nearest, ties to even), fp32 accumulation.
+ * The library copies what it needs (and precomputes conv-tap-scaled embedding
+ * tables) on hip_stream and synchronises that stream before returning, so the
+ * caller may free the inputs afterwards.
+ */
+tbs_status tbs_model_create(int32_t vocab_size, int32_t dim, int32_t context_size,
+                            const float *embed, const float *conv, const float *w_out,
+                            const float *b_out, tbs_joiner_dtype dtype, void *hip_stream,
+                            tbs_model **out);
+void tbs_model_destroy(tbs_model *model);
+
+/*
+ * Pruning constraints of Sec. 2.5, applied per stream on every frame after
+ * unpruned expansion and max-merge of equal (graph state, context) tuples:
+ *   beam          log-domain beam >= 0 (INFINITY = off): keep tuples whose score
+ *                 is >= best - beam (inclusive);
+ *   max_states    in [1, 256]: together with the beam, keep at most this many
+ *                 tuples, ranked by score descending, then (state, context)
+ *                 ascending;
+ *   max_contexts  >= 1: then keep the tuples of the max_contexts best contexts,
+ *                 a context scoring the max over its tuples, ties by context
+ *                 id ascending.
+ */
+typedef struct {
+  float beam;
+  int32_t max_states;
+  int32_t max_contexts;
+} tbs_beam_params;
+
+/*
+ * Batched decode (Algorithm 1 with the best path through the lattice, Sec. 2.5).
+ *   encoder_out    DEVICE float [B][T][C], contiguous; frames t >= lengths[b] are ignored.
+ *   lengths        HOST int32 [B], each in [0, T].
+ *   B >= 0 (B = 0 is a no-op), T >= 0.
+ *   out_tokens     DEVICE int32 [B][T]: the best path's non-blank labels, -1 padded
+ *                  (one symbol per frame at most, so T slots suffice).
+ *   out_num_tokens DEVICE int32 [B].
+ *   out_scores     DEVICE double [B]: log-domain score of the best path, final
+ *                  weight included.
+ *   out_status     DEVICE int32 [B] or NULL: 0 = the path ends in a final state;
+ *                  1 = no surviving tuple was final and the best non-final one
+ *                  was used (its score then has no final weight).
+ *   out_arcs       DEVICE int32 [B][T] or NULL: per frame, the graph arc id taken
+ *                  by the best path, -1 for blank, -2 for frames >= lengths[b].
+ *   trace          DEVICE int32 [T+1][B][max_states][4] or NULL: for frame index
+ *                  f, the surviving tuples of each stream as (ctx, state, parent,
+ *                  label), in (ctx, state) ascending order, -1 padded; f = 0 is
+ *                  the initial tuple (0, start, -1, -1).  Parents index the
+ *                  previous frame's list.  For parity testing.
+ * Scores are kept per stream in fp32 relative to the stream's best, plus an
+ * fp64 per-stream offset, so long streams keep fp32 resolution.
+ * All output buffers are caller-owned and fully written (including padding).
+ * The workspace (sized by B, T, max_states, max_contexts and the vocabulary)
+ * is allocated on first use and cached in the model.
+ * Errors: TBS_EINVAL for NULL handles/pointers, a model/graph vocabulary
+ * mismatch, a length outside [0, T], a NaN or negative beam or max_states /
+ * max_contexts < 1; TBS_ECAPACITY if max_states > 256 or
+ * max_states * (graph max out-degree + 1) >= 2^31; TBS_ENOMEM / TBS_EDEVICE.
+ */
+tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
+                      const tbs_beam_params *params, const float *encoder_out,
+                      const int32_t *lengths, int32_t B, int32_t T, int32_t *out_tokens,
+                      int32_t *out_num_tokens, double *out_scores, int32_t *out_status,
+                      int32_t *out_arcs, int32_t *trace, void *hip_stream);
+
+/*
+ * Decoder + joiner + log-softmax alone (Algorithm 1: Decoder, IndexSelect,
+ * joiner), for R (encoder row, context) pairs:
+ *   enc_rows  DEVICE float [R][C];  ctx DEVICE int32 [R], each a * V + b with
+ *             a, b in [0, V) (not checked on the device: the caller guarantees it);
+ *   out_logp  DEVICE float [R][V]: log-probabilities.
+ * R >= 0 (R = 0 is a no-op).
+ */
+tbs_status tbs_joiner_logp(const tbs_model *model, const float *enc_rows, const int32_t *ctx,
+                           int32_t R, float *out_logp, void *hip_stream);
+
+/* Message for the calling thread's last error ("" if none). */
+const char *tbs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TBS_H */

@@ -51,7 +51,7 @@ def _load():
         lib.oracle_logp.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _I, _P]
         lib.oracle_logp.restype = _I
         lib.oracle_decode.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I,
-                                       _I, _I, _P, _P, _P, _P, _P, _D, _I, _I, _I] + [_P] * 7)
+                                       _I, _I, _P, _P, _P, _P, _P, _D, _I, _I, _I] + [_P] * 8)
         lib.oracle_decode.restype = _I
         lib.oracle_rescore.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I,
                                        _P, _P, _P, _P, _P, _P]
@@ -88,9 +88,10 @@ def logp(model, enc_rows: np.ndarray, ctx_a: np.ndarray, ctx_b: np.ndarray,
 
 
 class OracleResult:
-    def __init__(self, tokens, ntok, scores, status, arcs, trace, margins):
+    def __init__(self, tokens, ntok, scores, status, arcs, trace, margins, frame_margins):
         self.tokens, self.ntok, self.scores, self.status = tokens, ntok, scores, status
         self.arcs, self.trace, self.margins = arcs, trace, margins
+        self.frame_margins = frame_margins
 
     def token_lists(self):
         return [list(self.tokens[b, : self.ntok[b]]) for b in range(self.tokens.shape[0])]
@@ -122,13 +123,14 @@ def decode(model, graph, encoder_out: np.ndarray, lengths: np.ndarray, beam: flo
     arcs = np.empty((B, T), dtype=np.int32) if want_arcs else None
     trace = np.empty((T + 1, B, max_states, 4), dtype=np.int32) if want_trace else None
     margins = np.empty(B, dtype=np.float64)
+    frame_margins = np.empty((B, T + 1), dtype=np.float64)
     beam_v = float(beam) if beam is not None else math.inf
     lib.oracle_decode(B, T, C, V, _ptr(enc), _ptr(lens), _ptr(E), _ptr(conv), _ptr(W),
                       _ptr(bias), int(bf16), graph.num_states, graph.start, _ptr(rp), _ptr(dest),
                       _ptr(lab), _ptr(q), _ptr(fin), beam_v, int(max_states), int(max_contexts),
                       int(nthreads), _ptr(tokens), _ptr(ntok), _ptr(scores), _ptr(status),
-                      _ptr(arcs), _ptr(trace), _ptr(margins))
-    return OracleResult(tokens, ntok, scores, status, arcs, trace, margins)
+                      _ptr(arcs), _ptr(trace), _ptr(margins), _ptr(frame_margins))
+    return OracleResult(tokens, ntok, scores, status, arcs, trace, margins, frame_margins)
 
 
 def rescore(model, graph, enc_stream: np.ndarray, arcs: np.ndarray, bf16: bool = False):

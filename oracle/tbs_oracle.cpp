@@ -136,6 +136,8 @@ struct StreamOut {
   double score = 0.0;
   int status = 0;
   double margin = std::numeric_limits<double>::infinity();
+  double final_margin = std::numeric_limits<double>::infinity();
+  std::vector<double> frame_margin;  // per frame: smallest decision margin of that frame
 };
 
 // Decodes one stream.  trace (optional) receives, for frame index f in
@@ -160,8 +162,10 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
   write_trace(0, H);
   double margin = std::numeric_limits<double>::infinity();
   std::vector<double> logp;
+  out.frame_margin.assign(len, std::numeric_limits<double>::infinity());
 
   for (int t = 0; t < len; ++t) {
+    double fmar = std::numeric_limits<double>::infinity();
     // GetContexts: the distinct contexts of the current tuples, ascending.
     std::vector<int64_t> ctxs;
     for (const Tup& x : H) ctxs.push_back(x.ctx);
@@ -228,10 +232,10 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     while (n_in_beam < ents.size() && ents[n_in_beam].best->score >= thr) ++n_in_beam;
     size_t n1 = std::min(n_in_beam, (size_t)p.Ns);
     if (n_in_beam > (size_t)p.Ns)
-      margin = std::min(margin, ents[p.Ns - 1].best->score - ents[p.Ns].best->score);
+      fmar = std::min(fmar, ents[p.Ns - 1].best->score - ents[p.Ns].best->score);
     if (std::isfinite(p.beam)) {
       const size_t lim = std::min(ents.size(), (size_t)p.Ns);
-      for (size_t i = 0; i < lim; ++i) margin = std::min(margin, std::fabs(ents[i].best->score - thr));
+      for (size_t i = 0; i < lim; ++i) fmar = std::min(fmar, std::fabs(ents[i].best->score - thr));
     }
     ents.resize(n1);
 
@@ -250,7 +254,7 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
       if (x.first != y.first) return x.first > y.first;
       return x.second < y.second;
     });
-    if (cl.size() > (size_t)p.Nc) margin = std::min(margin, cl[p.Nc - 1].first - cl[p.Nc].first);
+    if (cl.size() > (size_t)p.Nc) fmar = std::min(fmar, cl[p.Nc - 1].first - cl[p.Nc].first);
     std::vector<int64_t> kept_ctx;
     for (size_t i = 0; i < cl.size() && i < (size_t)p.Nc; ++i) kept_ctx.push_back(cl[i].second);
     std::sort(kept_ctx.begin(), kept_ctx.end());
@@ -259,13 +263,15 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     std::vector<Tup> nH;
     for (const Entry& e : ents) {
       if (!std::binary_search(kept_ctx.begin(), kept_ctx.end(), e.ctx)) continue;
-      if (e.runner_up != kNegInf) margin = std::min(margin, e.best->score - e.runner_up);
+      if (e.runner_up != kNegInf) fmar = std::min(fmar, e.best->score - e.runner_up);
       nH.push_back(Tup{e.ctx, e.s, e.best->score, e.best->parent, e.best->label, e.best->arc});
     }
     std::sort(nH.begin(), nH.end(), [](const Tup& x, const Tup& y) {
       if (x.ctx != y.ctx) return x.ctx < y.ctx;
       return x.s < y.s;
     });
+    out.frame_margin[t] = fmar;
+    margin = std::min(margin, fmar);
     hist.push_back(nH);
     H.swap(nH);
     write_trace(t + 1, H);
@@ -290,7 +296,8 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     }
     out.status = pass;
   }
-  if (second != kNegInf) margin = std::min(margin, pick_v - second);
+  out.final_margin = second != kNegInf ? pick_v - second : std::numeric_limits<double>::infinity();
+  margin = std::min(margin, out.final_margin);
   out.score = pick_v;
   out.margin = margin;
 
@@ -325,13 +332,15 @@ int oracle_logp(int C, int V, int R, const float* enc_rows, const int* ctx_a, co
 // status [B] (0 = ended in a final state, 1 = no final state survived),
 // arcs [B][T] or null (arc id per frame, -1 blank, -2 past the stream's end),
 // trace [T+1][B][Ns][4] or null (-1 padded), margins [B] or null (smallest
-// decision margin of the stream, +inf if no decision was contested).
+// decision margin of the stream, +inf if no decision was contested),
+// frame_margins [B][T+1] or null (entry t < len: smallest margin of the
+// decisions taken on frame t; entry T: margin of the final pick; others +inf).
 int oracle_decode(int B, int T, int C, int V, const float* enc, const int* lengths,
                   const float* E, const float* conv, const float* W, const float* bias,
                   int bf16, int S, int start, const int* rp, const int* dest, const int* label,
                   const float* q, const float* fin, double beam, int Ns, int Nc, int nthreads,
                   int* tokens, int* ntok, double* scores, int* status, int* arcs, int* trace,
-                  double* margins) {
+                  double* margins, double* frame_margins) {
   Model m{V, C, E, conv, W, bias, bf16};
   Graph g{S, start, rp, dest, label, q, fin};
   Params p{beam, Ns, Nc};
@@ -355,6 +364,12 @@ int oracle_decode(int B, int T, int C, int V, const float* enc, const int* lengt
       if (arcs)
         for (int t = 0; t < lengths[b]; ++t) arcs[(size_t)b * T + t] = o.arcs[t];
       if (margins) margins[b] = o.margin;
+      if (frame_margins) {
+        double* fm = frame_margins + (size_t)b * (T + 1);
+        for (int t = 0; t <= T; ++t) fm[t] = std::numeric_limits<double>::infinity();
+        for (int t = 0; t < lengths[b]; ++t) fm[t] = o.frame_margin[t];
+        fm[T] = o.final_margin;
+      }
     }
   };
   int nt = nthreads > 0 ? nthreads : (int)std::thread::hardware_concurrency();

@@ -1,0 +1,452 @@
+// Host runtime behind include/tbs.h: argument validation, graph/model handles,
+// the cached decode workspace and the frame loop that enqueues the gfx950
+// kernels (Algorithm 1 of Kang et al., arXiv 2211.00484).
+#include "tbs.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace tbs;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tbs_status fail(tbs_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+tbs_status hip_fail(hipError_t e, const char* what) {
+  return fail(e == hipErrorOutOfMemory ? TBS_ENOMEM : TBS_EDEVICE, "%s: %s", what,
+              hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                    \
+  do {                                         \
+    hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+template <class T>
+hipError_t dalloc(T** p, size_t n) {
+  *p = nullptr;
+  if (n == 0) n = 1;
+  return hipMalloc((void**)p, n * sizeof(T));
+}
+
+struct Workspace {
+  int B = 0, T = 0, Ns = 0, Nc = 0;
+  int* len = nullptr;
+  int* nsurv = nullptr;
+  int* surv_ctx = nullptr;
+  int* surv_state = nullptr;
+  float* surv_score = nullptr;
+  int* surv_row = nullptr;
+  int* nctx = nullptr;
+  int* ctx_list = nullptr;
+  double* offset = nullptr;
+  float* logits = nullptr;
+  float2* stats = nullptr;
+  int* hist_pl = nullptr;
+  int* hist_arc = nullptr;
+  int* path_lab = nullptr;
+  int* len_host = nullptr;  // pinned staging for lengths
+  hipEvent_t done = nullptr;
+  bool pending = false;
+
+  void release() {
+    hipFree(len); hipFree(nsurv); hipFree(surv_ctx); hipFree(surv_state); hipFree(surv_score);
+    hipFree(surv_row); hipFree(nctx); hipFree(ctx_list); hipFree(offset); hipFree(logits);
+    hipFree(stats); hipFree(hist_pl); hipFree(hist_arc); hipFree(path_lab);
+    if (len_host) hipHostFree(len_host);
+    if (done) hipEventDestroy(done);
+    *this = Workspace();
+  }
+};
+
+}  // namespace
+
+struct tbs_graph {
+  int S = 0, start = 0, V = 0, A = 0, maxdeg = 0;
+  int* rp = nullptr;
+  int* dest = nullptr;
+  int* label = nullptr;
+  float* q = nullptr;
+  float* fin = nullptr;
+};
+
+struct tbs_model {
+  int V = 0, C = 0, Kpad = 0, Vpad = 0, bf16 = 0;
+  float* P0 = nullptr;
+  float* P1 = nullptr;
+  float* Wf = nullptr;
+  uint16_t* Wb = nullptr;
+  float* bias = nullptr;
+  std::mutex mu;
+  Workspace ws;
+  // scratch for tbs_joiner_logp
+  int rows_cap = 0;
+  float* rows_logits = nullptr;
+  float2* rows_stats = nullptr;
+};
+
+namespace {
+
+ModelDev model_dev(const tbs_model* m) {
+  ModelDev d;
+  d.V = m->V;
+  d.C = m->C;
+  d.Kpad = m->Kpad;
+  d.Vpad = m->Vpad;
+  d.bf16 = m->bf16;
+  d.P0 = m->P0;
+  d.P1 = m->P1;
+  d.Wf = m->Wf;
+  d.Wb = m->Wb;
+  d.bias = m->bias;
+  return d;
+}
+
+GraphDev graph_dev(const tbs_graph* g) {
+  GraphDev d;
+  d.S = g->S;
+  d.start = g->start;
+  d.maxdeg = g->maxdeg;
+  d.rp = g->rp;
+  d.dest = g->dest;
+  d.label = g->label;
+  d.q = g->q;
+  d.fin = g->fin;
+  return d;
+}
+
+tbs_status graph_upload(tbs_graph* g, const int32_t* row_ptr, const int32_t* dest,
+                        const int32_t* label, const float* score, const float* final_score) {
+  const size_t A = (size_t)g->A, S = (size_t)g->S;
+  HIP_TRY(dalloc(&g->rp, S + 1), "hipMalloc(graph)");
+  HIP_TRY(dalloc(&g->dest, A), "hipMalloc(graph)");
+  HIP_TRY(dalloc(&g->label, A), "hipMalloc(graph)");
+  HIP_TRY(dalloc(&g->q, A), "hipMalloc(graph)");
+  HIP_TRY(hipMemcpy(g->rp, row_ptr, (S + 1) * 4, hipMemcpyHostToDevice), "hipMemcpy(graph)");
+  if (A) {
+    HIP_TRY(hipMemcpy(g->dest, dest, A * 4, hipMemcpyHostToDevice), "hipMemcpy(graph)");
+    HIP_TRY(hipMemcpy(g->label, label, A * 4, hipMemcpyHostToDevice), "hipMemcpy(graph)");
+    HIP_TRY(hipMemcpy(g->q, score, A * 4, hipMemcpyHostToDevice), "hipMemcpy(graph)");
+  }
+  if (final_score) {
+    HIP_TRY(dalloc(&g->fin, S), "hipMalloc(graph)");
+    HIP_TRY(hipMemcpy(g->fin, final_score, S * 4, hipMemcpyHostToDevice), "hipMemcpy(graph)");
+  }
+  return TBS_OK;
+}
+
+void graph_free(tbs_graph* g) {
+  if (!g) return;
+  hipFree(g->rp);
+  hipFree(g->dest);
+  hipFree(g->label);
+  hipFree(g->q);
+  hipFree(g->fin);
+  delete g;
+}
+
+tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc) {
+  Workspace& w = m->ws;
+  if (w.done && w.B >= B && w.T >= T && w.Ns == Ns && w.Nc == Nc) return TBS_OK;
+  if (w.done) {
+    if (w.pending) hipEventSynchronize(w.done);
+    w.release();
+  }
+  const int nvt = m->Vpad / kJoinerBN;
+  const size_t BN = (size_t)B * Ns, BC = (size_t)B * Nc;
+  HIP_TRY(dalloc(&w.len, B), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.nsurv, B), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.surv_ctx, BN), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.surv_state, BN), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.surv_score, BN), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.surv_row, BN), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.nctx, B), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.ctx_list, BC), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.offset, B), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.logits, BC * m->Vpad), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.stats, BC * nvt), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.hist_pl, (size_t)T * BN), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.hist_arc, (size_t)T * BN), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.path_lab, (size_t)B * T), "hipMalloc(workspace)");
+  HIP_TRY(hipHostMalloc((void**)&w.len_host, (size_t)(B > 0 ? B : 1) * 4, hipHostMallocDefault),
+          "hipHostMalloc(workspace)");
+  HIP_TRY(hipEventCreateWithFlags(&w.done, hipEventDisableTiming), "hipEventCreate");
+  w.B = B;
+  w.T = T;
+  w.Ns = Ns;
+  w.Nc = Nc;
+  return TBS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tbs_last_error(void) { return g_last_error.c_str(); }
+
+tbs_status tbs_graph_create(int32_t num_states, int32_t start_state, int32_t vocab_size,
+                            const int32_t* row_ptr, const int32_t* dest, const int32_t* label,
+                            const float* score, const float* final_score, tbs_graph** out) {
+  if (!out) return fail(TBS_EINVAL, "tbs_graph_create: out is NULL");
+  *out = nullptr;
+  if (num_states < 1) return fail(TBS_EINVAL, "tbs_graph_create: num_states must be >= 1");
+  if (start_state < 0 || start_state >= num_states)
+    return fail(TBS_EINVAL, "tbs_graph_create: start_state %d outside [0, %d)", start_state,
+                num_states);
+  if (vocab_size < 2 || vocab_size > 65535)
+    return fail(TBS_EINVAL, "tbs_graph_create: vocab_size %d outside [2, 65535]", vocab_size);
+  if (!row_ptr) return fail(TBS_EINVAL, "tbs_graph_create: row_ptr is NULL");
+  if (row_ptr[0] != 0) return fail(TBS_EINVAL, "tbs_graph_create: row_ptr[0] must be 0");
+  int maxdeg = 0;
+  for (int s = 0; s < num_states; ++s) {
+    const long long d = (long long)row_ptr[s + 1] - row_ptr[s];
+    if (d < 0)
+      return fail(TBS_EINVAL, "tbs_graph_create: row_ptr decreases at state %d", s);
+    if (d > maxdeg) maxdeg = (int)d;
+  }
+  const int A = row_ptr[num_states];
+  if (A > 0 && (!dest || !label || !score))
+    return fail(TBS_EINVAL, "tbs_graph_create: dest/label/score is NULL");
+  for (int j = 0; j < A; ++j) {
+    if (dest[j] < 0 || dest[j] >= num_states)
+      return fail(TBS_EINVAL, "tbs_graph_create: dest[%d] = %d outside [0, %d)", j, dest[j],
+                  num_states);
+    if (label[j] < 1 || label[j] >= vocab_size)
+      return fail(TBS_EINVAL,
+                  "tbs_graph_create: label[%d] = %d outside [1, %d] (the graph must be epsilon-free)",
+                  j, label[j], vocab_size - 1);
+    if (!std::isfinite(score[j]))
+      return fail(TBS_EINVAL, "tbs_graph_create: score[%d] is not finite", j);
+  }
+  if (final_score) {
+    for (int s = 0; s < num_states; ++s) {
+      const float f = final_score[s];
+      if (std::isnan(f) || f == INFINITY)
+        return fail(TBS_EINVAL, "tbs_graph_create: final_score[%d] must be finite or -inf", s);
+    }
+  }
+  tbs_graph* g = new tbs_graph();
+  g->S = num_states;
+  g->start = start_state;
+  g->V = vocab_size;
+  g->A = A;
+  g->maxdeg = maxdeg;
+  tbs_status st = graph_upload(g, row_ptr, dest, label, score, final_score);
+  if (st != TBS_OK) {
+    graph_free(g);
+    return st;
+  }
+  *out = g;
+  return TBS_OK;
+}
+
+tbs_status tbs_graph_create_trivial(int32_t vocab_size, tbs_graph** out) {
+  if (!out) return fail(TBS_EINVAL, "tbs_graph_create_trivial: out is NULL");
+  *out = nullptr;
+  if (vocab_size < 2 || vocab_size > 65535)
+    return fail(TBS_EINVAL, "tbs_graph_create_trivial: vocab_size %d outside [2, 65535]",
+                vocab_size);
+  const int A = vocab_size - 1;
+  std::vector<int32_t> rp = {0, A}, dest(A, 0), label(A);
+  std::vector<float> q(A, 0.f);
+  for (int j = 0; j < A; ++j) label[j] = j + 1;
+  return tbs_graph_create(1, 0, vocab_size, rp.data(), dest.data(), label.data(), q.data(),
+                          nullptr, out);
+}
+
+void tbs_graph_destroy(tbs_graph* graph) { graph_free(graph); }
+
+tbs_status tbs_model_create(int32_t vocab_size, int32_t dim, int32_t context_size,
+                            const float* embed, const float* conv, const float* w_out,
+                            const float* b_out, tbs_joiner_dtype dtype, void* hip_stream,
+                            tbs_model** out) {
+  if (!out) return fail(TBS_EINVAL, "tbs_model_create: out is NULL");
+  *out = nullptr;
+  if (context_size != 2)
+    return fail(TBS_EUNSUPPORTED, "tbs_model_create: context_size %d unsupported (must be 2)",
+                context_size);
+  if (vocab_size < 2 || vocab_size > 65535)
+    return fail(TBS_EINVAL, "tbs_model_create: vocab_size %d outside [2, 65535]", vocab_size);
+  if (dim < 1 || dim > kMaxDim)
+    return fail(TBS_EINVAL, "tbs_model_create: dim %d outside [1, %d]", dim, kMaxDim);
+  if (!embed || !conv || !w_out)
+    return fail(TBS_EINVAL, "tbs_model_create: embed/conv/w_out is NULL");
+  if (dtype != TBS_JOINER_FP32 && dtype != TBS_JOINER_BF16)
+    return fail(TBS_EINVAL, "tbs_model_create: unknown dtype %d", (int)dtype);
+  hipStream_t st = (hipStream_t)hip_stream;
+  tbs_model* m = new tbs_model();
+  m->V = vocab_size;
+  m->C = dim;
+  m->Kpad = round_up(dim, kKStep);
+  m->Vpad = round_up(vocab_size, kJoinerBN);
+  m->bf16 = dtype == TBS_JOINER_BF16;
+  const size_t VK = (size_t)m->V * m->Kpad, VpK = (size_t)m->Vpad * m->Kpad;
+  hipError_t e = hipSuccess;
+  if (e == hipSuccess) e = dalloc(&m->P0, VK);
+  if (e == hipSuccess) e = dalloc(&m->P1, VK);
+  if (e == hipSuccess) e = m->bf16 ? dalloc(&m->Wb, VpK) : dalloc(&m->Wf, VpK);
+  if (e == hipSuccess) e = dalloc(&m->bias, (size_t)m->V);
+  if (e == hipSuccess)
+    e = launch_model_setup(embed, conv, w_out, b_out, m->V, m->C, m->Kpad, m->Vpad, m->bf16,
+                           m->P0, m->P1, m->Wf, m->Wb, m->bias, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    tbs_model_destroy(m);
+    return hip_fail(e, "tbs_model_create");
+  }
+  *out = m;
+  return TBS_OK;
+}
+
+void tbs_model_destroy(tbs_model* m) {
+  if (!m) return;
+  {
+    std::lock_guard<std::mutex> lk(m->mu);
+    if (m->ws.done && m->ws.pending) hipEventSynchronize(m->ws.done);
+    m->ws.release();
+  }
+  hipFree(m->P0);
+  hipFree(m->P1);
+  hipFree(m->Wf);
+  hipFree(m->Wb);
+  hipFree(m->bias);
+  hipFree(m->rows_logits);
+  hipFree(m->rows_stats);
+  delete m;
+}
+
+tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
+                      const tbs_beam_params* params, const float* encoder_out,
+                      const int32_t* lengths, int32_t B, int32_t T, int32_t* out_tokens,
+                      int32_t* out_num_tokens, double* out_scores, int32_t* out_status,
+                      int32_t* out_arcs, int32_t* trace, void* hip_stream) {
+  if (!model || !graph || !params) return fail(TBS_EINVAL, "tbs_decode: NULL model/graph/params");
+  if (graph->V != model->V)
+    return fail(TBS_EINVAL, "tbs_decode: graph vocab_size %d != model vocab_size %d", graph->V,
+                model->V);
+  if (B < 0 || T < 0) return fail(TBS_EINVAL, "tbs_decode: B and T must be >= 0");
+  const float beam = params->beam;
+  const int Ns = params->max_states, Nc_req = params->max_contexts;
+  if (std::isnan(beam) || beam < 0.f)
+    return fail(TBS_EINVAL, "tbs_decode: beam must be >= 0 or INFINITY");
+  if (Ns < 1 || Nc_req < 1)
+    return fail(TBS_EINVAL, "tbs_decode: max_states and max_contexts must be >= 1");
+  if (Ns > kMaxStates)
+    return fail(TBS_ECAPACITY, "tbs_decode: max_states %d exceeds the limit %d", Ns, kMaxStates);
+  if ((long long)Ns * ((long long)graph->maxdeg + 1) >= (1ll << 31))
+    return fail(TBS_ECAPACITY,
+                "tbs_decode: max_states * (max out-degree + 1) = %lld must be < 2^31",
+                (long long)Ns * ((long long)graph->maxdeg + 1));
+  if (B == 0) return TBS_OK;
+  if (!lengths) return fail(TBS_EINVAL, "tbs_decode: lengths is NULL");
+  int maxlen = 0;
+  for (int b = 0; b < B; ++b) {
+    if (lengths[b] < 0 || lengths[b] > T)
+      return fail(TBS_EINVAL, "tbs_decode: lengths[%d] = %d outside [0, %d]", b, lengths[b], T);
+    if (lengths[b] > maxlen) maxlen = lengths[b];
+  }
+  if (maxlen > 0 && !encoder_out) return fail(TBS_EINVAL, "tbs_decode: encoder_out is NULL");
+  if (!out_num_tokens || !out_scores || (T > 0 && !out_tokens))
+    return fail(TBS_EINVAL, "tbs_decode: NULL output pointer");
+  // More contexts than tuples can never be active.
+  const int Nc = Nc_req < Ns ? Nc_req : Ns;
+
+  tbs_model* m = const_cast<tbs_model*>(model);
+  std::lock_guard<std::mutex> lk(m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  tbs_status s = ensure_workspace(m, B, T, Ns, Nc);
+  if (s != TBS_OK) return s;
+  Workspace& w = m->ws;
+  if (w.pending) HIP_TRY(hipStreamWaitEvent(st, w.done, 0), "hipStreamWaitEvent");
+  // lengths: wait until the previous decode consumed the pinned staging buffer
+  if (w.pending) HIP_TRY(hipEventSynchronize(w.done), "hipEventSynchronize");
+  std::memcpy(w.len_host, lengths, (size_t)B * 4);
+  HIP_TRY(hipMemcpyAsync(w.len, w.len_host, (size_t)B * 4, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(lengths)");
+
+  DecodeDev d;
+  d.B = B;
+  d.T = T;
+  d.Ns = Ns;
+  d.Nc = Nc;
+  d.nvt = m->Vpad / kJoinerBN;
+  d.len = w.len;
+  d.nsurv = w.nsurv;
+  d.surv_ctx = w.surv_ctx;
+  d.surv_state = w.surv_state;
+  d.surv_score = w.surv_score;
+  d.surv_row = w.surv_row;
+  d.nctx = w.nctx;
+  d.ctx_list = w.ctx_list;
+  d.offset = w.offset;
+  d.logits = w.logits;
+  d.stats = w.stats;
+  d.hist_pl = w.hist_pl;
+  d.hist_arc = w.hist_arc;
+  d.path_lab = w.path_lab;
+  const ModelDev md = model_dev(m);
+  const GraphDev gd = graph_dev(graph);
+
+  if (trace)
+    HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
+  HIP_TRY(launch_init(d, gd, trace, st), "launch(init)");
+  for (int t = 0; t < maxlen; ++t) {
+    HIP_TRY(launch_joiner_frame(md, d, encoder_out, t, st), "launch(joiner)");
+    HIP_TRY(launch_search_frame(md, gd, d, beam, t, trace, st), "launch(search)");
+  }
+  HIP_TRY(launch_final(gd, d, out_tokens, out_num_tokens, out_scores, out_status, out_arcs, st),
+          "launch(final)");
+  HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
+  w.pending = true;
+  return TBS_OK;
+}
+
+tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const int32_t* ctx,
+                           int32_t R, float* out_logp, void* hip_stream) {
+  if (!model) return fail(TBS_EINVAL, "tbs_joiner_logp: model is NULL");
+  if (R < 0) return fail(TBS_EINVAL, "tbs_joiner_logp: R must be >= 0");
+  if (R == 0) return TBS_OK;
+  if (!enc_rows || !ctx || !out_logp) return fail(TBS_EINVAL, "tbs_joiner_logp: NULL pointer");
+  tbs_model* m = const_cast<tbs_model*>(model);
+  std::lock_guard<std::mutex> lk(m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  const int nvt = m->Vpad / kJoinerBN;
+  const int Rpad = round_up(R, kJoinerBM);
+  if (Rpad > m->rows_cap) {
+    HIP_TRY(hipStreamSynchronize(st), "hipStreamSynchronize");
+    hipFree(m->rows_logits);
+    hipFree(m->rows_stats);
+    m->rows_logits = nullptr;
+    m->rows_stats = nullptr;
+    m->rows_cap = 0;
+    HIP_TRY(dalloc(&m->rows_logits, (size_t)Rpad * m->Vpad), "hipMalloc(rows)");
+    HIP_TRY(dalloc(&m->rows_stats, (size_t)Rpad * nvt), "hipMalloc(rows)");
+    m->rows_cap = Rpad;
+  }
+  HIP_TRY(launch_joiner_rows(model_dev(m), enc_rows, ctx, R, m->rows_logits, m->rows_stats,
+                             out_logp, st),
+          "launch(joiner_rows)");
+  return TBS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Internal declarations shared by the host runtime (api.cpp) and the gfx950
+// kernels (kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace tbs {
+
+constexpr int kMaxStates = 256;      // max_states limit (canonical ranking is O(Ns^2) per stream)
+constexpr int kMaxDim = 2048;        // joiner dimension limit (one 16-row h tile in LDS)
+constexpr int kJoinerBM = 16;        // joiner rows per tile (one MFMA M block)
+constexpr int kJoinerBN = 64;        // joiner vocabulary columns per tile (4 waves x 16)
+constexpr int kKStep = 64;           // K padding granule of the packed weights
+constexpr int kSearchThreads = 256;
+constexpr int kChunk = 2048;         // candidates merged per LDS pass
+constexpr int kHashSlots = 4096;     // LDS open-addressing table (load <= 0.57)
+
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+// Device-side model tables (padded: rows to Vpad, columns to Kpad, zeros).
+struct ModelDev {
+  int V, C, Kpad, Vpad;
+  int bf16;
+  const float* P0;          // [V][Kpad] conv tap 0 * embedding (older label)
+  const float* P1;          // [V][Kpad] conv tap 1 * embedding (newer label)
+  const float* Wf;          // [Vpad][Kpad] fp32 joiner weight (fp32 mode)
+  const uint16_t* Wb;       // [Vpad][Kpad] bf16 joiner weight (bf16 mode)
+  const float* bias;        // [V]
+};
+
+struct GraphDev {
+  int S, start, maxdeg;
+  const int* rp;
+  const int* dest;
+  const int* label;
+  const float* q;
+  const float* fin;         // [S] or null
+};
+
+// Per-decode device state.
+struct DecodeDev {
+  int B, T, Ns, Nc, nvt;    // nvt = number of joiner vocabulary tiles
+  const int* len;           // [B]
+  int* nsurv;               // [B]
+  int* surv_ctx;            // [B][Ns]
+  int* surv_state;          // [B][Ns]
+  float* surv_score;        // [B][Ns], relative to the stream's best
+  int* surv_row;            // [B][Ns], index of the tuple's context in ctx_list
+  int* nctx;                // [B]
+  int* ctx_list;            // [B][Nc], ascending
+  double* offset;           // [B]
+  float* logits;            // [B*Nc][Vpad]
+  float2* stats;            // [B*Nc][nvt]: (max, sum exp(z - max)) per vocabulary tile
+  int* hist_pl;             // [T][B][Ns]: parent << 16 | label
+  int* hist_arc;            // [T][B][Ns]: arc id, -1 blank
+  int* path_lab;            // [B][T] scratch for the traceback
+};
+
+hipError_t launch_model_setup(const float* embed, const float* conv, const float* w_out,
+                              const float* b_out, int V, int C, int Kpad, int Vpad, int bf16,
+                              float* P0, float* P1, float* Wf, uint16_t* Wb, float* bias,
+                              hipStream_t st);
+hipError_t launch_fill_i32(int* p, long long n, int v, hipStream_t st);
+hipError_t launch_init(const DecodeDev& d, const GraphDev& g, int* trace, hipStream_t st);
+hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const float* enc, int t,
+                               hipStream_t st);
+hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const DecodeDev& d,
+                               float beam, int t, int* trace, hipStream_t st);
+hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, int* out_ntok,
+                        double* out_scores, int* out_status, int* out_arcs, hipStream_t st);
+hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const int* ctx, int R,
+                              float* logits, float2* stats, float* out_logp, hipStream_t st);
+
+}  // namespace tbs

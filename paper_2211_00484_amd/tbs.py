@@ -1,0 +1,248 @@
+"""Python binding of libtbs.so (include/tbs.h): argument marshalling only.
+
+Every step of the decode runs in the HIP library; torch supplies device memory
+and the current HIP stream.  Importing this module does not load the library;
+the first call does, and raises if ``libtbs.so`` has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtbs.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "tbs.h")
+
+TBS_JOINER_FP32, TBS_JOINER_BF16 = 0, 1
+STATUS_NAMES = {0: "TBS_OK", -1: "TBS_EINVAL", -2: "TBS_ENOMEM", -3: "TBS_EDEVICE",
+                -4: "TBS_ECAPACITY", -5: "TBS_EUNSUPPORTED"}
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+
+
+class TbsError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class BeamParams(ctypes.Structure):
+    _fields_ = [("beam", ctypes.c_float), ("max_states", ctypes.c_int32),
+                ("max_contexts", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def declared_symbols() -> list:
+    """Names of the functions declared in include/tbs.h."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(tbs_[a-z_0-9]+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def lib():
+    """The loaded library; raises if it is missing (there is no fallback path)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(hipcc --offload-arch=gfx950); there is no CPU fallback")
+    L = ctypes.CDLL(LIB_PATH)
+    L.tbs_last_error.restype = ctypes.c_char_p
+    L.tbs_last_error.argtypes = []
+    L.tbs_graph_create.restype = _I32
+    L.tbs_graph_create.argtypes = [_I32, _I32, _I32, _P, _P, _P, _P, _P, ctypes.POINTER(_P)]
+    L.tbs_graph_create_trivial.restype = _I32
+    L.tbs_graph_create_trivial.argtypes = [_I32, ctypes.POINTER(_P)]
+    L.tbs_graph_destroy.restype = None
+    L.tbs_graph_destroy.argtypes = [_P]
+    L.tbs_model_create.restype = _I32
+    L.tbs_model_create.argtypes = [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, ctypes.POINTER(_P)]
+    L.tbs_model_destroy.restype = None
+    L.tbs_model_destroy.argtypes = [_P]
+    L.tbs_decode.restype = _I32
+    L.tbs_decode.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
+                             _P, _P, _P, _P, _P, _P, _P]
+    L.tbs_joiner_logp.restype = _I32
+    L.tbs_joiner_logp.argtypes = [_P, _P, _P, _I32, _P, _P]
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise TbsError(status, lib().tbs_last_error().decode())
+
+
+def _host_ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dev_ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("expected a contiguous device tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_ptr(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Graph:
+    """Device copy of an epsilon-free decoding graph (tbs_graph_create)."""
+
+    def __init__(self, handle, num_states: int, vocab_size: int, max_out_degree: int):
+        self._h = handle
+        self.num_states, self.vocab_size, self.max_out_degree = num_states, vocab_size, max_out_degree
+
+    @classmethod
+    def from_csr(cls, num_states, start, vocab_size, row_ptr, dest, label, score, final=None):
+        rp = np.ascontiguousarray(row_ptr, dtype=np.int32)
+        de = np.ascontiguousarray(dest, dtype=np.int32)
+        la = np.ascontiguousarray(label, dtype=np.int32)
+        sc = np.ascontiguousarray(score, dtype=np.float32)
+        fi = None if final is None else np.ascontiguousarray(final, dtype=np.float32)
+        h = _P()
+        _check(lib().tbs_graph_create(int(num_states), int(start), int(vocab_size), _host_ptr(rp),
+                                      _host_ptr(de), _host_ptr(la), _host_ptr(sc), _host_ptr(fi),
+                                      ctypes.byref(h)))
+        deg = int(np.max(np.diff(rp))) if len(rp) > 1 else 0
+        return cls(h, int(num_states), int(vocab_size), deg)
+
+    @classmethod
+    def trivial(cls, vocab_size: int):
+        h = _P()
+        _check(lib().tbs_graph_create_trivial(int(vocab_size), ctypes.byref(h)))
+        return cls(h, 1, int(vocab_size), int(vocab_size) - 1)
+
+    @classmethod
+    def from_synth(cls, g):
+        return cls.from_csr(g.num_states, g.start, g.vocab_size, g.row_ptr, g.dest, g.label,
+                            g.score, g.final)
+
+    def close(self):
+        if self._h is not None and _lib is not None:
+            _lib.tbs_graph_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        self.close()
+
+
+class Model:
+    """Stateless decoder + joiner weights on the device (tbs_model_create)."""
+
+    def __init__(self, vocab_size: int, dim: int, embed, conv, w_out, b_out=None,
+                 dtype: str = "fp32", stream=None):
+        import torch
+        dev = torch.device("cuda", torch.cuda.current_device())
+
+        def dt(x):
+            if x is None:
+                return None
+            if isinstance(x, np.ndarray):
+                x = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+            return x.to(device=dev, dtype=torch.float32).contiguous()
+
+        E, cv, W, b = dt(embed), dt(conv), dt(w_out), dt(b_out)
+        code = {"fp32": TBS_JOINER_FP32, "bf16": TBS_JOINER_BF16}[dtype]
+        h = _P()
+        _check(lib().tbs_model_create(int(vocab_size), int(dim), 2, _dev_ptr(E), _dev_ptr(cv),
+                                      _dev_ptr(W), _dev_ptr(b), code, _stream_ptr(stream),
+                                      ctypes.byref(h)))
+        self._h = h
+        self.vocab_size, self.dim, self.dtype = int(vocab_size), int(dim), dtype
+
+    @classmethod
+    def from_synth(cls, m, dtype: str = "fp32"):
+        return cls(m.vocab_size, m.dim, m.embed, m.conv, m.w_out, m.b_out, dtype=dtype)
+
+    def close(self):
+        if self._h is not None and _lib is not None:
+            _lib.tbs_model_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        self.close()
+
+
+@dataclass
+class DecodeOutput:
+    tokens: "object"      # int32 [B, T] device
+    num_tokens: "object"  # int32 [B]
+    scores: "object"      # float64 [B]
+    status: "object"      # int32 [B] or None
+    arcs: "object"        # int32 [B, T] or None
+    trace: "object"       # int32 [T+1, B, Ns, 4] or None
+
+    def token_lists(self):
+        tok = self.tokens.cpu().numpy()
+        n = self.num_tokens.cpu().numpy()
+        return [list(tok[b, : n[b]]) for b in range(tok.shape[0])]
+
+
+def allocate_outputs(B: int, T: int, max_states: int, status=True, arcs=False, trace=False,
+                     device=None) -> DecodeOutput:
+    import torch
+    dev = device or torch.device("cuda", torch.cuda.current_device())
+    i32 = dict(dtype=torch.int32, device=dev)
+    return DecodeOutput(
+        tokens=torch.empty((B, T), **i32), num_tokens=torch.empty(B, **i32),
+        scores=torch.empty(B, dtype=torch.float64, device=dev),
+        status=torch.empty(B, **i32) if status else None,
+        arcs=torch.empty((B, T), **i32) if arcs else None,
+        trace=torch.empty((T + 1, B, max_states, 4), **i32) if trace else None)
+
+
+def decode_into(model: Model, graph: Graph, encoder_out, lengths, beam: float, max_states: int,
+                max_contexts: int, out: DecodeOutput, stream=None) -> DecodeOutput:
+    """tbs_decode into preallocated outputs (stream-ordered; no synchronisation)."""
+    lens = np.ascontiguousarray(np.asarray(lengths), dtype=np.int32)
+    B, T = int(encoder_out.shape[0]), int(encoder_out.shape[1])
+    if encoder_out.dim() != 3 or encoder_out.shape[2] != model.dim:
+        raise ValueError("encoder_out must be [B, T, dim]")
+    if lens.shape != (B,):
+        raise ValueError("lengths must have shape [B]")
+    params = BeamParams(float(math.inf if beam is None else beam), int(max_states),
+                        int(max_contexts))
+    _check(lib().tbs_decode(model._h, graph._h, ctypes.byref(params), _dev_ptr(encoder_out),
+                            _host_ptr(lens), B, T, _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
+                            _dev_ptr(out.scores), _dev_ptr(out.status), _dev_ptr(out.arcs),
+                            _dev_ptr(out.trace), _stream_ptr(stream)))
+    return out
+
+
+def decode(model: Model, graph: Graph, encoder_out, lengths, beam: float = math.inf,
+           max_states: int = 4, max_contexts: int = 4, want_arcs: bool = False,
+           want_trace: bool = False, stream=None) -> DecodeOutput:
+    """Batched FSA-constrained one-symbol-per-frame beam search; outputs on the device."""
+    B, T = int(encoder_out.shape[0]), int(encoder_out.shape[1])
+    out = allocate_outputs(B, T, max_states, status=True, arcs=want_arcs, trace=want_trace,
+                           device=encoder_out.device)
+    return decode_into(model, graph, encoder_out, lengths, beam, max_states, max_contexts, out,
+                       stream)
+
+
+def joiner_logp(model: Model, enc_rows, ctx, stream=None):
+    """log P(. | ctx, enc row) [R, V] from the HIP joiner (tbs_joiner_logp)."""
+    import torch
+    R = int(enc_rows.shape[0])
+    out = torch.empty((R, model.vocab_size), dtype=torch.float32, device=enc_rows.device)
+    ctx = ctx.to(device=enc_rows.device, dtype=torch.int32).contiguous()
+    _check(lib().tbs_joiner_logp(model._h, _dev_ptr(enc_rows.contiguous()), _dev_ptr(ctx), R,
+                                 _dev_ptr(out), _stream_ptr(stream)))
+    return out

@@ -1,0 +1,48 @@
+"""HIP decoder + joiner + log-softmax (tbs_joiner_logp) against the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import say
+from paper_2211_00484_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # (V, C, sigma, R)
+    (16, 32, 0.1, 37),        # Tiny shapes, ragged row count
+    (500, 512, 0.05, 70),     # Standard / Graph / Throughput shapes
+    (5000, 512, 0.05, 20),    # Large shapes
+    (129, 100, 0.3, 33),      # ragged V and C (padding paths)
+]
+
+
+@pytest.mark.parametrize("V,C,sigma,R", SHAPES)
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_joiner_matches_oracle(V, C, sigma, R, dtype):
+    import torch
+    from paper_2211_00484_amd import tbs
+    say(f"joiner V={V} C={C} R={R} {dtype}")
+    rng = np.random.default_rng(V + C)
+    model_np = synth.make_model(rng, V, C, sigma)
+    enc = rng.standard_normal((R, C), dtype=np.float32)
+    a = rng.integers(0, V, R).astype(np.int32)
+    b = rng.integers(0, V, R).astype(np.int32)
+    model = tbs.Model.from_synth(model_np, dtype=dtype)
+    ctx = torch.from_numpy((a.astype(np.int64) * V + b).astype(np.int32))
+    got = tbs.joiner_logp(model, torch.from_numpy(enc).cuda(), ctx).cpu().numpy()
+    want = oracle.logp(model_np, enc, a, b, bf16=(dtype == "bf16"))
+    err = np.abs(got - want).max()
+    say(f"  max |dlogp| = {err:.3g}")
+    tol = 1e-4 if dtype == "fp32" else 2e-2
+    assert err <= tol
+    if dtype == "bf16":  # distance to the exact fp32-operand joiner, for the record
+        exact = oracle.logp(model_np, enc, a, b, bf16=False)
+        say(f"  bf16 vs fp32-operand oracle: {np.abs(got - exact).max():.3g}")
+
+
+def test_joiner_empty_batch():
+    import torch
+    from paper_2211_00484_amd import tbs
+    model = tbs.Model.from_synth(synth.make_model(np.random.default_rng(0), 8, 16, 0.1))
+    out = tbs.joiner_logp(model, torch.zeros((0, 16), device="cuda"), torch.zeros(0, dtype=torch.int32))
+    assert out.shape == (0, 8)
