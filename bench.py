@@ -1,0 +1,192 @@
+"""Benchmark: decoded frames/s of batched FSA-based one-symbol-per-frame beam search
+on one MI355X, with the dominant kernel's roofline fraction and the CPU oracle's rate.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload standard]
+
+A step is one tbs_decode of the whole batch (every frame of every stream: joiner,
+expansion, merge, pruning, history, traceback) on inputs already resident in HBM.
+Per-kernel durations come from HIP events the library records around each launch on
+the decode stream during the timed steps (tbs_model_set_profiling).  Algorithmic work
+(joiner FLOP, search bytes) is counted from the survivor trace of one untimed decode.
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decoded frames/sec (B×T) at beam 4; joiner MFMA util %; prune HBM GB/s"
+PEAK = {"fp32_mfma_tflops": 157.3, "bf16_mfma_tflops": 2500.0, "hbm_gbps": 8000.0}
+DEFAULT_STEPS = {"tiny": 50, "standard": 20, "graph": 20, "throughput": 10, "large": 3}
+CPU_SAMPLE_STREAMS = {"tiny": None, "standard": None, "graph": None, "throughput": 24,
+                      "large": 12}
+
+
+def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles):
+    """Joiner rows (contexts) and search traffic implied by a survivor trace."""
+    deg = np.diff(graph.row_ptr).astype(np.int64)
+    rows = 0
+    cands = 0
+    arcs = 0
+    survivors_in = 0
+    survivors_out = 0
+    for b in range(trace.shape[1]):
+        L = int(lengths[b])
+        for f in range(L):
+            cur = trace[f, b]
+            n = int((cur[:, 0] >= 0).sum())
+            rows += len(np.unique(cur[:n, 0]))
+            a = int(deg[cur[:n, 1]].sum())
+            arcs += a
+            cands += n + a
+            survivors_in += n
+            survivors_out += int((trace[f + 1, b, :, 0] >= 0).sum())
+    flop = 2.0 * rows * C * V
+    # search kernel bytes: arc record (dest, label, score) + gathered logit per arc,
+    # a logit per blank, survivor record in (ctx, state, row, score) + row_ptr pair,
+    # per-row softmax partials, survivor record out + history (parent|label, arc).
+    search_bytes = (arcs * (12 + 4) + (cands - arcs) * 4 + survivors_in * (16 + 8)
+                    + rows * Vpad_tiles * 8 + survivors_out * (16 + 8) + rows * 4)
+    return dict(rows=rows, flop=flop, candidates=cands, arcs=arcs, search_bytes=search_bytes,
+                survivors=survivors_in)
+
+
+def cpu_baseline(w, inputs, model_np, graph_np):
+    import oracle
+    sample = CPU_SAMPLE_STREAMS[w.name]
+    streams = list(range(inputs.B)) if sample is None else list(range(0, inputs.B, inputs.B // sample))[:sample]
+    threads = min(os.cpu_count() or 1, len(streams))
+    frames = int(inputs.lengths[streams].sum())
+    t0 = time.perf_counter()
+    oracle.decode(model_np, graph_np, inputs.encoder_out, inputs.lengths, w.beam, w.max_states,
+                  w.max_contexts, bf16=(w.dtype == "bf16"), nthreads=threads, want_trace=False,
+                  want_arcs=False, streams=streams)
+    dt = time.perf_counter() - t0
+    return {"value": frames / dt, "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(streams)} of {inputs.B} streams ({frames} frames), fp64 C++ oracle, "
+                      f"{threads} threads, {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="standard",
+                    choices=["tiny", "standard", "graph", "throughput", "large"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}): streams are "
+              "independent, so more GPUs would each decode their own share of the batch; "
+              "multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2211_00484_amd import synth, tbs
+
+    torch.cuda.set_device(0)
+    w, inputs, model_np, graph_np = synth.make_workload(args.workload, seed=0)
+    K = args.steps if args.steps is not None else DEFAULT_STEPS[w.name]
+    W = args.warmup
+    model = tbs.Model.from_synth(model_np, dtype=w.dtype)
+    graph = tbs.Graph.from_synth(graph_np)
+    enc = torch.from_numpy(inputs.encoder_out).cuda()
+    B, T = inputs.B, inputs.T
+    frames = int(inputs.lengths.sum())
+
+    # untimed decode with the survivor trace: algorithmic work of one step
+    tr_out = tbs.decode(model, graph, enc, inputs.lengths, beam=w.beam, max_states=w.max_states,
+                        max_contexts=w.max_contexts, want_trace=True)
+    torch.cuda.synchronize()
+    nvt = (w.V + 63) // 64
+    work = algorithmic_work(tr_out.trace.cpu().numpy(), inputs.lengths, graph_np, w.V, w.C, nvt)
+    del tr_out
+
+    out = tbs.allocate_outputs(B, T, w.max_states, status=True)
+    for _ in range(W):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+    torch.cuda.synchronize()
+
+    model.set_profiling(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = model.read_profile()
+    model.set_profiling(False)
+
+    # same steps without the timing events, for the event overhead
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(K):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+
+    ms_step = (t1 - t0) * 1e3 / K
+    ms_step_plain = (t3 - t2) * 1e3 / K
+    value = frames * K / (t1 - t0)
+
+    kernels = {}
+    for name, (n, ms) in prof.items():
+        kernels[name] = {"launches_per_step": n / K, "avg_us": 1e3 * ms / max(n, 1),
+                         "ms_per_step": ms / K}
+    j_avg_s = kernels["joiner"]["avg_us"] * 1e-6
+    s_avg_s = kernels["search"]["avg_us"] * 1e-6
+    j_launches = kernels["joiner"]["launches_per_step"]
+    flop_per_launch = work["flop"] / max(j_launches, 1)
+    bytes_per_launch = work["search_bytes"] / max(kernels["search"]["launches_per_step"], 1)
+    peak_j = PEAK["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+    j_tflops = flop_per_launch / j_avg_s / 1e12
+    s_gbps = bytes_per_launch / s_avg_s / 1e9
+    kernels["joiner"].update({"algorithmic_flop_per_launch": flop_per_launch, "tflops": j_tflops,
+                              "peak_tflops": peak_j, "frac": j_tflops / peak_j})
+    kernels["search"].update({"algorithmic_bytes_per_launch": bytes_per_launch, "gbps": s_gbps,
+                              "peak_gbps": PEAK["hbm_gbps"], "frac": s_gbps / PEAK["hbm_gbps"]})
+    if kernels["joiner"]["ms_per_step"] >= kernels["search"]["ms_per_step"]:
+        roofline = {"kernel": "k_joiner", "bound": "mfma", "achieved": j_tflops, "peak": peak_j,
+                    "unit": "TFLOP/s", "frac": j_tflops / peak_j, "traffic": None}
+    else:
+        roofline = {"kernel": "k_search", "bound": "hbm", "achieved": s_gbps,
+                    "peak": PEAK["hbm_gbps"], "unit": "GB/s", "frac": s_gbps / PEAK["hbm_gbps"],
+                    "traffic": None}
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "frames/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if w.dtype == "fp32" else "bf16 joiner operands, f32 accumulate/scores",
+        "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description, "B": B, "T_max": T,
+                   "frames": frames, "C": w.C, "V": w.V, "graph": w.graph,
+                   "graph_states": graph_np.num_states, "graph_arcs": graph_np.num_arcs,
+                   "beam": "inf" if math.isinf(w.beam) else w.beam,
+                   "max_states": w.max_states, "max_contexts": w.max_contexts,
+                   "joiner": w.dtype},
+        "roofline": roofline,
+        "kernels": kernels,
+        "joiner_mfma_util_pct": 100.0 * j_tflops / peak_j,
+        "search_hbm_gbps": s_gbps,
+        "ms_per_step_without_timing_events": ms_step_plain,
+        "per_frame_latency_us": 1e3 * ms_step / max(int(inputs.lengths.max()), 1),
+        "work_per_step": work,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, inputs, model_np, graph_np)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

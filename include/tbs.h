@@ -91,7 +91,7 @@ typedef enum { TBS_JOINER_FP32 = 0, TBS_JOINER_BF16 = 1 } tbs_joiner_dtype;
  *                      label a; no bias);
  *   joiner             logits = w_out . tanh(enc + dec) + b_out, then log-softmax
  *                      over all V outputs, blank included.
- *   vocab_size V in [2, 65535]; dim C in [1, 4096]; context_size must be 2
+ *   vocab_size V in [2, 65535]; dim C in [1, 2048]; context_size must be 2
  *   (TBS_EUNSUPPORTED otherwise).
  *   embed  DEVICE float [V][C];  conv DEVICE float [C][2];
  *   w_out  DEVICE float [V][C] (torch Linear layout);  b_out DEVICE float [V] or NULL (= 0).
@@ -171,6 +171,31 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
  */
 tbs_status tbs_joiner_logp(const tbs_model *model, const float *enc_rows, const int32_t *ctx,
                            int32_t R, float *out_logp, void *hip_stream);
+
+/*
+ * Per-kernel timing, for benchmarks.  While enabled on a model, every decode
+ * records a pair of HIP events around each kernel launch on its stream
+ * (joiner and search once per frame, final once per decode) and keeps them
+ * pending.  tbs_model_read_profile waits for those events, adds their elapsed
+ * times into out[TBS_KERNEL_COUNT] (indexed by tbs_kernel_id; launches and
+ * milliseconds since the last enable) and releases them.  Enabling resets the
+ * counters; disabling drops pending events.  The events sit between kernels
+ * that are stream-ordered anyway, so timing adds only the event packets.
+ */
+typedef enum {
+  TBS_KERNEL_JOINER = 0,
+  TBS_KERNEL_SEARCH = 1,
+  TBS_KERNEL_FINAL = 2,
+  TBS_KERNEL_COUNT = 3
+} tbs_kernel_id;
+
+typedef struct {
+  int32_t launches;
+  double total_ms;
+} tbs_kernel_time;
+
+tbs_status tbs_model_set_profiling(tbs_model *model, int32_t enable);
+tbs_status tbs_model_read_profile(tbs_model *model, tbs_kernel_time *out);
 
 /* Message for the calling thread's last error ("" if none). */
 const char *tbs_last_error(void);

@@ -99,6 +99,15 @@ struct tbs_model {
   float* bias = nullptr;
   std::mutex mu;
   Workspace ws;
+  // per-kernel timing (tbs_model_set_profiling)
+  bool prof = false;
+  struct Timed {
+    int kernel;
+    hipEvent_t start, stop;
+  };
+  std::vector<Timed> prof_pending;
+  std::vector<hipEvent_t> prof_pool;
+  tbs_kernel_time prof_acc[TBS_KERNEL_COUNT] = {};
   // scratch for tbs_joiner_logp
   int rows_cap = 0;
   float* rows_logits = nullptr;
@@ -163,6 +172,38 @@ void graph_free(tbs_graph* g) {
   hipFree(g->q);
   hipFree(g->fin);
   delete g;
+}
+
+hipError_t prof_event(tbs_model* m, hipEvent_t* ev) {
+  if (!m->prof_pool.empty()) {
+    *ev = m->prof_pool.back();
+    m->prof_pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(ev);
+}
+
+// Launches `fn` on st, bracketed by timing events when profiling is on.
+template <class F>
+hipError_t timed_launch(tbs_model* m, int kernel, hipStream_t st, F fn) {
+  if (!m->prof) return fn();
+  hipEvent_t a, b;
+  hipError_t e = prof_event(m, &a);
+  if (e == hipSuccess) e = prof_event(m, &b);
+  if (e == hipSuccess) e = hipEventRecord(a, st);
+  if (e == hipSuccess) e = fn();
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) m->prof_pending.push_back({kernel, a, b});
+  return e;
+}
+
+void prof_drop(tbs_model* m) {
+  for (auto& x : m->prof_pending) {
+    hipEventSynchronize(x.stop);
+    m->prof_pool.push_back(x.start);
+    m->prof_pool.push_back(x.stop);
+  }
+  m->prof_pending.clear();
 }
 
 tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc) {
@@ -325,6 +366,8 @@ void tbs_model_destroy(tbs_model* m) {
     if (m->ws.done && m->ws.pending) hipEventSynchronize(m->ws.done);
     m->ws.release();
   }
+  prof_drop(m);
+  for (hipEvent_t e : m->prof_pool) hipEventDestroy(e);
   hipFree(m->P0);
   hipFree(m->P1);
   hipFree(m->Wf);
@@ -411,10 +454,18 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(d, gd, trace, st), "launch(init)");
   for (int t = 0; t < maxlen; ++t) {
-    HIP_TRY(launch_joiner_frame(md, d, encoder_out, t, st), "launch(joiner)");
-    HIP_TRY(launch_search_frame(md, gd, d, beam, t, trace, st), "launch(search)");
+    HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
+                         [&] { return launch_joiner_frame(md, d, encoder_out, t, st); }),
+            "launch(joiner)");
+    HIP_TRY(timed_launch(m, TBS_KERNEL_SEARCH, st,
+                         [&] { return launch_search_frame(md, gd, d, beam, t, trace, st); }),
+            "launch(search)");
   }
-  HIP_TRY(launch_final(gd, d, out_tokens, out_num_tokens, out_scores, out_status, out_arcs, st),
+  HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
+                       [&] {
+                         return launch_final(gd, d, out_tokens, out_num_tokens, out_scores,
+                                             out_status, out_arcs, st);
+                       }),
           "launch(final)");
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
   w.pending = true;
@@ -446,6 +497,30 @@ tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const 
   HIP_TRY(launch_joiner_rows(model_dev(m), enc_rows, ctx, R, m->rows_logits, m->rows_stats,
                              out_logp, st),
           "launch(joiner_rows)");
+  return TBS_OK;
+}
+
+tbs_status tbs_model_set_profiling(tbs_model* model, int32_t enable) {
+  if (!model) return fail(TBS_EINVAL, "tbs_model_set_profiling: model is NULL");
+  std::lock_guard<std::mutex> lk(model->mu);
+  prof_drop(model);
+  for (auto& x : model->prof_acc) x = tbs_kernel_time{0, 0.0};
+  model->prof = enable != 0;
+  return TBS_OK;
+}
+
+tbs_status tbs_model_read_profile(tbs_model* model, tbs_kernel_time* out) {
+  if (!model || !out) return fail(TBS_EINVAL, "tbs_model_read_profile: NULL argument");
+  std::lock_guard<std::mutex> lk(model->mu);
+  for (auto& x : model->prof_pending) {
+    HIP_TRY(hipEventSynchronize(x.stop), "hipEventSynchronize");
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, x.start, x.stop), "hipEventElapsedTime");
+    model->prof_acc[x.kernel].launches += 1;
+    model->prof_acc[x.kernel].total_ms += ms;
+  }
+  prof_drop(model);
+  for (int k = 0; k < TBS_KERNEL_COUNT; ++k) out[k] = model->prof_acc[k];
   return TBS_OK;
 }
 

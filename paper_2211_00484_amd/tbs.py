@@ -33,6 +33,13 @@ class TbsError(RuntimeError):
         self.status = status
 
 
+class KernelTime(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
+
+
+KERNEL_NAMES = ("joiner", "search", "final")
+
+
 class BeamParams(ctypes.Structure):
     _fields_ = [("beam", ctypes.c_float), ("max_states", ctypes.c_int32),
                 ("max_contexts", ctypes.c_int32)]
@@ -73,6 +80,10 @@ def lib():
     L.tbs_decode.restype = _I32
     L.tbs_decode.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
                              _P, _P, _P, _P, _P, _P, _P]
+    L.tbs_model_set_profiling.restype = _I32
+    L.tbs_model_set_profiling.argtypes = [_P, _I32]
+    L.tbs_model_read_profile.restype = _I32
+    L.tbs_model_read_profile.argtypes = [_P, ctypes.POINTER(KernelTime)]
     L.tbs_joiner_logp.restype = _I32
     L.tbs_joiner_logp.argtypes = [_P, _P, _P, _I32, _P, _P]
     _lib = L
@@ -166,6 +177,15 @@ class Model:
                                       ctypes.byref(h)))
         self._h = h
         self.vocab_size, self.dim, self.dtype = int(vocab_size), int(dim), dtype
+
+    def set_profiling(self, enable: bool):
+        _check(lib().tbs_model_set_profiling(self._h, int(bool(enable))))
+
+    def read_profile(self) -> dict:
+        """{kernel: (launches, total_ms)} accumulated since profiling was enabled."""
+        arr = (KernelTime * len(KERNEL_NAMES))()
+        _check(lib().tbs_model_read_profile(self._h, arr))
+        return {n: (int(arr[i].launches), float(arr[i].total_ms)) for i, n in enumerate(KERNEL_NAMES)}
 
     @classmethod
     def from_synth(cls, m, dtype: str = "fp32"):
