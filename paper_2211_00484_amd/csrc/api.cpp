@@ -50,7 +50,8 @@ hipError_t dalloc(T** p, size_t n) {
 }
 
 struct Workspace {
-  int B = 0, T = 0, Ns = 0, Nc = 0;
+  int B = 0, T = 0, Ns = 0, Nc = 0, KT = 0;
+  bool has_logits = false;
   int* len = nullptr;
   int* nsurv = nullptr;
   int* surv_ctx = nullptr;
@@ -60,8 +61,12 @@ struct Workspace {
   int* nctx = nullptr;
   int* ctx_list = nullptr;
   double* offset = nullptr;
+  void* h = nullptr;
   float* logits = nullptr;
   float2* stats = nullptr;
+  float* tk_z = nullptr;
+  int* tk_c = nullptr;
+  float* z0 = nullptr;
   int* hist_pl = nullptr;
   int* hist_arc = nullptr;
   int* path_lab = nullptr;
@@ -71,8 +76,9 @@ struct Workspace {
 
   void release() {
     hipFree(len); hipFree(nsurv); hipFree(surv_ctx); hipFree(surv_state); hipFree(surv_score);
-    hipFree(surv_row); hipFree(nctx); hipFree(ctx_list); hipFree(offset); hipFree(logits);
-    hipFree(stats); hipFree(hist_pl); hipFree(hist_arc); hipFree(path_lab);
+    hipFree(surv_row); hipFree(nctx); hipFree(ctx_list); hipFree(offset); hipFree(h);
+    hipFree(logits); hipFree(stats); hipFree(tk_z); hipFree(tk_c); hipFree(z0);
+    hipFree(hist_pl); hipFree(hist_arc); hipFree(path_lab);
     if (len_host) hipHostFree(len_host);
     if (done) hipEventDestroy(done);
     *this = Workspace();
@@ -83,6 +89,7 @@ struct Workspace {
 
 struct tbs_graph {
   int S = 0, start = 0, V = 0, A = 0, maxdeg = 0;
+  int trivial = 0;  // one state, 0-weight loops 1..V-1 in label order, final weight 0
   int* rp = nullptr;
   int* dest = nullptr;
   int* label = nullptr;
@@ -110,6 +117,7 @@ struct tbs_model {
   tbs_kernel_time prof_acc[TBS_KERNEL_COUNT] = {};
   // scratch for tbs_joiner_logp
   int rows_cap = 0;
+  void* rows_h = nullptr;
   float* rows_logits = nullptr;
   float2* rows_stats = nullptr;
 };
@@ -136,6 +144,7 @@ GraphDev graph_dev(const tbs_graph* g) {
   d.S = g->S;
   d.start = g->start;
   d.maxdeg = g->maxdeg;
+  d.trivial = g->trivial;
   d.rp = g->rp;
   d.dest = g->dest;
   d.label = g->label;
@@ -206,15 +215,19 @@ void prof_drop(tbs_model* m) {
   m->prof_pending.clear();
 }
 
-tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc) {
+tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc, int KT,
+                            bool need_logits) {
   Workspace& w = m->ws;
-  if (w.done && w.B >= B && w.T >= T && w.Ns == Ns && w.Nc == Nc) return TBS_OK;
+  if (w.done && w.B >= B && w.T >= T && w.Ns == Ns && w.Nc == Nc && w.KT == KT &&
+      (w.has_logits || !need_logits))
+    return TBS_OK;
   if (w.done) {
     if (w.pending) hipEventSynchronize(w.done);
     w.release();
   }
   const int nvt = m->Vpad / kJoinerBN;
   const size_t BN = (size_t)B * Ns, BC = (size_t)B * Nc;
+  const size_t esz = m->bf16 ? 2 : 4;
   HIP_TRY(dalloc(&w.len, B), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.nsurv, B), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.surv_ctx, BN), "hipMalloc(workspace)");
@@ -224,8 +237,15 @@ tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc) {
   HIP_TRY(dalloc(&w.nctx, B), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.ctx_list, BC), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.offset, B), "hipMalloc(workspace)");
-  HIP_TRY(dalloc(&w.logits, BC * m->Vpad), "hipMalloc(workspace)");
+  HIP_TRY(dalloc((char**)&w.h, BC * m->Kpad * esz), "hipMalloc(workspace)");
+  if (need_logits) HIP_TRY(dalloc(&w.logits, BC * m->Vpad), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.stats, BC * nvt), "hipMalloc(workspace)");
+  if (KT > 0) {
+    const size_t nsub = (size_t)nvt * (kJoinerBN / 16);
+    HIP_TRY(dalloc(&w.tk_z, BC * nsub * KT), "hipMalloc(workspace)");
+    HIP_TRY(dalloc(&w.tk_c, BC * nsub * KT), "hipMalloc(workspace)");
+    HIP_TRY(dalloc(&w.z0, BC), "hipMalloc(workspace)");
+  }
   HIP_TRY(dalloc(&w.hist_pl, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.hist_arc, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.path_lab, (size_t)B * T), "hipMalloc(workspace)");
@@ -236,6 +256,8 @@ tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc) {
   w.T = T;
   w.Ns = Ns;
   w.Nc = Nc;
+  w.KT = KT;
+  w.has_logits = need_logits;
   return TBS_OK;
 }
 
@@ -292,6 +314,11 @@ tbs_status tbs_graph_create(int32_t num_states, int32_t start_state, int32_t voc
   g->V = vocab_size;
   g->A = A;
   g->maxdeg = maxdeg;
+  bool trivial = num_states == 1 && A == vocab_size - 1 &&
+                 (!final_score || final_score[0] == 0.f);
+  for (int j = 0; trivial && j < A; ++j)
+    trivial = label[j] == j + 1 && dest[j] == 0 && score[j] == 0.f;
+  g->trivial = trivial;
   tbs_status st = graph_upload(g, row_ptr, dest, label, score, final_score);
   if (st != TBS_OK) {
     graph_free(g);
@@ -373,6 +400,7 @@ void tbs_model_destroy(tbs_model* m) {
   hipFree(m->Wf);
   hipFree(m->Wb);
   hipFree(m->bias);
+  hipFree(m->rows_h);
   hipFree(m->rows_logits);
   hipFree(m->rows_stats);
   delete m;
@@ -414,10 +442,14 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   // More contexts than tuples can never be active.
   const int Nc = Nc_req < Ns ? Nc_req : Ns;
 
+  // Trivial graph with few tuples: the joiner keeps each row's best labels per
+  // vocabulary tile instead of materialising the logits.
+  const int KT = (graph->trivial && Ns <= kMaxTopK) ? Ns : 0;
+
   tbs_model* m = const_cast<tbs_model*>(model);
   std::lock_guard<std::mutex> lk(m->mu);
   hipStream_t st = (hipStream_t)hip_stream;
-  tbs_status s = ensure_workspace(m, B, T, Ns, Nc);
+  tbs_status s = ensure_workspace(m, B, T, Ns, Nc, KT, KT == 0);
   if (s != TBS_OK) return s;
   Workspace& w = m->ws;
   if (w.pending) HIP_TRY(hipStreamWaitEvent(st, w.done, 0), "hipStreamWaitEvent");
@@ -433,6 +465,8 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   d.Ns = Ns;
   d.Nc = Nc;
   d.nvt = m->Vpad / kJoinerBN;
+  d.KT = KT;
+  d.enc = encoder_out;
   d.len = w.len;
   d.nsurv = w.nsurv;
   d.surv_ctx = w.surv_ctx;
@@ -442,20 +476,25 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   d.nctx = w.nctx;
   d.ctx_list = w.ctx_list;
   d.offset = w.offset;
+  d.h = w.h;
   d.logits = w.logits;
   d.stats = w.stats;
+  d.tk_z = w.tk_z;
+  d.tk_c = w.tk_c;
+  d.z0 = w.z0;
   d.hist_pl = w.hist_pl;
   d.hist_arc = w.hist_arc;
   d.path_lab = w.path_lab;
   const ModelDev md = model_dev(m);
   const GraphDev gd = graph_dev(graph);
+  const JoinerPlan plan = plan_joiner(B * Nc, m->Vpad, m->Kpad, m->bf16);
 
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
-  HIP_TRY(launch_init(d, gd, trace, st), "launch(init)");
+  HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
   for (int t = 0; t < maxlen; ++t) {
     HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
-                         [&] { return launch_joiner_frame(md, d, encoder_out, t, st); }),
+                         [&] { return launch_joiner_frame(md, d, plan, t, st); }),
             "launch(joiner)");
     HIP_TRY(timed_launch(m, TBS_KERNEL_SEARCH, st,
                          [&] { return launch_search_frame(md, gd, d, beam, t, trace, st); }),
@@ -482,20 +521,24 @@ tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const 
   std::lock_guard<std::mutex> lk(m->mu);
   hipStream_t st = (hipStream_t)hip_stream;
   const int nvt = m->Vpad / kJoinerBN;
-  const int Rpad = round_up(R, kJoinerBM);
+  const int Rpad = round_up(R, 64);
   if (Rpad > m->rows_cap) {
     HIP_TRY(hipStreamSynchronize(st), "hipStreamSynchronize");
+    hipFree(m->rows_h);
     hipFree(m->rows_logits);
     hipFree(m->rows_stats);
+    m->rows_h = nullptr;
     m->rows_logits = nullptr;
     m->rows_stats = nullptr;
     m->rows_cap = 0;
+    HIP_TRY(dalloc((char**)&m->rows_h, (size_t)Rpad * m->Kpad * (m->bf16 ? 2 : 4)),
+            "hipMalloc(rows)");
     HIP_TRY(dalloc(&m->rows_logits, (size_t)Rpad * m->Vpad), "hipMalloc(rows)");
     HIP_TRY(dalloc(&m->rows_stats, (size_t)Rpad * nvt), "hipMalloc(rows)");
     m->rows_cap = Rpad;
   }
-  HIP_TRY(launch_joiner_rows(model_dev(m), enc_rows, ctx, R, m->rows_logits, m->rows_stats,
-                             out_logp, st),
+  HIP_TRY(launch_joiner_rows(model_dev(m), enc_rows, ctx, R, m->rows_h, m->rows_logits,
+                             m->rows_stats, out_logp, st),
           "launch(joiner_rows)");
   return TBS_OK;
 }

@@ -8,13 +8,16 @@
 namespace tbs {
 
 constexpr int kMaxStates = 256;      // max_states limit (canonical ranking is O(Ns^2) per stream)
-constexpr int kMaxDim = 2048;        // joiner dimension limit (one 16-row h tile in LDS)
-constexpr int kJoinerBM = 16;        // joiner rows per tile (one MFMA M block)
+constexpr int kMaxDim = 2048;        // joiner dimension limit
 constexpr int kJoinerBN = 64;        // joiner vocabulary columns per tile (4 waves x 16)
-constexpr int kKStep = 64;           // K padding granule of the packed weights
+constexpr int kKStep = 64;           // K padding granule of the packed weights and h rows
 constexpr int kSearchThreads = 256;
-constexpr int kChunk = 2048;         // candidates merged per LDS pass
+constexpr int kChunk = 2048;         // candidates merged per LDS pass (hash path)
 constexpr int kHashSlots = 4096;     // LDS open-addressing table (load <= 0.57)
+constexpr int kSmallCands = 256;     // candidate sets up to this size are ranked directly
+constexpr int kMaxTopK = 16;         // trivial-graph fast path: max_states limit
+constexpr int kStatStage = 8192;     // softmax partials staged in LDS per stream
+constexpr int kTopkStage = 4608;     // trivial-graph per-tile label lists staged in LDS
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -31,6 +34,7 @@ struct ModelDev {
 
 struct GraphDev {
   int S, start, maxdeg;
+  int trivial;              // one state, loops 1..V-1 in label order, q = 0, final 0
   const int* rp;
   const int* dest;
   const int* label;
@@ -41,6 +45,8 @@ struct GraphDev {
 // Per-decode device state.
 struct DecodeDev {
   int B, T, Ns, Nc, nvt;    // nvt = number of joiner vocabulary tiles
+  int KT;                   // trivial fast path: candidates kept per (row, tile); 0 = off
+  const float* enc;         // [B][T][C]
   const int* len;           // [B]
   int* nsurv;               // [B]
   int* surv_ctx;            // [B][Ns]
@@ -50,26 +56,41 @@ struct DecodeDev {
   int* nctx;                // [B]
   int* ctx_list;            // [B][Nc], ascending
   double* offset;           // [B]
-  float* logits;            // [B*Nc][Vpad]
+  void* h;                  // [B*Nc][Kpad] joiner input rows tanh(enc + dec) (fp32 or bf16)
+  float* logits;            // [B*Nc][Vpad] (general graphs)
   float2* stats;            // [B*Nc][nvt]: (max, sum exp(z - max)) per vocabulary tile
+  float* tk_z;              // [B*Nc][nvt*4][KT] trivial fast path: best logits per 16-column sub-tile
+  int* tk_c;                // [B*Nc][nvt*4][KT] and their labels (-1 = none)
+  float* z0;                // [B*Nc] blank logit (trivial fast path)
   int* hist_pl;             // [T][B][Ns]: parent << 16 | label
   int* hist_arc;            // [T][B][Ns]: arc id, -1 blank
   int* path_lab;            // [B][T] scratch for the traceback
 };
+
+struct JoinerPlan {
+  int MB;                   // 16-row MFMA blocks per tile
+  int n_rt, n_ct;           // row and column tiles
+  int grid;                 // workgroups (XCD-interleaved tile order)
+  size_t lds;               // dynamic LDS bytes
+};
+
+JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16);
 
 hipError_t launch_model_setup(const float* embed, const float* conv, const float* w_out,
                               const float* b_out, int V, int C, int Kpad, int Vpad, int bf16,
                               float* P0, float* P1, float* Wf, uint16_t* Wb, float* bias,
                               hipStream_t st);
 hipError_t launch_fill_i32(int* p, long long n, int v, hipStream_t st);
-hipError_t launch_init(const DecodeDev& d, const GraphDev& g, int* trace, hipStream_t st);
-hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const float* enc, int t,
+hipError_t launch_init(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,
+                       hipStream_t st);
+hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const JoinerPlan& p, int t,
                                hipStream_t st);
 hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const DecodeDev& d,
                                float beam, int t, int* trace, hipStream_t st);
 hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, int* out_ntok,
                         double* out_scores, int* out_status, int* out_arcs, hipStream_t st);
 hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const int* ctx, int R,
-                              float* logits, float2* stats, float* out_logp, hipStream_t st);
+                              void* h, float* logits, float2* stats, float* out_logp,
+                              hipStream_t st);
 
 }  // namespace tbs

@@ -1,16 +1,19 @@
 // gfx950 kernels for batched FSA-based one-symbol-per-frame transducer beam
 // search (Kang et al., arXiv 2211.00484, Sec. 2.2-2.5 and Algorithm 1).
 //
-// Per frame t (Algorithm 1 loop body):
-//   k_joiner  GetContexts rows -> decoder (ReLU of conv-tap-scaled embedding
-//             rows) + IndexSelect of enc[b, t] -> tanh -> joiner GEMM on MFMA
-//             -> logits and per-tile (max, sum exp) partials of the log-softmax.
-//   k_search  one workgroup per stream: log-softmax normaliser, ExpandArcs over
-//             the CSR graph without pruning, max-merge of equal (state, context)
-//             keys in an LDS hash table, beam + max-states selection by radix
-//             select, max-contexts selection, canonical (context, state) order,
-//             score renormalisation and the back-pointer history.
-// After the last frame, k_final picks the best final tuple and traces back.
+// Per frame t (the loop body of Algorithm 1):
+//   k_joiner  joiner GEMM on MFMA over the rows h = tanh(enc_t + dec(ctx)) of
+//             every active (stream, context): logits plus per-tile (max, sum
+//             exp) partials of the log-softmax; for the trivial graph the
+//             epilogue keeps only each row's best labels per tile.
+//   k_search  one workgroup per stream: log-softmax normaliser, ExpandArcs
+//             over the CSR graph without pruning, max-merge of equal (state,
+//             context) keys, beam + max-states selection, max-contexts
+//             selection, canonical (context, state) order, renormalisation,
+//             back-pointers; then GetContexts + decoder + IndexSelect + tanh
+//             for frame t+1, so the next joiner reads ready rows.
+// k_init seeds the initial tuple and its joiner row; k_final picks the best
+// final tuple and traces the back-pointers.
 #include "internal.h"
 
 #include <hip/hip_runtime.h>
@@ -47,6 +50,77 @@ __device__ __forceinline__ float ord2f(uint32_t o) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Cross-lane reductions on DPP row rotations (16-lane rows) and readlane, which
+// stay in the VALU instead of taking an LDS round trip per step.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+template <int CTRL>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long v) {
+  const int lo = dpp_i<CTRL>((int)(unsigned)v), hi = dpp_i<CTRL>((int)(unsigned)(v >> 32));
+  return ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo;
+}
+constexpr int kRor8 = 0x128, kRor4 = 0x124, kRor2 = 0x122, kRor1 = 0x121;
+
+// reductions over the 16 lanes of a DPP row; every lane of the row gets the result
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_f<kRor8>(v));
+  v = fmaxf(v, dpp_f<kRor4>(v));
+  v = fmaxf(v, dpp_f<kRor2>(v));
+  return fmaxf(v, dpp_f<kRor1>(v));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f<kRor8>(v);
+  v += dpp_f<kRor4>(v);
+  v += dpp_f<kRor2>(v);
+  return v + dpp_f<kRor1>(v);
+}
+__device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
+  return a > b ? a : b;
+}
+__device__ __forceinline__ unsigned long long row16_max_u64(unsigned long long v) {
+  v = umax64(v, dpp_u64<kRor8>(v));
+  v = umax64(v, dpp_u64<kRor4>(v));
+  v = umax64(v, dpp_u64<kRor2>(v));
+  return umax64(v, dpp_u64<kRor1>(v));
+}
+__device__ __forceinline__ float rdlane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+// whole-wave reductions (all 64 lanes active); uniform result
+__device__ __forceinline__ float wave_max_f(float v) {
+  v = row16_max(v);
+  return fmaxf(fmaxf(rdlane_f(v, 0), rdlane_f(v, 16)), fmaxf(rdlane_f(v, 32), rdlane_f(v, 48)));
+}
+__device__ __forceinline__ float wave_sum_f(float v) {
+  v = row16_sum(v);
+  return (rdlane_f(v, 0) + rdlane_f(v, 16)) + (rdlane_f(v, 32) + rdlane_f(v, 48));
+}
+__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
+  v = row16_max_u64(v);
+  unsigned long long r = 0;
+#pragma unroll
+  for (int l = 0; l < 64; l += 16) {
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)v, l);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v >> 32), l);
+    r = umax64(r, ((unsigned long long)hi << 32) | lo);
+  }
+  return r;
+}
+
+// log-sum-exp of one joiner row from its per-tile (max, sum exp) partials.  The
+// logarithm is taken in double: the device logf is biased low by a fraction of
+// an ulp, which would otherwise accumulate over the frames of a stream.
+__device__ __forceinline__ double lse_of(float M, float S) { return (double)M + log((double)S); }
+
+// log-probability of one logit, rounded once to fp32
+__device__ __forceinline__ float logp_of(float z, double lse) { return (float)((double)z - lse); }
+
 // ---------------------------------------------------------------------------
 // model setup: P0 = tap0 * E, P1 = tap1 * E (padded to Kpad), W packed to
 // [Vpad][Kpad] in fp32 or bf16, bias copied (zeros if absent).
@@ -82,175 +156,271 @@ __global__ void k_fill_i32(int* p, long long n, int v) {
 }
 
 // ---------------------------------------------------------------------------
-// joiner
-
-struct RowSrc {
-  // decode mode: row r = b * Nc + j is context j of stream b at frame t
-  const float* enc;
-  int T, t, Nc;
-  const int* len;
-  const int* nctx;
-  const int* ctx_list;
-  // explicit-rows mode
-  const float* enc_rows;
-  const int* ctx_rows;
-  int R;
-  int rows_mode;
-};
-
-__device__ __forceinline__ bool row_info(const RowSrc& s, int C, int r, const float*& enc_row,
-                                         int& ctx) {
-  if (r >= s.R) return false;
-  if (s.rows_mode) {
-    enc_row = s.enc_rows + (size_t)r * C;
-    ctx = s.ctx_rows[r];
-    return true;
+// Joiner input rows (Algorithm 1: decoder, IndexSelect of the encoder frame):
+// h[k] = tanh(enc[k] + ReLU(P0[a][k] + P1[b][k])) for k < C, 0 for C <= k < Kpad,
+// stored as fp32 or bf16 (RNE).  Rows r < nrows use context ctxs[r] and the
+// encoder row enc_rows + r * enc_stride (enc_stride = 0: one shared frame).
+// Loads are issued four iterations at a time for memory-level parallelism.
+template <int NT>
+__device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_rows,
+                             long long enc_stride, const int* ctxs, int nrows,
+                             void* __restrict__ hbase, int tid) {
+  constexpr int U = 16;  // elements per thread per batch: all loads of a batch in flight together
+  const int C = m.C, Kpad = m.Kpad, V = m.V;
+  const float* __restrict__ P0 = m.P0;
+  const float* __restrict__ P1 = m.P1;
+  const int total = nrows * Kpad;
+  for (int base = tid; base < total; base += U * NT) {
+    float e[U], p0[U], p1[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int idx = base + u * NT;
+      e[u] = 0.f;
+      p0[u] = 0.f;
+      p1[u] = 0.f;
+      if (idx < total) {
+        const int r = idx / Kpad, k = idx - r * Kpad;
+        if (k < C) {
+          const int ctx = ctxs[r];
+          const int a = ctx / V, b = ctx - a * V;
+          e[u] = enc_rows[(size_t)r * enc_stride + k];
+          p0[u] = P0[(size_t)a * Kpad + k];
+          p1[u] = P1[(size_t)b * Kpad + k];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int idx = base + u * NT;
+      if (idx >= total) continue;
+      const int k = idx - (idx / Kpad) * Kpad;
+      const float h = k < C ? tanhf(e[u] + fmaxf(p0[u] + p1[u], 0.f)) : 0.f;
+      if (m.bf16)
+        reinterpret_cast<uint16_t*>(hbase)[idx] = f32_to_bf16_rne(h);
+      else
+        reinterpret_cast<float*>(hbase)[idx] = h;
+    }
   }
-  const int b = r / s.Nc, j = r - b * s.Nc;
-  if (s.t >= s.len[b] || j >= s.nctx[b]) return false;
-  enc_row = s.enc + ((size_t)b * s.T + s.t) * C;
-  ctx = s.ctx_list[r];
-  return true;
 }
 
-// One 16-row x 64-column tile per workgroup; wave w owns columns 16w..16w+15.
-// The A operand h = tanh(enc + ReLU(P0[a] + P1[b])) is built in LDS (fp32 or
-// bf16 RNE); W is streamed from its packed [Vpad][Kpad] copy.
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_joiner(ModelDev m, RowSrc src, float* __restrict__ logits,
-                                                float2* __restrict__ stats, int nvt) {
+// h rows for explicit (encoder row, context) pairs: one workgroup per row.
+__global__ __launch_bounds__(256) void k_h_rows(ModelDev m, const float* __restrict__ enc_rows,
+                                                const int* __restrict__ ctx, void* __restrict__ h) {
+  const int r = blockIdx.x;
+  const size_t esz = m.bf16 ? 2 : 4;
+  write_h_rows<256>(m, enc_rows + (size_t)r * m.C, 0, ctx + r, 1,
+                    reinterpret_cast<char*>(h) + (size_t)r * m.Kpad * esz, threadIdx.x);
+}
+
+// ---------------------------------------------------------------------------
+// joiner
+
+struct JoinArgs {
+  const void* h;            // [R][Kpad]
+  float* logits;            // [R][Vpad] or null
+  float2* stats;            // [R][nvt]
+  float* tk_z;              // [R][nvt][KT] (TOPK)
+  int* tk_c;
+  float* z0;                // [R] (TOPK)
+  int KT;
+  int R, n_rt, n_ct;
+  int rows_mode;            // 1: every row < R is active
+  const int* len;
+  const int* nctx;
+  int t, Nc;
+};
+
+__device__ __forceinline__ bool joiner_row_active(const JoinArgs& a, int r) {
+  if (r >= a.R) return false;
+  if (a.rows_mode) return true;
+  const int b = r / a.Nc, j = r - b * a.Nc;
+  return a.t < a.len[b] && j < a.nctx[b];
+}
+
+// Tile = (16 * MB rows) x 64 vocabulary columns; wave w owns columns 16w..16w+15
+// and keeps its W fragment (16 columns x up to 512 of K) in registers while it
+// sweeps the tile's row blocks, whose h rows are staged once in LDS.  Tiles are
+// ordered so that the workgroups of one column tile land on the same XCD
+// (workgroups are dispatched round-robin over the 8 XCDs), keeping each W
+// column tile in that XCD's L2.
+template <bool BF16, int MB, bool TOPK>
+__global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ const float* s_enc[kJoinerBM];
-  __shared__ int s_a[kJoinerBM], s_b[kJoinerBM], s_act[kJoinerBM];
-  __shared__ float s_m[4][kJoinerBM], s_s[4][kJoinerBM];
-
-  const int vt = blockIdx.x, r0 = blockIdx.y * kJoinerBM, n0 = vt * kJoinerBN;
+  __shared__ int s_act[64];
+  __shared__ float s_m[4][64], s_s[4][64];
+  constexpr int BM = 16 * MB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int C = m.C, V = m.V, Kpad = m.Kpad;
+  const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
+  const int ct = xcd + 8 * (slot / a.n_rt), rt = slot - (slot / a.n_rt) * a.n_rt;
+  if (ct >= a.n_ct) return;
+  const int r0 = rt * BM, n0 = ct * kJoinerBN;
+  const int Kpad = m.Kpad, V = m.V, nvt = a.n_ct;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int col = n0 + 16 * wave + lr;
 
-  if (tid < kJoinerBM) {
-    const float* e = nullptr;
-    int ctx = 0;
-    const bool act = row_info(src, C, r0 + tid, e, ctx);
-    s_act[tid] = act;
-    s_enc[tid] = e;
-    s_a[tid] = act ? ctx / V : 0;
-    s_b[tid] = act ? ctx - (ctx / V) * V : 0;
-  }
+  if (tid < BM) s_act[tid] = joiner_row_active(a, r0 + tid);
   __syncthreads();
   int any = 0;
 #pragma unroll
-  for (int i = 0; i < kJoinerBM; ++i) any |= s_act[i];
+  for (int i = 0; i < BM; ++i) any |= s_act[i];
   if (!any) return;  // uniform across the workgroup
 
-  // prologue: h tile in LDS
-  const int ldk = BF16 ? Kpad + 8 : Kpad + 4;  // 16-byte row padding
-  float* hs = reinterpret_cast<float*>(smem);
-  uint16_t* hb = reinterpret_cast<uint16_t*>(smem);
-  for (int r = 0; r < kJoinerBM; ++r) {
-    const bool act = s_act[r];
-    const float* e = s_enc[r];
-    const float* p0 = m.P0 + (size_t)s_a[r] * Kpad;
-    const float* p1 = m.P1 + (size_t)s_b[r] * Kpad;
-    for (int k = tid; k < Kpad; k += 256) {
-      float h = 0.f;
-      if (act && k < C) {
-        const float d = fmaxf(p0[k] + p1[k], 0.f);
-        h = tanhf(e[k] + d);
+  // stage the tile's h rows in LDS (16-byte chunks, all loads in flight together)
+  constexpr int ESZ = BF16 ? 2 : 4;
+  const int ldk = Kpad + (BF16 ? 8 : 4);             // row stride in elements (16-byte pad)
+  const int cpr = Kpad * ESZ / 16;                   // 16-byte chunks per row
+  const int nchunk = BM * cpr;
+  const char* hsrc = reinterpret_cast<const char*>(a.h) + (size_t)r0 * Kpad * ESZ;
+  for (int base = tid; base < nchunk; base += 256 * 16) {
+    uint4 v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int c = base + u * 256;
+      v[u] = make_uint4(0, 0, 0, 0);
+      if (c < nchunk && s_act[c / cpr]) v[u] = reinterpret_cast<const uint4*>(hsrc)[c];
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int c = base + u * 256;
+      if (c < nchunk) {
+        const int r = c / cpr, cc = c - r * cpr;
+        *reinterpret_cast<uint4*>(smem + (size_t)r * ldk * ESZ + (size_t)cc * 16) = v[u];
       }
-      if (BF16)
-        hb[r * ldk + k] = f32_to_bf16_rne(h);
-      else
-        hs[r * ldk + k] = h;
-    }
-  }
-  __syncthreads();
-
-  // main loop: 16x16 output block per wave on MFMA
-  const int lr = lane & 15, lg = lane >> 4;
-  const int col = n0 + 16 * wave + lr;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (BF16) {
-    const uint16_t* wrow = m.Wb + (size_t)col * Kpad;
-    const uint16_t* hrow = hb + lr * ldk;
-    for (int k0 = 0; k0 < Kpad; k0 += 64) {
-      const int ko = k0 + 16 * lg;
-      const uint4 a0 = *reinterpret_cast<const uint4*>(hrow + ko);
-      const uint4 a1 = *reinterpret_cast<const uint4*>(hrow + ko + 8);
-      const uint4 b0 = *reinterpret_cast<const uint4*>(wrow + ko);
-      const uint4 b1 = *reinterpret_cast<const uint4*>(wrow + ko + 8);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), as_bf16x8(b0), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), as_bf16x8(b1), acc, 0, 0, 0);
-    }
-  } else {
-    const float* wrow = m.Wf + (size_t)col * Kpad;
-    const float* hrow = hs + lr * ldk;
-    for (int k0 = 0; k0 < Kpad; k0 += 16) {
-      const int ko = k0 + 4 * lg;
-      const float4 a = *reinterpret_cast<const float4*>(hrow + ko);
-      const float4 w = *reinterpret_cast<const float4*>(wrow + ko);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, w.x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, w.y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, w.z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, w.w, acc, 0, 0, 0);
     }
   }
 
-  // epilogue: bias, logits store, per-row (max, sum exp) over the tile
+  // NCH independent accumulator chains per row block keep the MFMA pipe busy
+  // (a single chain would wait out the full MFMA latency on every step)
+  constexpr int NCH = MB >= 4 ? 1 : 4 / MB;
+  f32x4 acc[MB][NCH];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) acc[mb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int kc = 0; kc < Kpad; kc += 512) {
+    const int kn = min(512, Kpad - kc);  // multiple of 64
+    if (BF16) {
+      const uint16_t* wrow = m.Wb + (size_t)col * Kpad + kc + 16 * lg;
+      uint4 wf[16];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        if (s * 64 < kn) {
+          wf[2 * s] = *reinterpret_cast<const uint4*>(wrow + s * 64);
+          wf[2 * s + 1] = *reinterpret_cast<const uint4*>(wrow + s * 64 + 8);
+        }
+      }
+      __syncthreads();
+      const uint16_t* hb = reinterpret_cast<const uint16_t*>(smem);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const uint16_t* hr = hb + (size_t)(mb * 16 + lr) * ldk + kc + 16 * lg;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          if (s * 64 < kn) {
+            const uint4 a0 = *reinterpret_cast<const uint4*>(hr + s * 64);
+            const uint4 a1 = *reinterpret_cast<const uint4*>(hr + s * 64 + 8);
+            f32x4& c0 = acc[mb][(2 * s) % NCH];
+            c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), as_bf16x8(wf[2 * s]), c0,
+                                                         0, 0, 0);
+            f32x4& c1 = acc[mb][(2 * s + 1) % NCH];
+            c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), as_bf16x8(wf[2 * s + 1]),
+                                                         c1, 0, 0, 0);
+          }
+        }
+      }
+    } else {
+      const float* wrow = m.Wf + (size_t)col * Kpad + kc + 4 * lg;
+      float4 wf[32];
+#pragma unroll
+      for (int s = 0; s < 32; ++s)
+        if (s * 16 < kn) wf[s] = *reinterpret_cast<const float4*>(wrow + s * 16);
+      __syncthreads();
+      const float* hs = reinterpret_cast<const float*>(smem);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const float* hr = hs + (size_t)(mb * 16 + lr) * ldk + kc + 4 * lg;
+#pragma unroll
+        for (int s = 0; s < 32; ++s) {
+          if (s * 16 < kn) {
+            const float4 av = *reinterpret_cast<const float4*>(hr + s * 16);
+            f32x4& c = acc[mb][s % NCH];
+            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, wf[s].x, c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, wf[s].y, c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, wf[s].z, c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, wf[s].w, c, 0, 0, 0);
+          }
+        }
+      }
+    }
+  }
+
+  // epilogue: bias, per-row (max, sum exp) over the tile, then logits (general
+  // graphs) or each row's best KT labels per 16-column sub-tile (trivial graph)
   const bool cvalid = col < V;
   const float bias = cvalid ? m.bias[col] : 0.f;
-  float z[4], mx[4], sm[4];
+  const int nsub = nvt * (kJoinerBN / 16);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) z[i] = cvalid ? acc[i] + bias : -INFINITY;
+  for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float v = z[i];
+    for (int i = 0; i < 4; ++i) {
+      const int row = mb * 16 + 4 * lg + i;  // the 16 lanes of a DPP row share this row
+      float zs = acc[mb][0][i];
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o));
-    mx[i] = v;
-    float e = cvalid ? expf(z[i] - v) : 0.f;
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) e += __shfl_xor(e, o);
-    sm[i] = e;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 4 * lg + i;
-    if (s_act[row] && cvalid) logits[(size_t)(r0 + row) * m.Vpad + col] = z[i];
-    if (lr == 0) {
-      s_m[wave][row] = mx[i];
-      s_s[wave][row] = sm[i];
+      for (int c = 1; c < NCH; ++c) zs += acc[mb][c][i];
+      const float z = cvalid ? zs + bias : -INFINITY;
+      const float mx = row16_max(z);
+      const float e = row16_sum(cvalid ? expf(z - mx) : 0.f);
+      if (lr == 0) {
+        s_m[wave][row] = mx;
+        s_s[wave][row] = e;
+      }
+      const bool act = s_act[row];
+      if (!TOPK) {
+        if (act && cvalid) a.logits[(size_t)(r0 + row) * (nvt * kJoinerBN) + col] = z;
+      } else {
+        unsigned long long key = (cvalid && col >= 1)
+                                     ? ((unsigned long long)f2ord(z) << 32) | (0xffffffffu - (unsigned)col)
+                                     : 0ull;
+        const size_t ob = ((size_t)(r0 + row) * nsub + ct * (kJoinerBN / 16) + wave) * a.KT;
+        for (int q = 0; q < a.KT; ++q) {
+          const unsigned long long best = row16_max_u64(key);
+          if (act && best != 0ull && key == best) {
+            a.tk_z[ob + q] = z;
+            a.tk_c[ob + q] = col;
+          }
+          if (act && best == 0ull && lr == 0) {
+            a.tk_z[ob + q] = -INFINITY;
+            a.tk_c[ob + q] = -1;
+          }
+          if (key == best) key = 0ull;
+        }
+        if (act && ct == 0 && wave == 0 && lr == 0) a.z0[r0 + row] = z;
+      }
     }
   }
   __syncthreads();
-  if (tid < kJoinerBM && s_act[tid]) {
+  if (tid < BM && s_act[tid]) {
     float M = s_m[0][tid];
     for (int w = 1; w < 4; ++w) M = fmaxf(M, s_m[w][tid]);
     float S = 0.f;
     for (int w = 0; w < 4; ++w) S += s_s[w][tid] == 0.f ? 0.f : s_s[w][tid] * expf(s_m[w][tid] - M);
-    stats[(size_t)(r0 + tid) * nvt + vt] = make_float2(M, S);
+    a.stats[(size_t)(r0 + tid) * nvt + ct] = make_float2(M, S);
   }
 }
-
-// log-sum-exp of one joiner row from its per-tile (max, sum exp) partials.  The
-// logarithm is taken in double: the device logf is biased low by a fraction of
-// an ulp, which would otherwise accumulate over the frames of a stream.
-__device__ __forceinline__ double row_lse(const float2* st, int nvt) {
-  float M = -INFINITY;
-  for (int i = 0; i < nvt; ++i) M = fmaxf(M, st[i].x);
-  float S = 0.f;
-  for (int i = 0; i < nvt; ++i) S += st[i].y == 0.f ? 0.f : st[i].y * expf(st[i].x - M);
-  return (double)M + log((double)S);
-}
-
-// log-probability of one logit, rounded once to fp32
-__device__ __forceinline__ float logp_of(float z, double lse) { return (float)((double)z - lse); }
 
 __global__ void k_logp_rows(const float* __restrict__ logits, const float2* __restrict__ stats,
                             int nvt, int V, int Vpad, float* __restrict__ out) {
   const int r = blockIdx.x;
   __shared__ double s_lse;
-  if (threadIdx.x == 0) s_lse = row_lse(stats + (size_t)r * nvt, nvt);
+  if (threadIdx.x == 0) {
+    const float2* st = stats + (size_t)r * nvt;
+    float M = -INFINITY;
+    for (int i = 0; i < nvt; ++i) M = fmaxf(M, st[i].x);
+    float S = 0.f;
+    for (int i = 0; i < nvt; ++i) S += st[i].y == 0.f ? 0.f : st[i].y * expf(st[i].x - M);
+    s_lse = lse_of(M, S);
+  }
   __syncthreads();
   const double l = s_lse;
   for (int v = threadIdx.x; v < V; v += blockDim.x)
@@ -260,32 +430,41 @@ __global__ void k_logp_rows(const float* __restrict__ logits, const float2* __re
 // ---------------------------------------------------------------------------
 // search
 
-__global__ void k_init(DecodeDev d, GraphDev g, int* __restrict__ trace) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= d.B) return;
-  d.nsurv[b] = 1;
-  d.surv_ctx[(size_t)b * d.Ns] = 0;
-  d.surv_state[(size_t)b * d.Ns] = g.start;
-  d.surv_score[(size_t)b * d.Ns] = 0.f;
-  d.surv_row[(size_t)b * d.Ns] = 0;
-  d.nctx[b] = 1;
-  d.ctx_list[(size_t)b * d.Nc] = 0;
-  d.offset[b] = 0.0;
-  if (trace) {
-    int* p = trace + (size_t)b * d.Ns * 4;
-    p[0] = 0;
-    p[1] = g.start;
-    p[2] = -1;
-    p[3] = -1;
+// initial tuple ((blank, blank), start) and its joiner row for frame 0
+__global__ __launch_bounds__(256) void k_init(ModelDev m, DecodeDev d, GraphDev g,
+                                              int* __restrict__ trace) {
+  const int b = blockIdx.x, tid = threadIdx.x;
+  if (tid == 0) {
+    d.nsurv[b] = 1;
+    d.surv_ctx[(size_t)b * d.Ns] = 0;
+    d.surv_state[(size_t)b * d.Ns] = g.start;
+    d.surv_score[(size_t)b * d.Ns] = 0.f;
+    d.surv_row[(size_t)b * d.Ns] = 0;
+    d.nctx[b] = 1;
+    d.ctx_list[(size_t)b * d.Nc] = 0;
+    d.offset[b] = 0.0;
+    if (trace) {
+      int* p = trace + (size_t)b * d.Ns * 4;
+      p[0] = 0;
+      p[1] = g.start;
+      p[2] = -1;
+      p[3] = -1;
+    }
+  }
+  if (d.len[b] > 0) {
+    const int zero_ctx = 0;
+    const size_t esz = m.bf16 ? 2 : 4;
+    write_h_rows<256>(m, d.enc + (size_t)b * d.T * m.C, 0, &zero_ctx, 1,
+                      reinterpret_cast<char*>(d.h) + (size_t)b * d.Nc * m.Kpad * esz, tid);
   }
 }
 
 struct SearchSmem {
-  unsigned long long hk[kHashSlots];
+  unsigned long long hk[kHashSlots];  // hash keys; also stages softmax partials
   unsigned long long hv[kHashSlots];
-  unsigned long long uk[kChunk + kMaxStates];
+  unsigned long long uk[kChunk + kMaxStates];  // merged entries / small-path candidates
   unsigned long long uv[kChunk + kMaxStates];
-  unsigned long long lk[kMaxStates];
+  unsigned long long lk[kMaxStates];  // running best list
   unsigned long long lv[kMaxStates];
   int s_ctx[kMaxStates], s_bprev[kMaxStates], s_state[kMaxStates], s_row[kMaxStates];
   int s_base[kMaxStates], s_off[kMaxStates + 1];
@@ -293,9 +472,14 @@ struct SearchSmem {
   double s_lse[kMaxStates];
   float f_score[kMaxStates], f_cs[kMaxStates];
   int f_keep1[kMaxStates], f_first[kMaxStates], f_keep2[kMaxStates];
+  int n_ctx_list[kMaxStates];
+  float rk_z[kMaxTopK * kMaxTopK];  // trivial graph: each row's best labels over all tiles
+  int rk_c[kMaxTopK * kMaxTopK];
+  float s_z0[kMaxTopK];
   unsigned hist[256];
+  int wsum[4];
   int misc[8];
-  int nU, nL, n_gt, n_eq;
+  int ns, nc, nU, nL, n_gt, n_eq, nK, nC;
   float best;
 };
 
@@ -371,152 +555,322 @@ __device__ unsigned long long kth_largest(SearchSmem& s, int n, int k, Get get) 
   return prefix;
 }
 
+// Top `Ns` of the nU merged entries in uk/uv by (score desc, key asc) into lk/lv.
+__device__ __forceinline__ void select_top(SearchSmem& s, int nU, int Ns) {
+  const int tid = threadIdx.x;
+  if (nU <= Ns) {
+    for (int i = tid; i < nU; i += blockDim.x) {
+      s.lk[i] = s.uk[i];
+      s.lv[i] = s.uv[i];
+    }
+    if (tid == 0) s.nL = nU;
+    __syncthreads();
+    return;
+  }
+  const unsigned theta = (unsigned)kth_largest<32>(s, nU, Ns, [&](int i, unsigned long long& v) {
+    v = s.uv[i] >> 32;
+    return true;
+  });
+  if (tid == 0) {
+    s.n_gt = 0;
+    s.n_eq = 0;
+    s.nL = 0;
+  }
+  __syncthreads();
+  for (int i = tid; i < nU; i += blockDim.x) {
+    const unsigned so = (unsigned)(s.uv[i] >> 32);
+    if (so > theta) atomicAdd(&s.n_gt, 1);
+    else if (so == theta) atomicAdd(&s.n_eq, 1);
+  }
+  __syncthreads();
+  const int m_need = Ns - s.n_gt;
+  unsigned long long keythr = kEmpty;
+  if (s.n_eq > m_need) {
+    const unsigned long long vk = kth_largest<64>(s, nU, m_need, [&](int i, unsigned long long& v) {
+      if ((unsigned)(s.uv[i] >> 32) != theta) return false;
+      v = ~s.uk[i];
+      return true;
+    });
+    keythr = ~vk;
+  }
+  for (int i = tid; i < nU; i += blockDim.x) {
+    const unsigned so = (unsigned)(s.uv[i] >> 32);
+    if (so > theta || (so == theta && s.uk[i] <= keythr)) {
+      const int p = atomicAdd(&s.nL, 1);
+      s.lk[p] = s.uk[i];
+      s.lv[p] = s.uv[i];
+    }
+  }
+  __syncthreads();
+}
+
+// Candidate c of the flattened list (trivial: survivor-major blank then per-tile
+// top labels; general: blanks then arcs).  Returns false if c is an empty slot.
+struct CandIdx {
+  int i, pos, lab, dest, arc;
+  float q, z;
+};
+
+template <bool TRIV>
 __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev g, DecodeDev d,
                                                            float beam, int t,
                                                            int* __restrict__ trace) {
   const int b = blockIdx.x;
-  if (t >= d.len[b]) return;
+  const int L = d.len[b];
+  if (t >= L) return;
   extern __shared__ __align__(16) unsigned char smem[];
   SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
-  const int tid = threadIdx.x;
-  const int Ns = d.Ns, Nc = d.Nc, V = m.V;
-  const int ns = d.nsurv[b], nc = d.nctx[b];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Ns = d.Ns, Nc = d.Nc, V = m.V, nvt = d.nvt;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
+  const size_t row0 = (size_t)b * Nc;
 
-  // survivors of frame t and the log-softmax normaliser of each context row
-  for (int i = tid; i < ns; i += blockDim.x) {
+  // ---- loads that do not depend on the survivor count ----
+  if (tid == 0) {
+    s.ns = d.nsurv[b];
+    s.nc = d.nctx[b];
+  }
+  float2* stage = reinterpret_cast<float2*>(s.hk);  // softmax partials, [Nc][nvt]
+  const bool staged = Nc * nvt <= kStatStage;
+  if (staged)
+    for (int i = tid; i < Nc * nvt; i += blockDim.x) stage[i] = d.stats[row0 * nvt + i];
+  for (int i = tid; i < Ns; i += blockDim.x) {
     const size_t o = (size_t)b * Ns + i;
-    const int ctx = d.surv_ctx[o], st = d.surv_state[o];
-    s.s_ctx[i] = ctx;
-    s.s_bprev[i] = ctx % V;
-    s.s_state[i] = st;
+    s.s_ctx[i] = d.surv_ctx[o];
+    s.s_state[i] = d.surv_state[o];
     s.s_row[i] = d.surv_row[o];
     s.s_score[i] = d.surv_score[o];
-    s.s_base[i] = g.rp[st];
-    s.s_off[i + 1] = g.rp[st + 1] - g.rp[st];
   }
-  for (int j = tid; j < nc; j += blockDim.x)
-    s.s_lse[j] = row_lse(d.stats + (size_t)(b * Nc + j) * d.nvt, d.nvt);
+  // trivial graph: the joiner's per-tile best labels of this stream's rows
+  const int E = TRIV ? nvt * (kJoinerBN / 16) * d.KT : 0;
+  float* tz = reinterpret_cast<float*>(s.uk);
+  int* tc = reinterpret_cast<int*>(s.uv);
+  const bool tstaged = TRIV && Nc * E <= kTopkStage;
+  if (TRIV) {
+    if (tstaged)
+      for (int i = tid; i < Nc * E; i += blockDim.x) {
+        tz[i] = d.tk_z[row0 * E + i];
+        tc[i] = d.tk_c[row0 * E + i];
+      }
+    for (int j = tid; j < Nc; j += blockDim.x) s.s_z0[j] = d.z0[row0 + j];
+  }
+  __syncthreads();
+  const int ns = s.ns, nc = s.nc;
+  // log-softmax normaliser of each context row: one wave per row
+  for (int j = wave; j < nc; j += 4) {
+    float M = -INFINITY;
+    for (int i = lane; i < nvt; i += 64)
+      M = fmaxf(M, staged ? stage[j * nvt + i].x : d.stats[(row0 + j) * nvt + i].x);
+    M = wave_max_f(M);
+    float S = 0.f;
+    for (int i = lane; i < nvt; i += 64) {
+      const float2 p = staged ? stage[j * nvt + i] : d.stats[(row0 + j) * nvt + i];
+      S += p.y == 0.f ? 0.f : p.y * expf(p.x - M);
+    }
+    S = wave_sum_f(S);
+    if (lane == 0) s.s_lse[j] = lse_of(M, S);
+  }
+  if (TRIV) {
+    for (int i = tid; i < ns; i += blockDim.x) {
+      s.s_bprev[i] = s.s_ctx[i] % V;
+      s.s_base[i] = 0;
+    }
+    // each row's best KT labels over all tiles (labels are unique within a row, so
+    // round q takes the largest key below round q-1's)
+    const int KT = d.KT;
+    for (int j = wave; j < nc; j += 4) {
+      unsigned long long prev = ~0ull;
+      for (int q = 0; q < KT; ++q) {
+        unsigned long long mine = 0ull;
+        for (int e = lane; e < E; e += 64) {
+          const int c = tstaged ? tc[j * E + e] : d.tk_c[(row0 + j) * E + e];
+          if (c < 0) continue;
+          const float z = tstaged ? tz[j * E + e] : d.tk_z[(row0 + j) * E + e];
+          const unsigned long long key =
+              ((unsigned long long)f2ord(z) << 32) | (0xffffffffu - (unsigned)c);
+          if (key < prev && key > mine) mine = key;
+        }
+        const unsigned long long best = wave_max_u64(mine);
+        if (lane == 0) {
+          s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
+          s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+        }
+        prev = best ? best : 1ull;
+      }
+    }
+  } else {
+    for (int i = tid; i < ns; i += blockDim.x) {
+      const int st = s.s_state[i];
+      const int lo = g.rp[st], hi = g.rp[st + 1];
+      s.s_bprev[i] = s.s_ctx[i] % V;
+      s.s_base[i] = lo;
+      s.s_off[i + 1] = hi - lo;
+    }
+  }
   if (tid == 0) {
     s.s_off[0] = 0;
     s.nL = 0;
   }
   __syncthreads();
-  if (tid == 0)  // inclusive scan of out-degrees (ns <= 256)
-    for (int i = 1; i <= ns; ++i) s.s_off[i] += s.s_off[i - 1];
-  __syncthreads();
-  const int N = ns + s.s_off[ns];
-  const float* zbase = d.logits + (size_t)b * Nc * m.Vpad;
-
-  for (int base = 0; base < N; base += kChunk) {
-    for (int i = tid; i < kHashSlots; i += blockDim.x) {
-      s.hk[i] = kEmpty;
-      s.hv[i] = 0ull;
+  // exclusive offsets of each survivor's candidates (block scan over <= 256 entries)
+  {
+    const int per = TRIV ? d.KT : 0;
+    int v = tid < ns ? (TRIV ? per : s.s_off[tid + 1]) : 0;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
     }
-    if (tid == 0) s.nU = 0;
+    if (lane == 63) s.wsum[wave] = incl;
     __syncthreads();
-    const int nL = s.nL;
-    for (int i = tid; i < nL; i += blockDim.x) hash_insert(s, s.lk[i], s.lv[i]);
-    const int end = min(N, base + kChunk);
-    for (int c = base + tid; c < end; c += blockDim.x) {
-      int i, pos;
-      if (c < ns) {
-        i = c;
-        pos = -1;
-      } else {
-        const int k = c - ns;
-        int lo = 0, hi = ns - 1;  // largest i with s_off[i] <= k
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (s.s_off[mid] <= k) lo = mid; else hi = mid - 1;
-        }
-        i = lo;
-        pos = k - s.s_off[i];
-      }
-      const float* z = zbase + (size_t)s.s_row[i] * m.Vpad;
-      const double lse = s.s_lse[s.s_row[i]];
-      float sc;
-      unsigned nctx;
-      int nst;
-      if (pos < 0) {
-        sc = s.s_score[i] + logp_of(z[0], lse);
-        nctx = (unsigned)s.s_ctx[i];
-        nst = s.s_state[i];
-      } else {
-        const int j = s.s_base[i] + pos;
-        const int lab = g.label[j];
-        sc = (s.s_score[i] + g.q[j]) + logp_of(z[lab], lse);
-        nctx = (unsigned)s.s_bprev[i] * (unsigned)V + (unsigned)lab;
-        nst = g.dest[j];
-      }
-      const unsigned tb = (unsigned)i * stride_tb + (unsigned)(pos + 1);
-      const unsigned long long key = ((unsigned long long)(unsigned)nst << 32) | nctx;
-      const unsigned long long val = ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - tb);
-      hash_insert(s, key, val);
-    }
-    __syncthreads();
-    for (int i = tid; i < kHashSlots; i += blockDim.x) {
-      if (s.hk[i] != kEmpty) {
-        const int u = atomicAdd(&s.nU, 1);
-        s.uk[u] = s.hk[i];
-        s.uv[u] = s.hv[i];
-      }
-    }
-    __syncthreads();
-    const int nU = s.nU;
-    if (nU <= Ns) {
-      for (int i = tid; i < nU; i += blockDim.x) {
-        s.lk[i] = s.uk[i];
-        s.lv[i] = s.uv[i];
-      }
-      if (tid == 0) s.nL = nU;
-      __syncthreads();
-      continue;
-    }
-    // beam/max-states order: score desc, then key = (state, ctx) asc
-    const unsigned theta = (unsigned)kth_largest<32>(s, nU, Ns, [&](int i, unsigned long long& v) {
-      v = s.uv[i] >> 32;
-      return true;
-    });
-    if (tid == 0) {
-      s.n_gt = 0;
-      s.n_eq = 0;
-      s.nL = 0;
-    }
-    __syncthreads();
-    for (int i = tid; i < nU; i += blockDim.x) {
-      const unsigned so = (unsigned)(s.uv[i] >> 32);
-      if (so > theta) atomicAdd(&s.n_gt, 1);
-      else if (so == theta) atomicAdd(&s.n_eq, 1);
-    }
-    __syncthreads();
-    const int m_need = Ns - s.n_gt;
-    unsigned long long keythr = kEmpty;
-    if (s.n_eq > m_need) {
-      const unsigned long long vk = kth_largest<64>(s, nU, m_need, [&](int i, unsigned long long& v) {
-        if ((unsigned)(s.uv[i] >> 32) != theta) return false;
-        v = ~s.uk[i];
-        return true;
-      });
-      keythr = ~vk;
-    }
-    for (int i = tid; i < nU; i += blockDim.x) {
-      const unsigned so = (unsigned)(s.uv[i] >> 32);
-      if (so > theta || (so == theta && s.uk[i] <= keythr)) {
-        const int p = atomicAdd(&s.nL, 1);
-        s.lk[p] = s.uk[i];
-        s.lv[p] = s.uv[i];
-      }
-    }
+    int woff = 0;
+    for (int w = 0; w < wave; ++w) woff += s.wsum[w];
+    if (tid < ns) s.s_off[tid + 1] = woff + incl;
     __syncthreads();
   }
+  const int N = ns + s.s_off[ns];
 
-  // beam, then max-contexts, then canonical (ctx, state) order
+  // candidate c -> (survivor, position) and its score/key inputs; loads batched by the caller
+  auto locate = [&](int c, int& i, int& pos) {
+    if (c < ns) {
+      i = c;
+      pos = -1;
+      return;
+    }
+    const int k = c - ns;
+    int lo = 0, hi = ns - 1;  // largest i with s_off[i] <= k
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s.s_off[mid] <= k) lo = mid; else hi = mid - 1;
+    }
+    i = lo;
+    pos = k - s.s_off[i];
+  };
+  const float* zbase = d.logits + row0 * (size_t)m.Vpad;
+  // (key, value) of candidate c; key = kEmpty for an empty trivial-graph slot
+  auto make_cand = [&](int c) -> ulonglong2 {
+    int i, pos;
+    locate(c, i, pos);
+    const int row = s.s_row[i];
+    const double lse = s.s_lse[row];
+    float sc;
+    unsigned nctx;
+    int nst, tbpos;
+    if (pos < 0) {
+      const float z = TRIV ? s.s_z0[row] : zbase[(size_t)row * m.Vpad];
+      sc = s.s_score[i] + logp_of(z, lse);
+      nctx = (unsigned)s.s_ctx[i];
+      nst = s.s_state[i];
+      tbpos = 0;
+    } else if (TRIV) {
+      const int lab = s.rk_c[row * d.KT + pos];
+      if (lab < 0) return make_ulonglong2(kEmpty, 0ull);
+      sc = s.s_score[i] + logp_of(s.rk_z[row * d.KT + pos], lse);
+      nctx = (unsigned)s.s_bprev[i] * (unsigned)V + (unsigned)lab;
+      nst = 0;
+      tbpos = lab;  // trivial graph: arc position = label - 1
+    } else {
+      const int j = s.s_base[i] + pos;
+      const int lab = g.label[j];
+      const float q = g.q[j];
+      nst = g.dest[j];
+      sc = (s.s_score[i] + q) + logp_of(zbase[(size_t)row * m.Vpad + lab], lse);
+      nctx = (unsigned)s.s_bprev[i] * (unsigned)V + (unsigned)lab;
+      tbpos = pos + 1;
+    }
+    const unsigned tb = (unsigned)i * stride_tb + (unsigned)tbpos;
+    return make_ulonglong2(((unsigned long long)(unsigned)nst << 32) | nctx,
+                           ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - tb));
+  };
+
+  if (N <= kSmallCands) {
+    // small candidate sets: merge and rank directly.  Loops run over a multiple
+    // of 8 padded entries without early exits so their LDS reads pipeline.
+    const int Np = (N + 7) & ~7;
+    unsigned long long myk = kEmpty, myv = 0;
+    if (tid < N) {
+      const ulonglong2 kv = make_cand(tid);
+      myk = kv.x;
+      myv = kv.y;
+    }
+    __syncthreads();  // trivial graph: uk/uv held the staged tile lists until here
+    if (tid < kSmallCands) {
+      s.uk[tid] = myk;
+      s.uv[tid] = myv;
+    }
+    __syncthreads();
+    // a candidate represents its key iff no candidate with that key has a larger value
+    bool rep = myk != kEmpty;
+    if (tid < N) {
+      bool dom = false;
+      for (int j0 = 0; j0 < Np; j0 += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) dom |= (s.uk[j0 + u] == myk) & (s.uv[j0 + u] > myv);
+      }
+      rep = rep && !dom;
+    }
+    __syncthreads();
+    if (tid < kSmallCands && !rep) s.uk[tid] = kEmpty;
+    __syncthreads();
+    if (rep) {
+      const unsigned so = (unsigned)(myv >> 32);
+      int rank = 0;
+      for (int j0 = 0; j0 < Np; j0 += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const unsigned long long kj = s.uk[j0 + u];
+          const unsigned soj = (unsigned)(s.uv[j0 + u] >> 32);
+          rank += (kj != kEmpty) & ((soj > so) | ((soj == so) & (kj < myk)));
+        }
+      }
+      if (rank < Ns) {
+        s.lk[rank] = myk;
+        s.lv[rank] = myv;
+        atomicAdd(&s.nL, 1);
+      }
+    }
+    __syncthreads();
+  } else {
+    constexpr int CPT = kChunk / kSearchThreads;
+    __syncthreads();
+    for (int base = 0; base < N; base += kChunk) {
+      for (int i = tid; i < kHashSlots; i += blockDim.x) {
+        s.hk[i] = kEmpty;
+        s.hv[i] = 0ull;
+      }
+      if (tid == 0) s.nU = 0;
+      __syncthreads();
+      const int nL = s.nL;
+      for (int i = tid; i < nL; i += blockDim.x) hash_insert(s, s.lk[i], s.lv[i]);
+      ulonglong2 kv[CPT];
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int c = base + tid + u * kSearchThreads;
+        kv[u] = c < N ? make_cand(c) : make_ulonglong2(kEmpty, 0ull);
+      }
+#pragma unroll
+      for (int u = 0; u < CPT; ++u)
+        if (kv[u].x != kEmpty) hash_insert(s, kv[u].x, kv[u].y);
+      __syncthreads();
+      for (int i = tid; i < kHashSlots; i += blockDim.x) {
+        if (s.hk[i] != kEmpty) {
+          const int u = atomicAdd(&s.nU, 1);
+          s.uk[u] = s.hk[i];
+          s.uv[u] = s.hv[i];
+        }
+      }
+      __syncthreads();
+      select_top(s, s.nU, Ns);
+    }
+  }
+
+  // ---- beam, then max-contexts, then canonical (ctx, state) order ----
   const int K = s.nL;
   if (tid < 64) {
     float bmax = -INFINITY;
     for (int i = tid; i < K; i += 64) bmax = fmaxf(bmax, ord2f((unsigned)(s.lv[i] >> 32)));
-    for (int o = 32; o >= 1; o >>= 1) bmax = fmaxf(bmax, __shfl_xor(bmax, o));
+    bmax = wave_max_f(bmax);
     if (tid == 0) s.best = bmax;
   }
   __syncthreads();
@@ -556,6 +910,10 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     }
     s.f_keep2[i] = keep;
   }
+  if (tid == 0) {
+    s.nK = 0;
+    s.nC = 0;
+  }
   __syncthreads();
   const size_t hbase = ((size_t)t * d.B + b) * Ns;
   int* tr = trace ? trace + ((size_t)(t + 1) * d.B + b) * Ns * 4 : nullptr;
@@ -573,13 +931,18 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     const int parent = (int)(tb / stride_tb);
     const int apos = (int)(tb - (unsigned)parent * stride_tb) - 1;
     const int arc = apos < 0 ? -1 : s.s_base[parent] + apos;
-    const int label = arc < 0 ? 0 : g.label[arc];
+    const int label = arc < 0 ? 0 : (TRIV ? arc + 1 : g.label[arc]);
     const size_t o = (size_t)b * Ns + pos;
     d.surv_ctx[o] = (int)ci;
     d.surv_state[o] = (int)sti;
     d.surv_score[o] = s.f_score[i] - best;
     d.surv_row[o] = crow;
-    if (s.f_first[i]) d.ctx_list[(size_t)b * Nc + crow] = (int)ci;
+    if (s.f_first[i]) {
+      d.ctx_list[row0 + crow] = (int)ci;
+      s.n_ctx_list[crow] = (int)ci;
+      atomicAdd(&s.nC, 1);
+    }
+    atomicAdd(&s.nK, 1);
     d.hist_pl[hbase + pos] = (parent << 16) | label;
     d.hist_arc[hbase + pos] = arc;
     if (tr) {
@@ -589,15 +952,17 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
       tr[4 * pos + 3] = label;
     }
   }
+  __syncthreads();
   if (tid == 0) {
-    int nk = 0, ncx = 0;
-    for (int i = 0; i < K; ++i) {
-      nk += s.f_keep2[i];
-      ncx += s.f_keep2[i] && s.f_first[i];
-    }
-    d.nsurv[b] = nk;
-    d.nctx[b] = ncx;
+    d.nsurv[b] = s.nK;
+    d.nctx[b] = s.nC;
     d.offset[b] += (double)best;
+  }
+  // joiner rows of the next frame: contexts in ascending order
+  if (t + 1 < L) {
+    const size_t esz = m.bf16 ? 2 : 4;
+    write_h_rows<kSearchThreads>(m, d.enc + ((size_t)b * d.T + t + 1) * m.C, 0, s.n_ctx_list,
+                                 s.nC, reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz, tid);
   }
 }
 
@@ -613,7 +978,7 @@ __global__ __launch_bounds__(256) void k_final(GraphDev g, DecodeDev d, int* __r
                                                int* __restrict__ out_arcs) {
   __shared__ int buf_pl[kFinalBuf];
   __shared__ int buf_arc[kFinalBuf];
-  __shared__ int s_idx, s_total;
+  __shared__ int s_idx;
   __shared__ int s_wsum[4];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int Ns = d.Ns, T = d.T, len = d.len[b];
@@ -700,17 +1065,62 @@ inline int grid_for(long long n, int threads, int cap = 4096) {
   return (int)g;
 }
 
-template <bool BF16>
-hipError_t launch_joiner_impl(const ModelDev& m, const RowSrc& src, float* logits, float2* stats,
-                              int R, int nvt, hipStream_t st) {
-  const int ldk = BF16 ? m.Kpad + 8 : m.Kpad + 4;
-  const size_t lds = (size_t)kJoinerBM * ldk * (BF16 ? 2 : 4);
-  dim3 grid(nvt, (R + kJoinerBM - 1) / kJoinerBM);
-  hipLaunchKernelGGL(k_joiner<BF16>, grid, dim3(256), lds, st, m, src, logits, stats, nvt);
+template <bool BF16, int MB, bool TOPK>
+hipError_t launch_joiner_t(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p,
+                           hipStream_t st) {
+  static size_t attr = 0;  // dynamic LDS limit granted so far (kernel default: 64 KiB)
+  if (p.lds > 65536 && p.lds > attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_joiner<BF16, MB, TOPK>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+    if (e != hipSuccess) return e;
+    attr = p.lds;
+  }
+  hipLaunchKernelGGL((k_joiner<BF16, MB, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
   return hipGetLastError();
 }
 
+template <bool BF16, bool TOPK>
+hipError_t launch_joiner_mb(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p,
+                            hipStream_t st) {
+  switch (p.MB) {
+    case 1: return launch_joiner_t<BF16, 1, TOPK>(m, a, p, st);
+    case 2: return launch_joiner_t<BF16, 2, TOPK>(m, a, p, st);
+    default: return launch_joiner_t<BF16, 4, TOPK>(m, a, p, st);
+  }
+}
+
+hipError_t launch_joiner(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p, bool topk,
+                         hipStream_t st) {
+  if (m.bf16)
+    return topk ? launch_joiner_mb<true, true>(m, a, p, st) : launch_joiner_mb<true, false>(m, a, p, st);
+  return topk ? launch_joiner_mb<false, true>(m, a, p, st) : launch_joiner_mb<false, false>(m, a, p, st);
+}
+
 }  // namespace
+
+JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16) {
+  JoinerPlan p;
+  const int esz = bf16 ? 2 : 4;
+  const int n_ct = Vpad / kJoinerBN;
+  // Largest row block (4 or 2 MFMA blocks, else 1) whose h tile leaves room for two
+  // workgroups per CU (so one's loads overlap the other's MFMAs) and that still
+  // yields a workgroup per CU; larger blocks re-read W less often.
+  int MB = 1;
+  for (int cand : {4, 2}) {
+    const size_t lds = (size_t)16 * cand * (Kpad + (bf16 ? 8 : 4)) * esz;
+    const long long tiles = (long long)((rows + 16 * cand - 1) / (16 * cand)) * n_ct;
+    if (lds <= 78 * 1024 && tiles >= 256) {
+      MB = cand;
+      break;
+    }
+  }
+  p.MB = MB;
+  p.n_rt = (rows + 16 * MB - 1) / (16 * MB);
+  p.n_ct = n_ct;
+  p.grid = 8 * ((n_ct + 7) / 8) * p.n_rt;
+  p.lds = (size_t)16 * MB * (Kpad + (bf16 ? 8 : 4)) * esz;
+  return p;
+}
 
 hipError_t launch_model_setup(const float* embed, const float* conv, const float* w_out,
                               const float* b_out, int V, int C, int Kpad, int Vpad, int bf16,
@@ -727,38 +1137,57 @@ hipError_t launch_fill_i32(int* p, long long n, int v, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_init(const DecodeDev& d, const GraphDev& g, int* trace, hipStream_t st) {
-  hipLaunchKernelGGL(k_init, dim3((d.B + 255) / 256), dim3(256), 0, st, d, g, trace);
+hipError_t launch_init(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,
+                       hipStream_t st) {
+  hipLaunchKernelGGL(k_init, dim3(d.B), dim3(256), 0, st, m, d, g, trace);
   return hipGetLastError();
 }
 
-hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const float* enc, int t,
+hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const JoinerPlan& p, int t,
                                hipStream_t st) {
-  RowSrc src{};
-  src.enc = enc;
-  src.T = d.T;
-  src.t = t;
-  src.Nc = d.Nc;
-  src.len = d.len;
-  src.nctx = d.nctx;
-  src.ctx_list = d.ctx_list;
-  src.R = d.B * d.Nc;
-  src.rows_mode = 0;
-  return m.bf16 ? launch_joiner_impl<true>(m, src, d.logits, d.stats, src.R, d.nvt, st)
-                : launch_joiner_impl<false>(m, src, d.logits, d.stats, src.R, d.nvt, st);
+  JoinArgs a{};
+  a.h = d.h;
+  a.logits = d.logits;
+  a.stats = d.stats;
+  a.tk_z = d.tk_z;
+  a.tk_c = d.tk_c;
+  a.z0 = d.z0;
+  a.KT = d.KT;
+  a.R = d.B * d.Nc;
+  a.n_rt = p.n_rt;
+  a.n_ct = p.n_ct;
+  a.rows_mode = 0;
+  a.len = d.len;
+  a.nctx = d.nctx;
+  a.t = t;
+  a.Nc = d.Nc;
+  return launch_joiner(m, a, p, d.KT > 0, st);
 }
 
 hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const DecodeDev& d,
                                float beam, int t, int* trace, hipStream_t st) {
-  static bool attr_set = false;
   const size_t lds = sizeof(SearchSmem);
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_search,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
+  if (d.KT > 0) {
+    static bool attr = false;
+    if (!attr) {
+      hipError_t e = hipFuncSetAttribute((const void*)k_search<true>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    hipLaunchKernelGGL(k_search<true>, dim3(d.B), dim3(kSearchThreads), lds, st, m, g, d, beam, t,
+                       trace);
+  } else {
+    static bool attr = false;
+    if (!attr) {
+      hipError_t e = hipFuncSetAttribute((const void*)k_search<false>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    hipLaunchKernelGGL(k_search<false>, dim3(d.B), dim3(kSearchThreads), lds, st, m, g, d, beam, t,
+                       trace);
   }
-  hipLaunchKernelGGL(k_search, dim3(d.B), dim3(kSearchThreads), lds, st, m, g, d, beam, t, trace);
   return hipGetLastError();
 }
 
@@ -770,17 +1199,23 @@ hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, 
 }
 
 hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const int* ctx, int R,
-                              float* logits, float2* stats, float* out_logp, hipStream_t st) {
-  const int nvt = m.Vpad / kJoinerBN;
-  RowSrc src{};
-  src.enc_rows = enc_rows;
-  src.ctx_rows = ctx;
-  src.R = R;
-  src.rows_mode = 1;
-  hipError_t e = m.bf16 ? launch_joiner_impl<true>(m, src, logits, stats, R, nvt, st)
-                        : launch_joiner_impl<false>(m, src, logits, stats, R, nvt, st);
+                              void* h, float* logits, float2* stats, float* out_logp,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(k_h_rows, dim3(R), dim3(256), 0, st, m, enc_rows, ctx, h);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_logp_rows, dim3(R), dim3(256), 0, st, logits, stats, nvt, m.V, m.Vpad,
+  const JoinerPlan p = plan_joiner(R, m.Vpad, m.Kpad, m.bf16);
+  JoinArgs a{};
+  a.h = h;
+  a.logits = logits;
+  a.stats = stats;
+  a.R = R;
+  a.n_rt = p.n_rt;
+  a.n_ct = p.n_ct;
+  a.rows_mode = 1;
+  e = launch_joiner(m, a, p, false, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_logp_rows, dim3(R), dim3(256), 0, st, logits, stats, p.n_ct, m.V, m.Vpad,
                      out_logp);
   return hipGetLastError();
 }
