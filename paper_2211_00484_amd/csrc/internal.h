@@ -10,7 +10,8 @@ namespace tbs {
 constexpr int kMaxStates = 256;      // max_states limit (canonical ranking is O(Ns^2) per stream)
 constexpr int kMaxDim = 2048;        // joiner dimension limit
 constexpr int kJoinerBN = 64;        // joiner vocabulary columns per tile (4 waves x 16)
-constexpr int kKStep = 64;           // K padding granule of the packed weights and h rows
+constexpr int kKStep = 512;          // K padding granule of the packed weights and h rows (one
+                                     // register-resident W chunk; keeps the MFMA loop branch-free)
 constexpr int kSearchThreads = 256;
 constexpr int kChunk = 2048;         // candidates merged per LDS pass (hash path)
 constexpr int kHashSlots = 4096;     // LDS open-addressing table (load <= 0.57)

@@ -165,7 +165,7 @@ template <int NT>
 __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_rows,
                              long long enc_stride, const int* ctxs, int nrows,
                              void* __restrict__ hbase, int tid) {
-  constexpr int U = 16;  // elements per thread per batch: all loads of a batch in flight together
+  constexpr int U = 32;  // elements per thread per batch: all loads of a batch in flight together
   const int C = m.C, Kpad = m.Kpad, V = m.V;
   const float* __restrict__ P0 = m.P0;
   const float* __restrict__ P1 = m.P1;
@@ -243,30 +243,54 @@ __device__ __forceinline__ bool joiner_row_active(const JoinArgs& a, int r) {
 // ordered so that the workgroups of one column tile land on the same XCD
 // (workgroups are dispatched round-robin over the 8 XCDs), keeping each W
 // column tile in that XCD's L2.
+struct JoinShared {
+  int act[64];
+  float m[4][64], s[4][64];
+};
+
+// One joiner tile (16 * MB rows x 64 vocabulary columns) of frame a.t.  Uniform
+// across the workgroup; a tile without active rows computes nothing.
 template <bool BF16, int MB, bool TOPK>
-__global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int s_act[64];
-  __shared__ float s_m[4][64], s_s[4][64];
+__device__ __forceinline__ void joiner_tile(const ModelDev& m, const JoinArgs& a, int ct, int rt,
+                                            unsigned char* smem, JoinShared& js) {
+  int* s_act = js.act;
+  float(*s_m)[64] = js.m;
+  float(*s_s)[64] = js.s;
   constexpr int BM = 16 * MB;
+  constexpr int ESZ = BF16 ? 2 : 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
-  const int ct = xcd + 8 * (slot / a.n_rt), rt = slot - (slot / a.n_rt) * a.n_rt;
-  if (ct >= a.n_ct) return;
   const int r0 = rt * BM, n0 = ct * kJoinerBN;
   const int Kpad = m.Kpad, V = m.V, nvt = a.n_ct;
   const int lr = lane & 15, lg = lane >> 4;
   const int col = n0 + 16 * wave + lr;
+  const bool cvalid = col < V;
 
   if (tid < BM) s_act[tid] = joiner_row_active(a, r0 + tid);
+  // W fragment of the first K chunk (registers) and the bias: issued before the
+  // h staging so that all of the tile's loads are in flight together
+  // (Kpad is a multiple of 512: one chunk of W per lane is 32 float4 or 16 uint4)
+  float4 wf[BF16 ? 1 : 32];
+  uint4 wb[BF16 ? 16 : 1];
+  if (BF16) {
+    const uint16_t* wrow = m.Wb + (size_t)col * Kpad + 16 * lg;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      wb[2 * s] = *reinterpret_cast<const uint4*>(wrow + s * 64);
+      wb[2 * s + 1] = *reinterpret_cast<const uint4*>(wrow + s * 64 + 8);
+    }
+  } else {
+    const float* wrow = m.Wf + (size_t)col * Kpad + 4 * lg;
+#pragma unroll
+    for (int s = 0; s < 32; ++s) wf[s] = *reinterpret_cast<const float4*>(wrow + s * 16);
+  }
+  const float bias = cvalid ? m.bias[col] : 0.f;
   __syncthreads();
   int any = 0;
 #pragma unroll
   for (int i = 0; i < BM; ++i) any |= s_act[i];
-  if (!any) return;  // uniform across the workgroup
+  if (!any) return;  // uniform across the workgroup: nothing to compute in this tile
 
   // stage the tile's h rows in LDS (16-byte chunks, all loads in flight together)
-  constexpr int ESZ = BF16 ? 2 : 4;
   const int ldk = Kpad + (BF16 ? 8 : 4);             // row stride in elements (16-byte pad)
   const int cpr = Kpad * ESZ / 16;                   // 16-byte chunks per row
   const int nchunk = BM * cpr;
@@ -289,92 +313,100 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
     }
   }
 
-  // NCH independent accumulator chains per row block keep the MFMA pipe busy
-  // (a single chain would wait out the full MFMA latency on every step)
-  constexpr int NCH = MB >= 4 ? 1 : 4 / MB;
-  f32x4 acc[MB][NCH];
+  // Four accumulator chains per row block, and consecutive MFMAs rotate over
+  // (row block, chain), so no MFMA waits for the one before it.
+  f32x4 acc[MB][4];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) acc[mb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < 4; ++c) acc[mb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int kc = 0; kc < Kpad; kc += 512) {
-    const int kn = min(512, Kpad - kc);  // multiple of 64
-    if (BF16) {
-      const uint16_t* wrow = m.Wb + (size_t)col * Kpad + kc + 16 * lg;
-      uint4 wf[16];
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        if (s * 64 < kn) {
-          wf[2 * s] = *reinterpret_cast<const uint4*>(wrow + s * 64);
-          wf[2 * s + 1] = *reinterpret_cast<const uint4*>(wrow + s * 64 + 8);
-        }
-      }
-      __syncthreads();
-      const uint16_t* hb = reinterpret_cast<const uint16_t*>(smem);
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const uint16_t* hr = hb + (size_t)(mb * 16 + lr) * ldk + kc + 16 * lg;
+    if (kc > 0) {  // later K chunks (C > 512)
+      if (BF16) {
+        const uint16_t* wrow = m.Wb + (size_t)col * Kpad + kc + 16 * lg;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-          if (s * 64 < kn) {
-            const uint4 a0 = *reinterpret_cast<const uint4*>(hr + s * 64);
-            const uint4 a1 = *reinterpret_cast<const uint4*>(hr + s * 64 + 8);
-            f32x4& c0 = acc[mb][(2 * s) % NCH];
-            c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), as_bf16x8(wf[2 * s]), c0,
-                                                         0, 0, 0);
-            f32x4& c1 = acc[mb][(2 * s + 1) % NCH];
-            c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), as_bf16x8(wf[2 * s + 1]),
-                                                         c1, 0, 0, 0);
-          }
+          wb[2 * s] = *reinterpret_cast<const uint4*>(wrow + s * 64);
+          wb[2 * s + 1] = *reinterpret_cast<const uint4*>(wrow + s * 64 + 8);
+        }
+      } else {
+        const float* wrow = m.Wf + (size_t)col * Kpad + kc + 4 * lg;
+#pragma unroll
+        for (int s = 0; s < 32; ++s) wf[s] = *reinterpret_cast<const float4*>(wrow + s * 16);
+      }
+    }
+    __syncthreads();
+    if (BF16) {
+      const uint16_t* hb = reinterpret_cast<const uint16_t*>(smem) + (size_t)lr * ldk + kc + 16 * lg;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const uint16_t* hr = hb + (size_t)mb * 16 * ldk + s * 64;
+          const uint4 a0 = *reinterpret_cast<const uint4*>(hr);
+          const uint4 a1 = *reinterpret_cast<const uint4*>(hr + 8);
+          f32x4& c0 = acc[mb][(2 * s) & 3];
+          f32x4& c1 = acc[mb][(2 * s + 1) & 3];
+          c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), as_bf16x8(wb[2 * s]), c0, 0, 0,
+                                                       0);
+          c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), as_bf16x8(wb[2 * s + 1]), c1,
+                                                       0, 0, 0);
         }
       }
     } else {
-      const float* wrow = m.Wf + (size_t)col * Kpad + kc + 4 * lg;
-      float4 wf[32];
+      const float* hs = reinterpret_cast<const float*>(smem) + (size_t)lr * ldk + kc + 4 * lg;
 #pragma unroll
-      for (int s = 0; s < 32; ++s)
-        if (s * 16 < kn) wf[s] = *reinterpret_cast<const float4*>(wrow + s * 16);
-      __syncthreads();
-      const float* hs = reinterpret_cast<const float*>(smem);
+      for (int s = 0; s < 32; ++s) {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const float* hr = hs + (size_t)(mb * 16 + lr) * ldk + kc + 4 * lg;
-#pragma unroll
-        for (int s = 0; s < 32; ++s) {
-          if (s * 16 < kn) {
-            const float4 av = *reinterpret_cast<const float4*>(hr + s * 16);
-            f32x4& c = acc[mb][s % NCH];
-            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, wf[s].x, c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, wf[s].y, c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, wf[s].z, c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, wf[s].w, c, 0, 0, 0);
-          }
+        for (int mb = 0; mb < MB; ++mb) {
+          const float4 av = *reinterpret_cast<const float4*>(hs + (size_t)mb * 16 * ldk + s * 16);
+          acc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, wf[s].x, acc[mb][0], 0, 0, 0);
+          acc[mb][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, wf[s].y, acc[mb][1], 0, 0, 0);
+          acc[mb][2] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, wf[s].z, acc[mb][2], 0, 0, 0);
+          acc[mb][3] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, wf[s].w, acc[mb][3], 0, 0, 0);
         }
       }
     }
   }
 
-  // epilogue: bias, per-row (max, sum exp) over the tile, then logits (general
-  // graphs) or each row's best KT labels per 16-column sub-tile (trivial graph)
-  const bool cvalid = col < V;
-  const float bias = cvalid ? m.bias[col] : 0.f;
-  const int nsub = nvt * (kJoinerBN / 16);
+  // epilogue.  First everything that needs the workgroup barrier (per-row max
+  // and sum exp over the tile, combined across the 4 waves in LDS); the global
+  // stores come after it, so the barrier never waits on them.
+  float zr[MB][4];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = mb * 16 + 4 * lg + i;  // the 16 lanes of a DPP row share this row
-      float zs = acc[mb][0][i];
-#pragma unroll
-      for (int c = 1; c < NCH; ++c) zs += acc[mb][c][i];
+      const float zs = (acc[mb][0][i] + acc[mb][1][i]) + (acc[mb][2][i] + acc[mb][3][i]);
       const float z = cvalid ? zs + bias : -INFINITY;
+      zr[mb][i] = z;
       const float mx = row16_max(z);
       const float e = row16_sum(cvalid ? expf(z - mx) : 0.f);
       if (lr == 0) {
         s_m[wave][row] = mx;
         s_s[wave][row] = e;
       }
+    }
+  }
+  __syncthreads();
+  if (tid < BM && s_act[tid]) {
+    float M = s_m[0][tid];
+    for (int w = 1; w < 4; ++w) M = fmaxf(M, s_m[w][tid]);
+    float S = 0.f;
+    for (int w = 0; w < 4; ++w) S += s_s[w][tid] == 0.f ? 0.f : s_s[w][tid] * expf(s_m[w][tid] - M);
+    a.stats[(size_t)(r0 + tid) * nvt + ct] = make_float2(M, S);
+  }
+  // logits (general graphs) or each row's best KT labels per 16-column sub-tile
+  // (trivial graph), found with DPP row reductions
+  const int nsub = nvt * (kJoinerBN / 16);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = mb * 16 + 4 * lg + i;
+      const float z = zr[mb][i];
       const bool act = s_act[row];
       if (!TOPK) {
         if (act && cvalid) a.logits[(size_t)(r0 + row) * (nvt * kJoinerBN) + col] = z;
@@ -399,14 +431,16 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
       }
     }
   }
-  __syncthreads();
-  if (tid < BM && s_act[tid]) {
-    float M = s_m[0][tid];
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, s_m[w][tid]);
-    float S = 0.f;
-    for (int w = 0; w < 4; ++w) S += s_s[w][tid] == 0.f ? 0.f : s_s[w][tid] * expf(s_m[w][tid] - M);
-    a.stats[(size_t)(r0 + tid) * nvt + ct] = make_float2(M, S);
-  }
+}
+
+template <bool BF16, int MB, bool TOPK>
+__global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ JoinShared js;
+  const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
+  const int ct = xcd + 8 * (slot / a.n_rt), rt = slot - (slot / a.n_rt) * a.n_rt;
+  if (ct >= a.n_ct) return;
+  joiner_tile<BF16, MB, TOPK>(m, a, ct, rt, smem, js);
 }
 
 __global__ void k_logp_rows(const float* __restrict__ logits, const float2* __restrict__ stats,
@@ -470,8 +504,10 @@ struct SearchSmem {
   int s_base[kMaxStates], s_off[kMaxStates + 1];
   float s_score[kMaxStates];
   double s_lse[kMaxStates];
-  float f_score[kMaxStates], f_cs[kMaxStates];
-  int f_keep1[kMaxStates], f_first[kMaxStates], f_keep2[kMaxStates];
+  uint4 fent[kMaxStates];    // final stage: (ctx, state, score bits, context-score bits)
+  int fflg[kMaxStates];      // bit 0 in beam, bit 1 first tuple of its context, bit 2 kept
+  float enc_next[kMaxDim];   // encoder frame t+1 of this stream (joiner rows of the next frame)
+  float wmax[4];
   int n_ctx_list[kMaxStates];
   float rk_z[kMaxTopK * kMaxTopK];  // trivial graph: each row's best labels over all tiles
   int rk_c[kMaxTopK * kMaxTopK];
@@ -640,6 +676,10 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     s.s_state[i] = d.surv_state[o];
     s.s_row[i] = d.surv_row[o];
     s.s_score[i] = d.surv_score[o];
+  }
+  if (t + 1 < L) {
+    const float* er = d.enc + ((size_t)b * d.T + t + 1) * m.C;
+    for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
   }
   // trivial graph: the joiner's per-tile best labels of this stream's rows
   const int E = TRIV ? nvt * (kJoinerBN / 16) * d.KT : 0;
@@ -866,103 +906,175 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
   }
 
   // ---- beam, then max-contexts, then canonical (ctx, state) order ----
+  // All LDS work and barriers precede the global stores, so no barrier waits
+  // for stores to complete.
   const int K = s.nL;
-  if (tid < 64) {
+  const int Kp = (K + 7) & ~7;
+  {
     float bmax = -INFINITY;
-    for (int i = tid; i < K; i += 64) bmax = fmaxf(bmax, ord2f((unsigned)(s.lv[i] >> 32)));
+    if (tid < K) bmax = ord2f((unsigned)(s.lv[tid] >> 32));
     bmax = wave_max_f(bmax);
-    if (tid == 0) s.best = bmax;
+    if (lane == 0) s.wmax[wave] = bmax;
   }
   __syncthreads();
-  const float best = s.best;
+  const float best = fmaxf(fmaxf(s.wmax[0], s.wmax[1]), fmaxf(s.wmax[2], s.wmax[3]));
   const float thr = best - beam;
-  for (int i = tid; i < K; i += blockDim.x) {
-    const float sc = ord2f((unsigned)(s.lv[i] >> 32));
-    s.f_score[i] = sc;
-    s.f_keep1[i] = sc >= thr;
+  unsigned my_ci = 0xffffffffu, my_st = 0xffffffffu;
+  float my_sc = -INFINITY;
+  int my_keep1 = 0;
+  if (tid < K) {
+    my_ci = (unsigned)s.lk[tid];
+    my_st = (unsigned)(s.lk[tid] >> 32);
+    my_sc = ord2f((unsigned)(s.lv[tid] >> 32));
+    my_keep1 = my_sc >= thr;
   }
-  __syncthreads();
-  for (int i = tid; i < K; i += blockDim.x) {
-    const unsigned ci = (unsigned)s.lk[i], sti = (unsigned)(s.lk[i] >> 32);
-    float cs = -INFINITY;
-    int first = s.f_keep1[i];
-    for (int j = 0; j < K; ++j) {
-      if (!s.f_keep1[j] || (unsigned)s.lk[j] != ci) continue;
-      cs = fmaxf(cs, s.f_score[j]);
-      if ((unsigned)(s.lk[j] >> 32) < sti) first = 0;
-    }
-    s.f_cs[i] = cs;
-    s.f_first[i] = first;
-  }
-  __syncthreads();
-  for (int i = tid; i < K; i += blockDim.x) {
-    int keep = 0;
-    if (s.f_keep1[i]) {
-      const unsigned ci = (unsigned)s.lk[i];
-      const float cs = s.f_cs[i];
-      int rank = 0;
-      for (int j = 0; j < K; ++j) {
-        if (!s.f_first[j]) continue;
-        const float csj = s.f_cs[j];
-        if (csj > cs || (csj == cs && (unsigned)s.lk[j] < ci)) ++rank;
-      }
-      keep = rank < Nc;
-    }
-    s.f_keep2[i] = keep;
+  if (tid < Kp) {
+    s.fent[tid] = make_uint4(my_ci, my_st, __float_as_uint(my_sc), 0u);
+    s.fflg[tid] = my_keep1;
   }
   if (tid == 0) {
     s.nK = 0;
     s.nC = 0;
   }
   __syncthreads();
-  const size_t hbase = ((size_t)t * d.B + b) * Ns;
-  int* tr = trace ? trace + ((size_t)(t + 1) * d.B + b) * Ns * 4 : nullptr;
-  for (int i = tid; i < K; i += blockDim.x) {
-    if (!s.f_keep2[i]) continue;
-    const unsigned ci = (unsigned)s.lk[i], sti = (unsigned)(s.lk[i] >> 32);
-    int pos = 0, crow = 0;
-    for (int j = 0; j < K; ++j) {
-      if (!s.f_keep2[j]) continue;
-      const unsigned cj = (unsigned)s.lk[j], stj = (unsigned)(s.lk[j] >> 32);
-      if (cj < ci || (cj == ci && stj < sti)) ++pos;
-      if (s.f_first[j] && cj < ci) ++crow;
+  int my_keep2 = 0, my_pos = 0, my_crow = 0, my_first = 0;
+  if (K <= 64) {
+    // One wave, one entry per lane; other lanes' entries are read with readlane
+    // (no LDS traffic).  Context score = max over the context's in-beam tuples;
+    // its first tuple is the one with the smallest state.
+    if (wave == 0) {
+      float my_cs = -INFINITY;
+      my_first = my_keep1;
+      for (int j = 0; j < K; ++j) {
+        const unsigned cj = (unsigned)__builtin_amdgcn_readlane((int)my_ci, j);
+        const unsigned sj = (unsigned)__builtin_amdgcn_readlane((int)my_st, j);
+        const float scj = rdlane_f(my_sc, j);
+        const int k1j = __builtin_amdgcn_readlane(my_keep1, j);
+        const bool same = k1j && cj == my_ci;
+        my_cs = same ? fmaxf(my_cs, scj) : my_cs;
+        my_first &= !(same && sj < my_st);
+      }
+      // max-contexts: rank of the tuple's context among the in-beam contexts
+      int rank = 0;
+      for (int j = 0; j < K; ++j) {
+        const int fj = __builtin_amdgcn_readlane(my_first, j);
+        const float csj = rdlane_f(my_cs, j);
+        const unsigned cj = (unsigned)__builtin_amdgcn_readlane((int)my_ci, j);
+        rank += fj && (csj > my_cs || (csj == my_cs && cj < my_ci));
+      }
+      my_keep2 = my_keep1 && rank < Nc;
+      // canonical position and context row of each kept tuple
+      for (int j = 0; j < K; ++j) {
+        const int k2j = __builtin_amdgcn_readlane(my_keep2, j);
+        const int fj = __builtin_amdgcn_readlane(my_first, j);
+        const unsigned cj = (unsigned)__builtin_amdgcn_readlane((int)my_ci, j);
+        const unsigned sj = (unsigned)__builtin_amdgcn_readlane((int)my_st, j);
+        my_pos += k2j && (cj < my_ci || (cj == my_ci && sj < my_st));
+        my_crow += k2j && fj && cj < my_ci;
+      }
+      const unsigned long long kept = __ballot(my_keep2);
+      const unsigned long long firsts = __ballot(my_keep2 && my_first);
+      if (my_keep2 && my_first) s.n_ctx_list[my_crow] = (int)my_ci;
+      if (lane == 0) {
+        s.nK = __popcll(kept);
+        s.nC = __popcll(firsts);
+      }
     }
-    const unsigned tb = 0xffffffffu - (unsigned)s.lv[i];
+  } else {
+    // Larger sets: every thread holds one entry and scans the others in LDS.
+    // The loads are unconditional (the asm statement pins them) so they pipeline.
+    float my_cs = -INFINITY;
+    my_first = my_keep1;
+    if (tid < K) {
+      for (int j0 = 0; j0 < Kp; j0 += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint4 e = s.fent[j0 + u];
+          const int f = s.fflg[j0 + u];
+          asm volatile("" ::"v"(e.x), "v"(e.y), "v"(e.z), "v"(f));
+          const bool same = (f & 1) && e.x == my_ci;
+          my_cs = same ? fmaxf(my_cs, __uint_as_float(e.z)) : my_cs;
+          my_first &= !(same && e.y < my_st);
+        }
+      }
+    }
+    __syncthreads();
+    if (tid < Kp) {
+      s.fent[tid].w = __float_as_uint(my_cs);
+      s.fflg[tid] = my_keep1 | (my_first << 1);
+    }
+    __syncthreads();
+    if (my_keep1) {
+      int rank = 0;
+      for (int j0 = 0; j0 < Kp; j0 += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint4 e = s.fent[j0 + u];
+          const int f = s.fflg[j0 + u];
+          asm volatile("" ::"v"(e.x), "v"(e.w), "v"(f));
+          const float csj = __uint_as_float(e.w);
+          rank += ((f >> 1) & 1) && (csj > my_cs || (csj == my_cs && e.x < my_ci));
+        }
+      }
+      my_keep2 = rank < Nc;
+    }
+    __syncthreads();
+    if (tid < Kp) s.fflg[tid] = my_keep1 | (my_first << 1) | (my_keep2 << 2);
+    __syncthreads();
+    if (my_keep2) {
+      for (int j0 = 0; j0 < Kp; j0 += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint4 e = s.fent[j0 + u];
+          const int f = s.fflg[j0 + u];
+          asm volatile("" ::"v"(e.x), "v"(e.y), "v"(f));
+          const bool k2 = (f >> 2) & 1;
+          my_pos += k2 && (e.x < my_ci || (e.x == my_ci && e.y < my_st));
+          my_crow += k2 && ((f >> 1) & 1) && e.x < my_ci;
+        }
+      }
+      atomicAdd(&s.nK, 1);
+      if (my_first) {
+        s.n_ctx_list[my_crow] = (int)my_ci;
+        atomicAdd(&s.nC, 1);
+      }
+    }
+  }
+  __syncthreads();
+  const int nC = s.nC;
+  // global stores: joiner rows of the next frame, survivors, history, trace
+  if (t + 1 < L) {
+    const size_t esz = m.bf16 ? 2 : 4;
+    write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_ctx_list, nC,
+                                 reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz, tid);
+  }
+  if (my_keep2) {
+    const unsigned tb = 0xffffffffu - (unsigned)s.lv[tid];
     const int parent = (int)(tb / stride_tb);
     const int apos = (int)(tb - (unsigned)parent * stride_tb) - 1;
     const int arc = apos < 0 ? -1 : s.s_base[parent] + apos;
     const int label = arc < 0 ? 0 : (TRIV ? arc + 1 : g.label[arc]);
-    const size_t o = (size_t)b * Ns + pos;
-    d.surv_ctx[o] = (int)ci;
-    d.surv_state[o] = (int)sti;
-    d.surv_score[o] = s.f_score[i] - best;
-    d.surv_row[o] = crow;
-    if (s.f_first[i]) {
-      d.ctx_list[row0 + crow] = (int)ci;
-      s.n_ctx_list[crow] = (int)ci;
-      atomicAdd(&s.nC, 1);
-    }
-    atomicAdd(&s.nK, 1);
-    d.hist_pl[hbase + pos] = (parent << 16) | label;
-    d.hist_arc[hbase + pos] = arc;
-    if (tr) {
-      tr[4 * pos + 0] = (int)ci;
-      tr[4 * pos + 1] = (int)sti;
-      tr[4 * pos + 2] = parent;
-      tr[4 * pos + 3] = label;
+    const size_t o = (size_t)b * Ns + my_pos;
+    d.surv_ctx[o] = (int)my_ci;
+    d.surv_state[o] = (int)my_st;
+    d.surv_score[o] = my_sc - best;
+    d.surv_row[o] = my_crow;
+    if (my_first) d.ctx_list[row0 + my_crow] = (int)my_ci;
+    const size_t hbase = ((size_t)t * d.B + b) * Ns;
+    d.hist_pl[hbase + my_pos] = (parent << 16) | label;
+    d.hist_arc[hbase + my_pos] = arc;
+    if (trace) {
+      int* tr = trace + (((size_t)(t + 1) * d.B + b) * Ns + my_pos) * 4;
+      tr[0] = (int)my_ci;
+      tr[1] = (int)my_st;
+      tr[2] = parent;
+      tr[3] = label;
     }
   }
-  __syncthreads();
   if (tid == 0) {
     d.nsurv[b] = s.nK;
-    d.nctx[b] = s.nC;
+    d.nctx[b] = nC;
     d.offset[b] += (double)best;
-  }
-  // joiner rows of the next frame: contexts in ascending order
-  if (t + 1 < L) {
-    const size_t esz = m.bf16 ? 2 : 4;
-    write_h_rows<kSearchThreads>(m, d.enc + ((size_t)b * d.T + t + 1) * m.C, 0, s.n_ctx_list,
-                                 s.nC, reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz, tid);
   }
 }
 
