@@ -156,49 +156,63 @@ __global__ void k_fill_i32(int* p, long long n, int v) {
 }
 
 // ---------------------------------------------------------------------------
+// tanh from the hardware exp and reciprocal: (e - 1) / (e + 1), e = exp(2x), with
+// x clamped to [-9, 9] (|tanh(9)| rounds to 1 in fp32).  Absolute error ~1e-7,
+// which moves a joiner logit by at most ~C * max|W| * 1e-7.
+__device__ __forceinline__ float tanh_fast(float x) {
+  const float xc = fminf(fmaxf(x, -9.f), 9.f);
+  const float e = __expf(2.f * xc);
+  return __fdividef(e - 1.f, e + 1.f);
+}
+
 // Joiner input rows (Algorithm 1: decoder, IndexSelect of the encoder frame):
 // h[k] = tanh(enc[k] + ReLU(P0[a][k] + P1[b][k])) for k < C, 0 for C <= k < Kpad,
-// stored as fp32 or bf16 (RNE).  Rows r < nrows use context ctxs[r] and the
-// encoder row enc_rows + r * enc_stride (enc_stride = 0: one shared frame).
-// Loads are issued four iterations at a time for memory-level parallelism.
+// stored as fp32 or bf16 (RNE).  Row r reads P0/P1 at rowoff[r] = (a * Kpad, b * Kpad)
+// and the encoder row enc_rows + r * enc_stride (enc_stride = 0: one shared frame).
+// Thread tid owns columns tid, tid + NT, ... of every row (Kpad is a multiple of
+// 512); a batch's loads are all issued before any tanh.
 template <int NT>
 __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_rows,
-                             long long enc_stride, const int* ctxs, int nrows,
+                             long long enc_stride, const int2* rowoff, int nrows,
                              void* __restrict__ hbase, int tid) {
-  constexpr int U = 32;  // elements per thread per batch: all loads of a batch in flight together
-  const int C = m.C, Kpad = m.Kpad, V = m.V;
+  constexpr int U = 16;  // (row, column) elements per thread per batch
+  const int C = m.C, Kpad = m.Kpad;
   const float* __restrict__ P0 = m.P0;
   const float* __restrict__ P1 = m.P1;
-  const int total = nrows * Kpad;
-  for (int base = tid; base < total; base += U * NT) {
+  const int cols = Kpad / NT;  // columns per thread per row
+  int r = 0, j = 0;            // (row, column slot) of the next element
+  while (r < nrows) {
     float e[U], p0[U], p1[U];
+    int ro[U], ko[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int idx = base + u * NT;
+      const int k = tid + j * NT;
+      ro[u] = r;
+      ko[u] = k;
       e[u] = 0.f;
       p0[u] = 0.f;
       p1[u] = 0.f;
-      if (idx < total) {
-        const int r = idx / Kpad, k = idx - r * Kpad;
-        if (k < C) {
-          const int ctx = ctxs[r];
-          const int a = ctx / V, b = ctx - a * V;
-          e[u] = enc_rows[(size_t)r * enc_stride + k];
-          p0[u] = P0[(size_t)a * Kpad + k];
-          p1[u] = P1[(size_t)b * Kpad + k];
-        }
+      if (r < nrows && k < C) {
+        const int2 off = rowoff[r];
+        e[u] = enc_rows[(size_t)r * enc_stride + k];
+        p0[u] = P0[(size_t)off.x + k];
+        p1[u] = P1[(size_t)off.y + k];
+      }
+      if (++j == cols) {
+        j = 0;
+        ++r;
       }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int idx = base + u * NT;
-      if (idx >= total) continue;
-      const int k = idx - (idx / Kpad) * Kpad;
-      const float h = k < C ? tanhf(e[u] + fmaxf(p0[u] + p1[u], 0.f)) : 0.f;
+      if (ro[u] >= nrows) continue;
+      const int k = ko[u];
+      const float h = k < C ? tanh_fast(e[u] + fmaxf(p0[u] + p1[u], 0.f)) : 0.f;
+      const size_t o = (size_t)ro[u] * Kpad + k;
       if (m.bf16)
-        reinterpret_cast<uint16_t*>(hbase)[idx] = f32_to_bf16_rne(h);
+        reinterpret_cast<uint16_t*>(hbase)[o] = f32_to_bf16_rne(h);
       else
-        reinterpret_cast<float*>(hbase)[idx] = h;
+        reinterpret_cast<float*>(hbase)[o] = h;
     }
   }
 }
@@ -206,9 +220,15 @@ __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_ro
 // h rows for explicit (encoder row, context) pairs: one workgroup per row.
 __global__ __launch_bounds__(256) void k_h_rows(ModelDev m, const float* __restrict__ enc_rows,
                                                 const int* __restrict__ ctx, void* __restrict__ h) {
+  __shared__ int2 off;
   const int r = blockIdx.x;
+  if (threadIdx.x == 0) {
+    const int c = ctx[r], a = c / m.V;
+    off = make_int2(a * m.Kpad, (c - a * m.V) * m.Kpad);
+  }
+  __syncthreads();
   const size_t esz = m.bf16 ? 2 : 4;
-  write_h_rows<256>(m, enc_rows + (size_t)r * m.C, 0, ctx + r, 1,
+  write_h_rows<256>(m, enc_rows + (size_t)r * m.C, 0, &off, 1,
                     reinterpret_cast<char*>(h) + (size_t)r * m.Kpad * esz, threadIdx.x);
 }
 
@@ -486,9 +506,9 @@ __global__ __launch_bounds__(256) void k_init(ModelDev m, DecodeDev d, GraphDev 
     }
   }
   if (d.len[b] > 0) {
-    const int zero_ctx = 0;
+    const int2 zero_off = make_int2(0, 0);  // context (blank, blank)
     const size_t esz = m.bf16 ? 2 : 4;
-    write_h_rows<256>(m, d.enc + (size_t)b * d.T * m.C, 0, &zero_ctx, 1,
+    write_h_rows<256>(m, d.enc + (size_t)b * d.T * m.C, 0, &zero_off, 1,
                       reinterpret_cast<char*>(d.h) + (size_t)b * d.Nc * m.Kpad * esz, tid);
   }
 }
@@ -509,6 +529,7 @@ struct SearchSmem {
   float enc_next[kMaxDim];   // encoder frame t+1 of this stream (joiner rows of the next frame)
   float wmax[4];
   int n_ctx_list[kMaxStates];
+  int2 n_rowoff[kMaxStates];  // (a * Kpad, b * Kpad) of each next-frame context (a, b)
   float rk_z[kMaxTopK * kMaxTopK];  // trivial graph: each row's best labels over all tiles
   int rk_c[kMaxTopK * kMaxTopK];
   float s_z0[kMaxTopK];
@@ -1042,10 +1063,15 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
   }
   __syncthreads();
   const int nC = s.nC;
+  if (tid < nC) {
+    const int c = s.n_ctx_list[tid], a = c / V;
+    s.n_rowoff[tid] = make_int2(a * m.Kpad, (c - a * V) * m.Kpad);
+  }
+  __syncthreads();
   // global stores: joiner rows of the next frame, survivors, history, trace
   if (t + 1 < L) {
     const size_t esz = m.bf16 ? 2 : 4;
-    write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_ctx_list, nC,
+    write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC,
                                  reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz, tid);
   }
   if (my_keep2) {
