@@ -28,12 +28,21 @@ if ROOT not in sys.path:
 METRIC = "decoded frames/sec (B×T) at beam 4; joiner MFMA util %; prune HBM GB/s"
 PEAK = {"fp32_mfma_tflops": 157.3, "bf16_mfma_tflops": 2500.0, "hbm_gbps": 8000.0}
 DEFAULT_STEPS = {"tiny": 50, "standard": 20, "graph": 20, "throughput": 10, "large": 3}
+KERNEL_SRC = os.path.join(ROOT, "paper_2211_00484_amd", "csrc", "kernels.hip")
+TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "traffic.md")
+COPY_BYTES = 256 << 20
 CPU_SAMPLE_STREAMS = {"tiny": None, "standard": None, "graph": None, "throughput": 24,
                       "large": 12}
 
 
-def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles):
-    """Joiner rows (contexts) and search traffic implied by a survivor trace."""
+def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles, Ns):
+    """Joiner rows (contexts) and search traffic implied by a survivor trace.
+
+    General graphs: the search reads each arc record (dest, label, score) and gathers
+    one logit per arc.  Trivial graph: arcs are implicit (every label); the joiner
+    keeps each row's best Ns labels per 16-column sub-tile, and the search reads those
+    lists (value + label) and the blank logit instead."""
+    trivial = graph.num_states == 1 and graph.num_arcs == V - 1
     deg = np.diff(graph.row_ptr).astype(np.int64)
     rows = 0
     cands = 0
@@ -55,10 +64,65 @@ def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles):
     # search kernel bytes: arc record (dest, label, score) + gathered logit per arc,
     # a logit per blank, survivor record in (ctx, state, row, score) + row_ptr pair,
     # per-row softmax partials, survivor record out + history (parent|label, arc).
-    search_bytes = (arcs * (12 + 4) + (cands - arcs) * 4 + survivors_in * (16 + 8)
-                    + rows * Vpad_tiles * 8 + survivors_out * (16 + 8) + rows * 4)
+    if trivial:
+        arc_bytes = rows * (Vpad_tiles * 4 * Ns * 8 + 4)
+    else:
+        arc_bytes = arcs * (12 + 4) + (cands - arcs) * 4
+    search_bytes = (arc_bytes + survivors_in * (16 + 8) + rows * Vpad_tiles * 8
+                    + survivors_out * (16 + 8) + rows * 4)
     return dict(rows=rows, flop=flop, candidates=cands, arcs=arcs, search_bytes=search_bytes,
                 survivors=survivors_in)
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter table
+    (FETCH_SIZE and WRITE_SIZE per dispatch, scaled by the copy-kernel factor), or
+    None if the table is absent, lacks the entry, or predates the current kernels."""
+    if not os.path.exists(TRAFFIC_TABLE):
+        return None
+    src_hash, ffetch, fwrite, rows = None, None, None, {}
+    for line in open(TRAFFIC_TABLE):
+        line = line.strip()
+        if line.startswith("kernels.hip sha256[:16]:"):
+            src_hash = line.split(":", 1)[1].strip().strip("`")
+        elif line.startswith("copy factor FETCH_SIZE:"):
+            ffetch = float(line.split(":", 1)[1].split()[0])
+        elif line.startswith("copy factor WRITE_SIZE:"):
+            fwrite = float(line.split(":", 1)[1].split()[0])
+        elif line.startswith("|") and not line.startswith("|---") and "workload" not in line:
+            cells = [c.strip().strip("`") for c in line.strip("|").split("|")]
+            if len(cells) >= 4:
+                rows[(cells[0], cells[1])] = (float(cells[2]), float(cells[3]))
+    if (src_hash != kernel_source_hash() or ffetch is None or fwrite is None
+            or (workload, kernel) not in rows):
+        return None
+    fetch_kib, write_kib = rows[(workload, kernel)]
+    return {"bytes_per_launch": (fetch_kib / ffetch + write_kib / fwrite) * 1024.0,
+            "fetch_kib_per_dispatch": fetch_kib, "write_kib_per_dispatch": write_kib,
+            "copy_factor_fetch": ffetch, "copy_factor_write": fwrite,
+            "source": "profiles/traffic.md"}
+
+
+def copy_calibration(steps: int):
+    """A plain device-to-device copy of COPY_BYTES, for scaling the traffic counters."""
+    import torch
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    print(json.dumps({"copy_bytes": COPY_BYTES, "read_kib": COPY_BYTES / 1024,
+                      "write_kib": COPY_BYTES / 1024, "gbps": 2 * COPY_BYTES / dt / 1e9}),
+          flush=True)
 
 
 def cpu_baseline(w, inputs, model_np, graph_np):
@@ -85,6 +149,8 @@ def main():
     ap.add_argument("--workload", default="standard",
                     choices=["tiny", "standard", "graph", "throughput", "large"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain copy of 256 MiB (traffic-counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}): streams are "
@@ -96,6 +162,9 @@ def main():
     from paper_2211_00484_amd import synth, tbs
 
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration(args.steps or 5)
+        return
     w, inputs, model_np, graph_np = synth.make_workload(args.workload, seed=0)
     K = args.steps if args.steps is not None else DEFAULT_STEPS[w.name]
     W = args.warmup
@@ -110,7 +179,8 @@ def main():
                         max_contexts=w.max_contexts, want_trace=True)
     torch.cuda.synchronize()
     nvt = (w.V + 63) // 64
-    work = algorithmic_work(tr_out.trace.cpu().numpy(), inputs.lengths, graph_np, w.V, w.C, nvt)
+    work = algorithmic_work(tr_out.trace.cpu().numpy(), inputs.lengths, graph_np, w.V, w.C, nvt,
+                            w.max_states)
     del tr_out
 
     out = tbs.allocate_outputs(B, T, w.max_states, status=True)
@@ -158,11 +228,14 @@ def main():
                               "peak_gbps": PEAK["hbm_gbps"], "frac": s_gbps / PEAK["hbm_gbps"]})
     if kernels["joiner"]["ms_per_step"] >= kernels["search"]["ms_per_step"]:
         roofline = {"kernel": "k_joiner", "bound": "mfma", "achieved": j_tflops, "peak": peak_j,
-                    "unit": "TFLOP/s", "frac": j_tflops / peak_j, "traffic": None}
+                    "unit": "TFLOP/s", "frac": j_tflops / peak_j}
     else:
         roofline = {"kernel": "k_search", "bound": "hbm", "achieved": s_gbps,
-                    "peak": PEAK["hbm_gbps"], "unit": "GB/s", "frac": s_gbps / PEAK["hbm_gbps"],
-                    "traffic": None}
+                    "peak": PEAK["hbm_gbps"], "unit": "GB/s", "frac": s_gbps / PEAK["hbm_gbps"]}
+    tr = measured_traffic(w.name, roofline["kernel"])
+    roofline["traffic"] = None if tr is None else tr["bytes_per_launch"]
+    if tr is not None:
+        roofline["traffic_detail"] = tr
 
     line = {
         "metric": METRIC, "value": value, "unit": "frames/s", "n_gpus": 1, "steps": K, "warmup": W,

@@ -259,10 +259,7 @@ __device__ __forceinline__ bool joiner_row_active(const JoinArgs& a, int r) {
 
 // Tile = (16 * MB rows) x 64 vocabulary columns; wave w owns columns 16w..16w+15
 // and keeps its W fragment (16 columns x up to 512 of K) in registers while it
-// sweeps the tile's row blocks, whose h rows are staged once in LDS.  Tiles are
-// ordered so that the workgroups of one column tile land on the same XCD
-// (workgroups are dispatched round-robin over the 8 XCDs), keeping each W
-// column tile in that XCD's L2.
+// sweeps the tile's row blocks, whose h rows are staged once in LDS.
 struct JoinShared {
   int act[64];
   float m[4][64], s[4][64];
@@ -457,8 +454,12 @@ template <bool BF16, int MB, bool TOPK>
 __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ JoinShared js;
+  // Workgroup i runs on XCD i mod 8.  XCD x owns the column tiles x, x + 8, ...
+  // and walks row tiles in order, its column tiles fastest: its W columns stay
+  // in its L2 while each h row tile is read once per XCD.
   const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
-  const int ct = xcd + 8 * (slot / a.n_rt), rt = slot - (slot / a.n_rt) * a.n_rt;
+  const int ncx = (a.n_ct + 7) >> 3;
+  const int rt = slot / ncx, ct = xcd + 8 * (slot - rt * ncx);
   if (ct >= a.n_ct) return;
   joiner_tile<BF16, MB, TOPK>(m, a, ct, rt, smem, js);
 }
