@@ -2,12 +2,14 @@
 on one MI355X, with the dominant kernel's roofline fraction and the CPU oracle's rate.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload standard]
+                    [--schedule auto|frame|stream]
 
 A step is one tbs_decode of the whole batch (every frame of every stream: joiner,
 expansion, merge, pruning, history, traceback) on inputs already resident in HBM.
-Per-kernel durations come from HIP events the library records around each launch on
-the decode stream during the timed steps (tbs_model_set_profiling).  Algorithmic work
-(joiner FLOP, search bytes) is counted from the survivor trace of one untimed decode.
+`value` is frames over the wall time of K plain steps.  Per-kernel durations come
+from K further steps during which the library records HIP events around each launch
+on the decode stream (tbs_model_set_profiling).  Algorithmic work (joiner FLOP,
+search bytes) is counted from the survivor trace of one untimed decode.
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -148,6 +150,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="standard",
                     choices=["tiny", "standard", "graph", "throughput", "large"])
+    ap.add_argument("--schedule", default="auto", choices=["auto", "frame", "stream"],
+                    help="frame loop: per-frame joiner + search kernels, or one persistent "
+                         "workgroup per stream (auto picks per shape)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of 256 MiB (traffic-counter calibration)")
@@ -169,6 +174,7 @@ def main():
     K = args.steps if args.steps is not None else DEFAULT_STEPS[w.name]
     W = args.warmup
     model = tbs.Model.from_synth(model_np, dtype=w.dtype)
+    model.set_schedule(args.schedule)
     graph = tbs.Graph.from_synth(graph_np)
     enc = torch.from_numpy(inputs.encoder_out).cuda()
     B, T = inputs.B, inputs.T
@@ -188,50 +194,76 @@ def main():
         tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
     torch.cuda.synchronize()
 
-    model.set_profiling(True)
+    # the timed steps: nothing but the decodes on the stream
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(K):
         tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    prof = model.read_profile()
-    model.set_profiling(False)
 
-    # same steps without the timing events, for the event overhead
+    # the same steps again with HIP events around every kernel launch: per-kernel
+    # durations for the roofline (the events add a little time between kernels)
+    model.set_profiling(True)
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     for _ in range(K):
         tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
     torch.cuda.synchronize()
     t3 = time.perf_counter()
+    prof = model.read_profile()
+    model.set_profiling(False)
 
     ms_step = (t1 - t0) * 1e3 / K
-    ms_step_plain = (t3 - t2) * 1e3 / K
+    ms_step_events = (t3 - t2) * 1e3 / K
     value = frames * K / (t1 - t0)
 
     kernels = {}
     for name, (n, ms) in prof.items():
+        if n == 0:
+            continue
         kernels[name] = {"launches_per_step": n / K, "avg_us": 1e3 * ms / max(n, 1),
                          "ms_per_step": ms / K}
-    j_avg_s = kernels["joiner"]["avg_us"] * 1e-6
-    s_avg_s = kernels["search"]["avg_us"] * 1e-6
-    j_launches = kernels["joiner"]["launches_per_step"]
-    flop_per_launch = work["flop"] / max(j_launches, 1)
-    bytes_per_launch = work["search_bytes"] / max(kernels["search"]["launches_per_step"], 1)
     peak_j = PEAK["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
-    j_tflops = flop_per_launch / j_avg_s / 1e12
-    s_gbps = bytes_per_launch / s_avg_s / 1e9
-    kernels["joiner"].update({"algorithmic_flop_per_launch": flop_per_launch, "tflops": j_tflops,
-                              "peak_tflops": peak_j, "frac": j_tflops / peak_j})
-    kernels["search"].update({"algorithmic_bytes_per_launch": bytes_per_launch, "gbps": s_gbps,
-                              "peak_gbps": PEAK["hbm_gbps"], "frac": s_gbps / PEAK["hbm_gbps"]})
-    if kernels["joiner"]["ms_per_step"] >= kernels["search"]["ms_per_step"]:
-        roofline = {"kernel": "k_joiner", "bound": "mfma", "achieved": j_tflops, "peak": peak_j,
+    if "stream" in kernels:
+        # one persistent kernel runs joiner and search for every frame: its joiner FLOP
+        # and search bytes are both divided by the whole kernel's duration
+        schedule = "stream"
+        st_avg_s = kernels["stream"]["avg_us"] * 1e-6
+        launches = max(kernels["stream"]["launches_per_step"], 1)
+        flop_per_launch = work["flop"] / launches
+        bytes_per_launch = work["search_bytes"] / launches
+        j_tflops = flop_per_launch / st_avg_s / 1e12
+        s_gbps = bytes_per_launch / st_avg_s / 1e9
+        kernels["stream"].update({"algorithmic_flop_per_launch": flop_per_launch,
+                                  "tflops": j_tflops, "peak_tflops": peak_j,
+                                  "frac": j_tflops / peak_j,
+                                  "algorithmic_search_bytes_per_launch": bytes_per_launch,
+                                  "search_gbps": s_gbps})
+        roofline = {"kernel": "k_stream", "bound": "mfma", "achieved": j_tflops, "peak": peak_j,
                     "unit": "TFLOP/s", "frac": j_tflops / peak_j}
     else:
-        roofline = {"kernel": "k_search", "bound": "hbm", "achieved": s_gbps,
-                    "peak": PEAK["hbm_gbps"], "unit": "GB/s", "frac": s_gbps / PEAK["hbm_gbps"]}
+        schedule = "frame"
+        j_avg_s = kernels["joiner"]["avg_us"] * 1e-6
+        s_avg_s = kernels["search"]["avg_us"] * 1e-6
+        j_launches = kernels["joiner"]["launches_per_step"]
+        flop_per_launch = work["flop"] / max(j_launches, 1)
+        bytes_per_launch = work["search_bytes"] / max(kernels["search"]["launches_per_step"], 1)
+        j_tflops = flop_per_launch / j_avg_s / 1e12
+        s_gbps = bytes_per_launch / s_avg_s / 1e9
+        kernels["joiner"].update({"algorithmic_flop_per_launch": flop_per_launch,
+                                  "tflops": j_tflops, "peak_tflops": peak_j,
+                                  "frac": j_tflops / peak_j})
+        kernels["search"].update({"algorithmic_bytes_per_launch": bytes_per_launch,
+                                  "gbps": s_gbps, "peak_gbps": PEAK["hbm_gbps"],
+                                  "frac": s_gbps / PEAK["hbm_gbps"]})
+        if kernels["joiner"]["ms_per_step"] >= kernels["search"]["ms_per_step"]:
+            roofline = {"kernel": "k_joiner", "bound": "mfma", "achieved": j_tflops,
+                        "peak": peak_j, "unit": "TFLOP/s", "frac": j_tflops / peak_j}
+        else:
+            roofline = {"kernel": "k_search", "bound": "hbm", "achieved": s_gbps,
+                        "peak": PEAK["hbm_gbps"], "unit": "GB/s",
+                        "frac": s_gbps / PEAK["hbm_gbps"]}
     tr = measured_traffic(w.name, roofline["kernel"])
     roofline["traffic"] = None if tr is None else tr["bytes_per_launch"]
     if tr is not None:
@@ -247,12 +279,12 @@ def main():
                    "graph_states": graph_np.num_states, "graph_arcs": graph_np.num_arcs,
                    "beam": "inf" if math.isinf(w.beam) else w.beam,
                    "max_states": w.max_states, "max_contexts": w.max_contexts,
-                   "joiner": w.dtype},
+                   "joiner": w.dtype, "schedule": schedule},
         "roofline": roofline,
         "kernels": kernels,
         "joiner_mfma_util_pct": 100.0 * j_tflops / peak_j,
         "search_hbm_gbps": s_gbps,
-        "ms_per_step_without_timing_events": ms_step_plain,
+        "ms_per_step_with_kernel_timing_events": ms_step_events,
         "per_frame_latency_us": 1e3 * ms_step / max(int(inputs.lengths.max()), 1),
         "work_per_step": work,
     }

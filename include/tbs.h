@@ -162,6 +162,35 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
                       int32_t *out_arcs, int32_t *trace, void *hip_stream);
 
 /*
+ * How tbs_decode drives the frame loop of Algorithm 1 (all schedules compute
+ * the same search; results agree within the fp32 rounding of the joiner):
+ *   TBS_SCHEDULE_FRAME   two kernels per frame over the whole batch: a joiner
+ *                        GEMM over every active (stream, context) row, then a
+ *                        search kernel with one workgroup per stream;
+ *   TBS_SCHEDULE_STREAM  one persistent kernel, one workgroup per stream, that
+ *                        runs joiner, log-softmax and search for every frame of
+ *                        its stream on one compute unit (no per-frame launch or
+ *                        global round trip).  Needs max_contexts (after
+ *                        clamping to max_states) <= 16, vocab_size <= 1024,
+ *                        for the trivial graph max_states <= 16, and one
+ *                        stream's joiner input and logit rows in LDS beside
+ *                        the search state: tbs_decode returns
+ *                        TBS_EUNSUPPORTED for shapes outside that;
+ *   TBS_SCHEDULE_AUTO    (default) STREAM when it fits, the joiner weight
+ *                        (V x dim) is at most 4 MiB and the joiner is bf16 or
+ *                        max_contexts <= 4; else FRAME.
+ * The setting is per model and applies to later tbs_decode calls; an unknown
+ * value returns TBS_EINVAL.
+ */
+typedef enum {
+  TBS_SCHEDULE_AUTO = 0,
+  TBS_SCHEDULE_FRAME = 1,
+  TBS_SCHEDULE_STREAM = 2
+} tbs_schedule;
+
+tbs_status tbs_model_set_schedule(tbs_model *model, int32_t schedule);
+
+/*
  * Decoder + joiner + log-softmax alone (Algorithm 1: Decoder, IndexSelect,
  * joiner), for R (encoder row, context) pairs:
  *   enc_rows  DEVICE float [R][C];  ctx DEVICE int32 [R], each a * V + b with
@@ -175,7 +204,8 @@ tbs_status tbs_joiner_logp(const tbs_model *model, const float *enc_rows, const 
 /*
  * Per-kernel timing, for benchmarks.  While enabled on a model, every decode
  * records a pair of HIP events around each kernel launch on its stream
- * (joiner and search once per frame, final once per decode) and keeps them
+ * (joiner and search once per frame, or the per-stream kernel once; final once
+ * per decode) and keeps them
  * pending.  tbs_model_read_profile waits for those events, adds their elapsed
  * times into out[TBS_KERNEL_COUNT] (indexed by tbs_kernel_id; launches and
  * milliseconds since the last enable) and releases them.  Enabling resets the
@@ -186,7 +216,8 @@ typedef enum {
   TBS_KERNEL_JOINER = 0,
   TBS_KERNEL_SEARCH = 1,
   TBS_KERNEL_FINAL = 2,
-  TBS_KERNEL_COUNT = 3
+  TBS_KERNEL_STREAM = 3, /* the persistent per-stream kernel (TBS_SCHEDULE_STREAM) */
+  TBS_KERNEL_COUNT = 4
 } tbs_kernel_id;
 
 typedef struct {

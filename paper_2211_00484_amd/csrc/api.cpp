@@ -103,7 +103,9 @@ struct tbs_model {
   float* P1 = nullptr;
   float* Wf = nullptr;
   uint16_t* Wb = nullptr;
+  void* Wi = nullptr;
   float* bias = nullptr;
+  int schedule = TBS_SCHEDULE_AUTO;
   std::mutex mu;
   Workspace ws;
   // per-kernel timing (tbs_model_set_profiling)
@@ -135,6 +137,7 @@ ModelDev model_dev(const tbs_model* m) {
   d.P1 = m->P1;
   d.Wf = m->Wf;
   d.Wb = m->Wb;
+  d.Wi = m->Wi;
   d.bias = m->bias;
   return d;
 }
@@ -373,10 +376,11 @@ tbs_status tbs_model_create(int32_t vocab_size, int32_t dim, int32_t context_siz
   if (e == hipSuccess) e = dalloc(&m->P0, VK);
   if (e == hipSuccess) e = dalloc(&m->P1, VK);
   if (e == hipSuccess) e = m->bf16 ? dalloc(&m->Wb, VpK) : dalloc(&m->Wf, VpK);
+  if (e == hipSuccess) e = dalloc((char**)&m->Wi, VpK * (m->bf16 ? 2 : 4));
   if (e == hipSuccess) e = dalloc(&m->bias, (size_t)m->V);
   if (e == hipSuccess)
     e = launch_model_setup(embed, conv, w_out, b_out, m->V, m->C, m->Kpad, m->Vpad, m->bf16,
-                           m->P0, m->P1, m->Wf, m->Wb, m->bias, st);
+                           m->P0, m->P1, m->Wf, m->Wb, m->Wi, m->bias, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) {
     tbs_model_destroy(m);
@@ -399,6 +403,7 @@ void tbs_model_destroy(tbs_model* m) {
   hipFree(m->P1);
   hipFree(m->Wf);
   hipFree(m->Wb);
+  hipFree(m->Wi);
   hipFree(m->bias);
   hipFree(m->rows_h);
   hipFree(m->rows_logits);
@@ -449,6 +454,22 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   tbs_model* m = const_cast<tbs_model*>(model);
   std::lock_guard<std::mutex> lk(m->mu);
   hipStream_t st = (hipStream_t)hip_stream;
+  const ModelDev md = model_dev(m);
+  const StreamPlan splan = plan_stream(md, Nc, KT, graph->trivial);
+  bool per_stream = false;
+  if (m->schedule == TBS_SCHEDULE_STREAM) {
+    if (!splan.ok)
+      return fail(TBS_EUNSUPPORTED,
+                  "tbs_decode: the per-stream schedule does not fit max_contexts %d / "
+                  "max_states %d with V %d and dim %d",
+                  Nc, Ns, m->V, m->C);
+    per_stream = true;
+  } else if (m->schedule == TBS_SCHEDULE_AUTO) {
+    // One compute unit streams the whole joiner weight every frame: worth it while
+    // W stays L2-resident and the fp32 rows (broadcast from LDS to VALU FMAs) are few.
+    per_stream = splan.ok && (size_t)m->Vpad * m->Kpad * (m->bf16 ? 2 : 4) <= (4u << 20) &&
+                 (m->bf16 || Nc <= 4);
+  }
   tbs_status s = ensure_workspace(m, B, T, Ns, Nc, KT, KT == 0);
   if (s != TBS_OK) return s;
   Workspace& w = m->ws;
@@ -485,14 +506,17 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   d.hist_pl = w.hist_pl;
   d.hist_arc = w.hist_arc;
   d.path_lab = w.path_lab;
-  const ModelDev md = model_dev(m);
   const GraphDev gd = graph_dev(graph);
   const JoinerPlan plan = plan_joiner(B * Nc, m->Vpad, m->Kpad, m->bf16);
 
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
-  for (int t = 0; t < maxlen; ++t) {
+  if (per_stream && maxlen > 0)
+    HIP_TRY(timed_launch(m, TBS_KERNEL_STREAM, st,
+                         [&] { return launch_stream(md, gd, d, beam, trace, splan, st); }),
+            "launch(stream)");
+  for (int t = 0; !per_stream && t < maxlen; ++t) {
     HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
                          [&] { return launch_joiner_frame(md, d, plan, t, st); }),
             "launch(joiner)");
@@ -540,6 +564,16 @@ tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const 
   HIP_TRY(launch_joiner_rows(model_dev(m), enc_rows, ctx, R, m->rows_h, m->rows_logits,
                              m->rows_stats, out_logp, st),
           "launch(joiner_rows)");
+  return TBS_OK;
+}
+
+tbs_status tbs_model_set_schedule(tbs_model* model, int32_t schedule) {
+  if (!model) return fail(TBS_EINVAL, "tbs_model_set_schedule: model is NULL");
+  if (schedule != TBS_SCHEDULE_AUTO && schedule != TBS_SCHEDULE_FRAME &&
+      schedule != TBS_SCHEDULE_STREAM)
+    return fail(TBS_EINVAL, "tbs_model_set_schedule: unknown schedule %d", schedule);
+  std::lock_guard<std::mutex> lk(model->mu);
+  model->schedule = schedule;
   return TBS_OK;
 }
 

@@ -13,12 +13,15 @@ constexpr int kJoinerBN = 64;        // joiner vocabulary columns per tile (4 wa
 constexpr int kKStep = 512;          // K padding granule of the packed weights and h rows (one
                                      // register-resident W chunk; keeps the MFMA loop branch-free)
 constexpr int kSearchThreads = 256;
-constexpr int kChunk = 2048;         // candidates merged per LDS pass (hash path)
-constexpr int kHashSlots = 4096;     // LDS open-addressing table (load <= 0.57)
+constexpr int kChunk = 1024;         // candidates merged per LDS pass (hash path)
+constexpr int kHashBits = 11;
+constexpr int kHashSlots = 1 << kHashBits;  // LDS open-addressing table (load <= 0.63)
 constexpr int kSmallCands = 256;     // candidate sets up to this size are ranked directly
 constexpr int kMaxTopK = 16;         // trivial-graph fast path: max_states limit
-constexpr int kStatStage = 8192;     // softmax partials staged in LDS per stream
-constexpr int kTopkStage = 4608;     // trivial-graph per-tile label lists staged in LDS
+constexpr int kStatStage = kHashSlots;  // softmax partials staged in LDS (in hk) per stream (frame kernels)
+constexpr int kTopkStage = 2 * (kChunk + kMaxStates);  // trivial-graph label lists staged in LDS (in uk)
+constexpr size_t kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
+constexpr int kStreamMaxV = 1024;    // per-stream kernel: vocabulary limit (logit rows in registers)
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -30,6 +33,8 @@ struct ModelDev {
   const float* P1;          // [V][Kpad] conv tap 1 * embedding (newer label)
   const float* Wf;          // [Vpad][Kpad] fp32 joiner weight (fp32 mode)
   const uint16_t* Wb;       // [Vpad][Kpad] bf16 joiner weight (bf16 mode)
+  const void* Wi;           // [Kpad/KQ][Vpad][KQ] W interleaved by 16-byte k slices (KQ = 4 fp32
+                            // or 8 bf16), read by the per-stream kernel
   const float* bias;        // [V]
 };
 
@@ -77,10 +82,23 @@ struct JoinerPlan {
 
 JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16);
 
+// Per-stream kernel (one workgroup runs every frame of one stream).
+struct StreamPlan {
+  int ok;                   // the shape fits (contexts, LDS)
+  int RG;                   // groups of 4 context rows (1 to 4)
+  int hoff, hstride;        // LDS offset of the joiner rows and their stride (elements)
+  int zoff;                 // LDS offset of the logit rows [4 RG][Vpad] fp32
+  size_t lds;               // dynamic LDS bytes
+};
+
+StreamPlan plan_stream(const ModelDev& m, int Nc, int KT, int trivial);
+hipError_t launch_stream(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                         int* trace, const StreamPlan& p, hipStream_t st);
+
 hipError_t launch_model_setup(const float* embed, const float* conv, const float* w_out,
                               const float* b_out, int V, int C, int Kpad, int Vpad, int bf16,
-                              float* P0, float* P1, float* Wf, uint16_t* Wb, float* bias,
-                              hipStream_t st);
+                              float* P0, float* P1, float* Wf, uint16_t* Wb, void* Wi,
+                              float* bias, hipStream_t st);
 hipError_t launch_fill_i32(int* p, long long n, int v, hipStream_t st);
 hipError_t launch_init(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,
                        hipStream_t st);

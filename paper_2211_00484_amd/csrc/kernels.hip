@@ -123,13 +123,17 @@ __device__ __forceinline__ float logp_of(float z, double lse) { return (float)((
 
 // ---------------------------------------------------------------------------
 // model setup: P0 = tap0 * E, P1 = tap1 * E (padded to Kpad), W packed to
-// [Vpad][Kpad] in fp32 or bf16, bias copied (zeros if absent).
+// [Vpad][Kpad] in fp32 or bf16, bias copied (zeros if absent).  Wi holds W once
+// more, interleaved as [Kpad / KQ][Vpad][KQ] (KQ = 16 bytes of elements: 4 fp32
+// or 8 bf16), so that 64 lanes loading 16 bytes each for 64 consecutive
+// vocabulary columns read one contiguous kilobyte (per-stream kernel).
 
 __global__ void k_model_setup(const float* __restrict__ E, const float* __restrict__ conv,
                               const float* __restrict__ W, const float* __restrict__ b_out, int V,
                               int C, int Kpad, int Vpad, int bf16, float* __restrict__ P0,
                               float* __restrict__ P1, float* __restrict__ Wf,
-                              uint16_t* __restrict__ Wb, float* __restrict__ bias) {
+                              uint16_t* __restrict__ Wb, void* __restrict__ Wi,
+                              float* __restrict__ bias) {
   const long long n = (long long)Vpad * Kpad;
   for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
        i += (long long)gridDim.x * blockDim.x) {
@@ -141,10 +145,14 @@ __global__ void k_model_setup(const float* __restrict__ E, const float* __restri
       P0[i] = in ? conv[2 * k + 0] * e : 0.f;
       P1[i] = in ? conv[2 * k + 1] * e : 0.f;
     }
-    if (bf16)
-      Wb[i] = f32_to_bf16_rne(w);
-    else
+    if (bf16) {
+      const uint16_t wb = f32_to_bf16_rne(w);
+      Wb[i] = wb;
+      reinterpret_cast<uint16_t*>(Wi)[((size_t)(k >> 3) * Vpad + v) * 8 + (k & 7)] = wb;
+    } else {
       Wf[i] = w;
+      reinterpret_cast<float*>(Wi)[((size_t)(k >> 2) * Vpad + v) * 4 + (k & 3)] = w;
+    }
     if (k == 0 && v < V) bias[v] = b_out ? b_out[v] : 0.f;
   }
 }
@@ -167,14 +175,15 @@ __device__ __forceinline__ float tanh_fast(float x) {
 
 // Joiner input rows (Algorithm 1: decoder, IndexSelect of the encoder frame):
 // h[k] = tanh(enc[k] + ReLU(P0[a][k] + P1[b][k])) for k < C, 0 for C <= k < Kpad,
-// stored as fp32 or bf16 (RNE).  Row r reads P0/P1 at rowoff[r] = (a * Kpad, b * Kpad)
-// and the encoder row enc_rows + r * enc_stride (enc_stride = 0: one shared frame).
+// stored as fp32 or bf16 (RNE) at hbase + r * hstride elements (global memory or
+// LDS).  Row r reads P0/P1 at rowoff[r] = (a * Kpad, b * Kpad) and the encoder
+// row enc_rows + r * enc_stride (enc_stride = 0: one shared frame).
 // Thread tid owns columns tid, tid + NT, ... of every row (Kpad is a multiple of
 // 512); a batch's loads are all issued before any tanh.
 template <int NT>
 __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_rows,
                              long long enc_stride, const int2* rowoff, int nrows,
-                             void* __restrict__ hbase, int tid) {
+                             void* __restrict__ hbase, int hstride, int tid) {
   constexpr int U = 16;  // (row, column) elements per thread per batch
   const int C = m.C, Kpad = m.Kpad;
   const float* __restrict__ P0 = m.P0;
@@ -208,7 +217,7 @@ __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_ro
       if (ro[u] >= nrows) continue;
       const int k = ko[u];
       const float h = k < C ? tanh_fast(e[u] + fmaxf(p0[u] + p1[u], 0.f)) : 0.f;
-      const size_t o = (size_t)ro[u] * Kpad + k;
+      const size_t o = (size_t)ro[u] * hstride + k;
       if (m.bf16)
         reinterpret_cast<uint16_t*>(hbase)[o] = f32_to_bf16_rne(h);
       else
@@ -229,7 +238,7 @@ __global__ __launch_bounds__(256) void k_h_rows(ModelDev m, const float* __restr
   __syncthreads();
   const size_t esz = m.bf16 ? 2 : 4;
   write_h_rows<256>(m, enc_rows + (size_t)r * m.C, 0, &off, 1,
-                    reinterpret_cast<char*>(h) + (size_t)r * m.Kpad * esz, threadIdx.x);
+                    reinterpret_cast<char*>(h) + (size_t)r * m.Kpad * esz, m.Kpad, threadIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -510,7 +519,7 @@ __global__ __launch_bounds__(256) void k_init(ModelDev m, DecodeDev d, GraphDev 
     const int2 zero_off = make_int2(0, 0);  // context (blank, blank)
     const size_t esz = m.bf16 ? 2 : 4;
     write_h_rows<256>(m, d.enc + (size_t)b * d.T * m.C, 0, &zero_off, 1,
-                      reinterpret_cast<char*>(d.h) + (size_t)b * d.Nc * m.Kpad * esz, tid);
+                      reinterpret_cast<char*>(d.h) + (size_t)b * d.Nc * m.Kpad * esz, m.Kpad, tid);
   }
 }
 
@@ -542,7 +551,7 @@ struct SearchSmem {
 };
 
 __device__ __forceinline__ uint32_t hash_slot(unsigned long long key) {
-  return (uint32_t)((key * 0x9E3779B97F4A7C15ull) >> 52) & (kHashSlots - 1);  // 12 bits
+  return (uint32_t)((key * 0x9E3779B97F4A7C15ull) >> (64 - kHashBits));
 }
 
 __device__ __forceinline__ void hash_insert(SearchSmem& s, unsigned long long key,
@@ -669,36 +678,38 @@ struct CandIdx {
   float q, z;
 };
 
-template <bool TRIV>
-__global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev g, DecodeDev d,
-                                                           float beam, int t,
-                                                           int* __restrict__ trace) {
-  const int b = blockIdx.x;
-  const int L = d.len[b];
-  if (t >= L) return;
-  extern __shared__ __align__(16) unsigned char smem[];
-  SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
+// One frame of the search for stream b (t < L), one workgroup.  FUSED (the
+// per-stream kernel): the survivors are in LDS and so are the frame's logit rows
+// (zl, [row][Vpad], -inf beyond V); the next frame's joiner rows go to LDS (hl,
+// row stride hstride) and the survivors stay in LDS; the global survivor arrays
+// are written at the stream's last frame only.
+template <bool TRIV, bool FUSED>
+__device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& g,
+                                             const DecodeDev& d, float beam, int t, int L, int b,
+                                             int* __restrict__ trace, SearchSmem& s, void* hl,
+                                             int hstride, const float* zl) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V, nvt = d.nvt;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
   const size_t row0 = (size_t)b * Nc;
 
   // ---- loads that do not depend on the survivor count ----
-  if (tid == 0) {
+  if (!FUSED && tid == 0) {
     s.ns = d.nsurv[b];
     s.nc = d.nctx[b];
   }
   float2* stage = reinterpret_cast<float2*>(s.hk);  // softmax partials, [Nc][nvt]
   const bool staged = Nc * nvt <= kStatStage;
-  if (staged)
+  if (!FUSED && staged)
     for (int i = tid; i < Nc * nvt; i += blockDim.x) stage[i] = d.stats[row0 * nvt + i];
-  for (int i = tid; i < Ns; i += blockDim.x) {
-    const size_t o = (size_t)b * Ns + i;
-    s.s_ctx[i] = d.surv_ctx[o];
-    s.s_state[i] = d.surv_state[o];
-    s.s_row[i] = d.surv_row[o];
-    s.s_score[i] = d.surv_score[o];
-  }
+  if (!FUSED)
+    for (int i = tid; i < Ns; i += blockDim.x) {
+      const size_t o = (size_t)b * Ns + i;
+      s.s_ctx[i] = d.surv_ctx[o];
+      s.s_state[i] = d.surv_state[o];
+      s.s_row[i] = d.surv_row[o];
+      s.s_score[i] = d.surv_score[o];
+    }
   if (t + 1 < L) {
     const float* er = d.enc + ((size_t)b * d.T + t + 1) * m.C;
     for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
@@ -708,7 +719,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
   float* tz = reinterpret_cast<float*>(s.uk);
   int* tc = reinterpret_cast<int*>(s.uv);
   const bool tstaged = TRIV && Nc * E <= kTopkStage;
-  if (TRIV) {
+  if (TRIV && !FUSED) {
     if (tstaged)
       for (int i = tid; i < Nc * E; i += blockDim.x) {
         tz[i] = d.tk_z[row0 * E + i];
@@ -719,7 +730,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
   __syncthreads();
   const int ns = s.ns, nc = s.nc;
   // log-softmax normaliser of each context row: one wave per row
-  for (int j = wave; j < nc; j += 4) {
+  for (int j = wave; !FUSED && j < nc; j += 4) {
     float M = -INFINITY;
     for (int i = lane; i < nvt; i += 64)
       M = fmaxf(M, staged ? stage[j * nvt + i].x : d.stats[(row0 + j) * nvt + i].x);
@@ -732,6 +743,51 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     S = wave_sum_f(S);
     if (lane == 0) s.s_lse[j] = lse_of(M, S);
   }
+  if (FUSED) {
+    // straight from the logit rows: normaliser, and for the trivial graph the blank
+    // logit and the row's best KT labels (labels are unique within a row, so round q
+    // takes the largest key below round q-1's); one wave per row, each lane holding
+    // its columns lane, lane + 64, ... in registers (at most kStreamMaxV / 64)
+    const int Vpad = m.Vpad, KT = d.KT;
+    constexpr int NPL = kStreamMaxV / 64;
+    for (int j = wave; j < nc; j += 4) {
+      const float* zr = zl + (size_t)j * Vpad;
+      float zv[NPL];
+#pragma unroll
+      for (int i = 0; i < NPL; ++i) zv[i] = 64 * i + lane < Vpad ? zr[64 * i + lane] : -INFINITY;
+      float M = zv[0];
+#pragma unroll
+      for (int i = 1; i < NPL; ++i) M = fmaxf(M, zv[i]);
+      M = wave_max_f(M);
+      float S = 0.f;
+#pragma unroll
+      for (int i = 0; i < NPL; ++i) S += expf(zv[i] - M);
+      S = wave_sum_f(S);
+      if (lane == 0) s.s_lse[j] = lse_of(M, S);
+      if (TRIV) {
+        unsigned long long kv[NPL];
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) {
+          const int c = 64 * i + lane;
+          kv[i] = (c >= 1 && c < V) ? ((unsigned long long)f2ord(zv[i]) << 32) | (0xffffffffu - (unsigned)c)
+                                    : 0ull;
+        }
+        unsigned long long prev = ~0ull;
+        for (int q = 0; q < KT; ++q) {
+          unsigned long long mine = 0ull;
+#pragma unroll
+          for (int i = 0; i < NPL; ++i) mine = (kv[i] < prev && kv[i] > mine) ? kv[i] : mine;
+          const unsigned long long best = wave_max_u64(mine);
+          if (lane == 0) {
+            s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
+            s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+          }
+          prev = best ? best : 1ull;
+        }
+        if (lane == 0) s.s_z0[j] = zv[0];
+      }
+    }
+  }
   if (TRIV) {
     for (int i = tid; i < ns; i += blockDim.x) {
       s.s_bprev[i] = s.s_ctx[i] % V;
@@ -740,7 +796,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     // each row's best KT labels over all tiles (labels are unique within a row, so
     // round q takes the largest key below round q-1's)
     const int KT = d.KT;
-    for (int j = wave; j < nc; j += 4) {
+    for (int j = wave; !FUSED && j < nc; j += 4) {
       unsigned long long prev = ~0ull;
       for (int q = 0; q < KT; ++q) {
         unsigned long long mine = 0ull;
@@ -809,7 +865,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     i = lo;
     pos = k - s.s_off[i];
   };
-  const float* zbase = d.logits + row0 * (size_t)m.Vpad;
+  const float* zbase = FUSED ? zl : d.logits + row0 * (size_t)m.Vpad;
   // (key, value) of candidate c; key = kEmpty for an empty trivial-graph slot
   auto make_cand = [&](int c) -> ulonglong2 {
     int i, pos;
@@ -1071,10 +1127,16 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
   __syncthreads();
   // global stores: joiner rows of the next frame, survivors, history, trace
   if (t + 1 < L) {
-    const size_t esz = m.bf16 ? 2 : 4;
-    write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC,
-                                 reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz, tid);
+    if (FUSED) {
+      write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC, hl, hstride, tid);
+    } else {
+      const size_t esz = m.bf16 ? 2 : 4;
+      write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC,
+                                   reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz, m.Kpad,
+                                   tid);
+    }
   }
+  const bool store_surv = !FUSED || t + 1 == L;
   if (my_keep2) {
     const unsigned tb = 0xffffffffu - (unsigned)s.lv[tid];
     const int parent = (int)(tb / stride_tb);
@@ -1082,11 +1144,19 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     const int arc = apos < 0 ? -1 : s.s_base[parent] + apos;
     const int label = arc < 0 ? 0 : (TRIV ? arc + 1 : g.label[arc]);
     const size_t o = (size_t)b * Ns + my_pos;
-    d.surv_ctx[o] = (int)my_ci;
-    d.surv_state[o] = (int)my_st;
-    d.surv_score[o] = my_sc - best;
-    d.surv_row[o] = my_crow;
-    if (my_first) d.ctx_list[row0 + my_crow] = (int)my_ci;
+    if (FUSED) {  // every read of the old survivors precedes the last barrier
+      s.s_ctx[my_pos] = (int)my_ci;
+      s.s_state[my_pos] = (int)my_st;
+      s.s_score[my_pos] = my_sc - best;
+      s.s_row[my_pos] = my_crow;
+    }
+    if (store_surv) {
+      d.surv_ctx[o] = (int)my_ci;
+      d.surv_state[o] = (int)my_st;
+      d.surv_score[o] = my_sc - best;
+      d.surv_row[o] = my_crow;
+      if (my_first) d.ctx_list[row0 + my_crow] = (int)my_ci;
+    }
     const size_t hbase = ((size_t)t * d.B + b) * Ns;
     d.hist_pl[hbase + my_pos] = (parent << 16) | label;
     d.hist_arc[hbase + my_pos] = arc;
@@ -1099,9 +1169,220 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
     }
   }
   if (tid == 0) {
-    d.nsurv[b] = s.nK;
-    d.nctx[b] = nC;
+    if (store_surv) {
+      d.nsurv[b] = s.nK;
+      d.nctx[b] = nC;
+    }
+    if (FUSED) {
+      s.ns = s.nK;
+      s.nc = nC;
+    }
     d.offset[b] += (double)best;
+  }
+}
+
+template <bool TRIV>
+__global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev g, DecodeDev d,
+                                                           float beam, int t,
+                                                           int* __restrict__ trace) {
+  const int b = blockIdx.x;
+  const int L = d.len[b];
+  if (t >= L) return;
+  extern __shared__ __align__(16) unsigned char smem[];
+  SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
+  search_frame<TRIV, false>(m, g, d, beam, t, L, b, trace, s, nullptr, 0, nullptr);
+}
+
+// ---------------------------------------------------------------------------
+// per-stream kernel: one workgroup owns one stream for all of its frames
+// (Algorithm 1's frame loop without a launch or a global round trip per frame).
+
+// Joiner of frame t for this stream's context rows (Algorithm 1: joiner; the
+// log-softmax is taken by the search from the rows this writes).  The rows h are
+// in LDS at hl (row stride hstride elements, RG groups of 4 rows; rows >= nc hold
+// stale or zero values whose outputs are never read); the logits go to LDS at zl
+// ([4 RG][Vpad] fp32, -inf beyond V).  Lane l of a wave owns vocabulary column
+// 64 cg + l of two 64-column groups at once, cg = wave + 4 (2p) and wave + 4 (2p + 1),
+// so that each h value read from LDS feeds both.  W is streamed as 16-byte k
+// slices of the interleaved copy (one contiguous kilobyte per wave and load), the
+// next chunk always in flight in ping-pong registers.  fp32: VALU FMAs with h
+// broadcast from LDS (with 4 to 16 rows, VALU outruns the 4x4 MFMA blocks).
+// bf16: v_mfma_f32_4x4x4bf16 computes 16 independent 4x4 blocks, lane l = 4j + c
+// supplying row c of A block j and column c of B block j, so A = h[4g + (l & 3)]
+// and B = W[64 cg + l] leave z[4g + v][64 cg + l] in accumulator element v.
+template <bool BF16, int RG>
+__device__ __forceinline__ void stream_joiner(const ModelDev& m, const DecodeDev& d, const void* hl,
+                                              int hstride, float* zl) {
+  constexpr int KQ = BF16 ? 8 : 4;   // k values per 16-byte slice
+  constexpr int CH = 8;              // slices per lane per column group and chunk
+  constexpr int NR = 4 * RG;         // rows computed
+  constexpr int ESZ = BF16 ? 2 : 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int V = m.V, Vpad = m.Vpad, nvt = d.nvt;
+  const int nch = m.Kpad / (KQ * CH);                  // chunks per column group
+  const int ncgw = (nvt - wave + 3) >> 2;              // column groups of this wave
+  const int steps = ((ncgw + 1) >> 1) * nch;           // pairs of groups x chunks
+  if (steps == 0) return;
+  const uint4* __restrict__ Wi = reinterpret_cast<const uint4*>(m.Wi);
+  const char* hrows = reinterpret_cast<const char*>(hl);
+  const size_t rstride = (size_t)hstride * ESZ;
+
+  // column groups of pair p; the second may not exist (then it repeats the first
+  // and is never written)
+  auto pair_cg = [&](int p, int& c0, int& c1) {
+    c0 = wave + 8 * p;
+    c1 = c0 + 4 < nvt ? c0 + 4 : c0;
+  };
+  auto load_chunk = [&](int step, uint4 (&w)[2][CH], float (&bias)[2]) {
+    const int p = step / nch, ch = step - p * nch;
+    int c0, c1;
+    pair_cg(p, c0, c1);
+    const uint4* s0 = Wi + (size_t)(ch * CH) * Vpad + c0 * 64 + lane;
+    const uint4* s1 = Wi + (size_t)(ch * CH) * Vpad + c1 * 64 + lane;
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      w[0][u] = s0[(size_t)u * Vpad];
+      w[1][u] = s1[(size_t)u * Vpad];
+    }
+    bias[0] = m.bias[min(c0 * 64 + lane, V - 1)];
+    bias[1] = m.bias[min(c1 * 64 + lane, V - 1)];
+  };
+
+  float acc[2][NR];
+  f32x4 macc[2][BF16 ? RG : 1][2];
+  auto reset = [&]() {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int r = 0; r < NR; ++r) acc[c][r] = 0.f;
+#pragma unroll
+      for (int g = 0; g < (BF16 ? RG : 1); ++g) {
+        macc[c][g][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+        macc[c][g][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  };
+  auto epilogue = [&](int c, int cg, float bias) {
+    const int col = cg * 64 + lane;
+    const bool cvalid = col < V;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      float zs;
+      if (BF16) {
+        const int g = r >> 2, v = r & 3;
+        zs = macc[c][g][0][v] + macc[c][g][1][v];
+      } else {
+        zs = acc[c][r];
+      }
+      zl[(size_t)r * Vpad + col] = cvalid ? zs + bias : -INFINITY;
+    }
+  };
+  // step >= steps (the odd tail of the ping-pong) computes on a repeated chunk and
+  // writes nothing
+  auto compute = [&](int step, const uint4 (&w)[2][CH], const float (&bias)[2]) {
+    const int p = step / nch, ch = step - p * nch;
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const size_t ko = (size_t)(ch * CH + u) * 16;  // byte offset of this k slice in a row
+      if (BF16) {
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+        for (int g = 0; g < RG; ++g) {
+          const uint4 a =
+              *reinterpret_cast<const uint4*>(hrows + (size_t)(4 * g + (lane & 3)) * rstride + ko);
+          const s16x4 alo = __builtin_bit_cast(s16x4, make_uint2(a.x, a.y));
+          const s16x4 ahi = __builtin_bit_cast(s16x4, make_uint2(a.z, a.w));
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            macc[c][g][0] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(
+                alo, __builtin_bit_cast(s16x4, make_uint2(w[c][u].x, w[c][u].y)), macc[c][g][0], 0,
+                0, 0);
+            macc[c][g][1] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(
+                ahi, __builtin_bit_cast(s16x4, make_uint2(w[c][u].z, w[c][u].w)), macc[c][g][1], 0,
+                0, 0);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+          const float4 a = *reinterpret_cast<const float4*>(hrows + (size_t)r * rstride + ko);
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            acc[c][r] = fmaf(a.x, __uint_as_float(w[c][u].x), acc[c][r]);
+            acc[c][r] = fmaf(a.y, __uint_as_float(w[c][u].y), acc[c][r]);
+            acc[c][r] = fmaf(a.z, __uint_as_float(w[c][u].z), acc[c][r]);
+            acc[c][r] = fmaf(a.w, __uint_as_float(w[c][u].w), acc[c][r]);
+          }
+        }
+      }
+    }
+    if (ch == nch - 1 && step < steps) {
+      int c0, c1;
+      pair_cg(p, c0, c1);
+      epilogue(0, c0, bias[0]);
+      if (c1 != c0) epilogue(1, c1, bias[1]);
+      reset();
+    }
+  };
+
+  reset();
+  uint4 wa[2][CH], wb[2][CH];
+  float ba[2], bb[2];
+  // Every load is issued unconditionally (clamped to the last chunk), so the wait
+  // before a chunk's first use counts only the loads issued after it.
+  load_chunk(0, wa, ba);
+  for (int step = 0; step < steps; step += 2) {
+    load_chunk(min(step + 1, steps - 1), wb, bb);
+    compute(step, wa, ba);
+    load_chunk(min(step + 2, steps - 1), wa, ba);
+    compute(step + 1, wb, bb);
+  }
+}
+
+template <bool BF16, bool TRIV, int RG>
+__global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev g, DecodeDev d,
+                                                           float beam, int* __restrict__ trace,
+                                                           int hoff, int hstride, int zoff) {
+  const int b = blockIdx.x;
+  const int L = d.len[b];
+  if (L == 0) return;
+  extern __shared__ __align__(16) unsigned char smem[];
+  SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
+  void* hl = smem + hoff;
+  float* zl = reinterpret_cast<float*>(smem + zoff);
+  const int tid = threadIdx.x;
+  const int Ns = d.Ns, Nc = d.Nc, V = m.V;
+  const size_t row0 = (size_t)b * Nc;
+  // state after the initial tuple (written by k_init), encoder frame 0, zeroed rows
+  if (tid == 0) {
+    s.ns = d.nsurv[b];
+    s.nc = d.nctx[b];
+  }
+  for (int i = tid; i < Ns; i += blockDim.x) {
+    const size_t o = (size_t)b * Ns + i;
+    s.s_ctx[i] = d.surv_ctx[o];
+    s.s_state[i] = d.surv_state[o];
+    s.s_row[i] = d.surv_row[o];
+    s.s_score[i] = d.surv_score[o];
+  }
+  for (int j = tid; j < Nc; j += blockDim.x) {
+    const int c = d.ctx_list[row0 + j], a = c / V;
+    s.n_rowoff[j] = make_int2(a * m.Kpad, (c - a * V) * m.Kpad);
+  }
+  {
+    const float* er = d.enc + (size_t)b * d.T * m.C;
+    for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
+    const int words = RG * 4 * hstride * (m.bf16 ? 2 : 4) / 4;
+    for (int i = tid; i < words; i += blockDim.x) reinterpret_cast<int*>(hl)[i] = 0;
+  }
+  __syncthreads();
+  write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, s.nc, hl, hstride, tid);
+  __syncthreads();
+  for (int t = 0; t < L; ++t) {
+    stream_joiner<BF16, RG>(m, d, hl, hstride, zl);
+    __syncthreads();
+    search_frame<TRIV, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, zl);
+    __syncthreads();
   }
 }
 
@@ -1263,10 +1544,10 @@ JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16) {
 
 hipError_t launch_model_setup(const float* embed, const float* conv, const float* w_out,
                               const float* b_out, int V, int C, int Kpad, int Vpad, int bf16,
-                              float* P0, float* P1, float* Wf, uint16_t* Wb, float* bias,
-                              hipStream_t st) {
+                              float* P0, float* P1, float* Wf, uint16_t* Wb, void* Wi,
+                              float* bias, hipStream_t st) {
   hipLaunchKernelGGL(k_model_setup, dim3(grid_for((long long)Vpad * Kpad, 256)), dim3(256), 0, st,
-                     embed, conv, w_out, b_out, V, C, Kpad, Vpad, bf16, P0, P1, Wf, Wb, bias);
+                     embed, conv, w_out, b_out, V, C, Kpad, Vpad, bf16, P0, P1, Wf, Wb, Wi, bias);
   return hipGetLastError();
 }
 
@@ -1328,6 +1609,57 @@ hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const Decod
                        trace);
   }
   return hipGetLastError();
+}
+
+StreamPlan plan_stream(const ModelDev& m, int Nc, int KT, int trivial) {
+  StreamPlan p{};
+  const int esz = m.bf16 ? 2 : 4;
+  const int nvt = m.Vpad / kJoinerBN;
+  p.RG = (Nc + 3) / 4;
+  p.hstride = m.Kpad + 16 / esz;
+  p.hoff = (int)round_up((int)sizeof(SearchSmem), 16);
+  p.zoff = p.hoff + p.RG * 4 * p.hstride * esz;
+  p.lds = (size_t)p.zoff + (size_t)p.RG * 4 * m.Vpad * 4;
+  p.ok = Nc <= 16 && m.Vpad <= kStreamMaxV && p.lds <= kMaxLds && (!trivial || KT > 0);
+  (void)nvt;
+  return p;
+}
+
+template <bool BF16, bool TRIV, int RG>
+hipError_t launch_stream_t(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                           int* trace, const StreamPlan& p, hipStream_t st) {
+  static size_t attr = 0;
+  if (p.lds > attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_stream<BF16, TRIV, RG>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+    if (e != hipSuccess) return e;
+    attr = p.lds;
+  }
+  hipLaunchKernelGGL((k_stream<BF16, TRIV, RG>), dim3(d.B), dim3(kSearchThreads), p.lds, st, m, g,
+                     d, beam, trace, p.hoff, p.hstride, p.zoff);
+  return hipGetLastError();
+}
+
+template <bool BF16, bool TRIV>
+hipError_t launch_stream_rg(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                            int* trace, const StreamPlan& p, hipStream_t st) {
+  switch (p.RG) {
+    case 1: return launch_stream_t<BF16, TRIV, 1>(m, g, d, beam, trace, p, st);
+    case 2: return launch_stream_t<BF16, TRIV, 2>(m, g, d, beam, trace, p, st);
+    case 3: return launch_stream_t<BF16, TRIV, 3>(m, g, d, beam, trace, p, st);
+    default: return launch_stream_t<BF16, TRIV, 4>(m, g, d, beam, trace, p, st);
+  }
+}
+
+hipError_t launch_stream(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                         int* trace, const StreamPlan& p, hipStream_t st) {
+  if (!p.ok) return hipErrorInvalidValue;
+  const bool triv = d.KT > 0;
+  if (m.bf16)
+    return triv ? launch_stream_rg<true, true>(m, g, d, beam, trace, p, st)
+                : launch_stream_rg<true, false>(m, g, d, beam, trace, p, st);
+  return triv ? launch_stream_rg<false, true>(m, g, d, beam, trace, p, st)
+              : launch_stream_rg<false, false>(m, g, d, beam, trace, p, st);
 }
 
 hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, int* out_ntok,

@@ -37,7 +37,8 @@ class KernelTime(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
 
 
-KERNEL_NAMES = ("joiner", "search", "final")
+KERNEL_NAMES = ("joiner", "search", "final", "stream")
+SCHEDULES = {"auto": 0, "frame": 1, "stream": 2}
 
 
 class BeamParams(ctypes.Structure):
@@ -80,6 +81,8 @@ def lib():
     L.tbs_decode.restype = _I32
     L.tbs_decode.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
                              _P, _P, _P, _P, _P, _P, _P]
+    L.tbs_model_set_schedule.restype = _I32
+    L.tbs_model_set_schedule.argtypes = [_P, _I32]
     L.tbs_model_set_profiling.restype = _I32
     L.tbs_model_set_profiling.argtypes = [_P, _I32]
     L.tbs_model_read_profile.restype = _I32
@@ -177,6 +180,10 @@ class Model:
                                       ctypes.byref(h)))
         self._h = h
         self.vocab_size, self.dim, self.dtype = int(vocab_size), int(dim), dtype
+
+    def set_schedule(self, schedule: str):
+        """Frame-loop schedule for later decodes: "auto", "frame" or "stream"."""
+        _check(lib().tbs_model_set_schedule(self._h, SCHEDULES[schedule]))
 
     def set_profiling(self, enable: bool):
         _check(lib().tbs_model_set_profiling(self._h, int(bool(enable))))

@@ -13,11 +13,13 @@ def say(msg: str):
 
 
 def gpu_decode(model_np, graph_np, inputs, beam, Ns, Nc, dtype="fp32", trace=True, arcs=True,
-               model=None, graph=None, repeat=1):
+               model=None, graph=None, repeat=1, schedule="auto"):
+    """Decode on the GPU with the given frame-loop schedule ("auto", "frame", "stream")."""
     import torch
     from paper_2211_00484_amd import tbs
     if model is None:
         model = tbs.Model.from_synth(model_np, dtype=dtype)
+    model.set_schedule(schedule)
     if graph is None:
         graph = tbs.Graph.from_synth(graph_np)
     enc = torch.from_numpy(inputs.encoder_out).cuda()

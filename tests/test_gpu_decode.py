@@ -1,5 +1,10 @@
 """HIP decode (tbs_decode) against the CPU oracle, element by element.
 
+Every case runs under both frame-loop schedules: "frame" (a joiner GEMM kernel and a
+search kernel per frame) and "stream" (one persistent workgroup per stream).  A shape
+the per-stream kernel cannot hold must be refused with TBS_EUNSUPPORTED; such a run is
+reported and skipped.
+
 Parity rule (see parity.py): survivor traces identical up to the first frame with a
 decision margin below MARGIN, and over whole streams where no decision is that close;
 tokens, arcs and status identical on such streams; scores within 1e-4 (fp32 joiner) or
@@ -25,14 +30,25 @@ FP32 = dict(margin=1e-4, score_tol=1e-4)
 BF16 = dict(margin=2e-3, score_tol=2e-2)
 
 
-def _run(name_or_parts, beam, Ns, Nc, dtype="fp32", streams=None, nthreads=0, seed=0, B=None):
+SCHEDULES = ["frame", "stream"]
+
+
+def _run(name_or_parts, beam, Ns, Nc, dtype="fp32", streams=None, nthreads=0, seed=0, B=None,
+         schedule="frame"):
+    from paper_2211_00484_amd import tbs
     if isinstance(name_or_parts, str):
         w, inputs, model, graph = synth.make_workload(name_or_parts, seed=seed, B=B)
     else:
         inputs, model, graph = name_or_parts
     say(f"decode B={inputs.B} T={inputs.T} V={model.vocab_size} C={model.dim} "
-        f"S={graph.num_states} beam={beam} Ns={Ns} Nc={Nc} {dtype}")
-    g = gpu_decode(model, graph, inputs, beam, Ns, Nc, dtype=dtype)
+        f"S={graph.num_states} beam={beam} Ns={Ns} Nc={Nc} {dtype} {schedule}")
+    try:
+        g = gpu_decode(model, graph, inputs, beam, Ns, Nc, dtype=dtype, schedule=schedule)
+    except tbs.TbsError as e:
+        if schedule == "stream" and e.status == -5:
+            say(f"  not supported by the per-stream kernel: {e}")
+            return None, None, None
+        raise
     streams = list(range(inputs.B)) if streams is None else list(streams)
     o = oracle.decode(model, graph, inputs.encoder_out, inputs.lengths, beam, Ns, Nc,
                       bf16=(dtype == "bf16"), nthreads=nthreads, streams=streams)
@@ -45,32 +61,36 @@ def _run(name_or_parts, beam, Ns, Nc, dtype="fp32", streams=None, nthreads=0, se
     return g, o, rep
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_tiny(dtype):
-    _, _, rep = _run("tiny", math.inf, 4, 4, dtype)
+def test_tiny(dtype, schedule):
+    _, _, rep = _run("tiny", math.inf, 4, 4, dtype, schedule=schedule)
     assert rep.streams == 2
 
 
 @pytest.mark.parametrize("beam,Ns,Nc", [(math.inf, 1, 1), (1.0, 3, 2), (0.5, 8, 3), (2.0, 16, 16),
-                                        (0.0, 4, 4)])
-def test_tiny_params(beam, Ns, Nc):
-    _run("tiny", beam, Ns, Nc, seed=3)
+                                        (0.0, 4, 4), (math.inf, 12, 12)])
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_tiny_params(beam, Ns, Nc, schedule):
+    _run("tiny", beam, Ns, Nc, seed=3, schedule=schedule)
 
 
-def test_ragged_and_empty_lengths():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_ragged_and_empty_lengths(schedule):
     rng = np.random.default_rng(9)
     model = synth.make_model(rng, 16, 32, 0.1)
     inputs = synth.make_inputs(rng, 7, 25, 32)
     inputs.lengths[:] = [0, 25, 1, 13, 0, 24, 7]
     for b in range(inputs.B):
         inputs.encoder_out[b, inputs.lengths[b]:] = 0.0
-    g, o, _ = _run((inputs, model, synth.trivial_graph(16)), math.inf, 4, 4)
+    g, o, _ = _run((inputs, model, synth.trivial_graph(16)), math.inf, 4, 4, schedule=schedule)
     for b in (0, 4):
         assert g["ntok"][b] == 0 and g["scores"][b] == 0.0 and (g["tokens"][b] == -1).all()
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("seed", range(12))
-def test_random_small_graphs(seed):
+def test_random_small_graphs(seed, schedule):
     rng = np.random.default_rng(100 + seed)
     V = int(rng.integers(3, 40))
     C = int(rng.integers(1, 70))
@@ -82,17 +102,22 @@ def test_random_small_graphs(seed):
     beam = [math.inf, 3.0, 1.0][seed % 3]
     Ns = int(rng.integers(1, 33))
     Nc = int(rng.integers(1, Ns + 1))
-    _run((inputs, model, graph), beam, Ns, Nc, dtype=["fp32", "bf16"][seed % 4 == 3])
+    _run((inputs, model, graph), beam, Ns, Nc, dtype=["fp32", "bf16"][seed % 4 == 3],
+         schedule=schedule)
 
 
-def test_many_candidate_chunks():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_many_candidate_chunks(schedule):
     # 8 tuples x 2999 arcs: the per-stream candidate set spans many LDS merge passes.
     rng = np.random.default_rng(5)
     V, C = 3000, 48
     model = synth.make_model(rng, V, C, 0.2)
     inputs = synth.make_inputs(rng, 3, 12, C)
-    _run((inputs, model, synth.trivial_graph(V)), math.inf, 8, 8)
-    _run((inputs, model, synth.trivial_graph(V)), 2.0, 8, 3)
+    _run((inputs, model, synth.trivial_graph(V)), math.inf, 8, 8, schedule=schedule)
+    _run((inputs, model, synth.trivial_graph(V)), 2.0, 8, 3, schedule=schedule)
+    # general graph over the same vocabulary: logits are gathered per arc
+    graph = synth.random_small_graph(rng, 20, V, max_degree=400)
+    _run((inputs, model, graph), 3.0, 16, 8, schedule=schedule)
 
 
 def test_heavy_tailed_states():
@@ -108,29 +133,34 @@ def test_heavy_tailed_states():
     _run((inputs, model, g), 6.0, 64, 16)
 
 
-def test_max_states_limit():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_max_states_limit(schedule):
     rng = np.random.default_rng(8)
     V, C = 40, 16
     model = synth.make_model(rng, V, C, 0.5)
     inputs = synth.make_inputs(rng, 2, 15, C)
     graph = synth.random_small_graph(rng, 30, V, max_degree=10)
-    _run((inputs, model, graph), math.inf, 256, 256)
-    _run((inputs, model, graph), math.inf, 256, 7)
+    _run((inputs, model, graph), math.inf, 256, 256, schedule=schedule)
+    _run((inputs, model, graph), math.inf, 256, 7, schedule=schedule)
 
 
-def test_standard():
-    _, _, rep = _run("standard", math.inf, 4, 4)
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_standard(schedule):
+    _, _, rep = _run("standard", math.inf, 4, 4, schedule=schedule)
     assert rep.streams == 32
 
 
-def test_graph():
-    _, _, rep = _run("graph", 4.0, 32, 8)
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_graph(schedule):
+    _, _, rep = _run("graph", 4.0, 32, 8, schedule=schedule)
     assert rep.streams == 32
 
 
-def test_throughput_sampled():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_throughput_sampled(schedule):
     # full B = 256 on the GPU (the configuration the benchmark times), 16 streams checked
-    _run("throughput", math.inf, 4, 4, dtype="bf16", streams=range(0, 256, 16))
+    _run("throughput", math.inf, 4, 4, dtype="bf16", streams=range(0, 256, 16),
+         schedule=schedule)
 
 
 def test_large_sampled():
@@ -138,14 +168,61 @@ def test_large_sampled():
     _run("large", 8.0, 64, 16, streams=[3, 77])
 
 
-def test_deterministic():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_deterministic(schedule):
     w, inputs, model, graph = synth.make_workload("graph")
     from paper_2211_00484_amd import tbs
     m, gr = tbs.Model.from_synth(model), tbs.Graph.from_synth(graph)
-    a = gpu_decode(model, graph, inputs, 4.0, 32, 8, model=m, graph=gr)
-    b = gpu_decode(model, graph, inputs, 4.0, 32, 8, model=m, graph=gr)
+    a = gpu_decode(model, graph, inputs, 4.0, 32, 8, model=m, graph=gr, schedule=schedule)
+    b = gpu_decode(model, graph, inputs, 4.0, 32, 8, model=m, graph=gr, schedule=schedule)
     for k in a:
         assert np.array_equal(a[k], b[k]), k
+
+
+def test_schedules_agree_on_clean_streams():
+    # Both schedules on one model: identical survivor traces up to each stream's first
+    # frame with a decision margin <= 1e-4 (oracle), and identical results on streams
+    # without one.
+    w, inputs, model, graph = synth.make_workload("graph")
+    from paper_2211_00484_amd import tbs
+    m, gr = tbs.Model.from_synth(model), tbs.Graph.from_synth(graph)
+    a = gpu_decode(model, graph, inputs, 4.0, 32, 8, model=m, graph=gr, schedule="frame")
+    b = gpu_decode(model, graph, inputs, 4.0, 32, 8, model=m, graph=gr, schedule="stream")
+    o = oracle.decode(model, graph, inputs.encoder_out, inputs.lengths, 4.0, 32, 8)
+    fm = o.frame_margins
+    compared = 0
+    for s in range(inputs.B):
+        L = int(inputs.lengths[s])
+        bad = [t for t in range(L) if fm[s, t] <= 1e-4]
+        t_star = bad[0] if bad else L
+        assert np.array_equal(a["trace"][: t_star + 1, s], b["trace"][: t_star + 1, s]), s
+        compared += t_star
+        if not bad and fm[s, inputs.T] > 1e-4:
+            assert np.array_equal(a["tokens"][s], b["tokens"][s]), s
+            assert abs(a["scores"][s] - b["scores"][s]) <= 1e-4, s
+    say(f"  {compared} of {int(inputs.lengths.sum())} frames compared")
+    assert compared >= inputs.lengths.sum() // 2
+
+
+def test_stream_schedule_refuses_what_it_cannot_hold():
+    import torch
+    from paper_2211_00484_amd import tbs
+    rng = np.random.default_rng(4)
+    model_np = synth.make_model(rng, 40, 32, 0.3)
+    inputs = synth.make_inputs(rng, 2, 6, 32)
+    graph_np = synth.random_small_graph(rng, 10, 40, max_degree=6)
+    model = tbs.Model.from_synth(model_np)
+    graph = tbs.Graph.from_synth(graph_np)
+    enc = torch.from_numpy(inputs.encoder_out).cuda()
+    model.set_schedule("stream")
+    with pytest.raises(tbs.TbsError, match="EUNSUPPORTED"):   # 32 joiner rows per stream
+        tbs.decode(model, graph, enc, inputs.lengths, max_states=32, max_contexts=32)
+    model.set_schedule("auto")                                # falls back to the frame kernels
+    out = tbs.decode(model, graph, enc, inputs.lengths, max_states=32, max_contexts=32)
+    torch.cuda.synchronize()
+    assert out.num_tokens.cpu().numpy().max() <= 6
+    with pytest.raises(tbs.TbsError, match="EINVAL"):
+        tbs._check(tbs.lib().tbs_model_set_schedule(model._h, 7))
 
 
 def test_zero_batch_and_zero_frames():
