@@ -171,7 +171,7 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
  *                        runs joiner, log-softmax and search for every frame of
  *                        its stream on one compute unit (no per-frame launch or
  *                        global round trip).  Needs max_contexts (after
- *                        clamping to max_states) <= 16, vocab_size <= 1024,
+ *                        clamping to max_states) <= 16, vocab_size <= 512,
  *                        for the trivial graph max_states <= 16, and one
  *                        stream's joiner input and logit rows in LDS beside
  *                        the search state: tbs_decode returns

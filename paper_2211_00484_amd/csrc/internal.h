@@ -21,7 +21,7 @@ constexpr int kMaxTopK = 16;         // trivial-graph fast path: max_states limi
 constexpr int kStatStage = kHashSlots;  // softmax partials staged in LDS (in hk) per stream (frame kernels)
 constexpr int kTopkStage = 2 * (kChunk + kMaxStates);  // trivial-graph label lists staged in LDS (in uk)
 constexpr size_t kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
-constexpr int kStreamMaxV = 1024;    // per-stream kernel: vocabulary limit (logit rows in registers)
+constexpr int kStreamMaxV = 512;     // per-stream kernel: vocabulary limit (8 logits per lane)
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 

@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstddef>
 #include <cstdint>
 
 namespace tbs {
@@ -165,12 +166,13 @@ __global__ void k_fill_i32(int* p, long long n, int v) {
 
 // ---------------------------------------------------------------------------
 // tanh from the hardware exp and reciprocal: (e - 1) / (e + 1), e = exp(2x), with
-// x clamped to [-9, 9] (|tanh(9)| rounds to 1 in fp32).  Absolute error ~1e-7,
-// which moves a joiner logit by at most ~C * max|W| * 1e-7.
+// x clamped to [-9, 9] (|tanh(9)| rounds to 1 in fp32); the quotient takes the
+// hardware reciprocal (1 ulp).  Absolute error ~2e-7, which moves a joiner logit
+// by at most ~C * max|W| * 2e-7.
 __device__ __forceinline__ float tanh_fast(float x) {
   const float xc = fminf(fmaxf(x, -9.f), 9.f);
   const float e = __expf(2.f * xc);
-  return __fdividef(e - 1.f, e + 1.f);
+  return (e - 1.f) * __builtin_amdgcn_rcpf(e + 1.f);
 }
 
 // Joiner input rows (Algorithm 1: decoder, IndexSelect of the encoder frame):
@@ -754,15 +756,25 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       const float* zr = zl + (size_t)j * Vpad;
       float zv[NPL];
 #pragma unroll
-      for (int i = 0; i < NPL; ++i) zv[i] = 64 * i + lane < Vpad ? zr[64 * i + lane] : -INFINITY;
-      float M = zv[0];
+      for (int i = 0; i < NPL; ++i) {
+        const int c = 64 * i + lane;
+        const float z = zr[min(c, Vpad - 1)];
+        zv[i] = c < Vpad ? z : -INFINITY;
+      }
+      float M0 = fmaxf(zv[0], zv[1]), M1 = fmaxf(zv[2], zv[3]);
 #pragma unroll
-      for (int i = 1; i < NPL; ++i) M = fmaxf(M, zv[i]);
-      M = wave_max_f(M);
-      float S = 0.f;
+      for (int i = 4; i < NPL; i += 2) {
+        M0 = fmaxf(M0, zv[i]);
+        M1 = fmaxf(M1, zv[i + 1]);
+      }
+      const float M = wave_max_f(fmaxf(M0, M1));
+      float S0 = 0.f, S1 = 0.f;
 #pragma unroll
-      for (int i = 0; i < NPL; ++i) S += expf(zv[i] - M);
-      S = wave_sum_f(S);
+      for (int i = 0; i < NPL; i += 2) {
+        S0 += __expf(zv[i] - M);
+        S1 += __expf(zv[i + 1] - M);
+      }
+      const float S = wave_sum_f(S0 + S1);
       if (lane == 0) s.s_lse[j] = lse_of(M, S);
       if (TRIV) {
         unsigned long long kv[NPL];
@@ -902,15 +914,58 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
                            ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - tb));
   };
 
-  if (N <= kSmallCands) {
+  // Beam pre-filter.  A candidate scoring below (best candidate - beam) can never
+  // be kept, and dropping it changes neither the max-merge of the others nor their
+  // ranks, so with a finite beam and a candidate set that fits uk/uv, all
+  // candidates are made once, their maximum taken, and only those within the beam
+  // are listed in hk/hv for merging and ranking (the hash path, when they are
+  // still many, skips the others on insertion).
+  int Nsel = N;
+  bool listed = false;
+  unsigned thr_ord = 0u;
+  if (N > kSmallCands && beam < INFINITY && N <= kChunk + kMaxStates) {
+    float lmax = -INFINITY;
+    __syncthreads();  // trivial graph: uk/uv held the staged tile lists until here
+    for (int c = tid; c < N; c += blockDim.x) {
+      const ulonglong2 kv = make_cand(c);
+      s.uk[c] = kv.x;
+      s.uv[c] = kv.y;
+      if (kv.x != kEmpty) lmax = fmaxf(lmax, ord2f((unsigned)(kv.y >> 32)));
+    }
+    lmax = wave_max_f(lmax);
+    if (lane == 0) s.wmax[wave] = lmax;
+    if (tid == 0) s.nU = 0;
+    __syncthreads();
+    const float thr0 = fmaxf(fmaxf(s.wmax[0], s.wmax[1]), fmaxf(s.wmax[2], s.wmax[3])) - beam;
+    thr_ord = f2ord(thr0);
+    for (int c = tid; c < N; c += blockDim.x) {
+      const unsigned long long k = s.uk[c], v = s.uv[c];
+      if (k != kEmpty && (unsigned)(v >> 32) >= thr_ord) {
+        const int p = atomicAdd(&s.nU, 1);
+        s.hk[p] = k;
+        s.hv[p] = v;
+      }
+    }
+    __syncthreads();
+    Nsel = s.nU;
+    listed = true;
+  }
+
+  if (Nsel <= kSmallCands) {
     // small candidate sets: merge and rank directly.  Loops run over a multiple
     // of 8 padded entries without early exits so their LDS reads pipeline.
+    const int N = Nsel;
     const int Np = (N + 7) & ~7;
     unsigned long long myk = kEmpty, myv = 0;
     if (tid < N) {
-      const ulonglong2 kv = make_cand(tid);
-      myk = kv.x;
-      myv = kv.y;
+      if (listed) {
+        myk = s.hk[tid];
+        myv = s.hv[tid];
+      } else {
+        const ulonglong2 kv = make_cand(tid);
+        myk = kv.x;
+        myv = kv.y;
+      }
     }
     __syncthreads();  // trivial graph: uk/uv held the staged tile lists until here
     if (tid < kSmallCands) {
@@ -969,7 +1024,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       }
 #pragma unroll
       for (int u = 0; u < CPT; ++u)
-        if (kv[u].x != kEmpty) hash_insert(s, kv[u].x, kv[u].y);
+        if (kv[u].x != kEmpty && (unsigned)(kv[u].y >> 32) >= thr_ord) hash_insert(s, kv[u].x, kv[u].y);
       __syncthreads();
       for (int i = tid; i < kHashSlots; i += blockDim.x) {
         if (s.hk[i] != kEmpty) {
@@ -1016,7 +1071,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   }
   __syncthreads();
   int my_keep2 = 0, my_pos = 0, my_crow = 0, my_first = 0;
-  if (K <= 64) {
+  if (K <= 16) {
     // One wave, one entry per lane; other lanes' entries are read with readlane
     // (no LDS traffic).  Context score = max over the context's in-beam tuples;
     // its first tuple is the one with the smallest state.
@@ -1059,20 +1114,31 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       }
     }
   } else {
-    // Larger sets: every thread holds one entry and scans the others in LDS.
-    // The loads are unconditional (the asm statement pins them) so they pipeline.
+    // Larger sets: every thread holds one entry and scans the others in LDS.  The
+    // loads are unconditional and issued eight at a time (the asm statements pin
+    // them before any use) so they pipeline.
     float my_cs = -INFINITY;
     my_first = my_keep1;
     if (tid < K) {
       for (int j0 = 0; j0 < Kp; j0 += 8) {
+        uint4 e[8];
+        int f[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const uint4 e = s.fent[j0 + u];
-          const int f = s.fflg[j0 + u];
-          asm volatile("" ::"v"(e.x), "v"(e.y), "v"(e.z), "v"(f));
-          const bool same = (f & 1) && e.x == my_ci;
-          my_cs = same ? fmaxf(my_cs, __uint_as_float(e.z)) : my_cs;
-          my_first &= !(same && e.y < my_st);
+          e[u] = s.fent[j0 + u];
+          f[u] = s.fflg[j0 + u];
+        }
+        asm volatile("" ::"v"(e[0].x), "v"(e[0].y), "v"(e[0].z), "v"(f[0]), "v"(e[1].x), "v"(e[1].y),
+                     "v"(e[1].z), "v"(f[1]), "v"(e[2].x), "v"(e[2].y), "v"(e[2].z), "v"(f[2]),
+                     "v"(e[3].x), "v"(e[3].y), "v"(e[3].z), "v"(f[3]));
+        asm volatile("" ::"v"(e[4].x), "v"(e[4].y), "v"(e[4].z), "v"(f[4]), "v"(e[5].x), "v"(e[5].y),
+                     "v"(e[5].z), "v"(f[5]), "v"(e[6].x), "v"(e[6].y), "v"(e[6].z), "v"(f[6]),
+                     "v"(e[7].x), "v"(e[7].y), "v"(e[7].z), "v"(f[7]));
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const bool same = (f[u] & 1) && e[u].x == my_ci;
+          my_cs = same ? fmaxf(my_cs, __uint_as_float(e[u].z)) : my_cs;
+          my_first &= !(same && e[u].y < my_st);
         }
       }
     }
@@ -1085,13 +1151,21 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     if (my_keep1) {
       int rank = 0;
       for (int j0 = 0; j0 < Kp; j0 += 8) {
+        uint4 e[8];
+        int f[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const uint4 e = s.fent[j0 + u];
-          const int f = s.fflg[j0 + u];
-          asm volatile("" ::"v"(e.x), "v"(e.w), "v"(f));
-          const float csj = __uint_as_float(e.w);
-          rank += ((f >> 1) & 1) && (csj > my_cs || (csj == my_cs && e.x < my_ci));
+          e[u] = s.fent[j0 + u];
+          f[u] = s.fflg[j0 + u];
+        }
+        asm volatile("" ::"v"(e[0].x), "v"(e[0].w), "v"(f[0]), "v"(e[1].x), "v"(e[1].w), "v"(f[1]),
+                     "v"(e[2].x), "v"(e[2].w), "v"(f[2]), "v"(e[3].x), "v"(e[3].w), "v"(f[3]));
+        asm volatile("" ::"v"(e[4].x), "v"(e[4].w), "v"(f[4]), "v"(e[5].x), "v"(e[5].w), "v"(f[5]),
+                     "v"(e[6].x), "v"(e[6].w), "v"(f[6]), "v"(e[7].x), "v"(e[7].w), "v"(f[7]));
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float csj = __uint_as_float(e[u].w);
+          rank += ((f[u] >> 1) & 1) && (csj > my_cs || (csj == my_cs && e[u].x < my_ci));
         }
       }
       my_keep2 = rank < Nc;
@@ -1101,14 +1175,22 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     __syncthreads();
     if (my_keep2) {
       for (int j0 = 0; j0 < Kp; j0 += 8) {
+        uint4 e[8];
+        int f[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const uint4 e = s.fent[j0 + u];
-          const int f = s.fflg[j0 + u];
-          asm volatile("" ::"v"(e.x), "v"(e.y), "v"(f));
-          const bool k2 = (f >> 2) & 1;
-          my_pos += k2 && (e.x < my_ci || (e.x == my_ci && e.y < my_st));
-          my_crow += k2 && ((f >> 1) & 1) && e.x < my_ci;
+          e[u] = s.fent[j0 + u];
+          f[u] = s.fflg[j0 + u];
+        }
+        asm volatile("" ::"v"(e[0].x), "v"(e[0].y), "v"(f[0]), "v"(e[1].x), "v"(e[1].y), "v"(f[1]),
+                     "v"(e[2].x), "v"(e[2].y), "v"(f[2]), "v"(e[3].x), "v"(e[3].y), "v"(f[3]));
+        asm volatile("" ::"v"(e[4].x), "v"(e[4].y), "v"(f[4]), "v"(e[5].x), "v"(e[5].y), "v"(f[5]),
+                     "v"(e[6].x), "v"(e[6].y), "v"(f[6]), "v"(e[7].x), "v"(e[7].y), "v"(f[7]));
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const bool k2 = (f[u] >> 2) & 1;
+          my_pos += k2 && (e[u].x < my_ci || (e[u].x == my_ci && e[u].y < my_st));
+          my_crow += k2 && ((f[u] >> 1) & 1) && e[u].x < my_ci;
         }
       }
       atomicAdd(&s.nK, 1);
