@@ -842,6 +842,95 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     s.nL = 0;
   }
   __syncthreads();
+
+  // What the selection leaves each thread: the kept tuple it places (if any), its
+  // canonical position and context row, and the frame's best score.
+  float best;
+  unsigned my_ci = 0xffffffffu, my_st = 0xffffffffu;
+  float my_sc = -INFINITY;
+  unsigned long long my_v = 0ull;  // score << 32 | ~back-pointer of the placed tuple
+  int my_keep2 = 0, my_pos = 0, my_crow = 0, my_first = 0;
+
+  if (TRIV && ns * (1 + d.KT) <= 64) {
+    // Trivial graph, at most 64 candidates (survivor-major: blank, then the row's
+    // KT best labels): one wave, one candidate per lane, other lanes' values read
+    // with readlane.  The key is the context alone (one graph state), so after
+    // the max-merge every context has one tuple: the context score is the tuple's
+    // score, the max-contexts rank equals the max-states rank among the in-beam
+    // tuples, and a tuple is kept iff it represents its key, ranks below
+    // min(max_states, max_contexts) and lies within the beam of the best.  Its
+    // canonical position is the number of kept contexts below its own.
+    if (wave == 0) {
+      const int KT = d.KT, P = 1 + KT, n = ns * P;
+      unsigned long long myk = kEmpty, myv = 0ull;
+      if (lane < n) {
+        const int i = lane / P, q = lane - i * P - 1;
+        const int row = s.s_row[i];
+        const double lse = s.s_lse[row];
+        if (q < 0) {
+          const float sc = s.s_score[i] + logp_of(s.s_z0[row], lse);
+          myk = ((unsigned long long)(unsigned)s.s_state[i] << 32) | (unsigned)s.s_ctx[i];
+          myv = ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - (unsigned)i * stride_tb);
+        } else {
+          const int lab = s.rk_c[row * KT + q];
+          if (lab >= 0) {
+            const float sc = s.s_score[i] + logp_of(s.rk_z[row * KT + q], lse);
+            myk = (unsigned)(s.s_ctx[i] % V) * (unsigned)V + (unsigned)lab;
+            myv = ((unsigned long long)f2ord(sc) << 32) |
+                  (0xffffffffu - ((unsigned)i * stride_tb + (unsigned)lab));
+          }
+        }
+      }
+      const unsigned klo = (unsigned)myk, khi = (unsigned)(myk >> 32);
+      const unsigned vlo = (unsigned)myv, vhi = (unsigned)(myv >> 32);
+      auto rd64 = [](unsigned lo, unsigned hi, int j) {
+        return ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)hi, j) << 32) |
+               (unsigned)__builtin_amdgcn_readlane((int)lo, j);
+      };
+      // max-merge: a candidate represents its key iff no candidate with that key
+      // has a larger value
+      int rep = myk != kEmpty;
+      for (int j = 0; j < n; ++j) {
+        const unsigned long long kj = rd64(klo, khi, j), vj = rd64(vlo, vhi, j);
+        rep &= !(kj == myk && vj > myv);
+      }
+      // rank among the representatives by (score desc, key asc)
+      int rank = 0;
+      for (int j = 0; j < n; ++j) {
+        const int rj = __builtin_amdgcn_readlane(rep, j);
+        const unsigned soj = (unsigned)__builtin_amdgcn_readlane((int)vhi, j);
+        const unsigned long long kj = rd64(klo, khi, j);
+        rank += rj && (soj > vhi || (soj == vhi && kj < myk));
+      }
+      const float sc = ord2f(vhi);
+      const int keep0 = rep && rank < Ns;
+      const float bst = wave_max_f(keep0 ? sc : -INFINITY);
+      const int keep2 = keep0 && sc >= bst - beam && rank < Nc;
+      int pos = 0;
+      for (int j = 0; j < n; ++j) {
+        const int k2j = __builtin_amdgcn_readlane(keep2, j);
+        const unsigned long long kj = rd64(klo, khi, j);
+        pos += k2j && kj < myk;
+      }
+      const unsigned long long kept = __ballot(keep2);
+      if (keep2) s.n_ctx_list[pos] = (int)klo;
+      if (lane == 0) {
+        s.nK = __popcll(kept);
+        s.nC = __popcll(kept);
+        s.best = bst;
+      }
+      my_keep2 = keep2;
+      my_pos = pos;
+      my_crow = pos;
+      my_first = 1;
+      my_ci = klo;
+      my_st = khi;
+      my_sc = sc;
+      my_v = myv;
+    }
+    __syncthreads();
+    best = s.best;
+  } else {
   // exclusive offsets of each survivor's candidates (block scan over <= 256 entries)
   {
     const int per = TRIV ? d.KT : 0;
@@ -1050,15 +1139,14 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     if (lane == 0) s.wmax[wave] = bmax;
   }
   __syncthreads();
-  const float best = fmaxf(fmaxf(s.wmax[0], s.wmax[1]), fmaxf(s.wmax[2], s.wmax[3]));
+  best = fmaxf(fmaxf(s.wmax[0], s.wmax[1]), fmaxf(s.wmax[2], s.wmax[3]));
   const float thr = best - beam;
-  unsigned my_ci = 0xffffffffu, my_st = 0xffffffffu;
-  float my_sc = -INFINITY;
   int my_keep1 = 0;
   if (tid < K) {
     my_ci = (unsigned)s.lk[tid];
     my_st = (unsigned)(s.lk[tid] >> 32);
     my_sc = ord2f((unsigned)(s.lv[tid] >> 32));
+    my_v = s.lv[tid];
     my_keep1 = my_sc >= thr;
   }
   if (tid < Kp) {
@@ -1070,7 +1158,6 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     s.nC = 0;
   }
   __syncthreads();
-  int my_keep2 = 0, my_pos = 0, my_crow = 0, my_first = 0;
   if (K <= 16) {
     // One wave, one entry per lane; other lanes' entries are read with readlane
     // (no LDS traffic).  Context score = max over the context's in-beam tuples;
@@ -1200,6 +1287,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       }
     }
   }
+  }  // general selection
   __syncthreads();
   const int nC = s.nC;
   if (tid < nC) {
@@ -1220,7 +1308,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   }
   const bool store_surv = !FUSED || t + 1 == L;
   if (my_keep2) {
-    const unsigned tb = 0xffffffffu - (unsigned)s.lv[tid];
+    const unsigned tb = 0xffffffffu - (unsigned)my_v;
     const int parent = (int)(tb / stride_tb);
     const int apos = (int)(tb - (unsigned)parent * stride_tb) - 1;
     const int arc = apos < 0 ? -1 : s.s_base[parent] + apos;
