@@ -92,7 +92,7 @@ def measured_traffic(workload: str, kernel: str):
     for line in open(TRAFFIC_TABLE):
         line = line.strip()
         if line.startswith("kernels.hip sha256[:16]:"):
-            src_hash = line.split(":", 1)[1].strip().strip("`")
+            src_hash = line.rsplit(":", 1)[1].strip().strip("`")
         elif line.startswith("copy factor FETCH_SIZE:"):
             ffetch = float(line.split(":", 1)[1].split()[0])
         elif line.startswith("copy factor WRITE_SIZE:"):
@@ -127,20 +127,27 @@ def copy_calibration(steps: int):
           flush=True)
 
 
-def cpu_baseline(w, inputs, model_np, graph_np):
+def cpu_baseline(w, inputs, model_np, graph_np, min_seconds=10.0, max_passes=100):
+    """The oracle (as it stands) on a bounded sample of the same workload: the sample's
+    streams are decoded repeatedly until about min_seconds of wall time have passed."""
     import oracle
     sample = CPU_SAMPLE_STREAMS[w.name]
     streams = list(range(inputs.B)) if sample is None else list(range(0, inputs.B, inputs.B // sample))[:sample]
     threads = min(os.cpu_count() or 1, len(streams))
     frames = int(inputs.lengths[streams].sum())
+    passes = 0
     t0 = time.perf_counter()
-    oracle.decode(model_np, graph_np, inputs.encoder_out, inputs.lengths, w.beam, w.max_states,
-                  w.max_contexts, bf16=(w.dtype == "bf16"), nthreads=threads, want_trace=False,
-                  want_arcs=False, streams=streams)
-    dt = time.perf_counter() - t0
-    return {"value": frames / dt, "unit": "frames/s", "cores": threads, "kind": "oracle",
-            "sample": f"{len(streams)} of {inputs.B} streams ({frames} frames), fp64 C++ oracle, "
-                      f"{threads} threads, {dt:.1f} s wall"}
+    while True:
+        oracle.decode(model_np, graph_np, inputs.encoder_out, inputs.lengths, w.beam,
+                      w.max_states, w.max_contexts, bf16=(w.dtype == "bf16"), nthreads=threads,
+                      want_trace=False, want_arcs=False, streams=streams)
+        passes += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds or passes >= max_passes:
+            break
+    return {"value": passes * frames / dt, "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(streams)} of {inputs.B} streams ({frames} frames) x {passes} passes, "
+                      f"fp64 C++ oracle, {threads} threads, {dt:.1f} s wall"}
 
 
 def main():
