@@ -127,19 +127,20 @@ def copy_calibration(steps: int):
           flush=True)
 
 
-def cpu_baseline(w, inputs, model_np, graph_np, min_seconds=10.0, max_passes=100):
+def cpu_baseline(w, inputs, model_np, graph_np, dtype, threads=None, min_seconds=10.0,
+                 max_passes=100):
     """The oracle (as it stands) on a bounded sample of the same workload: the sample's
     streams are decoded repeatedly until about min_seconds of wall time have passed."""
     import oracle
     sample = CPU_SAMPLE_STREAMS[w.name]
     streams = list(range(inputs.B)) if sample is None else list(range(0, inputs.B, inputs.B // sample))[:sample]
-    threads = min(os.cpu_count() or 1, len(streams))
+    threads = min(threads or os.cpu_count() or 1, len(streams))
     frames = int(inputs.lengths[streams].sum())
     passes = 0
     t0 = time.perf_counter()
     while True:
         oracle.decode(model_np, graph_np, inputs.encoder_out, inputs.lengths, w.beam,
-                      w.max_states, w.max_contexts, bf16=(w.dtype == "bf16"), nthreads=threads,
+                      w.max_states, w.max_contexts, bf16=(dtype == "bf16"), nthreads=threads,
                       want_trace=False, want_arcs=False, streams=streams)
         passes += 1
         dt = time.perf_counter() - t0
@@ -160,7 +161,11 @@ def main():
     ap.add_argument("--schedule", default="auto", choices=["auto", "frame", "stream"],
                     help="frame loop: per-frame joiner + search kernels, or one persistent "
                          "workgroup per stream (auto picks per shape)")
+    ap.add_argument("--joiner-dtype", choices=["fp32", "bf16"], default=None,
+                    help="override the workload's joiner dtype (e.g. Large in bf16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=None,
+                    help="threads for the oracle baseline (default: all host threads)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of 256 MiB (traffic-counter calibration)")
     args = ap.parse_args()
@@ -180,7 +185,8 @@ def main():
     w, inputs, model_np, graph_np = synth.make_workload(args.workload, seed=0)
     K = args.steps if args.steps is not None else DEFAULT_STEPS[w.name]
     W = args.warmup
-    model = tbs.Model.from_synth(model_np, dtype=w.dtype)
+    dtype = args.joiner_dtype or w.dtype
+    model = tbs.Model.from_synth(model_np, dtype=dtype)
     model.set_schedule(args.schedule)
     graph = tbs.Graph.from_synth(graph_np)
     enc = torch.from_numpy(inputs.encoder_out).cuda()
@@ -231,7 +237,7 @@ def main():
             continue
         kernels[name] = {"launches_per_step": n / K, "avg_us": 1e3 * ms / max(n, 1),
                          "ms_per_step": ms / K}
-    peak_j = PEAK["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+    peak_j = PEAK["bf16_mfma_tflops"] if dtype == "bf16" else PEAK["fp32_mfma_tflops"]
     if "stream" in kernels:
         # one persistent kernel runs joiner and search for every frame: its joiner FLOP
         # and search bytes are both divided by the whole kernel's duration
@@ -271,7 +277,7 @@ def main():
             roofline = {"kernel": "k_search", "bound": "hbm", "achieved": s_gbps,
                         "peak": PEAK["hbm_gbps"], "unit": "GB/s",
                         "frac": s_gbps / PEAK["hbm_gbps"]}
-    tr = measured_traffic(w.name, roofline["kernel"])
+    tr = measured_traffic(w.name if dtype == w.dtype else f"{w.name}-{dtype}", roofline["kernel"])
     roofline["traffic"] = None if tr is None else tr["bytes_per_launch"]
     if tr is not None:
         roofline["traffic_detail"] = tr
@@ -279,14 +285,14 @@ def main():
     line = {
         "metric": METRIC, "value": value, "unit": "frames/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32" if w.dtype == "fp32" else "bf16 joiner operands, f32 accumulate/scores",
+        "dtype": "f32" if dtype == "fp32" else "bf16 joiner operands, f32 accumulate/scores",
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "B": B, "T_max": T,
                    "frames": frames, "C": w.C, "V": w.V, "graph": w.graph,
                    "graph_states": graph_np.num_states, "graph_arcs": graph_np.num_arcs,
                    "beam": "inf" if math.isinf(w.beam) else w.beam,
                    "max_states": w.max_states, "max_contexts": w.max_contexts,
-                   "joiner": w.dtype, "schedule": schedule},
+                   "joiner": dtype, "schedule": schedule},
         "roofline": roofline,
         "kernels": kernels,
         "joiner_mfma_util_pct": 100.0 * j_tflops / peak_j,
@@ -296,7 +302,8 @@ def main():
         "work_per_step": work,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, inputs, model_np, graph_np)
+        line["cpu_baseline"] = cpu_baseline(w, inputs, model_np, graph_np, dtype,
+                                            threads=args.cpu_threads)
     print(json.dumps(line), flush=True)
 
 
