@@ -158,7 +158,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="standard",
                     choices=["tiny", "standard", "graph", "throughput", "large"])
-    ap.add_argument("--schedule", default="auto", choices=["auto", "frame", "stream"],
+    ap.add_argument("--schedule", default="auto", choices=["auto", "frame", "stream", "stream1"],
                     help="frame loop: per-frame joiner + search kernels, or one persistent "
                          "workgroup per stream (auto picks per shape)")
     ap.add_argument("--joiner-dtype", choices=["fp32", "bf16"], default=None,
@@ -238,22 +238,23 @@ def main():
         kernels[name] = {"launches_per_step": n / K, "avg_us": 1e3 * ms / max(n, 1),
                          "ms_per_step": ms / K}
     peak_j = PEAK["bf16_mfma_tflops"] if dtype == "bf16" else PEAK["fp32_mfma_tflops"]
-    if "stream" in kernels:
+    sk = "stream_group" if "stream_group" in kernels else "stream"
+    if sk in kernels:
         # one persistent kernel runs joiner and search for every frame: its joiner FLOP
         # and search bytes are both divided by the whole kernel's duration
-        schedule = "stream"
-        st_avg_s = kernels["stream"]["avg_us"] * 1e-6
-        launches = max(kernels["stream"]["launches_per_step"], 1)
+        schedule = sk
+        st_avg_s = kernels[sk]["avg_us"] * 1e-6
+        launches = max(kernels[sk]["launches_per_step"], 1)
         flop_per_launch = work["flop"] / launches
         bytes_per_launch = work["search_bytes"] / launches
         j_tflops = flop_per_launch / st_avg_s / 1e12
         s_gbps = bytes_per_launch / st_avg_s / 1e9
-        kernels["stream"].update({"algorithmic_flop_per_launch": flop_per_launch,
+        kernels[sk].update({"algorithmic_flop_per_launch": flop_per_launch,
                                   "tflops": j_tflops, "peak_tflops": peak_j,
                                   "frac": j_tflops / peak_j,
                                   "algorithmic_search_bytes_per_launch": bytes_per_launch,
                                   "search_gbps": s_gbps})
-        roofline = {"kernel": "k_stream", "bound": "mfma", "achieved": j_tflops, "peak": peak_j,
+        roofline = {"kernel": "k_" + sk, "bound": "mfma", "achieved": j_tflops, "peak": peak_j,
                     "unit": "TFLOP/s", "frac": j_tflops / peak_j}
     else:
         schedule = "frame"

@@ -137,7 +137,8 @@ typedef struct {
  *                  weight included.
  *   out_status     DEVICE int32 [B] or NULL: 0 = the path ends in a final state;
  *                  1 = no surviving tuple was final and the best non-final one
- *                  was used (its score then has no final weight).
+ *                  was used (its score then has no final weight); 2 = see
+ *                  TBS_SCHEDULE_STREAM (device exchange timed out).
  *   out_arcs       DEVICE int32 [B][T] or NULL: per frame, the graph arc id taken
  *                  by the best path, -1 for blank, -2 for frames >= lengths[b].
  *   trace          DEVICE int32 [T+1][B][max_states][4] or NULL: for frame index
@@ -167,7 +168,8 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
  *   TBS_SCHEDULE_FRAME   two kernels per frame over the whole batch: a joiner
  *                        GEMM over every active (stream, context) row, then a
  *                        search kernel with one workgroup per stream;
- *   TBS_SCHEDULE_STREAM  one persistent kernel, one workgroup per stream, that
+ *   TBS_SCHEDULE_STREAM_SINGLE
+ *                        one persistent kernel, one workgroup per stream, that
  *                        runs joiner, log-softmax and search for every frame of
  *                        its stream on one compute unit (no per-frame launch or
  *                        global round trip).  Needs max_contexts (after
@@ -176,6 +178,16 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
  *                        stream's joiner input and logit rows in LDS beside
  *                        the search state: tbs_decode returns
  *                        TBS_EUNSUPPORTED for shapes outside that;
+ *   TBS_SCHEDULE_STREAM  as STREAM_SINGLE, except that for the trivial graph
+ *                        with an fp32 joiner, when B x G workgroups fit the
+ *                        device at once (G = 8, 4 or 2, each with 64 or 128
+ *                        vocabulary columns), G workgroups share each stream:
+ *                        each computes its columns of the joiner, they exchange
+ *                        per-row normaliser terms and best labels every frame
+ *                        through tagged words in uncached device memory
+ *                        (cooperative launch), and all run the same search.
+ *                        out_status[b] = 2 reports an exchange wait that timed
+ *                        out (results of that decode are then not valid);
  *   TBS_SCHEDULE_AUTO    (default) STREAM when it fits, the joiner weight
  *                        (V x dim) is at most 4 MiB and the joiner is bf16 or
  *                        max_contexts <= 4; else FRAME.
@@ -185,7 +197,8 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
 typedef enum {
   TBS_SCHEDULE_AUTO = 0,
   TBS_SCHEDULE_FRAME = 1,
-  TBS_SCHEDULE_STREAM = 2
+  TBS_SCHEDULE_STREAM = 2,
+  TBS_SCHEDULE_STREAM_SINGLE = 3
 } tbs_schedule;
 
 tbs_status tbs_model_set_schedule(tbs_model *model, int32_t schedule);
@@ -216,8 +229,9 @@ typedef enum {
   TBS_KERNEL_JOINER = 0,
   TBS_KERNEL_SEARCH = 1,
   TBS_KERNEL_FINAL = 2,
-  TBS_KERNEL_STREAM = 3, /* the persistent per-stream kernel (TBS_SCHEDULE_STREAM) */
-  TBS_KERNEL_COUNT = 4
+  TBS_KERNEL_STREAM = 3, /* the persistent kernel, one workgroup per stream */
+  TBS_KERNEL_STREAM_GROUP = 4, /* the persistent kernel, several workgroups per stream */
+  TBS_KERNEL_COUNT = 5
 } tbs_kernel_id;
 
 typedef struct {

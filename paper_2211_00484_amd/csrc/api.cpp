@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -97,8 +98,27 @@ struct tbs_graph {
   float* fin = nullptr;
 };
 
+// Exchange buffers of the grouped per-stream kernel: uncached device memory, which
+// must not be freed once a kernel has read it, so a destroyed model returns its
+// buffer to a per-process free list for later models instead.  Words carry a
+// 16-bit decode epoch; when the process-wide epoch wraps, a buffer is cleared
+// before its next use.
+struct XBuf {
+  int dev = -1;
+  unsigned long long* p = nullptr;
+  size_t words = 0;
+  unsigned wrap = 0;  // epoch wrap count at the last clear
+};
+std::mutex g_xmu;
+std::vector<XBuf> g_xfree;
+std::atomic<unsigned> g_epoch{0};
+std::atomic<unsigned> g_wrap{0};
+
 struct tbs_model {
   int V = 0, C = 0, Kpad = 0, Vpad = 0, bf16 = 0;
+  int dev = 0, ncu = 0, coop = 0;   // device, compute units, cooperative launch support
+  XBuf xbuf;
+  unsigned* xerr = nullptr;         // exchange timeouts (device counter)
   float* P0 = nullptr;
   float* P1 = nullptr;
   float* Wf = nullptr;
@@ -264,6 +284,59 @@ tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc, int KT,
   return TBS_OK;
 }
 
+// The model's exchange buffer with at least `words` words, cleared if the epoch has
+// wrapped since its last clear (on st, before the decode that uses it).
+hipError_t ensure_xbuf(tbs_model* m, size_t words, hipStream_t st) {
+  if (m->xbuf.p && m->xbuf.words < words) {
+    std::lock_guard<std::mutex> xl(g_xmu);
+    g_xfree.push_back(m->xbuf);
+    m->xbuf = XBuf();
+  }
+  if (!m->xbuf.p) {
+    std::lock_guard<std::mutex> xl(g_xmu);
+    for (size_t i = 0; i < g_xfree.size(); ++i)
+      if (g_xfree[i].dev == m->dev && g_xfree[i].words >= words) {
+        m->xbuf = g_xfree[i];
+        g_xfree.erase(g_xfree.begin() + (long)i);
+        break;
+      }
+  }
+  if (!m->xbuf.p) {
+    XBuf x;
+    x.dev = m->dev;
+    x.words = words;
+    hipError_t e = hipExtMallocWithFlags((void**)&x.p, words * 8, hipDeviceMallocUncached);
+    if (e != hipSuccess) return e;
+    x.wrap = ~0u;  // cleared below
+    m->xbuf = x;
+  }
+  const unsigned wrap = g_wrap.load();
+  if (m->xbuf.wrap != wrap) {
+    hipError_t e = launch_fill_i32((int*)m->xbuf.p, (long long)m->xbuf.words * 2, 0, st);
+    if (e != hipSuccess) return e;
+    m->xbuf.wrap = wrap;
+  }
+  return hipSuccess;
+}
+
+// Next 16-bit decode epoch (never 0, so zeroed words never match a tag).
+unsigned next_epoch() {
+  for (;;) {
+    const unsigned e = (g_epoch.fetch_add(1) + 1) & 0xffffu;
+    if (e != 0) return e;
+    g_wrap.fetch_add(1);
+  }
+}
+
+// Workgroups per stream for the grouped per-stream kernel (1 = not grouped).
+int pick_group(const tbs_model* m, const StreamPlan& sp, int B, int KT, int maxlen, int trivial) {
+  if (!sp.ok || m->bf16 || !trivial || KT <= 0 || !m->coop || maxlen > 65535) return 1;
+  const int ncg = m->Vpad / kJoinerBN;
+  for (int G : {8, 4, 2})
+    if (ncg % G == 0 && ncg / G <= 2 && (long long)B * G <= m->ncu) return G;
+  return 1;
+}
+
 }  // namespace
 
 extern "C" {
@@ -372,7 +445,13 @@ tbs_status tbs_model_create(int32_t vocab_size, int32_t dim, int32_t context_siz
   m->Vpad = round_up(vocab_size, kJoinerBN);
   m->bf16 = dtype == TBS_JOINER_BF16;
   const size_t VK = (size_t)m->V * m->Kpad, VpK = (size_t)m->Vpad * m->Kpad;
-  hipError_t e = hipSuccess;
+  hipError_t e = hipGetDevice(&m->dev);
+  if (e == hipSuccess)
+    e = hipDeviceGetAttribute(&m->ncu, hipDeviceAttributeMultiprocessorCount, m->dev);
+  if (e == hipSuccess)
+    e = hipDeviceGetAttribute(&m->coop, hipDeviceAttributeCooperativeLaunch, m->dev);
+  if (e == hipSuccess) e = dalloc(&m->xerr, 1);
+  if (e == hipSuccess) e = hipMemsetAsync(m->xerr, 0, sizeof(unsigned), st);
   if (e == hipSuccess) e = dalloc(&m->P0, VK);
   if (e == hipSuccess) e = dalloc(&m->P1, VK);
   if (e == hipSuccess) e = m->bf16 ? dalloc(&m->Wb, VpK) : dalloc(&m->Wf, VpK);
@@ -405,6 +484,11 @@ void tbs_model_destroy(tbs_model* m) {
   hipFree(m->Wb);
   hipFree(m->Wi);
   hipFree(m->bias);
+  hipFree(m->xerr);
+  if (m->xbuf.p) {
+    std::lock_guard<std::mutex> xl(g_xmu);
+    g_xfree.push_back(m->xbuf);
+  }
   hipFree(m->rows_h);
   hipFree(m->rows_logits);
   hipFree(m->rows_stats);
@@ -457,7 +541,7 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   const ModelDev md = model_dev(m);
   const StreamPlan splan = plan_stream(md, Nc, KT, graph->trivial);
   bool per_stream = false;
-  if (m->schedule == TBS_SCHEDULE_STREAM) {
+  if (m->schedule == TBS_SCHEDULE_STREAM || m->schedule == TBS_SCHEDULE_STREAM_SINGLE) {
     if (!splan.ok)
       return fail(TBS_EUNSUPPORTED,
                   "tbs_decode: the per-stream schedule does not fit max_contexts %d / "
@@ -512,7 +596,27 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
-  if (per_stream && maxlen > 0)
+  const int G = (per_stream && m->schedule != TBS_SCHEDULE_STREAM_SINGLE)
+                    ? pick_group(m, splan, B, KT, maxlen, graph->trivial)
+                    : 1;
+  bool grouped = false;
+  if (G > 1 && maxlen > 0) {
+    HIP_TRY(ensure_xbuf(m, (size_t)B * G * 2 * group_words(Nc, KT), st), "exchange buffer");
+    HIP_TRY(launch_fill_i32((int*)m->xerr, 1, 0, st), "fill(exchange errors)");
+    const unsigned epoch = next_epoch();
+    hipError_t e = timed_launch(m, TBS_KERNEL_STREAM_GROUP, st, [&] {
+      return launch_stream_group(md, gd, d, beam, trace, splan, m->xbuf.p, G, epoch, 1u << 22,
+                                 m->xerr, st);
+    });
+    if (e == hipSuccess) {
+      grouped = true;
+    } else if (e == hipErrorCooperativeLaunchTooLarge) {
+      (void)hipGetLastError();  // not co-resident here: one workgroup per stream instead
+    } else {
+      return hip_fail(e, "launch(stream group)");
+    }
+  }
+  if (per_stream && !grouped && maxlen > 0)
     HIP_TRY(timed_launch(m, TBS_KERNEL_STREAM, st,
                          [&] { return launch_stream(md, gd, d, beam, trace, splan, st); }),
             "launch(stream)");
@@ -527,7 +631,8 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
                          return launch_final(gd, d, out_tokens, out_num_tokens, out_scores,
-                                             out_status, out_arcs, st);
+                                             out_status, out_arcs, grouped ? m->xerr : nullptr,
+                                             st);
                        }),
           "launch(final)");
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
@@ -570,7 +675,7 @@ tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const 
 tbs_status tbs_model_set_schedule(tbs_model* model, int32_t schedule) {
   if (!model) return fail(TBS_EINVAL, "tbs_model_set_schedule: model is NULL");
   if (schedule != TBS_SCHEDULE_AUTO && schedule != TBS_SCHEDULE_FRAME &&
-      schedule != TBS_SCHEDULE_STREAM)
+      schedule != TBS_SCHEDULE_STREAM && schedule != TBS_SCHEDULE_STREAM_SINGLE)
     return fail(TBS_EINVAL, "tbs_model_set_schedule: unknown schedule %d", schedule);
   std::lock_guard<std::mutex> lk(model->mu);
   model->schedule = schedule;

@@ -92,6 +92,15 @@ struct StreamPlan {
 };
 
 StreamPlan plan_stream(const ModelDev& m, int Nc, int KT, int trivial);
+
+// Grouped per-stream kernel (trivial graph, fp32): G workgroups per stream, each with
+// Vpad / 64 / G (1 or 2) column groups; cooperative launch of B * G workgroups.
+// xbuf: uncached device memory of at least B * G * 2 * group_words(Nc, KT) words.
+int group_words(int Nc, int KT);
+hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                               int* trace, const StreamPlan& p, unsigned long long* xbuf, int G,
+                               unsigned epoch, unsigned spin_limit, unsigned* err,
+                               hipStream_t st);
 hipError_t launch_stream(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
                          int* trace, const StreamPlan& p, hipStream_t st);
 
@@ -107,7 +116,8 @@ hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const Join
 hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const DecodeDev& d,
                                float beam, int t, int* trace, hipStream_t st);
 hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, int* out_ntok,
-                        double* out_scores, int* out_status, int* out_arcs, hipStream_t st);
+                        double* out_scores, int* out_status, int* out_arcs,
+                        const unsigned* exchange_err, hipStream_t st);
 hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const int* ctx, int R,
                               void* h, float* logits, float2* stats, float* out_logp,
                               hipStream_t st);

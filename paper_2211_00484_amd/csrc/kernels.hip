@@ -681,15 +681,20 @@ struct CandIdx {
 };
 
 // One frame of the search for stream b (t < L), one workgroup.  FUSED (the
-// per-stream kernel): the survivors are in LDS and so are the frame's logit rows
+// per-stream kernels): the survivors are in LDS and so are the frame's logit rows
 // (zl, [row][Vpad], -inf beyond V); the next frame's joiner rows go to LDS (hl,
 // row stride hstride) and the survivors stay in LDS; the global survivor arrays
-// are written at the stream's last frame only.
+// are written at the stream's last frame only.  prestats: the normalisers
+// (s_lse) and, for the trivial graph, the best labels and blank logits are
+// already in LDS.  writer: this workgroup writes the stream's history, trace,
+// survivors and offset (a stream run redundantly by several workgroups has one
+// writer).
 template <bool TRIV, bool FUSED>
 __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& g,
                                              const DecodeDev& d, float beam, int t, int L, int b,
                                              int* __restrict__ trace, SearchSmem& s, void* hl,
-                                             int hstride, const float* zl) {
+                                             int hstride, const float* zl, bool prestats = false,
+                                             bool writer = true) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V, nvt = d.nvt;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
@@ -745,7 +750,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     S = wave_sum_f(S);
     if (lane == 0) s.s_lse[j] = lse_of(M, S);
   }
-  if (FUSED) {
+  if (FUSED && !prestats) {
     // straight from the logit rows: normaliser, and for the trivial graph the blank
     // logit and the row's best KT labels (labels are unique within a row, so round q
     // takes the largest key below round q-1's); one wave per row, each lane holding
@@ -1306,7 +1311,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
                                    tid);
     }
   }
-  const bool store_surv = !FUSED || t + 1 == L;
+  const bool store_surv = writer && (!FUSED || t + 1 == L);
   if (my_keep2) {
     const unsigned tb = 0xffffffffu - (unsigned)my_v;
     const int parent = (int)(tb / stride_tb);
@@ -1328,9 +1333,11 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       if (my_first) d.ctx_list[row0 + my_crow] = (int)my_ci;
     }
     const size_t hbase = ((size_t)t * d.B + b) * Ns;
-    d.hist_pl[hbase + my_pos] = (parent << 16) | label;
-    d.hist_arc[hbase + my_pos] = arc;
-    if (trace) {
+    if (writer) {
+      d.hist_pl[hbase + my_pos] = (parent << 16) | label;
+      d.hist_arc[hbase + my_pos] = arc;
+    }
+    if (writer && trace) {
       int* tr = trace + (((size_t)(t + 1) * d.B + b) * Ns + my_pos) * 4;
       tr[0] = (int)my_ci;
       tr[1] = (int)my_st;
@@ -1347,7 +1354,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       s.ns = s.nK;
       s.nc = nC;
     }
-    d.offset[b] += (double)best;
+    if (writer) d.offset[b] += (double)best;
   }
 }
 
@@ -1557,6 +1564,274 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
 }
 
 // ---------------------------------------------------------------------------
+// grouped per-stream kernel: G workgroups share one stream (trivial graph, fp32).
+// Member g computes the joiner for its NCG 64-column groups starting at cg0 = g NCG,
+// and every member runs the same search on the same data, so they stay identical;
+// per frame they exchange each row's (max, sum exp), best KT labels and blank logit
+// through tagged 64-bit words in uncached memory.
+
+// Joiner of member columns [64 cg0, 64 (cg0 + NCG)) for all 4 RG rows, split over
+// K: wave w accumulates k slices [w Kpad / 16, (w + 1) Kpad / 16) (16-byte fp32
+// slices), lane l owning column 64 (cg0 + j) + l, h broadcast from LDS, W streamed
+// from the interleaved copy with the next chunk in flight.  The four waves' partial
+// sums meet in LDS (part, 4 x NCG x 4 RG x 64 floats) and are added in wave order.
+template <int RG, int NCG>
+__device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* hl, int hstride,
+                                                 float* zl, float* part, int cg0) {
+  constexpr int NR = 4 * RG;
+  constexpr int CH = 8 / NCG;  // k slices per chunk
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int V = m.V, Vpad = m.Vpad;
+  const int qw = m.Kpad / 16;  // k slices per wave (a multiple of 32)
+  const int q0 = wave * qw;
+  const int steps = qw / CH;   // even
+  const float4* __restrict__ Wi = reinterpret_cast<const float4*>(m.Wi);
+  const char* hrows = reinterpret_cast<const char*>(hl);
+  const size_t rstride = (size_t)hstride * 4;
+  auto load_chunk = [&](int step, float4 (&w)[CH][NCG]) {
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const size_t q = (size_t)(q0 + step * CH + u);
+#pragma unroll
+      for (int j = 0; j < NCG; ++j) w[u][j] = Wi[q * Vpad + (cg0 + j) * 64 + lane];
+    }
+  };
+  float acc[NCG][NR];
+#pragma unroll
+  for (int j = 0; j < NCG; ++j)
+#pragma unroll
+    for (int r = 0; r < NR; ++r) acc[j][r] = 0.f;
+  auto compute = [&](int step, const float4 (&w)[CH][NCG]) {
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const size_t ko = (size_t)(q0 + step * CH + u) * 16;
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        const float4 a = *reinterpret_cast<const float4*>(hrows + (size_t)r * rstride + ko);
+#pragma unroll
+        for (int j = 0; j < NCG; ++j) {
+          acc[j][r] = fmaf(a.x, w[u][j].x, acc[j][r]);
+          acc[j][r] = fmaf(a.y, w[u][j].y, acc[j][r]);
+          acc[j][r] = fmaf(a.z, w[u][j].z, acc[j][r]);
+          acc[j][r] = fmaf(a.w, w[u][j].w, acc[j][r]);
+        }
+      }
+    }
+  };
+  float4 wa[CH][NCG], wb[CH][NCG];
+  load_chunk(0, wa);
+  for (int step = 0; step < steps; step += 2) {
+    load_chunk(step + 1, wb);
+    compute(step, wa);
+    load_chunk(min(step + 2, steps - 1), wa);
+    compute(step + 1, wb);
+  }
+#pragma unroll
+  for (int j = 0; j < NCG; ++j)
+#pragma unroll
+    for (int r = 0; r < NR; ++r) part[((wave * NCG + j) * NR + r) * 64 + lane] = acc[j][r];
+  __syncthreads();
+  constexpr int PER = NCG * NR * 64;
+  for (int e = tid; e < PER; e += kSearchThreads) {
+    const int j = e / (NR * 64), r = (e / 64) % NR, l = e & 63;
+    const int col = (cg0 + j) * 64 + l;
+    const float z = ((part[e] + part[PER + e]) + part[2 * PER + e]) + part[3 * PER + e];
+    zl[(size_t)r * Vpad + col] = col < V ? z + m.bias[col] : -INFINITY;
+  }
+}
+
+// The member joiner's partial sums (4 waves x 2 column groups x 16 rows x 64 lanes)
+// live in hk and hv; the exchanged words of all members (8 x 16 rows x 35 words)
+// in uk and uv.
+static_assert(offsetof(SearchSmem, hv) == offsetof(SearchSmem, hk) + sizeof(SearchSmem::hk) &&
+                  sizeof(SearchSmem::hk) + sizeof(SearchSmem::hv) >= 4 * 2 * 16 * 64 * sizeof(float),
+              "member joiner partial sums do not fit hk and hv");
+static_assert(offsetof(SearchSmem, uv) == offsetof(SearchSmem, uk) + sizeof(SearchSmem::uk) &&
+                  sizeof(SearchSmem::uk) + sizeof(SearchSmem::uv) >= 8 * 16 * 35 * sizeof(unsigned),
+              "exchanged words do not fit uk and uv");
+
+// Exchange slot of (stream b, member g, frame parity): Nc rows of RW words.
+struct GroupX {
+  unsigned long long* buf;  // uncached device memory
+  int G, xwords;            // members per stream; words per slot
+  unsigned epoch;           // decode number (16 bits), tags are epoch << 16 | frame
+  unsigned spin_limit;      // polls before a wait is abandoned (recorded in err)
+  unsigned* err;
+};
+
+__device__ __forceinline__ unsigned long long* group_slot(const GroupX& x, int b, int g, int t) {
+  return x.buf + ((size_t)(b * x.G + g) * 2 + (t & 1)) * x.xwords;
+}
+
+template <int RG, int NCG>
+__global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, GraphDev g, DecodeDev d,
+                                                                 float beam, int* __restrict__ trace,
+                                                                 int hoff, int hstride, int zoff,
+                                                                 GroupX x) {
+  const int G = x.G;
+  const int b = blockIdx.x / G, mem = blockIdx.x - b * G;
+  const int L = d.len[b];
+  if (L == 0) return;  // every member of the stream returns here
+  extern __shared__ __align__(16) unsigned char smem[];
+  SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
+  void* hl = smem + hoff;
+  float* zl = reinterpret_cast<float*>(smem + zoff);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Ns = d.Ns, Nc = d.Nc, V = m.V, Vpad = m.Vpad, KT = d.KT;
+  const int RW = 3 + 2 * KT;  // words per row: max, sum exp, KT x (logit, label), blank logit
+  const int cg0 = mem * NCG;
+  const size_t row0 = (size_t)b * Nc;
+  if (tid == 0) {
+    s.ns = d.nsurv[b];
+    s.nc = d.nctx[b];
+  }
+  for (int i = tid; i < Ns; i += blockDim.x) {
+    const size_t o = (size_t)b * Ns + i;
+    s.s_ctx[i] = d.surv_ctx[o];
+    s.s_state[i] = d.surv_state[o];
+    s.s_row[i] = d.surv_row[o];
+    s.s_score[i] = d.surv_score[o];
+  }
+  for (int j = tid; j < Nc; j += blockDim.x) {
+    const int c = d.ctx_list[row0 + j], a = c / V;
+    s.n_rowoff[j] = make_int2(a * m.Kpad, (c - a * V) * m.Kpad);
+  }
+  {
+    const float* er = d.enc + (size_t)b * d.T * m.C;
+    for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
+    const int words = RG * 4 * hstride;
+    for (int i = tid; i < words; i += blockDim.x) reinterpret_cast<int*>(hl)[i] = 0;
+  }
+  __syncthreads();
+  write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, s.nc, hl, hstride, tid);
+  __syncthreads();
+  for (int t = 0; t < L; ++t) {
+    // the partial sums use the hash table's LDS, idle until the search
+    group_joiner_f32<RG, NCG>(m, hl, hstride, zl, reinterpret_cast<float*>(s.hk), cg0);
+    __syncthreads();
+    const int nc = s.nc;
+    const unsigned tag = (x.epoch << 16) | ((unsigned)t & 0xffffu);
+    // this member's row statistics over its columns -> tagged words
+    {
+      unsigned long long* slot = group_slot(x, b, mem, t);
+      for (int j = wave; j < nc; j += 4) {
+        float z[NCG];
+        unsigned long long key[NCG];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int jj = 0; jj < NCG; ++jj) {
+          const int col = (cg0 + jj) * 64 + lane;
+          z[jj] = zl[(size_t)j * Vpad + col];
+          mx = fmaxf(mx, z[jj]);
+          key[jj] = (col >= 1 && col < V)
+                        ? ((unsigned long long)f2ord(z[jj]) << 32) | (0xffffffffu - (unsigned)col)
+                        : 0ull;
+        }
+        const float M = wave_max_f(mx);
+        float se = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < NCG; ++jj) se += __expf(z[jj] - M);
+        const float S = wave_sum_f(se);
+        float my_z = -INFINITY;
+        int my_c = -1;
+        unsigned long long prev = ~0ull;
+        for (int q = 0; q < KT; ++q) {
+          unsigned long long mine = 0ull;
+#pragma unroll
+          for (int jj = 0; jj < NCG; ++jj) mine = (key[jj] < prev && key[jj] > mine) ? key[jj] : mine;
+          const unsigned long long best = wave_max_u64(mine);
+          if (lane == q && best != 0ull) {
+            my_z = ord2f((unsigned)(best >> 32));
+            my_c = (int)(0xffffffffu - (unsigned)best);
+          }
+          prev = best ? best : 1ull;
+        }
+        unsigned long long* w = slot + (size_t)j * RW;
+        const unsigned long long tg = (unsigned long long)tag << 32;
+        if (lane == 0) {
+          __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          const float z0 = cg0 == 0 ? zl[(size_t)j * Vpad] : 0.f;
+          __hip_atomic_store(w + 2 + 2 * KT, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        if (lane < KT) {
+          __hip_atomic_store(w + 2 + 2 * lane, tg | __float_as_uint(my_z), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_SYSTEM);
+          __hip_atomic_store(w + 3 + 2 * lane, tg | (unsigned)my_c, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+      }
+    }
+    // every member's words for this frame (bounded polls), payloads into LDS
+    unsigned* xs = reinterpret_cast<unsigned*>(s.uk);  // [G][nc][RW]
+    {
+      const int per = nc * RW, total = G * per;
+      for (int idx = tid; idx < total; idx += blockDim.x) {
+        const int g2 = idx / per, rest = idx - g2 * per;
+        const unsigned long long* w = group_slot(x, b, g2, t) + rest;
+        unsigned long long v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        unsigned n = 0;
+        while ((unsigned)(v >> 32) != tag) {
+          if (++n > x.spin_limit) {
+            atomicAdd(x.err, 1u);
+            break;
+          }
+          v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        xs[idx] = (unsigned)v;
+      }
+    }
+    __syncthreads();
+    // combine in member order (identical in every member): normaliser, blank logit,
+    // best KT labels over the G lists (the members' columns are disjoint)
+    for (int j = wave; j < nc; j += 4) {
+      if (lane == 0) {
+        float M = -INFINITY;
+        for (int g2 = 0; g2 < G; ++g2) M = fmaxf(M, __uint_as_float(xs[(g2 * nc + j) * RW]));
+        float S = 0.f;
+        for (int g2 = 0; g2 < G; ++g2) {
+          const float Sg = __uint_as_float(xs[(g2 * nc + j) * RW + 1]);
+          const float Mg = __uint_as_float(xs[(g2 * nc + j) * RW]);
+          S += Sg == 0.f ? 0.f : Sg * __expf(Mg - M);
+        }
+        s.s_lse[j] = lse_of(M, S);
+        s.s_z0[j] = __uint_as_float(xs[j * RW + 2 + 2 * KT]);
+      }
+      const int ne = G * KT;
+      unsigned long long kv[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int e = lane + 64 * h;
+        kv[h] = 0ull;
+        if (e < ne) {
+          const int g2 = e / KT, q = e - g2 * KT;
+          const unsigned* w = xs + (g2 * nc + j) * RW + 2 + 2 * q;
+          const int c = (int)w[1];
+          if (c >= 0)
+            kv[h] = ((unsigned long long)f2ord(__uint_as_float(w[0])) << 32) | (0xffffffffu - (unsigned)c);
+        }
+      }
+      unsigned long long prev = ~0ull;
+      for (int q = 0; q < KT; ++q) {
+        unsigned long long mine = 0ull;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) mine = (kv[h] < prev && kv[h] > mine) ? kv[h] : mine;
+        const unsigned long long best = wave_max_u64(mine);
+        if (lane == 0) {
+          s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
+          s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+        }
+        prev = best ? best : 1ull;
+      }
+    }
+    __syncthreads();
+    search_frame<true, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, zl, true, mem == 0);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // final selection and traceback
 
 constexpr int kFinalBuf = 4096;
@@ -1565,7 +1840,8 @@ __global__ __launch_bounds__(256) void k_final(GraphDev g, DecodeDev d, int* __r
                                                int* __restrict__ out_ntok,
                                                double* __restrict__ out_scores,
                                                int* __restrict__ out_status,
-                                               int* __restrict__ out_arcs) {
+                                               int* __restrict__ out_arcs,
+                                               const unsigned* __restrict__ xerr) {
   __shared__ int buf_pl[kFinalBuf];
   __shared__ int buf_arc[kFinalBuf];
   __shared__ int s_idx;
@@ -1592,6 +1868,7 @@ __global__ __launch_bounds__(256) void k_final(GraphDev g, DecodeDev d, int* __r
     const int st = d.surv_state[(size_t)b * Ns + pick];
     const double f = (status == 0 && g.fin) ? (double)g.fin[st] : 0.0;
     out_scores[b] = (double)d.surv_score[(size_t)b * Ns + pick] + d.offset[b] + f;
+    if (xerr && *xerr) status = 2;  // a grouped stream's exchange wait timed out
     if (out_status) out_status[b] = status;
     s_idx = pick;
   }
@@ -1832,10 +2109,56 @@ hipError_t launch_stream(const ModelDev& m, const GraphDev& g, const DecodeDev& 
               : launch_stream_rg<false, false>(m, g, d, beam, trace, p, st);
 }
 
+int group_words(int Nc, int KT) { return Nc * (3 + 2 * KT); }
+
+template <int RG, int NCG>
+hipError_t launch_group_t(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                          int* trace, const StreamPlan& p, const GroupX& x, hipStream_t st) {
+  static size_t attr = 0;
+  if (p.lds > attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_stream_group<RG, NCG>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+    if (e != hipSuccess) return e;
+    attr = p.lds;
+  }
+  ModelDev ma = m;
+  GraphDev ga = g;
+  DecodeDev da = d;
+  GroupX xa = x;
+  int hoff = p.hoff, hstride = p.hstride, zoff = p.zoff;
+  void* args[] = {&ma, &ga, &da, &beam, &trace, &hoff, &hstride, &zoff, &xa};
+  return hipLaunchCooperativeKernel((const void*)k_stream_group<RG, NCG>, dim3(d.B * x.G),
+                                    dim3(kSearchThreads), args, (unsigned)p.lds, st);
+}
+
+template <int NCG>
+hipError_t launch_group_rg(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                           int* trace, const StreamPlan& p, const GroupX& x, hipStream_t st) {
+  switch (p.RG) {
+    case 1: return launch_group_t<1, NCG>(m, g, d, beam, trace, p, x, st);
+    case 2: return launch_group_t<2, NCG>(m, g, d, beam, trace, p, x, st);
+    case 3: return launch_group_t<3, NCG>(m, g, d, beam, trace, p, x, st);
+    default: return launch_group_t<4, NCG>(m, g, d, beam, trace, p, x, st);
+  }
+}
+
+hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
+                               int* trace, const StreamPlan& p, unsigned long long* xbuf, int G,
+                               unsigned epoch, unsigned spin_limit, unsigned* err,
+                               hipStream_t st) {
+  const int ncg = m.Vpad / kJoinerBN;
+  if (!p.ok || m.bf16 || d.KT <= 0 || G < 2 || ncg % G != 0 || ncg / G > 2)
+    return hipErrorInvalidValue;
+  GroupX x{xbuf, G, group_words(d.Nc, d.KT), epoch & 0xffffu, spin_limit, err};
+  return ncg / G == 1 ? launch_group_rg<1>(m, g, d, beam, trace, p, x, st)
+                      : launch_group_rg<2>(m, g, d, beam, trace, p, x, st);
+}
+
 hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, int* out_ntok,
-                        double* out_scores, int* out_status, int* out_arcs, hipStream_t st) {
+                        double* out_scores, int* out_status, int* out_arcs,
+                        const unsigned* exchange_err, hipStream_t st) {
   hipLaunchKernelGGL(k_final, dim3(d.B), dim3(256), 0, st, g, d, out_tokens, out_ntok, out_scores,
-                     out_status, out_arcs);
+                     out_status, out_arcs, exchange_err);
   return hipGetLastError();
 }
 

@@ -37,8 +37,8 @@ class KernelTime(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
 
 
-KERNEL_NAMES = ("joiner", "search", "final", "stream")
-SCHEDULES = {"auto": 0, "frame": 1, "stream": 2}
+KERNEL_NAMES = ("joiner", "search", "final", "stream", "stream_group")
+SCHEDULES = {"auto": 0, "frame": 1, "stream": 2, "stream1": 3}
 
 
 class BeamParams(ctypes.Structure):
@@ -182,7 +182,8 @@ class Model:
         self.vocab_size, self.dim, self.dtype = int(vocab_size), int(dim), dtype
 
     def set_schedule(self, schedule: str):
-        """Frame-loop schedule for later decodes: "auto", "frame" or "stream"."""
+        """Frame-loop schedule for later decodes: "auto", "frame", "stream" (several
+        workgroups per stream where possible) or "stream1" (one per stream)."""
         _check(lib().tbs_model_set_schedule(self._h, SCHEDULES[schedule]))
 
     def set_profiling(self, enable: bool):

@@ -1,7 +1,9 @@
 """HIP decode (tbs_decode) against the CPU oracle, element by element.
 
 Every case runs under both frame-loop schedules: "frame" (a joiner GEMM kernel and a
-search kernel per frame) and "stream" (one persistent workgroup per stream).  A shape
+search kernel per frame) and "stream" (persistent workgroups: one per stream, or for
+the trivial graph with an fp32 joiner several per stream where the shape allows;
+"stream1" forces one).  A shape
 the per-stream kernel cannot hold must be refused with TBS_EUNSUPPORTED; such a run is
 reported and skipped.
 
@@ -144,7 +146,7 @@ def test_max_states_limit(schedule):
     _run((inputs, model, graph), math.inf, 256, 7, schedule=schedule)
 
 
-@pytest.mark.parametrize("schedule", SCHEDULES)
+@pytest.mark.parametrize("schedule", SCHEDULES + ["stream1"])
 def test_standard(schedule):
     _, _, rep = _run("standard", math.inf, 4, 4, schedule=schedule)
     assert rep.streams == 32
