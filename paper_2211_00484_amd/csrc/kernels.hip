@@ -866,7 +866,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     // min(max_states, max_contexts) and lies within the beam of the best.  Its
     // canonical position is the number of kept contexts below its own.
     if (wave == 0) {
-      const int KT = d.KT, P = 1 + KT, n = ns * P;
+      const int KT = d.KT, P = 1 + KT, n = ns * P, np = (n + 3) & ~3;
       unsigned long long myk = kEmpty, myv = 0ull;
       if (lane < n) {
         const int i = lane / P, q = lane - i * P - 1;
@@ -880,7 +880,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
           const int lab = s.rk_c[row * KT + q];
           if (lab >= 0) {
             const float sc = s.s_score[i] + logp_of(s.rk_z[row * KT + q], lse);
-            myk = (unsigned)(s.s_ctx[i] % V) * (unsigned)V + (unsigned)lab;
+            myk = (unsigned)s.s_bprev[i] * (unsigned)V + (unsigned)lab;
             myv = ((unsigned long long)f2ord(sc) << 32) |
                   (0xffffffffu - ((unsigned)i * stride_tb + (unsigned)lab));
           }
@@ -893,29 +893,41 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
                (unsigned)__builtin_amdgcn_readlane((int)lo, j);
       };
       // max-merge: a candidate represents its key iff no candidate with that key
-      // has a larger value
+      // has a larger value (lanes n..np-1 are empty and never match); loops take
+      // four lanes per step so that the readlanes of a step are independent
       int rep = myk != kEmpty;
-      for (int j = 0; j < n; ++j) {
-        const unsigned long long kj = rd64(klo, khi, j), vj = rd64(vlo, vhi, j);
-        rep &= !(kj == myk && vj > myv);
+      for (int j = 0; j < np; j += 4) {
+        int dom = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const unsigned long long kj = rd64(klo, khi, j + u), vj = rd64(vlo, vhi, j + u);
+          dom |= kj == myk && vj > myv;
+        }
+        rep &= !dom;
       }
       // rank among the representatives by (score desc, key asc)
       int rank = 0;
-      for (int j = 0; j < n; ++j) {
-        const int rj = __builtin_amdgcn_readlane(rep, j);
-        const unsigned soj = (unsigned)__builtin_amdgcn_readlane((int)vhi, j);
-        const unsigned long long kj = rd64(klo, khi, j);
-        rank += rj && (soj > vhi || (soj == vhi && kj < myk));
+      for (int j = 0; j < np; j += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int rj = __builtin_amdgcn_readlane(rep, j + u);
+          const unsigned soj = (unsigned)__builtin_amdgcn_readlane((int)vhi, j + u);
+          const unsigned long long kj = rd64(klo, khi, j + u);
+          rank += rj && (soj > vhi || (soj == vhi && kj < myk));
+        }
       }
       const float sc = ord2f(vhi);
       const int keep0 = rep && rank < Ns;
       const float bst = wave_max_f(keep0 ? sc : -INFINITY);
       const int keep2 = keep0 && sc >= bst - beam && rank < Nc;
       int pos = 0;
-      for (int j = 0; j < n; ++j) {
-        const int k2j = __builtin_amdgcn_readlane(keep2, j);
-        const unsigned long long kj = rd64(klo, khi, j);
-        pos += k2j && kj < myk;
+      for (int j = 0; j < np; j += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int k2j = __builtin_amdgcn_readlane(keep2, j + u);
+          const unsigned long long kj = rd64(klo, khi, j + u);
+          pos += k2j && kj < myk;
+        }
       }
       const unsigned long long kept = __ballot(keep2);
       if (keep2) s.n_ctx_list[pos] = (int)klo;
@@ -1786,15 +1798,12 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     // combine in member order (identical in every member): normaliser, blank logit,
     // best KT labels over the G lists (the members' columns are disjoint)
     for (int j = wave; j < nc; j += 4) {
+      // (the wave reductions combine in a fixed order, the same in every member)
+      const float Mg = lane < G ? __uint_as_float(xs[(lane * nc + j) * RW]) : -INFINITY;
+      const float Sg = lane < G ? __uint_as_float(xs[(lane * nc + j) * RW + 1]) : 0.f;
+      const float M = wave_max_f(Mg);
+      const float S = wave_sum_f(Sg == 0.f ? 0.f : Sg * __expf(Mg - M));
       if (lane == 0) {
-        float M = -INFINITY;
-        for (int g2 = 0; g2 < G; ++g2) M = fmaxf(M, __uint_as_float(xs[(g2 * nc + j) * RW]));
-        float S = 0.f;
-        for (int g2 = 0; g2 < G; ++g2) {
-          const float Sg = __uint_as_float(xs[(g2 * nc + j) * RW + 1]);
-          const float Mg = __uint_as_float(xs[(g2 * nc + j) * RW]);
-          S += Sg == 0.f ? 0.f : Sg * __expf(Mg - M);
-        }
         s.s_lse[j] = lse_of(M, S);
         s.s_z0[j] = __uint_as_float(xs[j * RW + 2 + 2 * KT]);
       }
