@@ -102,6 +102,39 @@ __device__ __forceinline__ float wave_sum_f(float v) {
   v = row16_sum(v);
   return (rdlane_f(v, 0) + rdlane_f(v, 16)) + (rdlane_f(v, 32) + rdlane_f(v, 48));
 }
+__device__ __forceinline__ unsigned long long umin64(unsigned long long a, unsigned long long b) {
+  return a < b ? a : b;
+}
+__device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
+  v = umin64(v, dpp_u64<kRor8>(v));
+  v = umin64(v, dpp_u64<kRor4>(v));
+  v = umin64(v, dpp_u64<kRor2>(v));
+  v = umin64(v, dpp_u64<kRor1>(v));
+  unsigned long long r = ~0ull;
+#pragma unroll
+  for (int l = 0; l < 64; l += 16) {
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)v, l);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v >> 32), l);
+    r = umin64(r, ((unsigned long long)hi << 32) | lo);
+  }
+  return r;
+}
+__device__ __forceinline__ unsigned wave_max_u32(unsigned v) {
+  v = max(v, (unsigned)dpp_i<kRor8>((int)v));
+  v = max(v, (unsigned)dpp_i<kRor4>((int)v));
+  v = max(v, (unsigned)dpp_i<kRor2>((int)v));
+  v = max(v, (unsigned)dpp_i<kRor1>((int)v));
+  return max(max((unsigned)__builtin_amdgcn_readlane((int)v, 0), (unsigned)__builtin_amdgcn_readlane((int)v, 16)),
+             max((unsigned)__builtin_amdgcn_readlane((int)v, 32), (unsigned)__builtin_amdgcn_readlane((int)v, 48)));
+}
+__device__ __forceinline__ unsigned wave_min_u32(unsigned v) {
+  v = min(v, (unsigned)dpp_i<kRor8>((int)v));
+  v = min(v, (unsigned)dpp_i<kRor4>((int)v));
+  v = min(v, (unsigned)dpp_i<kRor2>((int)v));
+  v = min(v, (unsigned)dpp_i<kRor1>((int)v));
+  return min(min((unsigned)__builtin_amdgcn_readlane((int)v, 0), (unsigned)__builtin_amdgcn_readlane((int)v, 16)),
+             min((unsigned)__builtin_amdgcn_readlane((int)v, 32), (unsigned)__builtin_amdgcn_readlane((int)v, 48)));
+}
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
   v = row16_max_u64(v);
   unsigned long long r = 0;
@@ -538,7 +571,7 @@ struct SearchSmem {
   double s_lse[kMaxStates];
   uint4 fent[kMaxStates];    // final stage: (ctx, state, score bits, context-score bits)
   int fflg[kMaxStates];      // bit 0 in beam, bit 1 first tuple of its context, bit 2 kept
-  float enc_next[kMaxDim];   // encoder frame t+1 of this stream (joiner rows of the next frame)
+  alignas(16) float enc_next[kMaxDim];  // encoder frame t+1 of this stream (next frame's joiner rows)
   float wmax[4];
   int n_ctx_list[kMaxStates];
   int2 n_rowoff[kMaxStates];  // (a * Kpad, b * Kpad) of each next-frame context (a, b)
@@ -548,6 +581,7 @@ struct SearchSmem {
   unsigned hist[256];
   int wsum[4];
   int misc[8];
+  int g_src[4];              // grouped fast path: decoder-row source of each new context row
   int ns, nc, nU, nL, n_gt, n_eq, nK, nC;
   float best;
 };
@@ -680,6 +714,114 @@ struct CandIdx {
   float q, z;
 };
 
+// Result of the one-wave selection for one lane (one candidate).
+struct WaveSel {
+  unsigned ci, st;          // the candidate's key (context, state)
+  float sc;                 // its score
+  unsigned long long v;     // score << 32 | ~back-pointer
+  int keep2, pos;           // kept, and its canonical position (= its context row)
+  int src;                  // i * KT + q for label q of survivor i; -(1 + row) for the
+                            // blank of a survivor on context row `row`
+  float best;               // the frame's best score (uniform)
+  int nk;                   // tuples kept (uniform)
+};
+
+// Trivial graph, at most 64 candidates (survivor-major: blank, then the row's KT
+// best labels): one wave, one candidate per lane.  The key is the context alone
+// (one graph state), so after the max-merge every context has one tuple: the
+// context score is the tuple's score, the max-contexts rank equals the max-states
+// rank among the in-beam tuples, and a tuple is kept iff it represents its key,
+// ranks below min(max_states, max_contexts) and lies within the beam of the best.
+// The kept tuples are extracted in rank order: each round takes the candidate with
+// the largest (score, then smaller key, then smaller back-pointer), which is its
+// key's representative and the best remaining one, and retires every candidate
+// with that key; the rounds stop at the rank limit, at the beam or when nothing is
+// left.  A kept tuple's canonical position is the number of kept keys below its
+// own.  Survivors are read at offset sb of the survivor arrays, with the row
+// normalisers and each row's best labels (rk_z, rk_c, s_z0).  publish: also write
+// n_ctx_list, nK, nC and best.
+__device__ __forceinline__ WaveSel trivial_select_wave(SearchSmem& s, int ns, int KT, int V, int Ns,
+                                                       int Nc, float beam, unsigned stride_tb,
+                                                       int lane, int sb, bool publish) {
+  const int P = 1 + KT, n = ns * P;
+  unsigned long long myk = kEmpty, myv = 0ull;
+  int src = 0;
+  if (lane < n) {
+    const int i = lane / P, q = lane - i * P - 1;
+    const int row = s.s_row[sb + i];
+    const double lse = s.s_lse[row];
+    if (q < 0) {
+      const float sc = s.s_score[sb + i] + logp_of(s.s_z0[row], lse);
+      myk = ((unsigned long long)(unsigned)s.s_state[sb + i] << 32) | (unsigned)s.s_ctx[sb + i];
+      myv = ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - (unsigned)i * stride_tb);
+      src = -(1 + row);
+    } else {
+      const int lab = s.rk_c[row * KT + q];
+      if (lab >= 0) {
+        const float sc = s.s_score[sb + i] + logp_of(s.rk_z[row * KT + q], lse);
+        myk = (unsigned)s.s_bprev[sb + i] * (unsigned)V + (unsigned)lab;
+        myv = ((unsigned long long)f2ord(sc) << 32) |
+              (0xffffffffu - ((unsigned)i * stride_tb + (unsigned)lab));
+      }
+      src = i * KT + q;
+    }
+  }
+  const unsigned vhi = (unsigned)(myv >> 32), vlo = (unsigned)myv;
+  const int K = min(Ns, Nc);
+  bool alive = myk != kEmpty;
+  int nk = 0, keep2 = 0, pos = 0;
+  float bst = -INFINITY;
+  for (int r = 0; r < K; ++r) {
+    const unsigned mo = wave_max_u32(alive ? vhi : 0u);
+    if (mo == 0u) break;  // no candidate left
+    const float scr = ord2f(mo);
+    if (r == 0) bst = scr;
+    else if (!(scr >= bst - beam)) break;  // ranks only fall from here on
+    unsigned long long bal = __ballot(alive && vhi == mo);
+    if (__popcll(bal) > 1) {  // equal scores: the smaller key, then the smaller back-pointer
+      const bool tie = alive && vhi == mo;
+      const unsigned long long kmin = wave_min_u64(tie ? myk : ~0ull);
+      bal = __ballot(tie && myk == kmin);
+      if (__popcll(bal) > 1) {
+        const unsigned vmax = wave_max_u32((tie && myk == kmin) ? vlo : 0u);
+        bal = __ballot(tie && myk == kmin && vlo == vmax);
+      }
+    }
+    const int wl = __ffsll((long long)bal) - 1;
+    const unsigned long long kr =
+        ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)(myk >> 32), wl) << 32) |
+        (unsigned)__builtin_amdgcn_readlane((int)(unsigned)myk, wl);
+    // canonical positions: kept keys above the new one move up by one
+    const unsigned long long below = __ballot(keep2 && myk < kr);
+    if (keep2 && myk > kr) ++pos;
+    if (lane == wl) {
+      keep2 = 1;
+      pos = __popcll(below);
+    }
+    alive = alive && myk != kr;
+    ++nk;
+  }
+  if (publish) {
+    if (keep2) s.n_ctx_list[pos] = (int)(unsigned)myk;
+    if (lane == 0) {
+      s.nK = nk;
+      s.nC = nk;
+      s.best = bst;
+    }
+  }
+  WaveSel r;
+  r.ci = (unsigned)myk;
+  r.st = (unsigned)(myk >> 32);
+  r.sc = ord2f(vhi);
+  r.v = myv;
+  r.keep2 = keep2;
+  r.pos = pos;
+  r.src = src;
+  r.best = bst;
+  r.nk = nk;
+  return r;
+}
+
 // One frame of the search for stream b (t < L), one workgroup.  FUSED (the
 // per-stream kernels): the survivors are in LDS and so are the frame's logit rows
 // (zl, [row][Vpad], -inf beyond V); the next frame's joiner rows go to LDS (hl,
@@ -688,13 +830,13 @@ struct CandIdx {
 // (s_lse) and, for the trivial graph, the best labels and blank logits are
 // already in LDS.  writer: this workgroup writes the stream's history, trace,
 // survivors and offset (a stream run redundantly by several workgroups has one
-// writer).
+// writer).  enc_ready: the caller has put encoder frame t+1 in enc_next.
 template <bool TRIV, bool FUSED>
 __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& g,
                                              const DecodeDev& d, float beam, int t, int L, int b,
                                              int* __restrict__ trace, SearchSmem& s, void* hl,
                                              int hstride, const float* zl, bool prestats = false,
-                                             bool writer = true) {
+                                             bool writer = true, bool enc_ready = false) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V, nvt = d.nvt;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
@@ -717,7 +859,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       s.s_row[i] = d.surv_row[o];
       s.s_score[i] = d.surv_score[o];
     }
-  if (t + 1 < L) {
+  if (t + 1 < L && !enc_ready) {
     const float* er = d.enc + ((size_t)b * d.T + t + 1) * m.C;
     for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
   }
@@ -857,93 +999,17 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   int my_keep2 = 0, my_pos = 0, my_crow = 0, my_first = 0;
 
   if (TRIV && ns * (1 + d.KT) <= 64) {
-    // Trivial graph, at most 64 candidates (survivor-major: blank, then the row's
-    // KT best labels): one wave, one candidate per lane, other lanes' values read
-    // with readlane.  The key is the context alone (one graph state), so after
-    // the max-merge every context has one tuple: the context score is the tuple's
-    // score, the max-contexts rank equals the max-states rank among the in-beam
-    // tuples, and a tuple is kept iff it represents its key, ranks below
-    // min(max_states, max_contexts) and lies within the beam of the best.  Its
-    // canonical position is the number of kept contexts below its own.
+    // trivial graph, at most 64 candidates: one wave (trivial_select_wave)
     if (wave == 0) {
-      const int KT = d.KT, P = 1 + KT, n = ns * P, np = (n + 3) & ~3;
-      unsigned long long myk = kEmpty, myv = 0ull;
-      if (lane < n) {
-        const int i = lane / P, q = lane - i * P - 1;
-        const int row = s.s_row[i];
-        const double lse = s.s_lse[row];
-        if (q < 0) {
-          const float sc = s.s_score[i] + logp_of(s.s_z0[row], lse);
-          myk = ((unsigned long long)(unsigned)s.s_state[i] << 32) | (unsigned)s.s_ctx[i];
-          myv = ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - (unsigned)i * stride_tb);
-        } else {
-          const int lab = s.rk_c[row * KT + q];
-          if (lab >= 0) {
-            const float sc = s.s_score[i] + logp_of(s.rk_z[row * KT + q], lse);
-            myk = (unsigned)s.s_bprev[i] * (unsigned)V + (unsigned)lab;
-            myv = ((unsigned long long)f2ord(sc) << 32) |
-                  (0xffffffffu - ((unsigned)i * stride_tb + (unsigned)lab));
-          }
-        }
-      }
-      const unsigned klo = (unsigned)myk, khi = (unsigned)(myk >> 32);
-      const unsigned vlo = (unsigned)myv, vhi = (unsigned)(myv >> 32);
-      auto rd64 = [](unsigned lo, unsigned hi, int j) {
-        return ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)hi, j) << 32) |
-               (unsigned)__builtin_amdgcn_readlane((int)lo, j);
-      };
-      // max-merge: a candidate represents its key iff no candidate with that key
-      // has a larger value (lanes n..np-1 are empty and never match); loops take
-      // four lanes per step so that the readlanes of a step are independent
-      int rep = myk != kEmpty;
-      for (int j = 0; j < np; j += 4) {
-        int dom = 0;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const unsigned long long kj = rd64(klo, khi, j + u), vj = rd64(vlo, vhi, j + u);
-          dom |= kj == myk && vj > myv;
-        }
-        rep &= !dom;
-      }
-      // rank among the representatives by (score desc, key asc)
-      int rank = 0;
-      for (int j = 0; j < np; j += 4) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int rj = __builtin_amdgcn_readlane(rep, j + u);
-          const unsigned soj = (unsigned)__builtin_amdgcn_readlane((int)vhi, j + u);
-          const unsigned long long kj = rd64(klo, khi, j + u);
-          rank += rj && (soj > vhi || (soj == vhi && kj < myk));
-        }
-      }
-      const float sc = ord2f(vhi);
-      const int keep0 = rep && rank < Ns;
-      const float bst = wave_max_f(keep0 ? sc : -INFINITY);
-      const int keep2 = keep0 && sc >= bst - beam && rank < Nc;
-      int pos = 0;
-      for (int j = 0; j < np; j += 4) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int k2j = __builtin_amdgcn_readlane(keep2, j + u);
-          const unsigned long long kj = rd64(klo, khi, j + u);
-          pos += k2j && kj < myk;
-        }
-      }
-      const unsigned long long kept = __ballot(keep2);
-      if (keep2) s.n_ctx_list[pos] = (int)klo;
-      if (lane == 0) {
-        s.nK = __popcll(kept);
-        s.nC = __popcll(kept);
-        s.best = bst;
-      }
-      my_keep2 = keep2;
-      my_pos = pos;
-      my_crow = pos;
+      const WaveSel r = trivial_select_wave(s, ns, d.KT, V, Ns, Nc, beam, stride_tb, lane, 0, true);
+      my_keep2 = r.keep2;
+      my_pos = r.pos;
+      my_crow = r.pos;
       my_first = 1;
-      my_ci = klo;
-      my_st = khi;
-      my_sc = sc;
-      my_v = myv;
+      my_ci = r.ci;
+      my_st = r.st;
+      my_sc = r.sc;
+      my_v = r.v;
     }
     __syncthreads();
     best = s.best;
@@ -1582,74 +1648,88 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
 // per frame they exchange each row's (max, sum exp), best KT labels and blank logit
 // through tagged 64-bit words in uncached memory.
 
+constexpr int kResSlices = kKStep / 16;  // 16-byte k slices per wave of a resident W slice
+
 // Joiner of member columns [64 cg0, 64 (cg0 + NCG)) for all 4 RG rows, split over
 // K: wave w accumulates k slices [w Kpad / 16, (w + 1) Kpad / 16) (16-byte fp32
-// slices), lane l owning column 64 (cg0 + j) + l, h broadcast from LDS, W streamed
-// from the interleaved copy with the next chunk in flight.  The four waves' partial
-// sums meet in LDS (part, 4 x NCG x 4 RG x 64 floats) and are added in wave order.
-template <int RG, int NCG>
+// slices), lane l owning column 64 (cg0 + j) + l, h broadcast from LDS.  RES
+// (NCG = 1, Kpad = 512): the lane's 32 slices of W are in registers (wres) for the
+// whole decode; otherwise W is streamed from the interleaved copy with the next
+// chunk in flight.  Both add the slices in the same order.  The four waves'
+// partial sums go to LDS (part, [wave][NCG][4 RG][64]); the caller adds them in
+// wave order.
+template <int RG, int NCG, bool RES>
 __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* hl, int hstride,
-                                                 float* zl, float* part, int cg0) {
+                                                 float* part, int cg0,
+                                                 const float4 (&wres)[kResSlices]) {
   constexpr int NR = 4 * RG;
   constexpr int CH = 8 / NCG;  // k slices per chunk
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int V = m.V, Vpad = m.Vpad;
+  const int Vpad = m.Vpad;
   const int qw = m.Kpad / 16;  // k slices per wave (a multiple of 32)
   const int q0 = wave * qw;
-  const int steps = qw / CH;   // even
-  const float4* __restrict__ Wi = reinterpret_cast<const float4*>(m.Wi);
   const char* hrows = reinterpret_cast<const char*>(hl);
   const size_t rstride = (size_t)hstride * 4;
-  auto load_chunk = [&](int step, float4 (&w)[CH][NCG]) {
-#pragma unroll
-    for (int u = 0; u < CH; ++u) {
-      const size_t q = (size_t)(q0 + step * CH + u);
-#pragma unroll
-      for (int j = 0; j < NCG; ++j) w[u][j] = Wi[q * Vpad + (cg0 + j) * 64 + lane];
-    }
-  };
   float acc[NCG][NR];
 #pragma unroll
   for (int j = 0; j < NCG; ++j)
 #pragma unroll
     for (int r = 0; r < NR; ++r) acc[j][r] = 0.f;
-  auto compute = [&](int step, const float4 (&w)[CH][NCG]) {
+  if (RES) {
 #pragma unroll
-    for (int u = 0; u < CH; ++u) {
-      const size_t ko = (size_t)(q0 + step * CH + u) * 16;
+    for (int u = 0; u < kResSlices; ++u) {
+      const size_t ko = (size_t)(q0 + u) * 16;
 #pragma unroll
       for (int r = 0; r < NR; ++r) {
         const float4 a = *reinterpret_cast<const float4*>(hrows + (size_t)r * rstride + ko);
-#pragma unroll
-        for (int j = 0; j < NCG; ++j) {
-          acc[j][r] = fmaf(a.x, w[u][j].x, acc[j][r]);
-          acc[j][r] = fmaf(a.y, w[u][j].y, acc[j][r]);
-          acc[j][r] = fmaf(a.z, w[u][j].z, acc[j][r]);
-          acc[j][r] = fmaf(a.w, w[u][j].w, acc[j][r]);
-        }
+        acc[0][r] = fmaf(a.x, wres[u].x, acc[0][r]);
+        acc[0][r] = fmaf(a.y, wres[u].y, acc[0][r]);
+        acc[0][r] = fmaf(a.z, wres[u].z, acc[0][r]);
+        acc[0][r] = fmaf(a.w, wres[u].w, acc[0][r]);
       }
     }
-  };
-  float4 wa[CH][NCG], wb[CH][NCG];
-  load_chunk(0, wa);
-  for (int step = 0; step < steps; step += 2) {
-    load_chunk(step + 1, wb);
-    compute(step, wa);
-    load_chunk(min(step + 2, steps - 1), wa);
-    compute(step + 1, wb);
+  } else {
+    const int steps = qw / CH;   // even
+    const float4* __restrict__ Wi = reinterpret_cast<const float4*>(m.Wi);
+    auto load_chunk = [&](int step, float4 (&w)[CH][NCG]) {
+#pragma unroll
+      for (int u = 0; u < CH; ++u) {
+        const size_t q = (size_t)(q0 + step * CH + u);
+#pragma unroll
+        for (int j = 0; j < NCG; ++j) w[u][j] = Wi[q * Vpad + (cg0 + j) * 64 + lane];
+      }
+    };
+    auto compute = [&](int step, const float4 (&w)[CH][NCG]) {
+#pragma unroll
+      for (int u = 0; u < CH; ++u) {
+        const size_t ko = (size_t)(q0 + step * CH + u) * 16;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+          const float4 a = *reinterpret_cast<const float4*>(hrows + (size_t)r * rstride + ko);
+#pragma unroll
+          for (int j = 0; j < NCG; ++j) {
+            acc[j][r] = fmaf(a.x, w[u][j].x, acc[j][r]);
+            acc[j][r] = fmaf(a.y, w[u][j].y, acc[j][r]);
+            acc[j][r] = fmaf(a.z, w[u][j].z, acc[j][r]);
+            acc[j][r] = fmaf(a.w, w[u][j].w, acc[j][r]);
+          }
+        }
+      }
+    };
+    float4 wa[CH][NCG], wb[CH][NCG];
+    load_chunk(0, wa);
+    for (int step = 0; step < steps; step += 2) {
+      load_chunk(step + 1, wb);
+      compute(step, wa);
+      load_chunk(min(step + 2, steps - 1), wa);
+      compute(step + 1, wb);
+    }
   }
 #pragma unroll
   for (int j = 0; j < NCG; ++j)
 #pragma unroll
     for (int r = 0; r < NR; ++r) part[((wave * NCG + j) * NR + r) * 64 + lane] = acc[j][r];
   __syncthreads();
-  constexpr int PER = NCG * NR * 64;
-  for (int e = tid; e < PER; e += kSearchThreads) {
-    const int j = e / (NR * 64), r = (e / 64) % NR, l = e & 63;
-    const int col = (cg0 + j) * 64 + l;
-    const float z = ((part[e] + part[PER + e]) + part[2 * PER + e]) + part[3 * PER + e];
-    zl[(size_t)r * Vpad + col] = col < V ? z + m.bias[col] : -INFINITY;
-  }
 }
 
 // The member joiner's partial sums (4 waves x 2 column groups x 16 rows x 64 lanes)
@@ -1671,28 +1751,62 @@ struct GroupX {
   unsigned* err;
 };
 
+// LDS layout of the grouped kernel beyond SearchSmem.
+struct GroupLds {
+  int hoff, hstride;        // joiner rows [4 RG][hstride] fp32 (byte offset, row stride)
+  int doff;                 // fast path: per-wave decoder rows of the candidates
+                            // [4 waves][20][64] float2 (byte offset)
+};
+constexpr int kFastDecEntries = 20;  // 16 label candidates (i KT + q) + 4 current rows
+
 __device__ __forceinline__ unsigned long long* group_slot(const GroupX& x, int b, int g, int t) {
   return x.buf + ((size_t)(b * x.G + g) * 2 + (t & 1)) * x.xwords;
 }
 
-template <int RG, int NCG>
+// Grouped per-stream kernel.  Per frame: member joiner (partial sums per wave),
+// per-row statistics of the member's columns published as tagged words, the other
+// members' words polled, combined in member order, then the search.
+//
+// FAST (RG = 1, NCG = 1, resident W, Kpad = 512, at most 4 tuples): every wave runs
+// the one-wave selection itself (the results are identical), so that each wave can
+// build its own quarter of the next frame's joiner rows, the quarter its joiner
+// reads, without a workgroup barrier: the decoder rows ReLU(P0[a] + P1[b]) of every
+// candidate context are gathered at the wave's 128 columns (two per lane) into
+// registers before the selection, so their latency hides behind it, and the
+// decoder rows of the current contexts stay in registers for the blank
+// candidates.  The survivors alternate between two LDS buffers (wave 0 writes the
+// next frame's while the other waves may still read the current one).
+template <int RG, int NCG, bool RES, bool FAST>
 __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, GraphDev g, DecodeDev d,
                                                                  float beam, int* __restrict__ trace,
-                                                                 int hoff, int hstride, int zoff,
-                                                                 GroupX x) {
+                                                                 GroupLds ly, GroupX x) {
+  static_assert(!FAST || (RG == 1 && NCG == 1 && RES), "the fast path is for 4 rows, resident W");
   const int G = x.G;
   const int b = blockIdx.x / G, mem = blockIdx.x - b * G;
   const int L = d.len[b];
   if (L == 0) return;  // every member of the stream returns here
   extern __shared__ __align__(16) unsigned char smem[];
   SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
-  void* hl = smem + hoff;
-  float* zl = reinterpret_cast<float*>(smem + zoff);
+  unsigned char* hl = smem + ly.hoff;
+  const int hstride = ly.hstride;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int Ns = d.Ns, Nc = d.Nc, V = m.V, Vpad = m.Vpad, KT = d.KT;
+  const int Ns = d.Ns, Nc = d.Nc, V = m.V, C = m.C, Kpad = m.Kpad, KT = d.KT;
   const int RW = 3 + 2 * KT;  // words per row: max, sum exp, KT x (logit, label), blank logit
   const int cg0 = mem * NCG;
   const size_t row0 = (size_t)b * Nc;
+  const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
+  const bool writer = mem == 0;
+  // the member's W slice (RES) and bias, for the whole decode
+  float4 wres[kResSlices];
+  if (RES) {
+    const float4* __restrict__ Wi = reinterpret_cast<const float4*>(m.Wi);
+    const int q0 = wave * kResSlices;
+#pragma unroll
+    for (int u = 0; u < kResSlices; ++u) wres[u] = Wi[(size_t)(q0 + u) * m.Vpad + cg0 * 64 + lane];
+  }
+  float bias_r[NCG];
+#pragma unroll
+  for (int jj = 0; jj < NCG; ++jj) bias_r[jj] = m.bias[min((cg0 + jj) * 64 + lane, V - 1)];
   if (tid == 0) {
     s.ns = d.nsurv[b];
     s.nc = d.nctx[b];
@@ -1703,67 +1817,129 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     s.s_state[i] = d.surv_state[o];
     s.s_row[i] = d.surv_row[o];
     s.s_score[i] = d.surv_score[o];
+    s.s_bprev[i] = s.s_ctx[i] % V;
   }
   for (int j = tid; j < Nc; j += blockDim.x) {
     const int c = d.ctx_list[row0 + j], a = c / V;
-    s.n_rowoff[j] = make_int2(a * m.Kpad, (c - a * V) * m.Kpad);
+    s.n_rowoff[j] = make_int2(a * Kpad, (c - a * V) * Kpad);
   }
   {
-    const float* er = d.enc + (size_t)b * d.T * m.C;
-    for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
+    const float* er = d.enc + (size_t)b * d.T * C;
+    for (int k = tid; k < C; k += blockDim.x) s.enc_next[k] = er[k];
     const int words = RG * 4 * hstride;
     for (int i = tid; i < words; i += blockDim.x) reinterpret_cast<int*>(hl)[i] = 0;
   }
   __syncthreads();
   write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, s.nc, hl, hstride, tid);
   __syncthreads();
+  // FAST: this lane's two columns, the decoder rows of the current contexts there,
+  // the survivor buffer and the tuple / context counts of the current frame
+  const int k0 = 128 * wave + 2 * lane;
+  float2* dstage = reinterpret_cast<float2*>(smem + ly.doff) + (size_t)wave * kFastDecEntries * 64;
+  float2 dcur[4];
+  int ns_r = s.ns, nc_r = s.nc, sb = 0;
+  if (FAST) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dcur[j] = make_float2(0.f, 0.f);
+      if (j < nc_r) {
+        const int2 off = s.n_rowoff[j];
+        dcur[j].x = fmaxf(m.P0[(size_t)off.x + k0] + m.P1[(size_t)off.y + k0], 0.f);
+        dcur[j].y = fmaxf(m.P0[(size_t)off.x + k0 + 1] + m.P1[(size_t)off.y + k0 + 1], 0.f);
+      }
+    }
+  }
+  constexpr int NEP = FAST ? 1 : kMaxDim / kSearchThreads;
   for (int t = 0; t < L; ++t) {
+    // encoder frame t + 1, in flight during the joiner and the exchange
+    float encp[NEP];
+    float2 encf = make_float2(0.f, 0.f);
+    if (FAST) {
+      if (t + 1 < L) {
+        const float* er = d.enc + ((size_t)b * d.T + t + 1) * C;
+        encf.x = k0 < C ? er[k0] : 0.f;
+        encf.y = k0 + 1 < C ? er[k0 + 1] : 0.f;
+      }
+    } else {
+      const float* er = d.enc + ((size_t)b * d.T + min(t + 1, L - 1)) * C;
+#pragma unroll
+      for (int u = 0; u < NEP; ++u) {
+        const int k = tid + u * kSearchThreads;
+        encp[u] = k < C ? er[k] : 0.f;
+      }
+    }
     // the partial sums use the hash table's LDS, idle until the search
-    group_joiner_f32<RG, NCG>(m, hl, hstride, zl, reinterpret_cast<float*>(s.hk), cg0);
-    __syncthreads();
-    const int nc = s.nc;
+    float* part = reinterpret_cast<float*>(s.hk);
+    group_joiner_f32<RG, NCG, RES>(m, hl, hstride, part, cg0, wres);
+    const int nc = FAST ? nc_r : s.nc;
     const unsigned tag = (x.epoch << 16) | ((unsigned)t & 0xffffu);
-    // this member's row statistics over its columns -> tagged words
+    // this member's row statistics over its columns (partial sums added in wave
+    // order, bias, -inf beyond V) -> tagged words
     {
+      constexpr int NR = 4 * RG, PER = NCG * NR * 64;
       unsigned long long* slot = group_slot(x, b, mem, t);
       for (int j = wave; j < nc; j += 4) {
         float z[NCG];
-        unsigned long long key[NCG];
         float mx = -INFINITY;
 #pragma unroll
         for (int jj = 0; jj < NCG; ++jj) {
           const int col = (cg0 + jj) * 64 + lane;
-          z[jj] = zl[(size_t)j * Vpad + col];
+          const int e = (jj * NR + j) * 64 + lane;
+          const float zs = ((part[e] + part[PER + e]) + part[2 * PER + e]) + part[3 * PER + e];
+          z[jj] = col < V ? zs + bias_r[jj] : -INFINITY;
           mx = fmaxf(mx, z[jj]);
-          key[jj] = (col >= 1 && col < V)
-                        ? ((unsigned long long)f2ord(z[jj]) << 32) | (0xffffffffu - (unsigned)col)
-                        : 0ull;
         }
         const float M = wave_max_f(mx);
         float se = 0.f;
 #pragma unroll
         for (int jj = 0; jj < NCG; ++jj) se += __expf(z[jj] - M);
         const float S = wave_sum_f(se);
+        // best KT labels in 1..V-1 by (logit desc, label asc); lane q keeps the q-th
         float my_z = -INFINITY;
         int my_c = -1;
-        unsigned long long prev = ~0ull;
-        for (int q = 0; q < KT; ++q) {
-          unsigned long long mine = 0ull;
-#pragma unroll
-          for (int jj = 0; jj < NCG; ++jj) mine = (key[jj] < prev && key[jj] > mine) ? key[jj] : mine;
-          const unsigned long long best = wave_max_u64(mine);
-          if (lane == q && best != 0ull) {
-            my_z = ord2f((unsigned)(best >> 32));
-            my_c = (int)(0xffffffffu - (unsigned)best);
+        if (NCG == 1) {
+          // one column per lane: the wave maximum of the order-preserving code, the
+          // smallest lane among equal codes (columns rise with the lane)
+          const int col = cg0 * 64 + lane;
+          unsigned o = (col >= 1 && col < V) ? f2ord(z[0]) : 0u;
+          for (int q = 0; q < KT; ++q) {
+            const unsigned mo = wave_max_u32(o);
+            if (mo == 0u) break;
+            const int wl = __ffsll((long long)__ballot(o == mo)) - 1;
+            if (lane == q) {
+              my_z = ord2f(mo);
+              my_c = cg0 * 64 + wl;
+            }
+            if (lane == wl) o = 0u;
           }
-          prev = best ? best : 1ull;
+        } else {
+          unsigned long long key[NCG];
+#pragma unroll
+          for (int jj = 0; jj < NCG; ++jj) {
+            const int col = (cg0 + jj) * 64 + lane;
+            key[jj] = (col >= 1 && col < V)
+                          ? ((unsigned long long)f2ord(z[jj]) << 32) | (0xffffffffu - (unsigned)col)
+                          : 0ull;
+          }
+          unsigned long long prev = ~0ull;
+          for (int q = 0; q < KT; ++q) {
+            unsigned long long mine = 0ull;
+#pragma unroll
+            for (int jj = 0; jj < NCG; ++jj) mine = (key[jj] < prev && key[jj] > mine) ? key[jj] : mine;
+            const unsigned long long best = wave_max_u64(mine);
+            if (lane == q && best != 0ull) {
+              my_z = ord2f((unsigned)(best >> 32));
+              my_c = (int)(0xffffffffu - (unsigned)best);
+            }
+            prev = best ? best : 1ull;
+          }
         }
         unsigned long long* w = slot + (size_t)j * RW;
         const unsigned long long tg = (unsigned long long)tag << 32;
         if (lane == 0) {
           __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
           __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-          const float z0 = cg0 == 0 ? zl[(size_t)j * Vpad] : 0.f;
+          const float z0 = cg0 == 0 ? z[0] : 0.f;  // lane 0 of the first member holds label 0
           __hip_atomic_store(w + 2 + 2 * KT, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_SYSTEM);
         }
@@ -1794,9 +1970,17 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         xs[idx] = (unsigned)v;
       }
     }
+    if (!FAST && t + 1 < L) {
+#pragma unroll
+      for (int u = 0; u < NEP; ++u) {
+        const int k = tid + u * kSearchThreads;
+        if (k < C) s.enc_next[k] = encp[u];
+      }
+    }
     __syncthreads();
     // combine in member order (identical in every member): normaliser, blank logit,
-    // best KT labels over the G lists (the members' columns are disjoint)
+    // best KT labels over the G lists (the members' columns are disjoint, so the
+    // labels are distinct)
     for (int j = wave; j < nc; j += 4) {
       // (the wave reductions combine in a fixed order, the same in every member)
       const float Mg = lane < G ? __uint_as_float(xs[(lane * nc + j) * RW]) : -INFINITY;
@@ -1808,35 +1992,183 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         s.s_z0[j] = __uint_as_float(xs[j * RW + 2 + 2 * KT]);
       }
       const int ne = G * KT;
-      unsigned long long kv[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int e = lane + 64 * h;
-        kv[h] = 0ull;
-        if (e < ne) {
-          const int g2 = e / KT, q = e - g2 * KT;
+      if (ne <= 64) {
+        // one entry per lane: wave maximum of the code; equal codes (rare) go to the
+        // smaller label
+        unsigned o = 0u, c = 0xffffffffu;
+        if (lane < ne) {
+          const int g2 = lane / KT, q = lane - g2 * KT;
           const unsigned* w = xs + (g2 * nc + j) * RW + 2 + 2 * q;
-          const int c = (int)w[1];
-          if (c >= 0)
-            kv[h] = ((unsigned long long)f2ord(__uint_as_float(w[0])) << 32) | (0xffffffffu - (unsigned)c);
+          if ((int)w[1] >= 0) {
+            o = f2ord(__uint_as_float(w[0]));
+            c = w[1];
+          }
         }
-      }
-      unsigned long long prev = ~0ull;
-      for (int q = 0; q < KT; ++q) {
-        unsigned long long mine = 0ull;
+        for (int q = 0; q < KT; ++q) {
+          const unsigned mo = wave_max_u32(o);
+          float zq = -INFINITY;
+          int cq = -1;
+          if (mo != 0u) {
+            unsigned long long bal = __ballot(o == mo);
+            if (__popcll(bal) > 1) {
+              const unsigned cm = wave_min_u32(o == mo ? c : 0xffffffffu);
+              bal = __ballot(o == mo && c == cm);
+            }
+            const int wl = __ffsll((long long)bal) - 1;
+            zq = ord2f(mo);
+            cq = __builtin_amdgcn_readlane((int)c, wl);
+            if (lane == wl) o = 0u;
+          }
+          if (lane == 0) {
+            s.rk_z[j * KT + q] = zq;
+            s.rk_c[j * KT + q] = cq;
+          }
+        }
+      } else {
+        unsigned long long kv[2];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) mine = (kv[h] < prev && kv[h] > mine) ? kv[h] : mine;
-        const unsigned long long best = wave_max_u64(mine);
-        if (lane == 0) {
-          s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
-          s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+        for (int h = 0; h < 2; ++h) {
+          const int e = lane + 64 * h;
+          kv[h] = 0ull;
+          if (e < ne) {
+            const int g2 = e / KT, q = e - g2 * KT;
+            const unsigned* w = xs + (g2 * nc + j) * RW + 2 + 2 * q;
+            const int c = (int)w[1];
+            if (c >= 0)
+              kv[h] = ((unsigned long long)f2ord(__uint_as_float(w[0])) << 32) | (0xffffffffu - (unsigned)c);
+          }
         }
-        prev = best ? best : 1ull;
+        unsigned long long prev = ~0ull;
+        for (int q = 0; q < KT; ++q) {
+          unsigned long long mine = 0ull;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) mine = (kv[h] < prev && kv[h] > mine) ? kv[h] : mine;
+          const unsigned long long best = wave_max_u64(mine);
+          if (lane == 0) {
+            s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
+            s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+          }
+          prev = best ? best : 1ull;
+        }
       }
     }
     __syncthreads();
-    search_frame<true, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, zl, true, mem == 0);
-    __syncthreads();
+    if (!FAST) {
+      search_frame<true, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, nullptr, true,
+                               writer, true);
+      __syncthreads();
+      continue;
+    }
+    // ---- fast path: no workgroup barrier until the next frame's joiner ----
+    // decoder-row inputs of every label candidate (survivor i, label q) at this
+    // lane's two columns; every load is issued (clamped), then the selection runs
+    // (on this path every context holds one tuple, so survivor i sits on context row
+    // i; all of these LDS reads are in bounds and issued together)
+    int pa[4], pb[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      pa[i] = s.s_bprev[sb + i];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pb[i][q] = s.rk_c[i * KT + q];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      pa[i] = i < ns_r ? pa[i] : 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pb[i][q] = (i < ns_r && q < KT) ? pb[i][q] : -1;
+    }
+    float2 p0[4], p1[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p0[i] = *reinterpret_cast<const float2*>(m.P0 + (size_t)pa[i] * kKStep + k0);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        p1[i][q] = *reinterpret_cast<const float2*>(m.P1 + (size_t)max(pb[i][q], 0) * kKStep + k0);
+    }
+    const WaveSel sel = trivial_select_wave(s, ns_r, KT, V, Ns, Nc, beam, stride_tb, lane, sb, false);
+    const int nk = sel.nk;
+    const float best = sel.best;
+    // decoder rows at this lane's columns of every candidate, staged in the wave's
+    // LDS area by source index: label candidate i KT + q, blank of row r at 16 + r
+    {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (q < KT)
+            dstage[(i * KT + q) * 64 + lane] =
+                make_float2(fmaxf(p0[i].x + p1[i][q].x, 0.f), fmaxf(p0[i].y + p1[i][q].y, 0.f));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dstage[(16 + r) * 64 + lane] = dcur[r];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // each new context row j: its decoder row and, unless this is the stream's last
+    // frame, its joiner row h = tanh(enc[t + 1] + decoder row) at this lane's columns
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const unsigned long long mj = __ballot(sel.keep2 && sel.pos == j);
+      if (mj == 0ull) continue;
+      const int src = __builtin_amdgcn_readlane(sel.src, __ffsll((long long)mj) - 1);
+      const float2 dv = dstage[(src >= 0 ? src : 15 - src) * 64 + lane];
+      dcur[j] = dv;
+      if (t + 1 < L) {
+        float2 h;
+        h.x = k0 < C ? tanh_fast(encf.x + dv.x) : 0.f;
+        h.y = k0 + 1 < C ? tanh_fast(encf.y + dv.y) : 0.f;
+        *reinterpret_cast<float2*>(hl + ((size_t)j * hstride + k0) * 4) = h;
+      }
+    }
+    // survivors of the next frame (other buffer), history, trace, outputs
+    const int nb = sb ^ 4;
+    const bool store_surv = writer && t + 1 == L;
+    if (wave == 0 && sel.keep2) {
+      const int pos = sel.pos;
+      const unsigned tb = 0xffffffffu - (unsigned)sel.v;
+      const int parent = (int)(tb / stride_tb);
+      const int arc = (int)(tb - (unsigned)parent * stride_tb) - 1;  // label - 1, or -1 (blank)
+      const int label = arc + 1;
+      s.s_ctx[nb + pos] = (int)sel.ci;
+      s.s_state[nb + pos] = (int)sel.st;
+      s.s_score[nb + pos] = sel.sc - best;
+      s.s_row[nb + pos] = pos;
+      s.s_bprev[nb + pos] = (int)(sel.ci % (unsigned)V);
+      if (store_surv) {
+        const size_t o = (size_t)b * Ns + pos;
+        d.surv_ctx[o] = (int)sel.ci;
+        d.surv_state[o] = (int)sel.st;
+        d.surv_score[o] = sel.sc - best;
+        d.surv_row[o] = pos;
+        d.ctx_list[row0 + pos] = (int)sel.ci;
+      }
+      if (writer) {
+        const size_t hb = ((size_t)t * d.B + b) * Ns + pos;
+        d.hist_pl[hb] = (parent << 16) | label;
+        d.hist_arc[hb] = arc;
+        if (trace) {
+          int* tr = trace + (((size_t)(t + 1) * d.B + b) * Ns + pos) * 4;
+          tr[0] = (int)sel.ci;
+          tr[1] = (int)sel.st;
+          tr[2] = parent;
+          tr[3] = label;
+        }
+      }
+    }
+    if (tid == 0 && writer) {
+      if (store_surv) {
+        d.nsurv[b] = nk;
+        d.nctx[b] = nk;
+      }
+      d.offset[b] += (double)best;
+    }
+    sb = nb;
+    ns_r = nk;
+    nc_r = nk;
+    // this wave's joiner reads only the rows it has just written
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
@@ -2120,34 +2452,36 @@ hipError_t launch_stream(const ModelDev& m, const GraphDev& g, const DecodeDev& 
 
 int group_words(int Nc, int KT) { return Nc * (3 + 2 * KT); }
 
-template <int RG, int NCG>
+template <int RG, int NCG, bool RES, bool FAST>
 hipError_t launch_group_t(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
-                          int* trace, const StreamPlan& p, const GroupX& x, hipStream_t st) {
+                          int* trace, const GroupLds& ly, size_t lds, const GroupX& x,
+                          hipStream_t st) {
   static size_t attr = 0;
-  if (p.lds > attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_stream_group<RG, NCG>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+  if (lds > attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_stream_group<RG, NCG, RES, FAST>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    attr = p.lds;
+    attr = lds;
   }
   ModelDev ma = m;
   GraphDev ga = g;
   DecodeDev da = d;
+  GroupLds la = ly;
   GroupX xa = x;
-  int hoff = p.hoff, hstride = p.hstride, zoff = p.zoff;
-  void* args[] = {&ma, &ga, &da, &beam, &trace, &hoff, &hstride, &zoff, &xa};
-  return hipLaunchCooperativeKernel((const void*)k_stream_group<RG, NCG>, dim3(d.B * x.G),
-                                    dim3(kSearchThreads), args, (unsigned)p.lds, st);
+  void* args[] = {&ma, &ga, &da, &beam, &trace, &la, &xa};
+  return hipLaunchCooperativeKernel((const void*)k_stream_group<RG, NCG, RES, FAST>,
+                                    dim3(d.B * x.G), dim3(kSearchThreads), args, (unsigned)lds, st);
 }
 
-template <int NCG>
-hipError_t launch_group_rg(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
-                           int* trace, const StreamPlan& p, const GroupX& x, hipStream_t st) {
-  switch (p.RG) {
-    case 1: return launch_group_t<1, NCG>(m, g, d, beam, trace, p, x, st);
-    case 2: return launch_group_t<2, NCG>(m, g, d, beam, trace, p, x, st);
-    case 3: return launch_group_t<3, NCG>(m, g, d, beam, trace, p, x, st);
-    default: return launch_group_t<4, NCG>(m, g, d, beam, trace, p, x, st);
+template <int NCG, bool RES>
+hipError_t launch_group_rg(int RG, const ModelDev& m, const GraphDev& g, const DecodeDev& d,
+                           float beam, int* trace, const GroupLds& ly, size_t lds, const GroupX& x,
+                           hipStream_t st) {
+  switch (RG) {
+    case 1: return launch_group_t<1, NCG, RES, false>(m, g, d, beam, trace, ly, lds, x, st);
+    case 2: return launch_group_t<2, NCG, RES, false>(m, g, d, beam, trace, ly, lds, x, st);
+    case 3: return launch_group_t<3, NCG, RES, false>(m, g, d, beam, trace, ly, lds, x, st);
+    default: return launch_group_t<4, NCG, RES, false>(m, g, d, beam, trace, ly, lds, x, st);
   }
 }
 
@@ -2159,8 +2493,18 @@ hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const Decod
   if (!p.ok || m.bf16 || d.KT <= 0 || G < 2 || ncg % G != 0 || ncg / G > 2)
     return hipErrorInvalidValue;
   GroupX x{xbuf, G, group_words(d.Nc, d.KT), epoch & 0xffffu, spin_limit, err};
-  return ncg / G == 1 ? launch_group_rg<1>(m, g, d, beam, trace, p, x, st)
-                      : launch_group_rg<2>(m, g, d, beam, trace, p, x, st);
+  // LDS: the search state, the joiner rows and (fast path) the staged decoder rows
+  GroupLds ly{p.hoff, p.hstride, p.hoff + p.RG * 4 * p.hstride * 4};
+  // one column group per member and K = 512: the member's W slice stays in registers;
+  // with at most 4 tuples (4 rows) the per-wave fast path
+  const bool res = ncg / G == 1 && m.Kpad == kKStep;
+  const bool fast = res && p.RG == 1 && d.Ns <= 4 && d.KT == d.Ns;
+  const size_t lds = (size_t)ly.doff + (fast ? (size_t)4 * kFastDecEntries * 64 * sizeof(float2) : 0);
+  if (lds > kMaxLds) return hipErrorInvalidValue;
+  if (ncg / G == 2) return launch_group_rg<2, false>(p.RG, m, g, d, beam, trace, ly, lds, x, st);
+  if (fast) return launch_group_t<1, 1, true, true>(m, g, d, beam, trace, ly, lds, x, st);
+  return res ? launch_group_rg<1, true>(p.RG, m, g, d, beam, trace, ly, lds, x, st)
+             : launch_group_rg<1, false>(p.RG, m, g, d, beam, trace, ly, lds, x, st);
 }
 
 hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, int* out_ntok,
