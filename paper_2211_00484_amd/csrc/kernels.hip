@@ -740,9 +740,12 @@ struct WaveSel {
 // own.  Survivors are read at offset sb of the survivor arrays, with the row
 // normalisers and each row's best labels (rk_z, rk_c, s_z0).  publish: also write
 // n_ctx_list, nK, nC and best.
-__device__ __forceinline__ WaveSel trivial_select_wave(SearchSmem& s, int ns, int KT, int V, int Ns,
+// KTC > 0: the number of labels per row is the compile-time KTC (KT is ignored).
+template <int KTC = 0>
+__device__ __forceinline__ WaveSel trivial_select_wave(SearchSmem& s, int ns, int KT_, int V, int Ns,
                                                        int Nc, float beam, unsigned stride_tb,
                                                        int lane, int sb, bool publish) {
+  const int KT = KTC > 0 ? KTC : KT_;
   const int P = 1 + KT, n = ns * P;
   unsigned long long myk = kEmpty, myv = 0ull;
   int src = 0;
@@ -1790,7 +1793,8 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
   unsigned char* hl = smem + ly.hoff;
   const int hstride = ly.hstride;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int Ns = d.Ns, Nc = d.Nc, V = m.V, C = m.C, Kpad = m.Kpad, KT = d.KT;
+  const int Ns = d.Ns, Nc = d.Nc, V = m.V, C = m.C, Kpad = m.Kpad;
+  const int KT = FAST ? 4 : d.KT;  // the fast path runs max_states = 4 (4 labels per row)
   const int RW = 3 + 2 * KT;  // words per row: max, sum exp, KT x (logit, label), blank logit
   const int cg0 = mem * NCG;
   const size_t row0 = (size_t)b * Nc;
@@ -2063,19 +2067,18 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     // decoder-row inputs of every label candidate (survivor i, label q) at this
     // lane's two columns; every load is issued (clamped), then the selection runs
     // (on this path every context holds one tuple, so survivor i sits on context row
-    // i; all of these LDS reads are in bounds and issued together)
+    // i.  The LDS reads are unconditional and issued together; entries of absent
+    // survivors or labels may hold anything and are mapped into row 0, never used)
     int pa[4], pb[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      pa[i] = s.s_bprev[sb + i];
+      const int a = s.s_bprev[sb + i];
+      pa[i] = (unsigned)a < (unsigned)V ? a : 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) pb[i][q] = s.rk_c[i * KT + q];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      pa[i] = i < ns_r ? pa[i] : 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) pb[i][q] = (i < ns_r && q < KT) ? pb[i][q] : -1;
+      for (int q = 0; q < 4; ++q) {
+        const int c = s.rk_c[i * 4 + q];
+        pb[i][q] = (unsigned)c < (unsigned)V ? c : 0;
+      }
     }
     float2 p0[4], p1[4][4];
 #pragma unroll
@@ -2083,42 +2086,44 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
       p0[i] = *reinterpret_cast<const float2*>(m.P0 + (size_t)pa[i] * kKStep + k0);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        p1[i][q] = *reinterpret_cast<const float2*>(m.P1 + (size_t)max(pb[i][q], 0) * kKStep + k0);
+        p1[i][q] = *reinterpret_cast<const float2*>(m.P1 + (size_t)pb[i][q] * kKStep + k0);
     }
-    const WaveSel sel = trivial_select_wave(s, ns_r, KT, V, Ns, Nc, beam, stride_tb, lane, sb, false);
+    const WaveSel sel =
+        trivial_select_wave<4>(s, ns_r, 4, V, Ns, Nc, beam, stride_tb, lane, sb, false);
     const int nk = sel.nk;
     const float best = sel.best;
     // decoder rows at this lane's columns of every candidate, staged in the wave's
-    // LDS area by source index: label candidate i KT + q, blank of row r at 16 + r
-    {
+    // LDS area by source index: label candidate 4 i + q, blank of row r at 16 + r
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (q < KT)
-            dstage[(i * KT + q) * 64 + lane] =
-                make_float2(fmaxf(p0[i].x + p1[i][q].x, 0.f), fmaxf(p0[i].y + p1[i][q].y, 0.f));
+      for (int q = 0; q < 4; ++q)
+        dstage[(4 * i + q) * 64 + lane] =
+            make_float2(fmaxf(p0[i].x + p1[i][q].x, 0.f), fmaxf(p0[i].y + p1[i][q].y, 0.f));
 #pragma unroll
-      for (int r = 0; r < 4; ++r) dstage[(16 + r) * 64 + lane] = dcur[r];
-    }
+    for (int r = 0; r < 4; ++r) dstage[(16 + r) * 64 + lane] = dcur[r];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // each new context row j: its decoder row and, unless this is the stream's last
-    // frame, its joiner row h = tanh(enc[t + 1] + decoder row) at this lane's columns
+    // each new context row j: its decoder row and its joiner row h = tanh(enc[t + 1] +
+    // decoder row) at this lane's columns.  Rows j >= nk are computed from a stale
+    // source and never read; columns k >= C come out exactly 0 (all inputs are zero
+    // there and tanh(0) = 0); at the stream's last frame the rows are not read.
+    int srcj[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const unsigned long long mj = __ballot(sel.keep2 && sel.pos == j);
-      if (mj == 0ull) continue;
-      const int src = __builtin_amdgcn_readlane(sel.src, __ffsll((long long)mj) - 1);
-      const float2 dv = dstage[(src >= 0 ? src : 15 - src) * 64 + lane];
-      dcur[j] = dv;
-      if (t + 1 < L) {
-        float2 h;
-        h.x = k0 < C ? tanh_fast(encf.x + dv.x) : 0.f;
-        h.y = k0 + 1 < C ? tanh_fast(encf.y + dv.y) : 0.f;
-        *reinterpret_cast<float2*>(hl + ((size_t)j * hstride + k0) * 4) = h;
-      }
+      const int sj = __builtin_amdgcn_readlane(sel.src, mj ? __ffsll((long long)mj) - 1 : 0);
+      srcj[j] = mj ? (sj >= 0 ? sj : 15 - sj) : 16;
+    }
+    float2 dv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dv[j] = dstage[srcj[j] * 64 + lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dcur[j] = dv[j];
+      const float2 h = make_float2(tanh_fast(encf.x + dv[j].x), tanh_fast(encf.y + dv[j].y));
+      *reinterpret_cast<float2*>(hl + ((size_t)j * hstride + k0) * 4) = h;
     }
     // survivors of the next frame (other buffer), history, trace, outputs
     const int nb = sb ^ 4;
@@ -2498,7 +2503,7 @@ hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const Decod
   // one column group per member and K = 512: the member's W slice stays in registers;
   // with at most 4 tuples (4 rows) the per-wave fast path
   const bool res = ncg / G == 1 && m.Kpad == kKStep;
-  const bool fast = res && p.RG == 1 && d.Ns <= 4 && d.KT == d.Ns;
+  const bool fast = res && p.RG == 1 && d.Ns == 4 && d.KT == 4;
   const size_t lds = (size_t)ly.doff + (fast ? (size_t)4 * kFastDecEntries * 64 * sizeof(float2) : 0);
   if (lds > kMaxLds) return hipErrorInvalidValue;
   if (ncg / G == 2) return launch_group_rg<2, false>(p.RG, m, g, d, beam, trace, ly, lds, x, st);
