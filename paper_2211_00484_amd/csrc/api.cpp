@@ -591,7 +591,7 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   d.hist_arc = w.hist_arc;
   d.path_lab = w.path_lab;
   const GraphDev gd = graph_dev(graph);
-  const JoinerPlan plan = plan_joiner(B * Nc, m->Vpad, m->Kpad, m->bf16);
+  const JoinerPlan plan = plan_joiner(B * Nc, m->Vpad, m->Kpad, m->bf16, m->ncu);
 
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
@@ -667,7 +667,7 @@ tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const 
     m->rows_cap = Rpad;
   }
   HIP_TRY(launch_joiner_rows(model_dev(m), enc_rows, ctx, R, m->rows_h, m->rows_logits,
-                             m->rows_stats, out_logp, st),
+                             m->rows_stats, out_logp, m->ncu, st),
           "launch(joiner_rows)");
   return TBS_OK;
 }

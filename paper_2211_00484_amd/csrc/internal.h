@@ -74,13 +74,13 @@ struct DecodeDev {
 };
 
 struct JoinerPlan {
-  int MB;                   // 16-row MFMA blocks per tile
+  int MB;                   // 0: 128 x 128 GEMM tiles; else 16 MB x 64 tiles
   int n_rt, n_ct;           // row and column tiles
   int grid;                 // workgroups (XCD-interleaved tile order)
   size_t lds;               // dynamic LDS bytes
 };
 
-JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16);
+JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu);
 
 // Per-stream kernel (one workgroup runs every frame of one stream).
 struct StreamPlan {
@@ -119,7 +119,7 @@ hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, 
                         double* out_scores, int* out_status, int* out_arcs,
                         const unsigned* exchange_err, hipStream_t st);
 hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const int* ctx, int R,
-                              void* h, float* logits, float2* stats, float* out_logp,
+                              void* h, float* logits, float2* stats, float* out_logp, int ncu,
                               hipStream_t st);
 
 }  // namespace tbs

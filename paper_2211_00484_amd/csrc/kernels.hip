@@ -287,7 +287,8 @@ struct JoinArgs {
   int* tk_c;
   float* z0;                // [R] (TOPK)
   int KT;
-  int R, n_rt, n_ct;
+  int R, n_rt, n_ct;        // rows; row and column tiles (128 x 128)
+  int nvt;                  // 64-column vocabulary tiles (stats and label lists)
   int rows_mode;            // 1: every row < R is active
   const int* len;
   const int* nctx;
@@ -301,7 +302,8 @@ __device__ __forceinline__ bool joiner_row_active(const JoinArgs& a, int r) {
   return a.t < a.len[b] && j < a.nctx[b];
 }
 
-// Tile = (16 * MB rows) x 64 vocabulary columns; wave w owns columns 16w..16w+15
+// Small joiner tile, for batches too small to give every compute unit a 128 x 128
+// tile: (16 * MB rows) x 64 vocabulary columns; wave w owns columns 16w..16w+15
 // and keeps its W fragment (16 columns x up to 512 of K) in registers while it
 // sweeps the tile's row blocks, whose h rows are staged once in LDS.
 struct JoinShared {
@@ -312,7 +314,7 @@ struct JoinShared {
 // One joiner tile (16 * MB rows x 64 vocabulary columns) of frame a.t.  Uniform
 // across the workgroup; a tile without active rows computes nothing.
 template <bool BF16, int MB, bool TOPK>
-__device__ __forceinline__ void joiner_tile(const ModelDev& m, const JoinArgs& a, int ct, int rt,
+__device__ __forceinline__ void joiner_tile_small(const ModelDev& m, const JoinArgs& a, int ct, int rt,
                                             unsigned char* smem, JoinShared& js) {
   int* s_act = js.act;
   float(*s_m)[64] = js.m;
@@ -495,7 +497,7 @@ __device__ __forceinline__ void joiner_tile(const ModelDev& m, const JoinArgs& a
 }
 
 template <bool BF16, int MB, bool TOPK>
-__global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
+__global__ __launch_bounds__(256) void k_joiner_small(ModelDev m, JoinArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ JoinShared js;
   // Workgroup i runs on XCD i mod 8.  XCD x owns the column tiles x, x + 8, ...
@@ -505,7 +507,180 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
   const int ncx = (a.n_ct + 7) >> 3;
   const int rt = slot / ncx, ct = xcd + 8 * (slot - rt * ncx);
   if (ct >= a.n_ct) return;
-  joiner_tile<BF16, MB, TOPK>(m, a, ct, rt, smem, js);
+  joiner_tile_small<BF16, MB, TOPK>(m, a, ct, rt, smem, js);
+}
+
+// Joiner GEMM tile: 128 rows x 128 vocabulary columns, four waves in a 2 x 2 grid,
+// each wave 64 rows x 64 columns (4 x 4 MFMA blocks of 16 x 16).  Both operands go
+// through LDS in K slices of 128 bytes per row (64 bf16 or 32 fp32 values), two
+// buffers deep: while the waves run the MFMAs of slice s, slice s + 1 is fetched
+// into registers and then written to the other buffer (one barrier per slice).  A
+// wave's 64 columns are one vocabulary tile, so its epilogue produces that tile's
+// (max, sum exp) per row and either the logits or each row's best labels per
+// 16-column sub-tile.
+constexpr int kJBM = 128, kJBN = 128;          // tile rows, columns
+constexpr int kJSlice = 128;                   // bytes of K per row and slice
+constexpr int kJRow = kJSlice + 16;            // LDS row stride (pad: conflict-free fragment reads)
+constexpr int kJStage = (kJBM + kJBN) * kJRow; // bytes per buffer: A rows, then B rows
+constexpr size_t kJLds = 2 * (size_t)kJStage;  // 73,728 bytes
+
+template <bool BF16, bool TOPK>
+__global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int s_act[kJBM];
+  // Workgroup i runs on XCD i mod 8.  XCD x owns the column tiles x, x + 8, ...
+  // and walks row tiles in order, its column tiles fastest: its W columns stay
+  // in its L2 while each h row tile is read once per XCD.
+  const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
+  const int ncx = (a.n_ct + 7) >> 3;
+  const int rt = slot / ncx, ct = xcd + 8 * (slot - rt * ncx);
+  if (ct >= a.n_ct) return;
+  constexpr int ESZ = BF16 ? 2 : 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int r0 = rt * kJBM, c0 = ct * kJBN;
+  const int Kpad = m.Kpad, V = m.V, Vpad = m.Vpad, nvt = a.nvt;
+  const int vt = 2 * ct + wc;  // this wave's vocabulary tile
+  const int act = tid < kJBM ? (int)joiner_row_active(a, r0 + tid) : 0;
+  if (tid < kJBM) s_act[tid] = act;
+  if (!__syncthreads_or(act)) return;  // uniform: no active row in this tile
+
+  // slice loads: 4 chunks of 16 bytes per thread for each operand (128 rows x 8 chunks)
+  const char* hsrc = reinterpret_cast<const char*>(a.h);
+  const char* wsrc = BF16 ? reinterpret_cast<const char*>(m.Wb) : reinterpret_cast<const char*>(m.Wf);
+  const size_t rowb = (size_t)Kpad * ESZ;
+  uint4 ra[4], rb[4];
+  auto gload = [&](int s) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = tid + 256 * u, row = c >> 3, part = c & 7;
+      const size_t off = (size_t)s * kJSlice + part * 16;
+      ra[u] = r0 + row < a.R ? *reinterpret_cast<const uint4*>(hsrc + (size_t)(r0 + row) * rowb + off)
+                             : make_uint4(0, 0, 0, 0);
+      rb[u] = c0 + row < Vpad ? *reinterpret_cast<const uint4*>(wsrc + (size_t)(c0 + row) * rowb + off)
+                              : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto lstore = [&](int buf) {
+    unsigned char* base = smem + (size_t)buf * kJStage;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = tid + 256 * u, row = c >> 3, part = c & 7;
+      *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + part * 16) = ra[u];
+      *reinterpret_cast<uint4*>(base + (size_t)(kJBM + row) * kJRow + part * 16) = rb[u];
+    }
+  };
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // one slice of MFMAs from LDS buffer buf; fragments: lane (lr, lg) reads 16 bytes
+  // of row lr of a block at byte 64 j + 16 lg of the slice (bf16: k-step j of 32;
+  // fp32: group j of 16, the four values feeding four k-steps)
+  auto compute = [&](int buf) {
+    const unsigned char* base = smem + (size_t)buf * kJStage;
+    const unsigned char* abase = base + (size_t)(64 * wr + lr) * kJRow + 16 * lg;
+    const unsigned char* bbase = base + (size_t)(kJBM + 64 * wc + lr) * kJRow + 16 * lg;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      uint4 fa[4], fb[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + 64 * j);
+        fb[q] = *reinterpret_cast<const uint4*>(bbase + (size_t)16 * q * kJRow + 64 * j);
+      }
+      if (BF16) {
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[mb]), as_bf16x8(fb[nb]),
+                                                                  acc[mb][nb], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) {
+              const float av = __uint_as_float(u == 0 ? fa[mb].x : u == 1 ? fa[mb].y : u == 2 ? fa[mb].z : fa[mb].w);
+              const float bv = __uint_as_float(u == 0 ? fb[nb].x : u == 1 ? fb[nb].y : u == 2 ? fb[nb].z : fb[nb].w);
+              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[mb][nb], 0, 0, 0);
+            }
+      }
+    }
+  };
+  const int nsl = (int)(rowb / kJSlice);  // Kpad is a multiple of 512: 8 (bf16) or 16 (fp32) per 512
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int s = 0; s < nsl; ++s) {
+    if (s + 1 < nsl) gload(s + 1);
+    compute(s & 1);
+    if (s + 1 < nsl) lstore((s + 1) & 1);
+    __syncthreads();
+  }
+
+  // epilogue of this wave's vocabulary tile (none beyond the padded vocabulary)
+  if (vt >= nvt) return;
+  float bias[4];
+  bool cvalid[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    const int col = 64 * vt + 16 * nb + lr;
+    cvalid[nb] = col < V;
+    bias[nb] = cvalid[nb] ? m.bias[col] : 0.f;
+  }
+  const int nsub = nvt * (kJoinerBN / 16);
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 64 * wr + 16 * mb + 4 * lg + i;  // the 16 lanes of a DPP row share it
+      const bool ract = s_act[row];
+      float z[4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        z[nb] = cvalid[nb] ? acc[mb][nb][i] + bias[nb] : -INFINITY;
+        mx = fmaxf(mx, z[nb]);
+      }
+      const float M = row16_max(mx);
+      float e = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) e += cvalid[nb] ? expf(z[nb] - M) : 0.f;
+      const float S = row16_sum(e);
+      if (ract && lr == 0) a.stats[(size_t)(r0 + row) * nvt + vt] = make_float2(M, S);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int col = 64 * vt + 16 * nb + lr;
+        if (!TOPK) {
+          if (ract && cvalid[nb]) a.logits[(size_t)(r0 + row) * (nvt * kJoinerBN) + col] = z[nb];
+        } else {
+          // each row's best KT labels of this 16-column sub-tile (DPP row reductions)
+          unsigned long long key = (cvalid[nb] && col >= 1)
+                                       ? ((unsigned long long)f2ord(z[nb]) << 32) | (0xffffffffu - (unsigned)col)
+                                       : 0ull;
+          const size_t ob = ((size_t)(r0 + row) * nsub + vt * (kJoinerBN / 16) + nb) * a.KT;
+          for (int q = 0; q < a.KT; ++q) {
+            const unsigned long long best = row16_max_u64(key);
+            if (ract && best != 0ull && key == best) {
+              a.tk_z[ob + q] = z[nb];
+              a.tk_c[ob + q] = col;
+            }
+            if (ract && best == 0ull && lr == 0) {
+              a.tk_z[ob + q] = -INFINITY;
+              a.tk_c[ob + q] = -1;
+            }
+            if (key == best) key = 0ull;
+          }
+        }
+      }
+      if (TOPK && ract && vt == 0 && lr == 0) a.z0[r0 + row] = z[0];
+    }
+  }
 }
 
 __global__ void k_logp_rows(const float* __restrict__ logits, const float2* __restrict__ stats,
@@ -2278,59 +2453,86 @@ inline int grid_for(long long n, int threads, int cap = 4096) {
   return (int)g;
 }
 
-template <bool BF16, int MB, bool TOPK>
+template <bool BF16, bool TOPK>
 hipError_t launch_joiner_t(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p,
                            hipStream_t st) {
   static size_t attr = 0;  // dynamic LDS limit granted so far (kernel default: 64 KiB)
   if (p.lds > 65536 && p.lds > attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_joiner<BF16, MB, TOPK>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_joiner<BF16, TOPK>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
     if (e != hipSuccess) return e;
     attr = p.lds;
   }
-  hipLaunchKernelGGL((k_joiner<BF16, MB, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
+  hipLaunchKernelGGL((k_joiner<BF16, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
+  return hipGetLastError();
+}
+
+template <bool BF16, int MB, bool TOPK>
+hipError_t launch_joiner_small_t(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p,
+                                 hipStream_t st) {
+  static size_t attr = 0;
+  if (p.lds > 65536 && p.lds > attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_joiner_small<BF16, MB, TOPK>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+    if (e != hipSuccess) return e;
+    attr = p.lds;
+  }
+  hipLaunchKernelGGL((k_joiner_small<BF16, MB, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
   return hipGetLastError();
 }
 
 template <bool BF16, bool TOPK>
-hipError_t launch_joiner_mb(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p,
-                            hipStream_t st) {
+hipError_t launch_joiner_small(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p,
+                               hipStream_t st) {
   switch (p.MB) {
-    case 1: return launch_joiner_t<BF16, 1, TOPK>(m, a, p, st);
-    case 2: return launch_joiner_t<BF16, 2, TOPK>(m, a, p, st);
-    default: return launch_joiner_t<BF16, 4, TOPK>(m, a, p, st);
+    case 1: return launch_joiner_small_t<BF16, 1, TOPK>(m, a, p, st);
+    case 2: return launch_joiner_small_t<BF16, 2, TOPK>(m, a, p, st);
+    default: return launch_joiner_small_t<BF16, 4, TOPK>(m, a, p, st);
   }
 }
 
 hipError_t launch_joiner(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p, bool topk,
                          hipStream_t st) {
+  if (p.MB == 0) {
+    if (m.bf16)
+      return topk ? launch_joiner_t<true, true>(m, a, p, st) : launch_joiner_t<true, false>(m, a, p, st);
+    return topk ? launch_joiner_t<false, true>(m, a, p, st) : launch_joiner_t<false, false>(m, a, p, st);
+  }
   if (m.bf16)
-    return topk ? launch_joiner_mb<true, true>(m, a, p, st) : launch_joiner_mb<true, false>(m, a, p, st);
-  return topk ? launch_joiner_mb<false, true>(m, a, p, st) : launch_joiner_mb<false, false>(m, a, p, st);
+    return topk ? launch_joiner_small<true, true>(m, a, p, st) : launch_joiner_small<true, false>(m, a, p, st);
+  return topk ? launch_joiner_small<false, true>(m, a, p, st) : launch_joiner_small<false, false>(m, a, p, st);
 }
 
 }  // namespace
 
-JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16) {
+JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu) {
   JoinerPlan p;
   const int esz = bf16 ? 2 : 4;
-  const int n_ct = Vpad / kJoinerBN;
-  // Largest row block (4 or 2 MFMA blocks, else 1) whose h tile leaves room for two
-  // workgroups per CU (so one's loads overlap the other's MFMAs) and that still
-  // yields a workgroup per CU; larger blocks re-read W less often.
+  const int nvt = Vpad / kJoinerBN;
+  // 128 x 128 GEMM tiles when they give every compute unit one (MB = 0)
+  p.n_rt = (rows + kJBM - 1) / kJBM;
+  p.n_ct = (nvt + 1) / 2;
+  if ((long long)p.n_rt * p.n_ct >= ncu) {
+    p.MB = 0;
+    p.grid = 8 * ((p.n_ct + 7) / 8) * p.n_rt;
+    p.lds = kJLds;
+    return p;
+  }
+  // Otherwise small tiles: the largest row block (4 or 2 MFMA blocks, else 1) whose h
+  // tile leaves room for two workgroups per CU and still yields a workgroup per CU.
   int MB = 1;
   for (int cand : {4, 2}) {
     const size_t lds = (size_t)16 * cand * (Kpad + (bf16 ? 8 : 4)) * esz;
-    const long long tiles = (long long)((rows + 16 * cand - 1) / (16 * cand)) * n_ct;
-    if (lds <= 78 * 1024 && tiles >= 256) {
+    const long long tiles = (long long)((rows + 16 * cand - 1) / (16 * cand)) * nvt;
+    if (lds <= 78 * 1024 && tiles >= ncu) {
       MB = cand;
       break;
     }
   }
   p.MB = MB;
   p.n_rt = (rows + 16 * MB - 1) / (16 * MB);
-  p.n_ct = n_ct;
-  p.grid = 8 * ((n_ct + 7) / 8) * p.n_rt;
+  p.n_ct = nvt;
+  p.grid = 8 * ((nvt + 7) / 8) * p.n_rt;
   p.lds = (size_t)16 * MB * (Kpad + (bf16 ? 8 : 4)) * esz;
   return p;
 }
@@ -2369,6 +2571,7 @@ hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const Join
   a.R = d.B * d.Nc;
   a.n_rt = p.n_rt;
   a.n_ct = p.n_ct;
+  a.nvt = m.Vpad / kJoinerBN;
   a.rows_mode = 0;
   a.len = d.len;
   a.nctx = d.nctx;
@@ -2521,12 +2724,12 @@ hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, 
 }
 
 hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const int* ctx, int R,
-                              void* h, float* logits, float2* stats, float* out_logp,
+                              void* h, float* logits, float2* stats, float* out_logp, int ncu,
                               hipStream_t st) {
   hipLaunchKernelGGL(k_h_rows, dim3(R), dim3(256), 0, st, m, enc_rows, ctx, h);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const JoinerPlan p = plan_joiner(R, m.Vpad, m.Kpad, m.bf16);
+  const JoinerPlan p = plan_joiner(R, m.Vpad, m.Kpad, m.bf16, ncu);
   JoinArgs a{};
   a.h = h;
   a.logits = logits;
@@ -2534,10 +2737,11 @@ hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const in
   a.R = R;
   a.n_rt = p.n_rt;
   a.n_ct = p.n_ct;
+  a.nvt = m.Vpad / kJoinerBN;
   a.rows_mode = 1;
   e = launch_joiner(m, a, p, false, st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_logp_rows, dim3(R), dim3(256), 0, st, logits, stats, p.n_ct, m.V, m.Vpad,
+  hipLaunchKernelGGL(k_logp_rows, dim3(R), dim3(256), 0, st, logits, stats, a.nvt, m.V, m.Vpad,
                      out_logp);
   return hipGetLastError();
 }

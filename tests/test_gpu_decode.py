@@ -165,6 +165,17 @@ def test_throughput_sampled(schedule):
          schedule=schedule)
 
 
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_trivial_wide_frame_joiner(dtype):
+    # trivial graph on the frame schedule with enough joiner rows (B = 256, 8 contexts)
+    # and columns (V = 2,000) for the 128 x 128 GEMM tiles: their top-label epilogue
+    rng = np.random.default_rng(11)
+    model = synth.make_model(rng, 2000, 256, 0.05)
+    inputs = synth.make_inputs(rng, 256, 6, 256, length_range=(0, 6))
+    _run((inputs, model, synth.trivial_graph(2000)), math.inf, 8, 8, dtype=dtype,
+         streams=range(0, 256, 32), schedule="frame")
+
+
 def test_large_sampled():
     # full B = 128 on the GPU, V = 5,000 and the 1M-state power-law graph; 2 streams checked
     _run("large", 8.0, 64, 16, streams=[3, 77])

@@ -13,6 +13,9 @@ SHAPES = [  # (V, C, sigma, R)
     (500, 512, 0.05, 70),     # Standard / Graph / Throughput shapes
     (5000, 512, 0.05, 20),    # Large shapes
     (129, 100, 0.3, 33),      # ragged V and C (padding paths)
+    # enough rows for the 128 x 128 GEMM tiles (at least one per compute unit):
+    (5000, 512, 0.05, 2100),  # Large shapes, ragged row tile
+    (129, 100, 0.3, 16500),   # odd number of 64-column tiles, ragged K and rows
 ]
 
 
