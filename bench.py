@@ -37,7 +37,7 @@ CPU_SAMPLE_STREAMS = {"tiny": None, "standard": None, "graph": None, "throughput
                       "large": 12}
 
 
-def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles, Ns):
+def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles, Ns, frames=None):
     """Joiner rows (contexts) and search traffic implied by a survivor trace.
 
     General graphs: the search reads each arc record (dest, label, score) and gathers
@@ -53,7 +53,7 @@ def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles, Ns):
     survivors_out = 0
     for b in range(trace.shape[1]):
         L = int(lengths[b])
-        for f in range(L):
+        for f in (range(L) if frames is None else range(frames[0], min(frames[1], L))):
             cur = trace[f, b]
             n = int((cur[:, 0] >= 0).sum())
             rows += len(np.unique(cur[:n, 0]))
@@ -151,6 +151,73 @@ def cpu_baseline(w, inputs, model_np, graph_np, dtype, threads=None, min_seconds
                       f"fp64 C++ oracle, {threads} threads, {dt:.1f} s wall"}
 
 
+SCALED = {"B": 8192, "T_short": 4, "T_long": 8}
+
+
+def scaled_microbench(dtype: str, steps: int):
+    """Labelled scaled microbenchmark (not a workload figure): the Large model and
+    1M-state graph with B = 8,192 streams of fixed length, so that one frame's search
+    (expansion over the CSR graph, max-merge, beam / max-states / max-contexts
+    pruning) and joiner GEMM each fill the GPU.  Per-frame kernel times are the
+    difference between decodes of T_long and T_short frames, divided by the frame
+    difference (frames T_short..T_long-1, after the survivor sets have filled);
+    algorithmic bytes and FLOP come from the survivor trace of those frames."""
+    import torch
+    from paper_2211_00484_amd import synth, tbs
+    w = synth.WORKLOADS["large"]
+    B, T1, T2 = SCALED["B"], SCALED["T_short"], SCALED["T_long"]
+    rng = np.random.default_rng(0)
+    inputs = synth.make_inputs(rng, B, T2, w.C)
+    model_np = synth.make_model(rng, w.V, w.C, w.sigma)
+    graph_np = synth.make_graph(w.graph, w.V)
+    model = tbs.Model.from_synth(model_np, dtype=dtype)
+    model.set_schedule("frame")
+    graph = tbs.Graph.from_synth(graph_np)
+    enc = torch.from_numpy(inputs.encoder_out).cuda()
+    tr = tbs.decode(model, graph, enc, inputs.lengths, beam=w.beam, max_states=w.max_states,
+                    max_contexts=w.max_contexts, want_trace=True)
+    torch.cuda.synchronize()
+    nvt = (w.V + 63) // 64
+    work = algorithmic_work(tr.trace.cpu().numpy(), inputs.lengths, graph_np, w.V, w.C, nvt,
+                            w.max_states, frames=(T1, T2))
+    del tr
+    res = {}
+    for T in (T1, T2):
+        lens = np.full(B, T, dtype=np.int32)
+        out = tbs.allocate_outputs(B, T, w.max_states)
+        e = enc[:, :T].contiguous()
+        tbs.decode_into(model, graph, e, lens, w.beam, w.max_states, w.max_contexts, out)
+        torch.cuda.synchronize()
+        model.set_profiling(True)
+        for _ in range(steps):
+            tbs.decode_into(model, graph, e, lens, w.beam, w.max_states, w.max_contexts, out)
+        prof = model.read_profile()
+        model.set_profiling(False)
+        res[T] = {k: v[1] / steps for k, v in prof.items()}  # ms per decode
+        del out, e
+    nf = T2 - T1
+    s_us = 1e3 * (res[T2]["search"] - res[T1]["search"]) / nf
+    j_us = 1e3 * (res[T2]["joiner"] - res[T1]["joiner"]) / nf
+    s_bytes = work["search_bytes"] / nf
+    j_flop = work["flop"] / nf
+    peak_j = PEAK["bf16_mfma_tflops"] if dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+    line = {
+        "microbenchmark": "scaled search + joiner, one frame at B = 8,192 (not a workload figure)",
+        "config": {"model": "large (V=5,000, C=512)", "graph": "powerlaw1m", "B": B,
+                   "frames_timed": f"{T1}..{T2 - 1}", "beam": w.beam, "max_states": w.max_states,
+                   "max_contexts": w.max_contexts, "joiner": dtype, "steps": steps},
+        "search": {"us_per_frame": s_us, "algorithmic_bytes_per_frame": s_bytes,
+                   "gbps": s_bytes / (s_us * 1e-6) / 1e9, "peak_gbps": PEAK["hbm_gbps"],
+                   "frac": s_bytes / (s_us * 1e-6) / 1e9 / PEAK["hbm_gbps"],
+                   "arcs_per_frame": work["arcs"] / nf, "survivors_per_frame": work["survivors"] / nf},
+        "joiner": {"us_per_frame": j_us, "algorithmic_flop_per_frame": j_flop,
+                   "tflops": j_flop / (j_us * 1e-6) / 1e12, "peak_tflops": peak_j,
+                   "frac": j_flop / (j_us * 1e-6) / 1e12 / peak_j,
+                   "rows_per_frame": work["rows"] / nf},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -168,6 +235,9 @@ def main():
                     help="threads for the oracle baseline (default: all host threads)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain copy of 256 MiB (traffic-counter calibration)")
+    ap.add_argument("--scaled-microbench", action="store_true",
+                    help="only run the labelled scaled search + joiner microbenchmark "
+                         "(Large model and graph, B = 8,192)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (got --gpus {args.gpus}): streams are "
@@ -181,6 +251,9 @@ def main():
     torch.cuda.set_device(0)
     if args.copy_calibration:
         copy_calibration(args.steps or 5)
+        return
+    if args.scaled_microbench:
+        scaled_microbench(args.joiner_dtype or "fp32", args.steps or 3)
         return
     w, inputs, model_np, graph_np = synth.make_workload(args.workload, seed=0)
     K = args.steps if args.steps is not None else DEFAULT_STEPS[w.name]
