@@ -215,11 +215,10 @@ __device__ __forceinline__ float tanh_fast(float x) {
 // row enc_rows + r * enc_stride (enc_stride = 0: one shared frame).
 // Thread tid owns columns tid, tid + NT, ... of every row (Kpad is a multiple of
 // 512); a batch's loads are all issued before any tanh.
-template <int NT>
+template <int NT, int U = 16>  // U: (row, column) elements per thread per batch
 __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_rows,
                              long long enc_stride, const int2* rowoff, int nrows,
                              void* __restrict__ hbase, int hstride, int tid) {
-  constexpr int U = 16;  // (row, column) elements per thread per batch
   const int C = m.C, Kpad = m.Kpad;
   const float* __restrict__ P0 = m.P0;
   const float* __restrict__ P1 = m.P1;
@@ -1056,19 +1055,22 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   }
   __syncthreads();
   const int ns = s.ns, nc = s.nc;
-  // log-softmax normaliser of each context row: one wave per row
-  for (int j = wave; !FUSED && j < nc; j += 4) {
+  // log-softmax normaliser of each context row: 16 threads (one DPP row) per row,
+  // 16 rows at a time
+  for (int j0 = 0; !FUSED && j0 < nc; j0 += kSearchThreads / 16) {
+    const int j = j0 + (tid >> 4), l16 = tid & 15;
+    const bool rv = j < nc;
     float M = -INFINITY;
-    for (int i = lane; i < nvt; i += 64)
+    for (int i = l16; rv && i < nvt; i += 16)
       M = fmaxf(M, staged ? stage[j * nvt + i].x : d.stats[(row0 + j) * nvt + i].x);
-    M = wave_max_f(M);
+    M = row16_max(M);
     float S = 0.f;
-    for (int i = lane; i < nvt; i += 64) {
+    for (int i = l16; rv && i < nvt; i += 16) {
       const float2 p = staged ? stage[j * nvt + i] : d.stats[(row0 + j) * nvt + i];
       S += p.y == 0.f ? 0.f : p.y * expf(p.x - M);
     }
-    S = wave_sum_f(S);
-    if (lane == 0) s.s_lse[j] = lse_of(M, S);
+    S = row16_sum(S);
+    if (rv && l16 == 0) s.s_lse[j] = lse_of(M, S);
   }
   if (FUSED && !prestats) {
     // straight from the logit rows: normaliser, and for the trivial graph the blank
@@ -1461,6 +1463,81 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
         s.nC = __popcll(firsts);
       }
     }
+  } else if (K <= 64) {
+    // One wave.  The entries are sorted by (context, state) with a bitonic network
+    // across the lanes, so that each context is a run of lanes: its score is the run
+    // maximum of the in-beam scores, its first tuple the run's first in-beam lane; a
+    // context's rank among the contexts (score desc, context asc) is counted over the
+    // run heads staged in LDS; canonical positions and context rows are prefix counts
+    // of ballots, because the sorted order is the canonical one.
+    if (wave == 0) {
+      auto xor64 = [](unsigned long long v, int m) {
+        const int lo = __shfl_xor((int)(unsigned)v, m), hi = __shfl_xor((int)(unsigned)(v >> 32), m);
+        return ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo;
+      };
+      unsigned long long sk = tid < K ? ((unsigned long long)my_ci << 32) | my_st : ~0ull;  // sentinels last
+      unsigned long long sv = tid < K ? my_v : 0ull;
+      for (int k = 2; k <= 64; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+          const unsigned long long pk = xor64(sk, j), pv = xor64(sv, j);
+          const bool up = (lane & k) == 0, lower = (lane & j) == 0;
+          if (lower == up ? pk < sk : pk > sk) {
+            sk = pk;
+            sv = pv;
+          }
+        }
+      const bool valid = sk != ~0ull;
+      const unsigned ci = (unsigned)(sk >> 32), stt = (unsigned)sk;
+      const float sc = valid ? ord2f((unsigned)(sv >> 32)) : -INFINITY;
+      const bool k1 = valid && sc >= thr;
+      const unsigned prev = (unsigned)__shfl_up((int)ci, 1);
+      const bool head = valid && (lane == 0 || prev != ci);
+      const unsigned long long H = __ballot(head), K1 = __ballot(k1);
+      const unsigned long long below = lane ? ~0ull >> (64 - lane) : 0ull;  // lanes < this one
+      const unsigned long long self = 1ull << lane;
+      const int rs = 63 - __clzll((long long)(H & (below | self)));         // run start
+      const unsigned long long hnext = H & ~(below | self);
+      const int re = hnext ? __ffsll((long long)hnext) - 2 : K - 1;          // run end
+      const unsigned long long k1run = K1 & (~0ull << rs);
+      const int fl = k1run ? __ffsll((long long)k1run) - 1 : 63;             // run's first in-beam lane
+      const bool first = k1 && lane == fl;
+      float run = k1 ? sc : -INFINITY;  // run maxima by a segmented inclusive scan
+#pragma unroll
+      for (int dd = 1; dd < 64; dd <<= 1) {
+        const float upv = __shfl_up(run, dd);
+        if (lane - dd >= rs) run = fmaxf(run, upv);
+      }
+      const float cs = __shfl(run, valid ? re : lane);
+      const unsigned co = first ? f2ord(cs) : 0u;
+      s.hist[lane] = co;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      int rank = 0;
+      for (int q0 = 0; q0 < 64; q0 += 8) {
+        unsigned r[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) r[u] = s.hist[q0 + u];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) rank += (r[u] > co) | ((r[u] == co) & (q0 + u < lane));
+      }
+      const int fkeep = first && rank < Nc;
+      const int keep2 = k1 && __shfl(fkeep, fl);
+      const unsigned long long K2 = __ballot(keep2), F2 = __ballot(keep2 && first);
+      my_pos = __popcll(K2 & below);
+      my_crow = __popcll(F2 & (rs ? ~0ull >> (64 - rs) : 0ull));
+      my_first = first;
+      my_keep2 = keep2;
+      my_ci = ci;
+      my_st = stt;
+      my_sc = sc;
+      my_v = sv;
+      if (keep2 && first) s.n_ctx_list[my_crow] = (int)ci;
+      if (lane == 0) {
+        s.nK = __popcll(K2);
+        s.nC = __popcll(F2);
+      }
+    }
   } else {
     // Larger sets: every thread holds one entry and scans the others in LDS.  The
     // loads are unconditional and issued eight at a time (the asm statements pin
@@ -1561,10 +1638,11 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     if (FUSED) {
       write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC, hl, hstride, tid);
     } else {
+      // (32 elements per thread: the gathers of up to 16 rows of K = 512 in one batch)
       const size_t esz = m.bf16 ? 2 : 4;
-      write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC,
-                                   reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz, m.Kpad,
-                                   tid);
+      write_h_rows<kSearchThreads, 32>(m, s.enc_next, 0, s.n_rowoff, nC,
+                                       reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz,
+                                       m.Kpad, tid);
     }
   }
   const bool store_surv = writer && (!FUSED || t + 1 == L);
