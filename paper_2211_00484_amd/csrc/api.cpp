@@ -215,17 +215,33 @@ hipError_t prof_event(tbs_model* m, hipEvent_t* ev) {
   return hipEventCreate(ev);
 }
 
-// Launches `fn` on st, bracketed by timing events when profiling is on.
+// Launches `fn` on st, timed when profiling is on: a single kernel launch records the
+// two events in its own dispatch packet; the cooperative grouped kernel (one launch
+// of milliseconds) is bracketed by events recorded on the stream.
 template <class F>
 hipError_t timed_launch(tbs_model* m, int kernel, hipStream_t st, F fn) {
   if (!m->prof) return fn();
   hipEvent_t a, b;
   hipError_t e = prof_event(m, &a);
   if (e == hipSuccess) e = prof_event(m, &b);
-  if (e == hipSuccess) e = hipEventRecord(a, st);
-  if (e == hipSuccess) e = fn();
-  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e != hipSuccess) return e;
+  if (kernel == TBS_KERNEL_STREAM_GROUP) {
+    e = hipEventRecord(a, st);
+    if (e == hipSuccess) e = fn();
+    if (e == hipSuccess) e = hipEventRecord(b, st);
+  } else {
+    set_launch_events(a, b);
+    e = fn();
+    if (launch_events_pending()) {  // not taken by a launch (failed before it)
+      set_launch_events(nullptr, nullptr);
+      if (e == hipSuccess) e = hipErrorUnknown;
+    }
+  }
   if (e == hipSuccess) m->prof_pending.push_back({kernel, a, b});
+  else {
+    m->prof_pool.push_back(a);
+    m->prof_pool.push_back(b);
+  }
   return e;
 }
 

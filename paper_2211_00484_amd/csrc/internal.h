@@ -82,6 +82,11 @@ struct JoinerPlan {
 
 JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu);
 
+// Events for the next non-cooperative kernel launch of the calling thread, recorded in
+// that launch's dispatch packet (per-kernel profiling); pending until a launch takes them.
+void set_launch_events(hipEvent_t start, hipEvent_t stop);
+bool launch_events_pending();
+
 // Per-stream kernel (one workgroup runs every frame of one stream).
 struct StreamPlan {
   int ok;                   // the shape fits (contexts, LDS)

@@ -16,6 +16,7 @@
 // final tuple and traces the back-pointers.
 #include "internal.h"
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -2524,6 +2525,21 @@ __global__ __launch_bounds__(256) void k_final(GraphDev g, DecodeDev d, int* __r
   if (tid == 0) out_ntok[b] = total;
 }
 
+// Timing events for the next launch (per-kernel profiling): when set, the launch
+// records them in its own dispatch packet (hipExtLaunchKernel), so the interval
+// between them is the kernel's execution and not the enqueue around it.
+thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+
+template <typename F, typename... Args>
+void launch_k(F kernel, dim3 grid, dim3 block, unsigned shmem, hipStream_t st, Args... args) {
+  if (g_ev_start) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, g_ev_start, g_ev_stop, 0u, args...);
+    g_ev_start = g_ev_stop = nullptr;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, st, args...);
+  }
+}
+
 inline int grid_for(long long n, int threads, int cap = 4096) {
   long long g = (n + threads - 1) / threads;
   if (g < 1) g = 1;
@@ -2541,7 +2557,7 @@ hipError_t launch_joiner_t(const ModelDev& m, const JoinArgs& a, const JoinerPla
     if (e != hipSuccess) return e;
     attr = p.lds;
   }
-  hipLaunchKernelGGL((k_joiner<BF16, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
+  launch_k((k_joiner<BF16, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
   return hipGetLastError();
 }
 
@@ -2555,7 +2571,7 @@ hipError_t launch_joiner_small_t(const ModelDev& m, const JoinArgs& a, const Joi
     if (e != hipSuccess) return e;
     attr = p.lds;
   }
-  hipLaunchKernelGGL((k_joiner_small<BF16, MB, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
+  launch_k((k_joiner_small<BF16, MB, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
   return hipGetLastError();
 }
 
@@ -2582,6 +2598,13 @@ hipError_t launch_joiner(const ModelDev& m, const JoinArgs& a, const JoinerPlan&
 }
 
 }  // namespace
+
+void set_launch_events(hipEvent_t start, hipEvent_t stop) {
+  g_ev_start = start;
+  g_ev_stop = stop;
+}
+
+bool launch_events_pending() { return g_ev_start != nullptr; }
 
 JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu) {
   JoinerPlan p;
@@ -2669,7 +2692,7 @@ hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const Decod
       if (e != hipSuccess) return e;
       attr = true;
     }
-    hipLaunchKernelGGL(k_search<true>, dim3(d.B), dim3(kSearchThreads), lds, st, m, g, d, beam, t,
+    launch_k(k_search<true>, dim3(d.B), dim3(kSearchThreads), lds, st, m, g, d, beam, t,
                        trace);
   } else {
     static bool attr = false;
@@ -2679,7 +2702,7 @@ hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const Decod
       if (e != hipSuccess) return e;
       attr = true;
     }
-    hipLaunchKernelGGL(k_search<false>, dim3(d.B), dim3(kSearchThreads), lds, st, m, g, d, beam, t,
+    launch_k(k_search<false>, dim3(d.B), dim3(kSearchThreads), lds, st, m, g, d, beam, t,
                        trace);
   }
   return hipGetLastError();
@@ -2709,7 +2732,7 @@ hipError_t launch_stream_t(const ModelDev& m, const GraphDev& g, const DecodeDev
     if (e != hipSuccess) return e;
     attr = p.lds;
   }
-  hipLaunchKernelGGL((k_stream<BF16, TRIV, RG>), dim3(d.B), dim3(kSearchThreads), p.lds, st, m, g,
+  launch_k((k_stream<BF16, TRIV, RG>), dim3(d.B), dim3(kSearchThreads), p.lds, st, m, g,
                      d, beam, trace, p.hoff, p.hstride, p.zoff);
   return hipGetLastError();
 }
@@ -2796,7 +2819,7 @@ hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const Decod
 hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, int* out_ntok,
                         double* out_scores, int* out_status, int* out_arcs,
                         const unsigned* exchange_err, hipStream_t st) {
-  hipLaunchKernelGGL(k_final, dim3(d.B), dim3(256), 0, st, g, d, out_tokens, out_ntok, out_scores,
+  launch_k(k_final, dim3(d.B), dim3(256), 0, st, g, d, out_tokens, out_ntok, out_scores,
                      out_status, out_arcs, exchange_err);
   return hipGetLastError();
 }
