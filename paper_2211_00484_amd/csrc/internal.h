@@ -93,6 +93,7 @@ struct StreamPlan {
   int RG;                   // groups of 4 context rows (1 to 4)
   int hoff, hstride;        // LDS offset of the joiner rows and their stride (elements)
   int zoff;                 // LDS offset of the logit rows [4 RG][Vpad] fp32
+  int doff;                 // LDS offset of the staged decoder rows (0: none)
   size_t lds;               // dynamic LDS bytes
 };
 

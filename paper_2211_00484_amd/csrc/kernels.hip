@@ -1008,13 +1008,18 @@ __device__ __forceinline__ WaveSel trivial_select_wave(SearchSmem& s, int ns, in
 // (s_lse) and, for the trivial graph, the best labels and blank logits are
 // already in LDS.  writer: this workgroup writes the stream's history, trace,
 // survivors and offset (a stream run redundantly by several workgroups has one
-// writer).  enc_ready: the caller has put encoder frame t+1 in enc_next.
+// writer).  enc_ready: the caller has put encoder frame t+1 in enc_next.  dspec
+// (trivial graph, max_states = 4, FUSED): LDS decoder rows, [16][Kpad] of the label
+// candidates (gathered by waves 1-3 while wave 0 selects) and [2][4][Kpad] of the
+// contexts (buffer dcur_buf holds the current ones); the next frame's joiner rows
+// are built from them (enc_next must be zero from C to Kpad).
 template <bool TRIV, bool FUSED>
 __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& g,
                                              const DecodeDev& d, float beam, int t, int L, int b,
                                              int* __restrict__ trace, SearchSmem& s, void* hl,
                                              int hstride, const float* zl, bool prestats = false,
-                                             bool writer = true, bool enc_ready = false) {
+                                             bool writer = true, bool enc_ready = false,
+                                             float* dspec = nullptr, int dcur_buf = 0) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V, nvt = d.nvt;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
@@ -1105,24 +1110,43 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       const float S = wave_sum_f(S0 + S1);
       if (lane == 0) s.s_lse[j] = lse_of(M, S);
       if (TRIV) {
-        unsigned long long kv[NPL];
+        // best KT labels by (logit desc, label asc): each lane's best remaining slot
+        // (ties to its smaller column), the wave maximum of the order-preserving
+        // code, ties across lanes to the smaller column; the winner's slot retires
+        unsigned o[NPL];
 #pragma unroll
         for (int i = 0; i < NPL; ++i) {
           const int c = 64 * i + lane;
-          kv[i] = (c >= 1 && c < V) ? ((unsigned long long)f2ord(zv[i]) << 32) | (0xffffffffu - (unsigned)c)
-                                    : 0ull;
+          o[i] = (c >= 1 && c < V) ? f2ord(zv[i]) : 0u;
         }
-        unsigned long long prev = ~0ull;
         for (int q = 0; q < KT; ++q) {
-          unsigned long long mine = 0ull;
+          unsigned lm = 0u;
+          int li = 0;
 #pragma unroll
-          for (int i = 0; i < NPL; ++i) mine = (kv[i] < prev && kv[i] > mine) ? kv[i] : mine;
-          const unsigned long long best = wave_max_u64(mine);
-          if (lane == 0) {
-            s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
-            s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+          for (int i = 0; i < NPL; ++i)
+            if (o[i] > lm) {
+              lm = o[i];
+              li = i;
+            }
+          const unsigned mo = wave_max_u32(lm);
+          float zq = -INFINITY;
+          int cq = -1;
+          if (mo != 0u) {
+            const unsigned cand = lm == mo ? (unsigned)(64 * li + lane) : 0xffffffffu;
+            const unsigned long long bal = __ballot(lm == mo);
+            const unsigned cmin = __popcll(bal) == 1
+                                      ? (unsigned)__builtin_amdgcn_readlane((int)cand, __ffsll((long long)bal) - 1)
+                                      : wave_min_u32(cand);
+            zq = ord2f(mo);
+            cq = (int)cmin;
+#pragma unroll
+            for (int i = 0; i < NPL; ++i)
+              if (lane == (int)(cmin & 63) && i == (int)(cmin >> 6)) o[i] = 0u;
           }
-          prev = best ? best : 1ull;
+          if (lane == 0) {
+            s.rk_z[j * KT + q] = zq;
+            s.rk_c[j * KT + q] = cq;
+          }
         }
         if (lane == 0) s.s_z0[j] = zv[0];
       }
@@ -1183,6 +1207,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     // trivial graph, at most 64 candidates: one wave (trivial_select_wave)
     if (wave == 0) {
       const WaveSel r = trivial_select_wave(s, ns, d.KT, V, Ns, Nc, beam, stride_tb, lane, 0, true);
+      if (dspec && r.keep2) s.g_src[r.pos] = r.src;
       my_keep2 = r.keep2;
       my_pos = r.pos;
       my_crow = r.pos;
@@ -1191,6 +1216,40 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       my_st = r.st;
       my_sc = r.sc;
       my_v = r.v;
+    } else if (dspec && t + 1 < L) {
+      // decoder rows ReLU(P0[a] + P1[b]) of every label candidate (survivor i on context
+      // row i, label q): unconditional LDS reads, absent entries mapped into row 0
+      const int kq4 = m.Kpad / 4;
+      int pa[4], pb[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int a = s.s_bprev[i];
+        pa[i] = (i < ns && (unsigned)a < (unsigned)V) ? a : 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = s.rk_c[i * 4 + q];
+          pb[i][q] = (i < ns && (unsigned)c < (unsigned)V) ? c : 0;
+        }
+      }
+      const float4* __restrict__ P0 = reinterpret_cast<const float4*>(m.P0);
+      const float4* __restrict__ P1 = reinterpret_cast<const float4*>(m.P1);
+      float4* dc4 = reinterpret_cast<float4*>(dspec);
+      for (int kq = tid - 64; kq < kq4; kq += kSearchThreads - 64) {
+        float4 p0[4], p1[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          p0[i] = P0[(size_t)pa[i] * kq4 + kq];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) p1[i][q] = P1[(size_t)pb[i][q] * kq4 + kq];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            dc4[(4 * i + q) * kq4 + kq] =
+                make_float4(fmaxf(p0[i].x + p1[i][q].x, 0.f), fmaxf(p0[i].y + p1[i][q].y, 0.f),
+                            fmaxf(p0[i].z + p1[i][q].z, 0.f), fmaxf(p0[i].w + p1[i][q].w, 0.f));
+      }
     }
     __syncthreads();
     best = s.best;
@@ -1636,7 +1695,32 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   __syncthreads();
   // global stores: joiner rows of the next frame, survivors, history, trace
   if (t + 1 < L) {
-    if (FUSED) {
+    if (FUSED && dspec) {
+      // h = tanh(enc[t + 1] + decoder row) from the staged rows; the new contexts'
+      // decoder rows go to the other context buffer
+      const int kq4 = m.Kpad / 4;
+      const float4* dc4 = reinterpret_cast<const float4*>(dspec);
+      const float4* du4 = reinterpret_cast<const float4*>(dspec + (size_t)(16 + 4 * dcur_buf) * m.Kpad);
+      float4* dn4 = reinterpret_cast<float4*>(dspec + (size_t)(16 + 4 * (dcur_buf ^ 1)) * m.Kpad);
+      const float4* en4 = reinterpret_cast<const float4*>(s.enc_next);
+      for (int e = tid; e < nC * kq4; e += blockDim.x) {
+        const int j = e / kq4, kq = e - j * kq4;
+        const int src = s.g_src[j];
+        const float4 dv = src >= 0 ? dc4[src * kq4 + kq] : du4[(-src - 1) * kq4 + kq];
+        const float4 ev = en4[kq];
+        const float h0 = tanh_fast(ev.x + dv.x), h1 = tanh_fast(ev.y + dv.y);
+        const float h2 = tanh_fast(ev.z + dv.z), h3 = tanh_fast(ev.w + dv.w);
+        if (m.bf16) {
+          const uint2 hb = make_uint2((unsigned)f32_to_bf16_rne(h0) | ((unsigned)f32_to_bf16_rne(h1) << 16),
+                                      (unsigned)f32_to_bf16_rne(h2) | ((unsigned)f32_to_bf16_rne(h3) << 16));
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(hl) + (size_t)j * hstride + 4 * kq) = hb;
+        } else {
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(hl) + (size_t)j * hstride + 4 * kq) =
+              make_float4(h0, h1, h2, h3);
+        }
+        dn4[e] = dv;
+      }
+    } else if (FUSED) {
       write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC, hl, hstride, tid);
     } else {
       // (32 elements per thread: the gathers of up to 16 rows of K = 512 in one batch)
@@ -1854,7 +1938,8 @@ __device__ __forceinline__ void stream_joiner(const ModelDev& m, const DecodeDev
 template <bool BF16, bool TRIV, int RG>
 __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev g, DecodeDev d,
                                                            float beam, int* __restrict__ trace,
-                                                           int hoff, int hstride, int zoff) {
+                                                           int hoff, int hstride, int zoff,
+                                                           int doff) {
   const int b = blockIdx.x;
   const int L = d.len[b];
   if (L == 0) return;
@@ -1883,18 +1968,47 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
   }
   {
     const float* er = d.enc + (size_t)b * d.T * m.C;
-    for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
+    for (int k = tid; k < m.Kpad; k += blockDim.x) s.enc_next[k] = k < m.C ? er[k] : 0.f;
     const int words = RG * 4 * hstride * (m.bf16 ? 2 : 4) / 4;
     for (int i = tid; i < words; i += blockDim.x) reinterpret_cast<int*>(hl)[i] = 0;
   }
   __syncthreads();
   write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, s.nc, hl, hstride, tid);
+  // staged decoder rows (trivial graph, max_states = 4): those of the initial contexts
+  float* dspec = (TRIV && doff) ? reinterpret_cast<float*>(smem + doff) : nullptr;
+  if (dspec)
+    for (int e = tid; e < s.nc * m.Kpad; e += blockDim.x) {
+      const int j = e / m.Kpad, k = e - j * m.Kpad;
+      const int2 off = s.n_rowoff[j];
+      dspec[(size_t)16 * m.Kpad + e] = fmaxf(m.P0[(size_t)off.x + k] + m.P1[(size_t)off.y + k], 0.f);
+    }
   __syncthreads();
+  int cur = 0;
+  constexpr int NEP = kMaxDim / kSearchThreads;
   for (int t = 0; t < L; ++t) {
+    // encoder frame t + 1, in flight during the joiner
+    float encp[NEP];
+    {
+      const float* er = d.enc + ((size_t)b * d.T + min(t + 1, L - 1)) * m.C;
+#pragma unroll
+      for (int u = 0; u < NEP; ++u) {
+        const int k = tid + u * kSearchThreads;
+        encp[u] = k < m.C ? er[k] : 0.f;
+      }
+    }
     stream_joiner<BF16, RG>(m, d, hl, hstride, zl);
+    if (t + 1 < L) {
+#pragma unroll
+      for (int u = 0; u < NEP; ++u) {
+        const int k = tid + u * kSearchThreads;
+        if (k < m.C) s.enc_next[k] = encp[u];
+      }
+    }
     __syncthreads();
-    search_frame<TRIV, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, zl);
+    search_frame<TRIV, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, zl, false, true, true,
+                             dspec, cur);
     __syncthreads();
+    cur ^= 1;
   }
 }
 
@@ -2718,6 +2832,13 @@ StreamPlan plan_stream(const ModelDev& m, int Nc, int KT, int trivial) {
   p.zoff = p.hoff + p.RG * 4 * p.hstride * esz;
   p.lds = (size_t)p.zoff + (size_t)p.RG * 4 * m.Vpad * 4;
   p.ok = Nc <= 16 && m.Vpad <= kStreamMaxV && p.lds <= kMaxLds && (!trivial || KT > 0);
+  // trivial graph with max_states = 4: staged decoder rows of the candidates and contexts
+  p.doff = 0;
+  const size_t dbeg = (p.lds + 15) / 16 * 16, dend = dbeg + (size_t)(16 + 8) * m.Kpad * 4;
+  if (trivial && KT == 4 && dend <= kMaxLds) {
+    p.doff = (int)dbeg;
+    p.lds = dend;
+  }
   (void)nvt;
   return p;
 }
@@ -2732,8 +2853,8 @@ hipError_t launch_stream_t(const ModelDev& m, const GraphDev& g, const DecodeDev
     if (e != hipSuccess) return e;
     attr = p.lds;
   }
-  launch_k((k_stream<BF16, TRIV, RG>), dim3(d.B), dim3(kSearchThreads), p.lds, st, m, g,
-                     d, beam, trace, p.hoff, p.hstride, p.zoff);
+  launch_k((k_stream<BF16, TRIV, RG>), dim3(d.B), dim3(kSearchThreads), p.lds, st, m, g, d, beam,
+           trace, p.hoff, p.hstride, p.zoff, p.doff);
   return hipGetLastError();
 }
 
