@@ -163,6 +163,52 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
                       int32_t *out_arcs, int32_t *trace, void *hip_stream);
 
 /*
+ * Streaming decode: tbs_decode split into chunks of frames (the decoding state of
+ * Algorithm 1 carried across calls).  A decode state holds, for each of B streams,
+ * the surviving tuples, the fp64 score offset and the back-pointers of every frame
+ * decoded so far.  tbs_decode_chunk continues each stream from where it stopped;
+ * tbs_state_finish traces the best paths back over all decoded frames.  Splitting
+ * a stream's frames into chunks in any way gives the same outputs as tbs_decode
+ * over all of them on the same schedule, bit for bit.
+ *
+ * tbs_state_create
+ *   model, graph, params as for tbs_decode; the state keeps references to the
+ *   model and graph, which must outlive it.  The model's schedule at this call
+ *   applies to every chunk.  B >= 1 streams; max_frames >= 1 frames per stream
+ *   at most (history capacity).  Initialisation is enqueued on hip_stream.
+ *   Errors as for tbs_decode, TBS_EINVAL for B or max_frames < 1.
+ * tbs_decode_chunk
+ *   encoder_chunk  DEVICE float [B][Tc][C]: the next frames of every stream
+ *                  (row t of stream b is its frame done_b + t);
+ *   chunk_lengths  HOST int32 [B], each in [0, Tc]: frames of this chunk per
+ *                  stream (0 = the stream does not advance);
+ *   trace          DEVICE int32 [max_frames+1][B][max_states][4] or NULL: the
+ *                  survivor trace of tbs_decode at absolute frame indices; only
+ *                  kept tuples are written (fill the buffer with -1 first), and
+ *                  frame 0 (the initial tuple) when a stream's first chunk runs.
+ *   Errors: TBS_EINVAL for bad lengths or a NULL chunk, TBS_ECAPACITY when a
+ *   stream would exceed max_frames (nothing is enqueued then).
+ * tbs_state_finish
+ *   outputs as for tbs_decode with T = max_frames.  The state stays valid: more
+ *   chunks may follow, and finish may be called again.
+ * Calls on one state are stream-ordered on the hip_stream of each call and
+ * serialised with every other decode on the same model; a state must not be used
+ * from two threads at once.
+ */
+typedef struct tbs_state tbs_state;
+
+tbs_status tbs_state_create(const tbs_model *model, const tbs_graph *graph,
+                            const tbs_beam_params *params, int32_t B, int32_t max_frames,
+                            void *hip_stream, tbs_state **out);
+tbs_status tbs_decode_chunk(tbs_state *state, const float *encoder_chunk,
+                            const int32_t *chunk_lengths, int32_t Tc, int32_t *trace,
+                            void *hip_stream);
+tbs_status tbs_state_finish(tbs_state *state, int32_t *out_tokens, int32_t *out_num_tokens,
+                            double *out_scores, int32_t *out_status, int32_t *out_arcs,
+                            void *hip_stream);
+void tbs_state_destroy(tbs_state *state);
+
+/*
  * How tbs_decode drives the frame loop of Algorithm 1 (all schedules compute
  * the same search; results agree within the fp32 rounding of the joiner):
  *   TBS_SCHEDULE_FRAME   two kernels per frame over the whole batch: a joiner
@@ -216,14 +262,13 @@ tbs_status tbs_joiner_logp(const tbs_model *model, const float *enc_rows, const 
 
 /*
  * Per-kernel timing, for benchmarks.  While enabled on a model, every decode
- * records a pair of HIP events around each kernel launch on its stream
- * (joiner and search once per frame, or the per-stream kernel once; final once
- * per decode) and keeps them
- * pending.  tbs_model_read_profile waits for those events, adds their elapsed
+ * records a pair of HIP events for each kernel launch (joiner and search once
+ * per frame, or the per-stream kernel once; final once per decode): inside the
+ * launch's own dispatch packet, or for the cooperative grouped kernel on its
+ * stream around the launch, and keeps them pending.  tbs_model_read_profile waits for those events, adds their elapsed
  * times into out[TBS_KERNEL_COUNT] (indexed by tbs_kernel_id; launches and
  * milliseconds since the last enable) and releases them.  Enabling resets the
- * counters; disabling drops pending events.  The events sit between kernels
- * that are stream-ordered anyway, so timing adds only the event packets.
+ * counters; disabling drops pending events.
  */
 typedef enum {
   TBS_KERNEL_JOINER = 0,

@@ -71,7 +71,7 @@ struct Workspace {
   int* hist_pl = nullptr;
   int* hist_arc = nullptr;
   int* path_lab = nullptr;
-  int* len_host = nullptr;  // pinned staging for lengths
+  int* len_host = nullptr;  // pinned staging for lengths (and frame bases), [2B]
   hipEvent_t done = nullptr;
   bool pending = false;
 
@@ -128,6 +128,10 @@ struct tbs_model {
   int schedule = TBS_SCHEDULE_AUTO;
   std::mutex mu;
   Workspace ws;
+  // device work of every decode and chunk on this model is serialised on this event
+  // (they share the exchange buffer and, for tbs_decode, the workspace)
+  hipEvent_t busy = nullptr;
+  bool busy_pending = false;
   // per-kernel timing (tbs_model_set_profiling)
   bool prof = false;
   struct Timed {
@@ -254,20 +258,14 @@ void prof_drop(tbs_model* m) {
   m->prof_pending.clear();
 }
 
-tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc, int KT,
-                            bool need_logits) {
-  Workspace& w = m->ws;
-  if (w.done && w.B >= B && w.T >= T && w.Ns == Ns && w.Nc == Nc && w.KT == KT &&
-      (w.has_logits || !need_logits))
-    return TBS_OK;
-  if (w.done) {
-    if (w.pending) hipEventSynchronize(w.done);
-    w.release();
-  }
+// Allocates w for (B, T, Ns, Nc, KT); w must be empty.  w.len holds 2B entries: the
+// frame counts of a call, then (chunked decode) each stream's frame base.
+tbs_status alloc_workspace(const tbs_model* m, Workspace& w, int B, int T, int Ns, int Nc, int KT,
+                           bool need_logits) {
   const int nvt = m->Vpad / kJoinerBN;
   const size_t BN = (size_t)B * Ns, BC = (size_t)B * Nc;
   const size_t esz = m->bf16 ? 2 : 4;
-  HIP_TRY(dalloc(&w.len, B), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.len, 2 * (size_t)B), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.nsurv, B), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.surv_ctx, BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.surv_state, BN), "hipMalloc(workspace)");
@@ -288,7 +286,7 @@ tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc, int KT,
   HIP_TRY(dalloc(&w.hist_pl, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.hist_arc, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.path_lab, (size_t)B * T), "hipMalloc(workspace)");
-  HIP_TRY(hipHostMalloc((void**)&w.len_host, (size_t)(B > 0 ? B : 1) * 4, hipHostMallocDefault),
+  HIP_TRY(hipHostMalloc((void**)&w.len_host, (size_t)(B > 0 ? 2 * B : 1) * 4, hipHostMallocDefault),
           "hipHostMalloc(workspace)");
   HIP_TRY(hipEventCreateWithFlags(&w.done, hipEventDisableTiming), "hipEventCreate");
   w.B = B;
@@ -298,6 +296,21 @@ tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc, int KT,
   w.KT = KT;
   w.has_logits = need_logits;
   return TBS_OK;
+}
+
+tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc, int KT,
+                            bool need_logits) {
+  Workspace& w = m->ws;
+  if (w.done && w.B >= B && w.T >= T && w.Ns == Ns && w.Nc == Nc && w.KT == KT &&
+      (w.has_logits || !need_logits))
+    return TBS_OK;
+  if (w.done) {
+    if (w.pending) hipEventSynchronize(w.done);
+    w.release();
+  }
+  tbs_status st = alloc_workspace(m, w, B, T, Ns, Nc, KT, need_logits);
+  if (st != TBS_OK) w.release();
+  return st;
 }
 
 // The model's exchange buffer with at least `words` words, cleared if the epoch has
@@ -353,7 +366,149 @@ int pick_group(const tbs_model* m, const StreamPlan& sp, int B, int KT, int maxl
   return 1;
 }
 
+// Frame-loop schedule of a decode (tbs_model_set_schedule): persistent per-stream
+// kernels or two kernels per frame.
+tbs_status choose_schedule(const tbs_model* m, const StreamPlan& splan, int Ns, int Nc,
+                           const char* who, bool* per_stream) {
+  *per_stream = false;
+  if (m->schedule == TBS_SCHEDULE_STREAM || m->schedule == TBS_SCHEDULE_STREAM_SINGLE) {
+    if (!splan.ok)
+      return fail(TBS_EUNSUPPORTED,
+                  "%s: the per-stream schedule does not fit max_contexts %d / "
+                  "max_states %d with V %d and dim %d",
+                  who, Nc, Ns, m->V, m->C);
+    *per_stream = true;
+  } else if (m->schedule == TBS_SCHEDULE_AUTO) {
+    // One compute unit streams the whole joiner weight every frame: worth it while
+    // W stays L2-resident and the fp32 rows (broadcast from LDS to VALU FMAs) are few.
+    *per_stream = splan.ok && (size_t)m->Vpad * m->Kpad * (m->bf16 ? 2 : 4) <= (4u << 20) &&
+                  (m->bf16 || Nc <= 4);
+  }
+  return TBS_OK;
+}
+
+DecodeDev decode_dev(const tbs_model* m, const Workspace& w, int B, int T, int Ns, int Nc, int KT,
+                     const float* enc, const int* len, const int* base) {
+  DecodeDev d;
+  d.B = B;
+  d.T = T;
+  d.Ns = Ns;
+  d.Nc = Nc;
+  d.nvt = m->Vpad / kJoinerBN;
+  d.KT = KT;
+  d.enc = enc;
+  d.len = len;
+  d.base = base;
+  d.nsurv = w.nsurv;
+  d.surv_ctx = w.surv_ctx;
+  d.surv_state = w.surv_state;
+  d.surv_score = w.surv_score;
+  d.surv_row = w.surv_row;
+  d.nctx = w.nctx;
+  d.ctx_list = w.ctx_list;
+  d.offset = w.offset;
+  d.h = w.h;
+  d.logits = w.logits;
+  d.stats = w.stats;
+  d.tk_z = w.tk_z;
+  d.tk_c = w.tk_c;
+  d.z0 = w.z0;
+  d.hist_pl = w.hist_pl;
+  d.hist_arc = w.hist_arc;
+  d.path_lab = w.path_lab;
+  return d;
+}
+
+// Enqueues frames 0 .. maxlen-1 of d: the grouped or single-workgroup persistent
+// kernel, or the joiner and search kernels per frame.  xerr: the exchange-timeout
+// counter the grouped kernel adds to.  *grouped: whether the grouped kernel ran.
+tbs_status enqueue_frames(tbs_model* m, const tbs_graph* graph, float beam,
+                          const StreamPlan& splan, bool per_stream, const DecodeDev& d,
+                          int maxlen, int* trace, unsigned* xerr, hipStream_t st, bool* grouped) {
+  *grouped = false;
+  if (maxlen <= 0) return TBS_OK;
+  const ModelDev md = model_dev(m);
+  const GraphDev gd = graph_dev(graph);
+  const int G = (per_stream && m->schedule != TBS_SCHEDULE_STREAM_SINGLE)
+                    ? pick_group(m, splan, d.B, d.KT, maxlen, graph->trivial)
+                    : 1;
+  if (G > 1) {
+    HIP_TRY(ensure_xbuf(m, (size_t)d.B * G * 2 * group_words(d.Nc, d.KT), st), "exchange buffer");
+    const unsigned epoch = next_epoch();
+    hipError_t e = timed_launch(m, TBS_KERNEL_STREAM_GROUP, st, [&] {
+      return launch_stream_group(md, gd, d, beam, trace, splan, m->xbuf.p, G, epoch, 1u << 22,
+                                 xerr, st);
+    });
+    if (e == hipSuccess) {
+      *grouped = true;
+    } else if (e == hipErrorCooperativeLaunchTooLarge) {
+      (void)hipGetLastError();  // not co-resident here: one workgroup per stream instead
+    } else {
+      return hip_fail(e, "launch(stream group)");
+    }
+  }
+  if (per_stream && !*grouped)
+    HIP_TRY(timed_launch(m, TBS_KERNEL_STREAM, st,
+                         [&] { return launch_stream(md, gd, d, beam, trace, splan, st); }),
+            "launch(stream)");
+  if (!per_stream) {
+    const JoinerPlan plan = plan_joiner(d.B * d.Nc, m->Vpad, m->Kpad, m->bf16, m->ncu);
+    for (int t = 0; t < maxlen; ++t) {
+      HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
+                           [&] { return launch_joiner_frame(md, d, plan, t, st); }),
+              "launch(joiner)");
+      HIP_TRY(timed_launch(m, TBS_KERNEL_SEARCH, st,
+                           [&] { return launch_search_frame(md, gd, d, beam, t, trace, st); }),
+              "launch(search)");
+    }
+  }
+  return TBS_OK;
+}
+
+// Checks shared by tbs_decode and tbs_state_create.
+tbs_status check_params(const tbs_model* model, const tbs_graph* graph,
+                        const tbs_beam_params* params, const char* who) {
+  if (!model || !graph || !params) return fail(TBS_EINVAL, "%s: NULL model/graph/params", who);
+  if (graph->V != model->V)
+    return fail(TBS_EINVAL, "%s: graph vocab_size %d != model vocab_size %d", who, graph->V,
+                model->V);
+  const float beam = params->beam;
+  const int Ns = params->max_states, Nc = params->max_contexts;
+  if (std::isnan(beam) || beam < 0.f)
+    return fail(TBS_EINVAL, "%s: beam must be >= 0 or INFINITY", who);
+  if (Ns < 1 || Nc < 1)
+    return fail(TBS_EINVAL, "%s: max_states and max_contexts must be >= 1", who);
+  if (Ns > kMaxStates)
+    return fail(TBS_ECAPACITY, "%s: max_states %d exceeds the limit %d", who, Ns, kMaxStates);
+  if ((long long)Ns * ((long long)graph->maxdeg + 1) >= (1ll << 31))
+    return fail(TBS_ECAPACITY, "%s: max_states * (max out-degree + 1) = %lld must be < 2^31", who,
+                (long long)Ns * ((long long)graph->maxdeg + 1));
+  return TBS_OK;
+}
+
+// Waits (on st) for the model's previous device work; marks st's work as the latest.
+hipError_t model_wait(tbs_model* m, hipStream_t st) {
+  return m->busy_pending ? hipStreamWaitEvent(st, m->busy, 0) : hipSuccess;
+}
+hipError_t model_mark(tbs_model* m, hipStream_t st) {
+  hipError_t e = hipEventRecord(m->busy, st);
+  if (e == hipSuccess) m->busy_pending = true;
+  return e;
+}
+
 }  // namespace
+
+struct tbs_state {
+  tbs_model* m = nullptr;
+  const tbs_graph* g = nullptr;
+  float beam = 0.f;
+  int Ns = 0, Nc = 0, KT = 0, B = 0, Tcap = 0;
+  bool per_stream = false;
+  StreamPlan splan{};
+  Workspace w;
+  unsigned* xerr = nullptr;  // exchange timeouts over all chunks
+  std::vector<int> done;     // frames decoded so far per stream
+};
 
 extern "C" {
 
@@ -466,6 +621,7 @@ tbs_status tbs_model_create(int32_t vocab_size, int32_t dim, int32_t context_siz
     e = hipDeviceGetAttribute(&m->ncu, hipDeviceAttributeMultiprocessorCount, m->dev);
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&m->coop, hipDeviceAttributeCooperativeLaunch, m->dev);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&m->busy, hipEventDisableTiming);
   if (e == hipSuccess) e = dalloc(&m->xerr, 1);
   if (e == hipSuccess) e = hipMemsetAsync(m->xerr, 0, sizeof(unsigned), st);
   if (e == hipSuccess) e = dalloc(&m->P0, VK);
@@ -501,6 +657,10 @@ void tbs_model_destroy(tbs_model* m) {
   hipFree(m->Wi);
   hipFree(m->bias);
   hipFree(m->xerr);
+  if (m->busy) {
+    if (m->busy_pending) hipEventSynchronize(m->busy);
+    hipEventDestroy(m->busy);
+  }
   if (m->xbuf.p) {
     std::lock_guard<std::mutex> xl(g_xmu);
     g_xfree.push_back(m->xbuf);
@@ -516,23 +676,11 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
                       const int32_t* lengths, int32_t B, int32_t T, int32_t* out_tokens,
                       int32_t* out_num_tokens, double* out_scores, int32_t* out_status,
                       int32_t* out_arcs, int32_t* trace, void* hip_stream) {
-  if (!model || !graph || !params) return fail(TBS_EINVAL, "tbs_decode: NULL model/graph/params");
-  if (graph->V != model->V)
-    return fail(TBS_EINVAL, "tbs_decode: graph vocab_size %d != model vocab_size %d", graph->V,
-                model->V);
+  tbs_status s = check_params(model, graph, params, "tbs_decode");
+  if (s != TBS_OK) return s;
   if (B < 0 || T < 0) return fail(TBS_EINVAL, "tbs_decode: B and T must be >= 0");
   const float beam = params->beam;
   const int Ns = params->max_states, Nc_req = params->max_contexts;
-  if (std::isnan(beam) || beam < 0.f)
-    return fail(TBS_EINVAL, "tbs_decode: beam must be >= 0 or INFINITY");
-  if (Ns < 1 || Nc_req < 1)
-    return fail(TBS_EINVAL, "tbs_decode: max_states and max_contexts must be >= 1");
-  if (Ns > kMaxStates)
-    return fail(TBS_ECAPACITY, "tbs_decode: max_states %d exceeds the limit %d", Ns, kMaxStates);
-  if ((long long)Ns * ((long long)graph->maxdeg + 1) >= (1ll << 31))
-    return fail(TBS_ECAPACITY,
-                "tbs_decode: max_states * (max out-degree + 1) = %lld must be < 2^31",
-                (long long)Ns * ((long long)graph->maxdeg + 1));
   if (B == 0) return TBS_OK;
   if (!lengths) return fail(TBS_EINVAL, "tbs_decode: lengths is NULL");
   int maxlen = 0;
@@ -546,7 +694,6 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
     return fail(TBS_EINVAL, "tbs_decode: NULL output pointer");
   // More contexts than tuples can never be active.
   const int Nc = Nc_req < Ns ? Nc_req : Ns;
-
   // Trivial graph with few tuples: the joiner keeps each row's best labels per
   // vocabulary tile instead of materialising the logits.
   const int KT = (graph->trivial && Ns <= kMaxTopK) ? Ns : 0;
@@ -557,22 +704,12 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   const ModelDev md = model_dev(m);
   const StreamPlan splan = plan_stream(md, Nc, KT, graph->trivial);
   bool per_stream = false;
-  if (m->schedule == TBS_SCHEDULE_STREAM || m->schedule == TBS_SCHEDULE_STREAM_SINGLE) {
-    if (!splan.ok)
-      return fail(TBS_EUNSUPPORTED,
-                  "tbs_decode: the per-stream schedule does not fit max_contexts %d / "
-                  "max_states %d with V %d and dim %d",
-                  Nc, Ns, m->V, m->C);
-    per_stream = true;
-  } else if (m->schedule == TBS_SCHEDULE_AUTO) {
-    // One compute unit streams the whole joiner weight every frame: worth it while
-    // W stays L2-resident and the fp32 rows (broadcast from LDS to VALU FMAs) are few.
-    per_stream = splan.ok && (size_t)m->Vpad * m->Kpad * (m->bf16 ? 2 : 4) <= (4u << 20) &&
-                 (m->bf16 || Nc <= 4);
-  }
-  tbs_status s = ensure_workspace(m, B, T, Ns, Nc, KT, KT == 0);
+  s = choose_schedule(m, splan, Ns, Nc, "tbs_decode", &per_stream);
+  if (s != TBS_OK) return s;
+  s = ensure_workspace(m, B, T, Ns, Nc, KT, KT == 0);
   if (s != TBS_OK) return s;
   Workspace& w = m->ws;
+  HIP_TRY(model_wait(m, st), "hipStreamWaitEvent");
   if (w.pending) HIP_TRY(hipStreamWaitEvent(st, w.done, 0), "hipStreamWaitEvent");
   // lengths: wait until the previous decode consumed the pinned staging buffer
   if (w.pending) HIP_TRY(hipEventSynchronize(w.done), "hipEventSynchronize");
@@ -580,70 +717,15 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   HIP_TRY(hipMemcpyAsync(w.len, w.len_host, (size_t)B * 4, hipMemcpyHostToDevice, st),
           "hipMemcpyAsync(lengths)");
 
-  DecodeDev d;
-  d.B = B;
-  d.T = T;
-  d.Ns = Ns;
-  d.Nc = Nc;
-  d.nvt = m->Vpad / kJoinerBN;
-  d.KT = KT;
-  d.enc = encoder_out;
-  d.len = w.len;
-  d.nsurv = w.nsurv;
-  d.surv_ctx = w.surv_ctx;
-  d.surv_state = w.surv_state;
-  d.surv_score = w.surv_score;
-  d.surv_row = w.surv_row;
-  d.nctx = w.nctx;
-  d.ctx_list = w.ctx_list;
-  d.offset = w.offset;
-  d.h = w.h;
-  d.logits = w.logits;
-  d.stats = w.stats;
-  d.tk_z = w.tk_z;
-  d.tk_c = w.tk_c;
-  d.z0 = w.z0;
-  d.hist_pl = w.hist_pl;
-  d.hist_arc = w.hist_arc;
-  d.path_lab = w.path_lab;
+  const DecodeDev d = decode_dev(m, w, B, T, Ns, Nc, KT, encoder_out, w.len, nullptr);
   const GraphDev gd = graph_dev(graph);
-  const JoinerPlan plan = plan_joiner(B * Nc, m->Vpad, m->Kpad, m->bf16, m->ncu);
-
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
-  const int G = (per_stream && m->schedule != TBS_SCHEDULE_STREAM_SINGLE)
-                    ? pick_group(m, splan, B, KT, maxlen, graph->trivial)
-                    : 1;
+  HIP_TRY(launch_fill_i32((int*)m->xerr, 1, 0, st), "fill(exchange errors)");
   bool grouped = false;
-  if (G > 1 && maxlen > 0) {
-    HIP_TRY(ensure_xbuf(m, (size_t)B * G * 2 * group_words(Nc, KT), st), "exchange buffer");
-    HIP_TRY(launch_fill_i32((int*)m->xerr, 1, 0, st), "fill(exchange errors)");
-    const unsigned epoch = next_epoch();
-    hipError_t e = timed_launch(m, TBS_KERNEL_STREAM_GROUP, st, [&] {
-      return launch_stream_group(md, gd, d, beam, trace, splan, m->xbuf.p, G, epoch, 1u << 22,
-                                 m->xerr, st);
-    });
-    if (e == hipSuccess) {
-      grouped = true;
-    } else if (e == hipErrorCooperativeLaunchTooLarge) {
-      (void)hipGetLastError();  // not co-resident here: one workgroup per stream instead
-    } else {
-      return hip_fail(e, "launch(stream group)");
-    }
-  }
-  if (per_stream && !grouped && maxlen > 0)
-    HIP_TRY(timed_launch(m, TBS_KERNEL_STREAM, st,
-                         [&] { return launch_stream(md, gd, d, beam, trace, splan, st); }),
-            "launch(stream)");
-  for (int t = 0; !per_stream && t < maxlen; ++t) {
-    HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
-                         [&] { return launch_joiner_frame(md, d, plan, t, st); }),
-            "launch(joiner)");
-    HIP_TRY(timed_launch(m, TBS_KERNEL_SEARCH, st,
-                         [&] { return launch_search_frame(md, gd, d, beam, t, trace, st); }),
-            "launch(search)");
-  }
+  s = enqueue_frames(m, graph, beam, splan, per_stream, d, maxlen, trace, m->xerr, st, &grouped);
+  if (s != TBS_OK) return s;
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
                          return launch_final(gd, d, out_tokens, out_num_tokens, out_scores,
@@ -653,7 +735,147 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
           "launch(final)");
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
   w.pending = true;
+  HIP_TRY(model_mark(m, st), "hipEventRecord");
   return TBS_OK;
+}
+
+tbs_status tbs_state_create(const tbs_model* model, const tbs_graph* graph,
+                            const tbs_beam_params* params, int32_t B, int32_t max_frames,
+                            void* hip_stream, tbs_state** out) {
+  if (!out) return fail(TBS_EINVAL, "tbs_state_create: out is NULL");
+  *out = nullptr;
+  tbs_status s = check_params(model, graph, params, "tbs_state_create");
+  if (s != TBS_OK) return s;
+  if (B < 1 || max_frames < 1)
+    return fail(TBS_EINVAL, "tbs_state_create: B and max_frames must be >= 1");
+  tbs_model* m = const_cast<tbs_model*>(model);
+  std::lock_guard<std::mutex> lk(m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  tbs_state* S = new tbs_state();
+  S->m = m;
+  S->g = graph;
+  S->beam = params->beam;
+  S->Ns = params->max_states;
+  S->Nc = params->max_contexts < S->Ns ? params->max_contexts : S->Ns;
+  S->KT = (graph->trivial && S->Ns <= kMaxTopK) ? S->Ns : 0;
+  S->B = B;
+  S->Tcap = max_frames;
+  S->done.assign(B, 0);
+  const ModelDev md = model_dev(m);
+  S->splan = plan_stream(md, S->Nc, S->KT, graph->trivial);
+  s = choose_schedule(m, S->splan, S->Ns, S->Nc, "tbs_state_create", &S->per_stream);
+  if (s == TBS_OK) s = alloc_workspace(m, S->w, B, max_frames, S->Ns, S->Nc, S->KT, S->KT == 0);
+  hipError_t e = hipSuccess;
+  if (s == TBS_OK) {
+    e = dalloc(&S->xerr, 1);
+    if (e == hipSuccess) e = launch_fill_i32((int*)S->xerr, 1, 0, st);
+    // the initial tuple of every stream (k_init with zero lengths writes no joiner row)
+    if (e == hipSuccess) e = launch_fill_i32(S->w.len, 2 * (long long)B, 0, st);
+    if (e == hipSuccess) {
+      const DecodeDev d = decode_dev(m, S->w, B, max_frames, S->Ns, S->Nc, S->KT, nullptr,
+                                     S->w.len, nullptr);
+      e = launch_init(md, d, graph_dev(graph), nullptr, st);
+    }
+    if (e == hipSuccess) e = hipEventRecord(S->w.done, st);
+    if (e == hipSuccess) S->w.pending = true;
+    if (e != hipSuccess) s = hip_fail(e, "tbs_state_create");
+  }
+  if (s != TBS_OK) {
+    if (S->w.pending) hipEventSynchronize(S->w.done);
+    S->w.release();
+    hipFree(S->xerr);
+    delete S;
+    return s;
+  }
+  *out = S;
+  return TBS_OK;
+}
+
+tbs_status tbs_decode_chunk(tbs_state* S, const float* encoder_chunk,
+                            const int32_t* chunk_lengths, int32_t Tc, int32_t* trace,
+                            void* hip_stream) {
+  if (!S) return fail(TBS_EINVAL, "tbs_decode_chunk: state is NULL");
+  if (Tc < 0) return fail(TBS_EINVAL, "tbs_decode_chunk: Tc must be >= 0");
+  if (!chunk_lengths) return fail(TBS_EINVAL, "tbs_decode_chunk: chunk_lengths is NULL");
+  const int B = S->B;
+  int maxlen = 0;
+  for (int b = 0; b < B; ++b) {
+    if (chunk_lengths[b] < 0 || chunk_lengths[b] > Tc)
+      return fail(TBS_EINVAL, "tbs_decode_chunk: chunk_lengths[%d] = %d outside [0, %d]", b,
+                  chunk_lengths[b], Tc);
+    if ((long long)S->done[b] + chunk_lengths[b] > S->Tcap)
+      return fail(TBS_ECAPACITY,
+                  "tbs_decode_chunk: stream %d would reach %lld frames, beyond max_frames %d", b,
+                  (long long)S->done[b] + chunk_lengths[b], S->Tcap);
+    if (chunk_lengths[b] > maxlen) maxlen = chunk_lengths[b];
+  }
+  if (maxlen > 0 && !encoder_chunk)
+    return fail(TBS_EINVAL, "tbs_decode_chunk: encoder_chunk is NULL");
+  if (maxlen == 0) return TBS_OK;
+  tbs_model* m = S->m;
+  std::lock_guard<std::mutex> lk(m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  Workspace& w = S->w;
+  HIP_TRY(model_wait(m, st), "hipStreamWaitEvent");
+  if (w.pending) HIP_TRY(hipStreamWaitEvent(st, w.done, 0), "hipStreamWaitEvent");
+  if (w.pending) HIP_TRY(hipEventSynchronize(w.done), "hipEventSynchronize");
+  // chunk lengths and each stream's frame base, through the pinned staging buffer
+  std::memcpy(w.len_host, chunk_lengths, (size_t)B * 4);
+  std::memcpy(w.len_host + B, S->done.data(), (size_t)B * 4);
+  HIP_TRY(hipMemcpyAsync(w.len, w.len_host, (size_t)2 * B * 4, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(lengths)");
+  const DecodeDev d = decode_dev(m, w, B, Tc, S->Ns, S->Nc, S->KT, encoder_chunk, w.len,
+                                 w.len + B);
+  HIP_TRY(launch_resume(model_dev(m), d, graph_dev(S->g), trace, S->per_stream ? 0 : 1, st),
+          "launch(resume)");
+  bool grouped = false;
+  tbs_status s = enqueue_frames(m, S->g, S->beam, S->splan, S->per_stream, d, maxlen, trace,
+                                S->xerr, st, &grouped);
+  if (s != TBS_OK) return s;
+  HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
+  w.pending = true;
+  HIP_TRY(model_mark(m, st), "hipEventRecord");
+  for (int b = 0; b < B; ++b) S->done[b] += chunk_lengths[b];
+  return TBS_OK;
+}
+
+tbs_status tbs_state_finish(tbs_state* S, int32_t* out_tokens, int32_t* out_num_tokens,
+                            double* out_scores, int32_t* out_status, int32_t* out_arcs,
+                            void* hip_stream) {
+  if (!S) return fail(TBS_EINVAL, "tbs_state_finish: state is NULL");
+  if (!out_tokens || !out_num_tokens || !out_scores)
+    return fail(TBS_EINVAL, "tbs_state_finish: NULL output pointer");
+  tbs_model* m = S->m;
+  std::lock_guard<std::mutex> lk(m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  Workspace& w = S->w;
+  if (w.pending) HIP_TRY(hipStreamWaitEvent(st, w.done, 0), "hipStreamWaitEvent");
+  if (w.pending) HIP_TRY(hipEventSynchronize(w.done), "hipEventSynchronize");
+  std::memcpy(w.len_host, S->done.data(), (size_t)S->B * 4);
+  HIP_TRY(hipMemcpyAsync(w.len, w.len_host, (size_t)S->B * 4, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(lengths)");
+  const DecodeDev d = decode_dev(m, w, S->B, S->Tcap, S->Ns, S->Nc, S->KT, nullptr, w.len,
+                                 nullptr);
+  HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
+                       [&] {
+                         return launch_final(graph_dev(S->g), d, out_tokens, out_num_tokens,
+                                             out_scores, out_status, out_arcs, S->xerr, st);
+                       }),
+          "launch(final)");
+  HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
+  w.pending = true;
+  return TBS_OK;
+}
+
+void tbs_state_destroy(tbs_state* S) {
+  if (!S) return;
+  {
+    std::lock_guard<std::mutex> lk(S->m->mu);
+    if (S->w.pending) hipEventSynchronize(S->w.done);
+    S->w.release();
+  }
+  hipFree(S->xerr);
+  delete S;
 }
 
 tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const int32_t* ctx,

@@ -54,6 +54,7 @@ struct DecodeDev {
   int KT;                   // trivial fast path: candidates kept per (row, tile); 0 = off
   const float* enc;         // [B][T][C]
   const int* len;           // [B]
+  const int* base;          // [B] absolute index of frame 0 of this call (chunked decode) or null
   int* nsurv;               // [B]
   int* surv_ctx;            // [B][Ns]
   int* surv_state;          // [B][Ns]
@@ -117,6 +118,8 @@ hipError_t launch_model_setup(const float* embed, const float* conv, const float
 hipError_t launch_fill_i32(int* p, long long n, int v, hipStream_t st);
 hipError_t launch_init(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,
                        hipStream_t st);
+hipError_t launch_resume(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,
+                         int rows_needed, hipStream_t st);
 hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const JoinerPlan& p, int t,
                                hipStream_t st);
 hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const DecodeDev& d,

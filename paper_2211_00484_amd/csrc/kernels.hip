@@ -733,6 +733,39 @@ __global__ __launch_bounds__(256) void k_init(ModelDev m, DecodeDev d, GraphDev 
   }
 }
 
+// Start of a decode chunk (streaming decode): for each stream that advances in this
+// chunk, the joiner rows of its current contexts from the chunk's first encoder
+// frame (frame schedule: rows_needed), and for a stream still at its absolute frame
+// 0 the trace row of its initial tuple.
+__global__ __launch_bounds__(256) void k_resume(ModelDev m, DecodeDev d, GraphDev g,
+                                                int* __restrict__ trace, int rows_needed) {
+  __shared__ int2 s_off[kMaxStates];
+  __shared__ int s_nc;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  if (d.len[b] == 0) return;
+  if (tid == 0) {
+    s_nc = d.nctx[b];
+    if (trace && d.base[b] == 0) {
+      int* p = trace + (size_t)b * d.Ns * 4;
+      p[0] = d.surv_ctx[(size_t)b * d.Ns];
+      p[1] = d.surv_state[(size_t)b * d.Ns];
+      p[2] = -1;
+      p[3] = -1;
+    }
+  }
+  __syncthreads();
+  if (!rows_needed) return;
+  const int nc = s_nc;
+  for (int j = tid; j < nc; j += blockDim.x) {
+    const int c = d.ctx_list[(size_t)b * d.Nc + j], a = c / m.V;
+    s_off[j] = make_int2(a * m.Kpad, (c - a * m.V) * m.Kpad);
+  }
+  __syncthreads();
+  const size_t esz = m.bf16 ? 2 : 4;
+  write_h_rows<256>(m, d.enc + (size_t)b * d.T * m.C, 0, s_off, nc,
+                    reinterpret_cast<char*>(d.h) + (size_t)b * d.Nc * m.Kpad * esz, m.Kpad, tid);
+}
+
 struct SearchSmem {
   unsigned long long hk[kHashSlots];  // hash keys; also stages softmax partials
   unsigned long long hv[kHashSlots];
@@ -1012,14 +1045,16 @@ __device__ __forceinline__ WaveSel trivial_select_wave(SearchSmem& s, int ns, in
 // (trivial graph, max_states = 4, FUSED): LDS decoder rows, [16][Kpad] of the label
 // candidates (gathered by waves 1-3 while wave 0 selects) and [2][4][Kpad] of the
 // contexts (buffer dcur_buf holds the current ones); the next frame's joiner rows
-// are built from them (enc_next must be zero from C to Kpad).
+// are built from them (enc_next must be zero from C to Kpad).  fb: the stream's
+// absolute index of frame 0 of this call (history and trace rows; chunked decode).
 template <bool TRIV, bool FUSED>
 __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& g,
                                              const DecodeDev& d, float beam, int t, int L, int b,
                                              int* __restrict__ trace, SearchSmem& s, void* hl,
                                              int hstride, const float* zl, bool prestats = false,
                                              bool writer = true, bool enc_ready = false,
-                                             float* dspec = nullptr, int dcur_buf = 0) {
+                                             float* dspec = nullptr, int dcur_buf = 0,
+                                             int fb = 0) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V, nvt = d.nvt;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
@@ -1751,13 +1786,13 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       d.surv_row[o] = my_crow;
       if (my_first) d.ctx_list[row0 + my_crow] = (int)my_ci;
     }
-    const size_t hbase = ((size_t)t * d.B + b) * Ns;
+    const size_t hbase = ((size_t)(fb + t) * d.B + b) * Ns;
     if (writer) {
       d.hist_pl[hbase + my_pos] = (parent << 16) | label;
       d.hist_arc[hbase + my_pos] = arc;
     }
     if (writer && trace) {
-      int* tr = trace + (((size_t)(t + 1) * d.B + b) * Ns + my_pos) * 4;
+      int* tr = trace + (((size_t)(fb + t + 1) * d.B + b) * Ns + my_pos) * 4;
       tr[0] = (int)my_ci;
       tr[1] = (int)my_st;
       tr[2] = parent;
@@ -1786,7 +1821,9 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
   if (t >= L) return;
   extern __shared__ __align__(16) unsigned char smem[];
   SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
-  search_frame<TRIV, false>(m, g, d, beam, t, L, b, trace, s, nullptr, 0, nullptr);
+  const int fb = d.base ? d.base[b] : 0;
+  search_frame<TRIV, false>(m, g, d, beam, t, L, b, trace, s, nullptr, 0, nullptr, false, true,
+                            false, nullptr, 0, fb);
 }
 
 // ---------------------------------------------------------------------------
@@ -1949,6 +1986,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
   float* zl = reinterpret_cast<float*>(smem + zoff);
   const int tid = threadIdx.x;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V;
+  const int fb = d.base ? d.base[b] : 0;  // absolute index of this call's frame 0
   const size_t row0 = (size_t)b * Nc;
   // state after the initial tuple (written by k_init), encoder frame 0, zeroed rows
   if (tid == 0) {
@@ -2006,7 +2044,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
     }
     __syncthreads();
     search_frame<TRIV, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, zl, false, true, true,
-                             dspec, cur);
+                             dspec, cur, fb);
     __syncthreads();
     cur ^= 1;
   }
@@ -2168,6 +2206,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
   const size_t row0 = (size_t)b * Nc;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
   const bool writer = mem == 0;
+  const int fb = d.base ? d.base[b] : 0;  // absolute index of this call's frame 0
   // the member's W slice (RES) and bias, for the whole decode
   float4 wres[kResSlices];
   if (RES) {
@@ -2427,7 +2466,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     __syncthreads();
     if (!FAST) {
       search_frame<true, true>(m, g, d, beam, t, L, b, trace, s, hl, hstride, nullptr, true,
-                               writer, true);
+                               writer, true, nullptr, 0, fb);
       __syncthreads();
       continue;
     }
@@ -2516,11 +2555,11 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         d.ctx_list[row0 + pos] = (int)sel.ci;
       }
       if (writer) {
-        const size_t hb = ((size_t)t * d.B + b) * Ns + pos;
+        const size_t hb = ((size_t)(fb + t) * d.B + b) * Ns + pos;
         d.hist_pl[hb] = (parent << 16) | label;
         d.hist_arc[hb] = arc;
         if (trace) {
-          int* tr = trace + (((size_t)(t + 1) * d.B + b) * Ns + pos) * 4;
+          int* tr = trace + (((size_t)(fb + t + 1) * d.B + b) * Ns + pos) * 4;
           tr[0] = (int)sel.ci;
           tr[1] = (int)sel.st;
           tr[2] = parent;
@@ -2764,6 +2803,12 @@ hipError_t launch_model_setup(const float* embed, const float* conv, const float
 hipError_t launch_fill_i32(int* p, long long n, int v, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(n, 256)), dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_resume(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,
+                         int rows_needed, hipStream_t st) {
+  hipLaunchKernelGGL(k_resume, dim3(d.B), dim3(256), 0, st, m, d, g, trace, rows_needed);
   return hipGetLastError();
 }
 

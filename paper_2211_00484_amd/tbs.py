@@ -89,6 +89,15 @@ def lib():
     L.tbs_model_read_profile.argtypes = [_P, ctypes.POINTER(KernelTime)]
     L.tbs_joiner_logp.restype = _I32
     L.tbs_joiner_logp.argtypes = [_P, _P, _P, _I32, _P, _P]
+    L.tbs_state_create.restype = _I32
+    L.tbs_state_create.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _I32, _I32, _P,
+                                   ctypes.POINTER(_P)]
+    L.tbs_decode_chunk.restype = _I32
+    L.tbs_decode_chunk.argtypes = [_P, _P, _P, _I32, _P, _P]
+    L.tbs_state_finish.restype = _I32
+    L.tbs_state_finish.argtypes = [_P, _P, _P, _P, _P, _P, _P]
+    L.tbs_state_destroy.restype = None
+    L.tbs_state_destroy.argtypes = [_P]
     _lib = L
     return L
 
@@ -274,3 +283,47 @@ def joiner_logp(model: Model, enc_rows, ctx, stream=None):
     _check(lib().tbs_joiner_logp(model._h, _dev_ptr(enc_rows.contiguous()), _dev_ptr(ctx), R,
                                  _dev_ptr(out), _stream_ptr(stream)))
     return out
+
+
+class DecodeState:
+    """Streaming decode (tbs_state_create / tbs_decode_chunk / tbs_state_finish):
+    each chunk continues every stream from where it stopped; finish traces the best
+    paths back over all decoded frames."""
+
+    def __init__(self, model: Model, graph: Graph, B: int, max_frames: int,
+                 beam: float = math.inf, max_states: int = 4, max_contexts: int = 4,
+                 stream=None):
+        params = BeamParams(float(math.inf if beam is None else beam), int(max_states),
+                            int(max_contexts))
+        h = _P()
+        _check(lib().tbs_state_create(model._h, graph._h, ctypes.byref(params), int(B),
+                                      int(max_frames), _stream_ptr(stream), ctypes.byref(h)))
+        self._h = h
+        self._refs = (model, graph)  # the state must not outlive them
+        self.B, self.max_frames, self.max_states = int(B), int(max_frames), int(max_states)
+
+    def chunk(self, encoder_chunk, lengths, trace=None, stream=None):
+        """Decode the next frames: encoder_chunk [B, Tc, C] on the device, lengths [B]
+        frames per stream (host); trace: optional [max_frames+1, B, Ns, 4] int32 buffer."""
+        lens = np.ascontiguousarray(np.asarray(lengths), dtype=np.int32)
+        B, Tc = int(encoder_chunk.shape[0]), int(encoder_chunk.shape[1])
+        if B != self.B or lens.shape != (B,):
+            raise ValueError("encoder_chunk / lengths do not match the state's batch")
+        _check(lib().tbs_decode_chunk(self._h, _dev_ptr(encoder_chunk.contiguous()),
+                                      _host_ptr(lens), Tc, _dev_ptr(trace), _stream_ptr(stream)))
+
+    def finish(self, want_arcs: bool = False, stream=None) -> DecodeOutput:
+        out = allocate_outputs(self.B, self.max_frames, self.max_states, status=True,
+                               arcs=want_arcs)
+        _check(lib().tbs_state_finish(self._h, _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
+                                      _dev_ptr(out.scores), _dev_ptr(out.status),
+                                      _dev_ptr(out.arcs), _stream_ptr(stream)))
+        return out
+
+    def close(self):
+        if self._h is not None and _lib is not None:
+            _lib.tbs_state_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        self.close()
