@@ -163,6 +163,23 @@ tbs_status tbs_decode(const tbs_model *model, const tbs_graph *graph,
                       int32_t *out_arcs, int32_t *trace, void *hip_stream);
 
 /*
+ * tbs_decode with one decoding graph per stream (Algorithm 1 takes the graph of
+ * stream i from a vector of graphs): graphs is a HOST array of B graph handles
+ * (entries may repeat); stream b searches graphs[b], and every output of stream b
+ * is what tbs_decode gives for that stream alone with graph graphs[b].  Other
+ * arguments, outputs and errors as for tbs_decode, with every graph checked
+ * against the model and params (B >= 1 needs graphs != NULL).  The graphs must
+ * stay alive until the decode has completed on hip_stream.  Every stream takes the
+ * general search path (no trivial-graph fast path), so a batch of trivial graphs
+ * decodes more slowly here than through tbs_decode.
+ */
+tbs_status tbs_decode_graphs(const tbs_model *model, const tbs_graph *const *graphs,
+                             const tbs_beam_params *params, const float *encoder_out,
+                             const int32_t *lengths, int32_t B, int32_t T, int32_t *out_tokens,
+                             int32_t *out_num_tokens, double *out_scores, int32_t *out_status,
+                             int32_t *out_arcs, int32_t *trace, void *hip_stream);
+
+/*
  * Streaming decode: tbs_decode split into chunks of frames (the decoding state of
  * Algorithm 1 carried across calls).  A decode state holds, for each of B streams,
  * the surviving tuples, the fp64 score offset and the back-pointers of every frame
@@ -200,6 +217,11 @@ typedef struct tbs_state tbs_state;
 tbs_status tbs_state_create(const tbs_model *model, const tbs_graph *graph,
                             const tbs_beam_params *params, int32_t B, int32_t max_frames,
                             void *hip_stream, tbs_state **out);
+/* tbs_state_create with one graph per stream (HOST array graphs[B], as for
+ * tbs_decode_graphs); the state keeps references to the graphs. */
+tbs_status tbs_state_create_graphs(const tbs_model *model, const tbs_graph *const *graphs,
+                                   const tbs_beam_params *params, int32_t B, int32_t max_frames,
+                                   void *hip_stream, tbs_state **out);
 tbs_status tbs_decode_chunk(tbs_state *state, const float *encoder_chunk,
                             const int32_t *chunk_lengths, int32_t Tc, int32_t *trace,
                             void *hip_stream);

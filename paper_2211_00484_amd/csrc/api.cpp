@@ -72,6 +72,8 @@ struct Workspace {
   int* hist_arc = nullptr;
   int* path_lab = nullptr;
   int* len_host = nullptr;  // pinned staging for lengths (and frame bases), [2B]
+  GraphDev* gtab = nullptr;       // [B] per-stream graph table (decodes with one graph per stream)
+  GraphDev* gtab_host = nullptr;  // pinned staging for it
   hipEvent_t done = nullptr;
   bool pending = false;
 
@@ -80,7 +82,9 @@ struct Workspace {
     hipFree(surv_row); hipFree(nctx); hipFree(ctx_list); hipFree(offset); hipFree(h);
     hipFree(logits); hipFree(stats); hipFree(tk_z); hipFree(tk_c); hipFree(z0);
     hipFree(hist_pl); hipFree(hist_arc); hipFree(path_lab);
+    hipFree(gtab);
     if (len_host) hipHostFree(len_host);
+    if (gtab_host) hipHostFree(gtab_host);
     if (done) hipEventDestroy(done);
     *this = Workspace();
   }
@@ -286,7 +290,11 @@ tbs_status alloc_workspace(const tbs_model* m, Workspace& w, int B, int T, int N
   HIP_TRY(dalloc(&w.hist_pl, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.hist_arc, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.path_lab, (size_t)B * T), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.gtab, B), "hipMalloc(workspace)");
   HIP_TRY(hipHostMalloc((void**)&w.len_host, (size_t)(B > 0 ? 2 * B : 1) * 4, hipHostMallocDefault),
+          "hipHostMalloc(workspace)");
+  HIP_TRY(hipHostMalloc((void**)&w.gtab_host, (size_t)(B > 0 ? B : 1) * sizeof(GraphDev),
+                        hipHostMallocDefault),
           "hipHostMalloc(workspace)");
   HIP_TRY(hipEventCreateWithFlags(&w.done, hipEventDisableTiming), "hipEventCreate");
   w.B = B;
@@ -388,7 +396,7 @@ tbs_status choose_schedule(const tbs_model* m, const StreamPlan& splan, int Ns, 
 }
 
 DecodeDev decode_dev(const tbs_model* m, const Workspace& w, int B, int T, int Ns, int Nc, int KT,
-                     const float* enc, const int* len, const int* base) {
+                     const float* enc, const int* len, const int* base, bool per_graph) {
   DecodeDev d;
   d.B = B;
   d.T = T;
@@ -399,6 +407,7 @@ DecodeDev decode_dev(const tbs_model* m, const Workspace& w, int B, int T, int N
   d.enc = enc;
   d.len = len;
   d.base = base;
+  d.graphs = per_graph ? w.gtab : nullptr;
   d.nsurv = w.nsurv;
   d.surv_ctx = w.surv_ctx;
   d.surv_state = w.surv_state;
@@ -422,15 +431,14 @@ DecodeDev decode_dev(const tbs_model* m, const Workspace& w, int B, int T, int N
 // Enqueues frames 0 .. maxlen-1 of d: the grouped or single-workgroup persistent
 // kernel, or the joiner and search kernels per frame.  xerr: the exchange-timeout
 // counter the grouped kernel adds to.  *grouped: whether the grouped kernel ran.
-tbs_status enqueue_frames(tbs_model* m, const tbs_graph* graph, float beam,
+tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
                           const StreamPlan& splan, bool per_stream, const DecodeDev& d,
                           int maxlen, int* trace, unsigned* xerr, hipStream_t st, bool* grouped) {
   *grouped = false;
   if (maxlen <= 0) return TBS_OK;
   const ModelDev md = model_dev(m);
-  const GraphDev gd = graph_dev(graph);
   const int G = (per_stream && m->schedule != TBS_SCHEDULE_STREAM_SINGLE)
-                    ? pick_group(m, splan, d.B, d.KT, maxlen, graph->trivial)
+                    ? pick_group(m, splan, d.B, d.KT, maxlen, gd.trivial)
                     : 1;
   if (G > 1) {
     HIP_TRY(ensure_xbuf(m, (size_t)d.B * G * 2 * group_words(d.Nc, d.KT), st), "exchange buffer");
@@ -486,6 +494,39 @@ tbs_status check_params(const tbs_model* model, const tbs_graph* graph,
   return TBS_OK;
 }
 
+// The graphs of a decode: one shared graph, or one per stream (graphs[B], host array).
+// The returned descriptor is the shared graph's, or (per-stream graphs) the first
+// graph's with the largest out-degree of all and no trivial-graph fast path; the
+// kernels then take each stream's own descriptor from the workspace's graph table.
+tbs_status graph_set(const tbs_model* model, const tbs_graph* graph,
+                     const tbs_graph* const* graphs, int B, const tbs_beam_params* params,
+                     const char* who, GraphDev* out) {
+  if (!graphs) {
+    tbs_status s = check_params(model, graph, params, who);
+    if (s == TBS_OK) *out = graph_dev(graph);
+    return s;
+  }
+  if (B < 1) return fail(TBS_EINVAL, "%s: B must be >= 1", who);
+  int maxdeg = 0;
+  for (int b = 0; b < B; ++b) {
+    if (!graphs[b]) return fail(TBS_EINVAL, "%s: graphs[%d] is NULL", who, b);
+    tbs_status s = check_params(model, graphs[b], params, who);
+    if (s != TBS_OK) return s;
+    if (graphs[b]->maxdeg > maxdeg) maxdeg = graphs[b]->maxdeg;
+  }
+  *out = graph_dev(graphs[0]);
+  out->maxdeg = maxdeg;
+  out->trivial = 0;
+  return TBS_OK;
+}
+
+// Stages the per-stream graph table of w (w's previous device work must be done).
+hipError_t upload_graphs(Workspace& w, const tbs_graph* const* graphs, int B, hipStream_t st) {
+  for (int b = 0; b < B; ++b) w.gtab_host[b] = graph_dev(graphs[b]);
+  return hipMemcpyAsync(w.gtab, w.gtab_host, (size_t)B * sizeof(GraphDev), hipMemcpyHostToDevice,
+                        st);
+}
+
 // Waits (on st) for the model's previous device work; marks st's work as the latest.
 hipError_t model_wait(tbs_model* m, hipStream_t st) {
   return m->busy_pending ? hipStreamWaitEvent(st, m->busy, 0) : hipSuccess;
@@ -500,7 +541,8 @@ hipError_t model_mark(tbs_model* m, hipStream_t st) {
 
 struct tbs_state {
   tbs_model* m = nullptr;
-  const tbs_graph* g = nullptr;
+  GraphDev gd{};            // the shared graph, or the per-stream graphs' summary
+  bool per_graph = false;   // one graph per stream (table in w.gtab)
   float beam = 0.f;
   int Ns = 0, Nc = 0, KT = 0, B = 0, Tcap = 0;
   bool per_stream = false;
@@ -671,60 +713,68 @@ void tbs_model_destroy(tbs_model* m) {
   delete m;
 }
 
-tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
-                      const tbs_beam_params* params, const float* encoder_out,
-                      const int32_t* lengths, int32_t B, int32_t T, int32_t* out_tokens,
-                      int32_t* out_num_tokens, double* out_scores, int32_t* out_status,
-                      int32_t* out_arcs, int32_t* trace, void* hip_stream) {
-  tbs_status s = check_params(model, graph, params, "tbs_decode");
+}  // extern "C"
+
+namespace {
+
+// tbs_decode and tbs_decode_graphs: one shared graph, or graphs[B] (one per stream).
+tbs_status decode_impl(const tbs_model* model, const tbs_graph* graph,
+                       const tbs_graph* const* graphs, const tbs_beam_params* params,
+                       const float* encoder_out, const int32_t* lengths, int32_t B, int32_t T,
+                       int32_t* out_tokens, int32_t* out_num_tokens, double* out_scores,
+                       int32_t* out_status, int32_t* out_arcs, int32_t* trace, void* hip_stream,
+                       const char* who) {
+  if (B < 0 || T < 0) return fail(TBS_EINVAL, "%s: B and T must be >= 0", who);
+  if (B == 0) return graphs ? TBS_OK : check_params(model, graph, params, who);
+  GraphDev gd;
+  tbs_status s = graph_set(model, graph, graphs, B, params, who, &gd);
   if (s != TBS_OK) return s;
-  if (B < 0 || T < 0) return fail(TBS_EINVAL, "tbs_decode: B and T must be >= 0");
   const float beam = params->beam;
   const int Ns = params->max_states, Nc_req = params->max_contexts;
-  if (B == 0) return TBS_OK;
-  if (!lengths) return fail(TBS_EINVAL, "tbs_decode: lengths is NULL");
+  if (!lengths) return fail(TBS_EINVAL, "%s: lengths is NULL", who);
   int maxlen = 0;
   for (int b = 0; b < B; ++b) {
     if (lengths[b] < 0 || lengths[b] > T)
-      return fail(TBS_EINVAL, "tbs_decode: lengths[%d] = %d outside [0, %d]", b, lengths[b], T);
+      return fail(TBS_EINVAL, "%s: lengths[%d] = %d outside [0, %d]", who, b, lengths[b], T);
     if (lengths[b] > maxlen) maxlen = lengths[b];
   }
-  if (maxlen > 0 && !encoder_out) return fail(TBS_EINVAL, "tbs_decode: encoder_out is NULL");
+  if (maxlen > 0 && !encoder_out) return fail(TBS_EINVAL, "%s: encoder_out is NULL", who);
   if (!out_num_tokens || !out_scores || (T > 0 && !out_tokens))
-    return fail(TBS_EINVAL, "tbs_decode: NULL output pointer");
+    return fail(TBS_EINVAL, "%s: NULL output pointer", who);
   // More contexts than tuples can never be active.
   const int Nc = Nc_req < Ns ? Nc_req : Ns;
   // Trivial graph with few tuples: the joiner keeps each row's best labels per
   // vocabulary tile instead of materialising the logits.
-  const int KT = (graph->trivial && Ns <= kMaxTopK) ? Ns : 0;
+  const int KT = (gd.trivial && Ns <= kMaxTopK) ? Ns : 0;
 
   tbs_model* m = const_cast<tbs_model*>(model);
   std::lock_guard<std::mutex> lk(m->mu);
   hipStream_t st = (hipStream_t)hip_stream;
   const ModelDev md = model_dev(m);
-  const StreamPlan splan = plan_stream(md, Nc, KT, graph->trivial);
+  const StreamPlan splan = plan_stream(md, Nc, KT, gd.trivial);
   bool per_stream = false;
-  s = choose_schedule(m, splan, Ns, Nc, "tbs_decode", &per_stream);
+  s = choose_schedule(m, splan, Ns, Nc, who, &per_stream);
   if (s != TBS_OK) return s;
   s = ensure_workspace(m, B, T, Ns, Nc, KT, KT == 0);
   if (s != TBS_OK) return s;
   Workspace& w = m->ws;
   HIP_TRY(model_wait(m, st), "hipStreamWaitEvent");
   if (w.pending) HIP_TRY(hipStreamWaitEvent(st, w.done, 0), "hipStreamWaitEvent");
-  // lengths: wait until the previous decode consumed the pinned staging buffer
+  // lengths: wait until the previous decode consumed the pinned staging buffers
   if (w.pending) HIP_TRY(hipEventSynchronize(w.done), "hipEventSynchronize");
   std::memcpy(w.len_host, lengths, (size_t)B * 4);
   HIP_TRY(hipMemcpyAsync(w.len, w.len_host, (size_t)B * 4, hipMemcpyHostToDevice, st),
           "hipMemcpyAsync(lengths)");
+  if (graphs) HIP_TRY(upload_graphs(w, graphs, B, st), "hipMemcpyAsync(graphs)");
 
-  const DecodeDev d = decode_dev(m, w, B, T, Ns, Nc, KT, encoder_out, w.len, nullptr);
-  const GraphDev gd = graph_dev(graph);
+  const DecodeDev d =
+      decode_dev(m, w, B, T, Ns, Nc, KT, encoder_out, w.len, nullptr, graphs != nullptr);
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
   HIP_TRY(launch_fill_i32((int*)m->xerr, 1, 0, st), "fill(exchange errors)");
   bool grouped = false;
-  s = enqueue_frames(m, graph, beam, splan, per_stream, d, maxlen, trace, m->xerr, st, &grouped);
+  s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, m->xerr, st, &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
@@ -739,31 +789,33 @@ tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
   return TBS_OK;
 }
 
-tbs_status tbs_state_create(const tbs_model* model, const tbs_graph* graph,
-                            const tbs_beam_params* params, int32_t B, int32_t max_frames,
-                            void* hip_stream, tbs_state** out) {
-  if (!out) return fail(TBS_EINVAL, "tbs_state_create: out is NULL");
+tbs_status state_create_impl(const tbs_model* model, const tbs_graph* graph,
+                             const tbs_graph* const* graphs, const tbs_beam_params* params,
+                             int32_t B, int32_t max_frames, void* hip_stream, tbs_state** out,
+                             const char* who) {
+  if (!out) return fail(TBS_EINVAL, "%s: out is NULL", who);
   *out = nullptr;
-  tbs_status s = check_params(model, graph, params, "tbs_state_create");
+  if (B < 1 || max_frames < 1) return fail(TBS_EINVAL, "%s: B and max_frames must be >= 1", who);
+  GraphDev gd;
+  tbs_status s = graph_set(model, graph, graphs, B, params, who, &gd);
   if (s != TBS_OK) return s;
-  if (B < 1 || max_frames < 1)
-    return fail(TBS_EINVAL, "tbs_state_create: B and max_frames must be >= 1");
   tbs_model* m = const_cast<tbs_model*>(model);
   std::lock_guard<std::mutex> lk(m->mu);
   hipStream_t st = (hipStream_t)hip_stream;
   tbs_state* S = new tbs_state();
   S->m = m;
-  S->g = graph;
+  S->gd = gd;
+  S->per_graph = graphs != nullptr;
   S->beam = params->beam;
   S->Ns = params->max_states;
   S->Nc = params->max_contexts < S->Ns ? params->max_contexts : S->Ns;
-  S->KT = (graph->trivial && S->Ns <= kMaxTopK) ? S->Ns : 0;
+  S->KT = (gd.trivial && S->Ns <= kMaxTopK) ? S->Ns : 0;
   S->B = B;
   S->Tcap = max_frames;
   S->done.assign(B, 0);
   const ModelDev md = model_dev(m);
-  S->splan = plan_stream(md, S->Nc, S->KT, graph->trivial);
-  s = choose_schedule(m, S->splan, S->Ns, S->Nc, "tbs_state_create", &S->per_stream);
+  S->splan = plan_stream(md, S->Nc, S->KT, gd.trivial);
+  s = choose_schedule(m, S->splan, S->Ns, S->Nc, who, &S->per_stream);
   if (s == TBS_OK) s = alloc_workspace(m, S->w, B, max_frames, S->Ns, S->Nc, S->KT, S->KT == 0);
   hipError_t e = hipSuccess;
   if (s == TBS_OK) {
@@ -771,14 +823,16 @@ tbs_status tbs_state_create(const tbs_model* model, const tbs_graph* graph,
     if (e == hipSuccess) e = launch_fill_i32((int*)S->xerr, 1, 0, st);
     // the initial tuple of every stream (k_init with zero lengths writes no joiner row)
     if (e == hipSuccess) e = launch_fill_i32(S->w.len, 2 * (long long)B, 0, st);
+    // the graph table stays for the state's lifetime
+    if (e == hipSuccess && graphs) e = upload_graphs(S->w, graphs, B, st);
     if (e == hipSuccess) {
       const DecodeDev d = decode_dev(m, S->w, B, max_frames, S->Ns, S->Nc, S->KT, nullptr,
-                                     S->w.len, nullptr);
-      e = launch_init(md, d, graph_dev(graph), nullptr, st);
+                                     S->w.len, nullptr, S->per_graph);
+      e = launch_init(md, d, gd, nullptr, st);
     }
     if (e == hipSuccess) e = hipEventRecord(S->w.done, st);
     if (e == hipSuccess) S->w.pending = true;
-    if (e != hipSuccess) s = hip_fail(e, "tbs_state_create");
+    if (e != hipSuccess) s = hip_fail(e, who);
   }
   if (s != TBS_OK) {
     if (S->w.pending) hipEventSynchronize(S->w.done);
@@ -789,6 +843,55 @@ tbs_status tbs_state_create(const tbs_model* model, const tbs_graph* graph,
   }
   *out = S;
   return TBS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
+                      const tbs_beam_params* params, const float* encoder_out,
+                      const int32_t* lengths, int32_t B, int32_t T, int32_t* out_tokens,
+                      int32_t* out_num_tokens, double* out_scores, int32_t* out_status,
+                      int32_t* out_arcs, int32_t* trace, void* hip_stream) {
+  if (!graph) return fail(TBS_EINVAL, "tbs_decode: graph is NULL");
+  return decode_impl(model, graph, nullptr, params, encoder_out, lengths, B, T, out_tokens,
+                     out_num_tokens, out_scores, out_status, out_arcs, trace, hip_stream,
+                     "tbs_decode");
+}
+
+tbs_status tbs_decode_graphs(const tbs_model* model, const tbs_graph* const* graphs,
+                             const tbs_beam_params* params, const float* encoder_out,
+                             const int32_t* lengths, int32_t B, int32_t T, int32_t* out_tokens,
+                             int32_t* out_num_tokens, double* out_scores, int32_t* out_status,
+                             int32_t* out_arcs, int32_t* trace, void* hip_stream) {
+  if (!graphs && B > 0) return fail(TBS_EINVAL, "tbs_decode_graphs: graphs is NULL");
+  if (!model || !params) return fail(TBS_EINVAL, "tbs_decode_graphs: NULL model/params");
+  return decode_impl(model, nullptr, graphs, params, encoder_out, lengths, B, T, out_tokens,
+                     out_num_tokens, out_scores, out_status, out_arcs, trace, hip_stream,
+                     "tbs_decode_graphs");
+}
+
+tbs_status tbs_state_create(const tbs_model* model, const tbs_graph* graph,
+                            const tbs_beam_params* params, int32_t B, int32_t max_frames,
+                            void* hip_stream, tbs_state** out) {
+  if (!graph) {
+    if (out) *out = nullptr;
+    return fail(TBS_EINVAL, "tbs_state_create: graph is NULL");
+  }
+  return state_create_impl(model, graph, nullptr, params, B, max_frames, hip_stream, out,
+                           "tbs_state_create");
+}
+
+tbs_status tbs_state_create_graphs(const tbs_model* model, const tbs_graph* const* graphs,
+                                   const tbs_beam_params* params, int32_t B, int32_t max_frames,
+                                   void* hip_stream, tbs_state** out) {
+  if (!graphs || !model || !params) {
+    if (out) *out = nullptr;
+    return fail(TBS_EINVAL, "tbs_state_create_graphs: NULL model/graphs/params");
+  }
+  return state_create_impl(model, nullptr, graphs, params, B, max_frames, hip_stream, out,
+                           "tbs_state_create_graphs");
 }
 
 tbs_status tbs_decode_chunk(tbs_state* S, const float* encoder_chunk,
@@ -825,11 +928,11 @@ tbs_status tbs_decode_chunk(tbs_state* S, const float* encoder_chunk,
   HIP_TRY(hipMemcpyAsync(w.len, w.len_host, (size_t)2 * B * 4, hipMemcpyHostToDevice, st),
           "hipMemcpyAsync(lengths)");
   const DecodeDev d = decode_dev(m, w, B, Tc, S->Ns, S->Nc, S->KT, encoder_chunk, w.len,
-                                 w.len + B);
-  HIP_TRY(launch_resume(model_dev(m), d, graph_dev(S->g), trace, S->per_stream ? 0 : 1, st),
+                                 w.len + B, S->per_graph);
+  HIP_TRY(launch_resume(model_dev(m), d, S->gd, trace, S->per_stream ? 0 : 1, st),
           "launch(resume)");
   bool grouped = false;
-  tbs_status s = enqueue_frames(m, S->g, S->beam, S->splan, S->per_stream, d, maxlen, trace,
+  tbs_status s = enqueue_frames(m, S->gd, S->beam, S->splan, S->per_stream, d, maxlen, trace,
                                 S->xerr, st, &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
@@ -855,10 +958,10 @@ tbs_status tbs_state_finish(tbs_state* S, int32_t* out_tokens, int32_t* out_num_
   HIP_TRY(hipMemcpyAsync(w.len, w.len_host, (size_t)S->B * 4, hipMemcpyHostToDevice, st),
           "hipMemcpyAsync(lengths)");
   const DecodeDev d = decode_dev(m, w, S->B, S->Tcap, S->Ns, S->Nc, S->KT, nullptr, w.len,
-                                 nullptr);
+                                 nullptr, S->per_graph);
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
-                         return launch_final(graph_dev(S->g), d, out_tokens, out_num_tokens,
+                         return launch_final(S->gd, d, out_tokens, out_num_tokens,
                                              out_scores, out_status, out_arcs, S->xerr, st);
                        }),
           "launch(final)");

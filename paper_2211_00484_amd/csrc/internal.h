@@ -55,6 +55,7 @@ struct DecodeDev {
   const float* enc;         // [B][T][C]
   const int* len;           // [B]
   const int* base;          // [B] absolute index of frame 0 of this call (chunked decode) or null
+  const GraphDev* graphs;   // [B] per-stream decoding graphs, or null (one shared graph)
   int* nsurv;               // [B]
   int* surv_ctx;            // [B][Ns]
   int* surv_state;          // [B][Ns]

@@ -708,6 +708,7 @@ __global__ void k_logp_rows(const float* __restrict__ logits, const float2* __re
 __global__ __launch_bounds__(256) void k_init(ModelDev m, DecodeDev d, GraphDev g,
                                               int* __restrict__ trace) {
   const int b = blockIdx.x, tid = threadIdx.x;
+  if (d.graphs) g = d.graphs[b];  // per-stream graphs
   if (tid == 0) {
     d.nsurv[b] = 1;
     d.surv_ctx[(size_t)b * d.Ns] = 0;
@@ -1822,6 +1823,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_search(ModelDev m, GraphDev 
   extern __shared__ __align__(16) unsigned char smem[];
   SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
   const int fb = d.base ? d.base[b] : 0;
+  if (d.graphs) g = d.graphs[b];  // per-stream graphs
   search_frame<TRIV, false>(m, g, d, beam, t, L, b, trace, s, nullptr, 0, nullptr, false, true,
                             false, nullptr, 0, fb);
 }
@@ -1987,6 +1989,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
   const int tid = threadIdx.x;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V;
   const int fb = d.base ? d.base[b] : 0;  // absolute index of this call's frame 0
+  if (d.graphs) g = d.graphs[b];          // per-stream graphs
   const size_t row0 = (size_t)b * Nc;
   // state after the initial tuple (written by k_init), encoder frame 0, zeroed rows
   if (tid == 0) {
@@ -2601,6 +2604,7 @@ __global__ __launch_bounds__(256) void k_final(GraphDev g, DecodeDev d, int* __r
   __shared__ int s_wsum[4];
   const int b = blockIdx.x, tid = threadIdx.x;
   const int Ns = d.Ns, T = d.T, len = d.len[b];
+  if (d.graphs) g = d.graphs[b];  // per-stream graphs
   if (tid == 0) {
     const int ns = d.nsurv[b];
     int pick = -1, status = 0;

@@ -81,6 +81,9 @@ def lib():
     L.tbs_decode.restype = _I32
     L.tbs_decode.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
                              _P, _P, _P, _P, _P, _P, _P]
+    L.tbs_decode_graphs.restype = _I32
+    L.tbs_decode_graphs.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
+                                    _P, _P, _P, _P, _P, _P, _P]
     L.tbs_model_set_schedule.restype = _I32
     L.tbs_model_set_schedule.argtypes = [_P, _I32]
     L.tbs_model_set_profiling.restype = _I32
@@ -92,6 +95,9 @@ def lib():
     L.tbs_state_create.restype = _I32
     L.tbs_state_create.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _I32, _I32, _P,
                                    ctypes.POINTER(_P)]
+    L.tbs_state_create_graphs.restype = _I32
+    L.tbs_state_create_graphs.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _I32, _I32, _P,
+                                          ctypes.POINTER(_P)]
     L.tbs_decode_chunk.restype = _I32
     L.tbs_decode_chunk.argtypes = [_P, _P, _P, _I32, _P, _P]
     L.tbs_state_finish.restype = _I32
@@ -172,6 +178,7 @@ class Model:
     def __init__(self, vocab_size: int, dim: int, embed, conv, w_out, b_out=None,
                  dtype: str = "fp32", stream=None):
         import torch
+        self._h = None
         dev = torch.device("cuda", torch.cuda.current_device())
 
         def dt(x):
@@ -245,9 +252,19 @@ def allocate_outputs(B: int, T: int, max_states: int, status=True, arcs=False, t
         trace=torch.empty((T + 1, B, max_states, 4), **i32) if trace else None)
 
 
-def decode_into(model: Model, graph: Graph, encoder_out, lengths, beam: float, max_states: int,
+def _graph_table(graphs, B: int):
+    """Host array of B graph handles (kept alive by the caller's list)."""
+    graphs = list(graphs)
+    if len(graphs) != B:
+        raise ValueError(f"need one graph per stream: {len(graphs)} graphs for B = {B}")
+    return (_P * max(B, 1))(*[g._h for g in graphs])
+
+
+def decode_into(model: Model, graph, encoder_out, lengths, beam: float, max_states: int,
                 max_contexts: int, out: DecodeOutput, stream=None) -> DecodeOutput:
-    """tbs_decode into preallocated outputs (stream-ordered; no synchronisation)."""
+    """tbs_decode into preallocated outputs (stream-ordered; no synchronisation).
+    ``graph`` is one Graph shared by every stream, or a list of B graphs, one per
+    stream (tbs_decode_graphs)."""
     lens = np.ascontiguousarray(np.asarray(lengths), dtype=np.int32)
     B, T = int(encoder_out.shape[0]), int(encoder_out.shape[1])
     if encoder_out.dim() != 3 or encoder_out.shape[2] != model.dim:
@@ -256,17 +273,22 @@ def decode_into(model: Model, graph: Graph, encoder_out, lengths, beam: float, m
         raise ValueError("lengths must have shape [B]")
     params = BeamParams(float(math.inf if beam is None else beam), int(max_states),
                         int(max_contexts))
-    _check(lib().tbs_decode(model._h, graph._h, ctypes.byref(params), _dev_ptr(encoder_out),
-                            _host_ptr(lens), B, T, _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
-                            _dev_ptr(out.scores), _dev_ptr(out.status), _dev_ptr(out.arcs),
-                            _dev_ptr(out.trace), _stream_ptr(stream)))
+    if isinstance(graph, Graph):
+        fn, gh = lib().tbs_decode, graph._h
+    else:
+        fn, gh = lib().tbs_decode_graphs, _graph_table(graph, B)
+    _check(fn(model._h, gh, ctypes.byref(params), _dev_ptr(encoder_out),
+              _host_ptr(lens), B, T, _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
+              _dev_ptr(out.scores), _dev_ptr(out.status), _dev_ptr(out.arcs),
+              _dev_ptr(out.trace), _stream_ptr(stream)))
     return out
 
 
-def decode(model: Model, graph: Graph, encoder_out, lengths, beam: float = math.inf,
+def decode(model: Model, graph, encoder_out, lengths, beam: float = math.inf,
            max_states: int = 4, max_contexts: int = 4, want_arcs: bool = False,
            want_trace: bool = False, stream=None) -> DecodeOutput:
-    """Batched FSA-constrained one-symbol-per-frame beam search; outputs on the device."""
+    """Batched FSA-constrained one-symbol-per-frame beam search; outputs on the device.
+    ``graph``: one Graph for every stream, or a list of one Graph per stream."""
     B, T = int(encoder_out.shape[0]), int(encoder_out.shape[1])
     out = allocate_outputs(B, T, max_states, status=True, arcs=want_arcs, trace=want_trace,
                            device=encoder_out.device)
@@ -290,14 +312,21 @@ class DecodeState:
     each chunk continues every stream from where it stopped; finish traces the best
     paths back over all decoded frames."""
 
-    def __init__(self, model: Model, graph: Graph, B: int, max_frames: int,
+    def __init__(self, model: Model, graph, B: int, max_frames: int,
                  beam: float = math.inf, max_states: int = 4, max_contexts: int = 4,
                  stream=None):
+        """``graph``: one Graph for every stream, or a list of one Graph per stream."""
+        self._h = None
         params = BeamParams(float(math.inf if beam is None else beam), int(max_states),
                             int(max_contexts))
         h = _P()
-        _check(lib().tbs_state_create(model._h, graph._h, ctypes.byref(params), int(B),
-                                      int(max_frames), _stream_ptr(stream), ctypes.byref(h)))
+        if isinstance(graph, Graph):
+            fn, gh = lib().tbs_state_create, graph._h
+        else:
+            graph = list(graph)
+            fn, gh = lib().tbs_state_create_graphs, _graph_table(graph, int(B))
+        _check(fn(model._h, gh, ctypes.byref(params), int(B), int(max_frames),
+                  _stream_ptr(stream), ctypes.byref(h)))
         self._h = h
         self._refs = (model, graph)  # the state must not outlive them
         self.B, self.max_frames, self.max_states = int(B), int(max_frames), int(max_states)

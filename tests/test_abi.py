@@ -77,6 +77,13 @@ def test_decode_null_handles():
                       None, None, None)
     assert st == EINVAL
     assert L.tbs_joiner_logp(None, None, None, 1, None, None) == EINVAL
+    st = L.tbs_decode_graphs(None, None, ctypes.byref(p), None, None, 1, 1, None, None, None,
+                             None, None, None, None)
+    assert st == EINVAL and "graphs is NULL" in L.tbs_last_error().decode()
+    h = ctypes.c_void_p()
+    assert L.tbs_state_create_graphs(None, None, ctypes.byref(p), 1, 1, None,
+                                     ctypes.byref(h)) == EINVAL
+    assert h.value is None
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
