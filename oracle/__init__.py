@@ -10,6 +10,13 @@ unpruned search against exhaustive enumeration and a Viterbi recursion; Ns = Nc 
 trivial graph against per-frame argmax greedy search.  The exact tie-breaking of the
 finite beam / max-states / max-contexts selection is this implementation's reading of
 Sec. 2.5 and is pinned only by invariants ("parity unpinned" for those tie rules).
+
+Lattice and label-sequence search (Sec. 2.5, the "LogAdd" rows of Tables 3 and 6): the
+unpruned lattice's total probability, the total probability of a label sequence and the
+best label sequence are pinned against exhaustive enumeration of alignments; path
+sampling against the exact path posteriors of small lattices.  Which expansions a pruned
+lattice keeps (every arc into a surviving tuple) is this implementation's reading and is
+pinned by invariants only.
 """
 from __future__ import annotations
 
@@ -56,6 +63,19 @@ def _load():
         lib.oracle_rescore.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I,
                                        _P, _P, _P, _P, _P, _P]
         lib.oracle_rescore.restype = _I
+        lib.oracle_lattice.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I,
+                                        _I, _I, _P, _P, _P, _P, _P, _D, _I, _I, _I, _P])
+        lib.oracle_lattice.restype = _P
+        lib.oracle_lattice_free.argtypes = [_P]
+        lib.oracle_lattice_free.restype = None
+        lib.oracle_lattice_sizes.argtypes = [_P, _I, _P, _P, _P]
+        lib.oracle_lattice_sizes.restype = _I
+        lib.oracle_lattice_get.argtypes = [_P, _I, _P, _P, _P, _P, _P, _P, _P]
+        lib.oracle_lattice_get.restype = _I
+        lib.oracle_lattice_nbest.argtypes = [_P, _I, _I, _P, _P, _P, _P, _P, _P]
+        lib.oracle_lattice_nbest.restype = _I
+        lib.oracle_lattice_seqscore.argtypes = [_P, _I, _P, _I]
+        lib.oracle_lattice_seqscore.restype = _D
         _lib = lib
     return _lib
 
@@ -151,3 +171,126 @@ def rescore(model, graph, enc_stream: np.ndarray, arcs: np.ndarray, bf16: bool =
                               graph.num_states, graph.start, _ptr(rp), _ptr(dest), _ptr(lab),
                               _ptr(q), _ptr(fin), ctypes.byref(out))
     return int(code), float(out.value)
+
+
+class StreamLattice:
+    """One stream's lattice: nodes[f] [n_f, 4] (ctx, state, parent, label) for f = 0..len;
+    arcs[f] [a_f, 4] (src, dst, label, graph arc) with weights w[f] [a_f] (fp64), ordered by
+    (dst, src, arc position) with blank first; fw: final weights of the last frame's nodes;
+    alpha[f]: forward log scores; total: log of the sum over complete paths; status as in
+    decode."""
+
+    def __init__(self, len_, nodes, arcs, w, fw, alpha, total, status):
+        self.len, self.nodes, self.arcs, self.w = len_, nodes, arcs, w
+        self.fw, self.alpha, self.total, self.status = fw, alpha, total, status
+
+
+class NBest:
+    """Result of the n-best label-sequence search on one stream (see Lattice.nbest)."""
+
+    def __init__(self, paths, margins, first, scores, best, seqs):
+        self.paths, self.margins, self.first, self.scores = paths, margins, first, scores
+        self.best, self.seqs = best, seqs
+
+    @property
+    def tokens(self):
+        return self.seqs[self.best]
+
+    @property
+    def score(self):
+        return float(self.scores[self.best])
+
+
+class Lattice:
+    """Lattices of a batch from the oracle search (Sec. 2.5); see tbs_oracle.cpp."""
+
+    def __init__(self, handle, B, T, frame_margins, streams):
+        self._h, self.B, self.T = handle, B, T
+        self.frame_margins, self.streams = frame_margins, streams
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and _lib is not None:
+            _lib.oracle_lattice_free(self._h)
+            self._h = None
+
+    def stream(self, k: int) -> StreamLattice:
+        """Lattice of the k-th decoded stream (index into ``streams``)."""
+        lib = _load()
+        ln = ctypes.c_int(0)
+        lib.oracle_lattice_sizes(self._h, k, ctypes.byref(ln), None, None)
+        L = ln.value
+        nn = np.empty(L + 1, dtype=np.int32)
+        na = np.empty(max(L, 1), dtype=np.int32)
+        lib.oracle_lattice_sizes(self._h, k, ctypes.byref(ln), _ptr(nn), _ptr(na))
+        na = na[:L]
+        nodes = np.empty((int(nn.sum()), 4), dtype=np.int32)
+        arcs = np.empty((max(int(na.sum()), 1), 4), dtype=np.int32)
+        w = np.empty(max(int(na.sum()), 1), dtype=np.float64)
+        fw = np.empty(int(nn[L]), dtype=np.float64)
+        alpha = np.empty(int(nn.sum()), dtype=np.float64)
+        tot = ctypes.c_double(0.0)
+        st = ctypes.c_int(0)
+        lib.oracle_lattice_get(self._h, k, _ptr(nodes), _ptr(arcs), _ptr(w), _ptr(fw),
+                               _ptr(alpha), ctypes.byref(tot), ctypes.byref(st))
+        no = np.concatenate([[0], np.cumsum(nn)])
+        ao = np.concatenate([[0], np.cumsum(na)]).astype(np.int64)
+        return StreamLattice(L, [nodes[no[f]:no[f + 1]] for f in range(L + 1)],
+                             [arcs[ao[f]:ao[f + 1]] for f in range(L)],
+                             [w[ao[f]:ao[f + 1]] for f in range(L)], fw,
+                             [alpha[no[f]:no[f + 1]] for f in range(L + 1)], tot.value, st.value)
+
+    def nbest(self, k: int, uniforms: np.ndarray) -> NBest:
+        """n-best label-sequence search on the k-th stream; uniforms [n, len+1] in [0, 1)."""
+        lib = _load()
+        ln = ctypes.c_int(0)
+        lib.oracle_lattice_sizes(self._h, k, ctypes.byref(ln), None, None)
+        L = ln.value
+        u = np.ascontiguousarray(uniforms, dtype=np.float64)
+        n = int(u.shape[0])
+        if n < 1 or u.shape != (n, L + 1):
+            raise ValueError(f"uniforms must be [n >= 1, {L + 1}]")
+        paths = np.empty((n, L + 1), dtype=np.int32)
+        margins = np.empty((n, L + 1), dtype=np.float64)
+        first = np.empty(n, dtype=np.int32)
+        scores = np.empty(n, dtype=np.float64)
+        best = ctypes.c_int(0)
+        nu = lib.oracle_lattice_nbest(self._h, k, n, _ptr(u), _ptr(paths), _ptr(margins),
+                                      _ptr(first), _ptr(scores), ctypes.byref(best))
+        lat = self.stream(k)
+        seqs = []
+        for p in first[:nu]:
+            seqs.append([int(lat.arcs[f][paths[p, f], 2]) for f in range(L)
+                         if lat.arcs[f][paths[p, f], 2] > 0])
+        return NBest(paths, margins, first[:nu], scores[:nu], best.value, seqs)
+
+    def sequence_score(self, k: int, y) -> float:
+        """Total probability (log) of label sequence y in the k-th stream's lattice."""
+        y = _i32(np.asarray(list(y), dtype=np.int64))
+        return float(_load().oracle_lattice_seqscore(self._h, k, _ptr(y), int(y.shape[0])))
+
+
+def lattice(model, graph, encoder_out: np.ndarray, lengths: np.ndarray, beam: float,
+            max_states: int, max_contexts: int, bf16: bool = False, nthreads: int = 0,
+            streams=None) -> Lattice:
+    """Runs the search and keeps every stream's lattice (Sec. 2.5)."""
+    lib = _load()
+    enc = _f32(encoder_out)
+    lens = _i32(lengths)
+    if streams is not None:
+        idx = np.asarray(streams, dtype=np.int64)
+        enc = np.ascontiguousarray(enc[idx])
+        lens = np.ascontiguousarray(lens[idx])
+    B, T, C = enc.shape
+    if max_states < 1 or max_contexts < 1:
+        raise ValueError("max_states and max_contexts must be >= 1")
+    E, conv, W = _f32(model.embed), _f32(model.conv), _f32(model.w_out)
+    bias = None if model.b_out is None else _f32(model.b_out)
+    rp, dest, lab, q = _i32(graph.row_ptr), _i32(graph.dest), _i32(graph.label), _f32(graph.score)
+    fin = None if graph.final is None else _f32(graph.final)
+    fm = np.empty((B, T + 1), dtype=np.float64)
+    beam_v = float(beam) if beam is not None else math.inf
+    h = lib.oracle_lattice(B, T, C, model.vocab_size, _ptr(enc), _ptr(lens), _ptr(E), _ptr(conv),
+                           _ptr(W), _ptr(bias), int(bf16), graph.num_states, graph.start,
+                           _ptr(rp), _ptr(dest), _ptr(lab), _ptr(q), _ptr(fin), beam_v,
+                           int(max_states), int(max_contexts), int(nthreads), _ptr(fm))
+    return Lattice(h, B, T, fm, list(range(B)) if streams is None else list(streams))

@@ -120,6 +120,26 @@ struct Cand {
   int pos;    // arc position within the parent's state, -1 = blank
   int label;
   int arc;
+  double w;   // weight of the expansion: q + log P(label), or log P(blank)
+};
+
+// Lattice of one stream (Sec. 2.4 / 2.5: the search's output is an FSA whose
+// states are the surviving tuples of each frame).  Arcs of frame f run from a
+// survivor of frame f to a survivor of frame f+1: every unpruned expansion
+// (blank or graph arc) whose (state, context) survived, whichever candidate won
+// the max-merge.  Order within a frame: destination ascending, then source
+// ascending, then arc position within the source state (blank first).
+struct LatArc {
+  int src, dst, label, arc;
+  double w;
+};
+
+struct Lattice {
+  int len = 0;
+  std::vector<std::vector<Tup>> nodes;    // nodes[f], f = 0..len, canonical order
+  std::vector<std::vector<LatArc>> arcs;  // arcs[f], f = 0..len-1
+  std::vector<double> fw;                 // final weight of each node of frame len
+  int status = 0;                         // 1: no survivor of frame len is final
 };
 
 // (score desc, then (parent, arc position) asc): the candidate kept when
@@ -143,7 +163,8 @@ struct StreamOut {
 // Decodes one stream.  trace (optional) receives, for frame index f in
 // [0, len], the surviving tuples (ctx, state, parent, label) in canonical order.
 void decode_stream(const Model& m, const Graph& g, const Params& p, const float* enc, int T,
-                   int len, StreamOut& out, int* trace, int trace_stride_frame) {
+                   int len, StreamOut& out, int* trace, int trace_stride_frame,
+                   Lattice* lat = nullptr) {
   const int V = m.V, C = m.C;
   std::vector<Tup> H;
   H.push_back(Tup{0, g.start, 0.0, -1, -1, -1});  // ((blank, blank), 0, start), Sec. 2.2 / 2.4
@@ -160,6 +181,11 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     }
   };
   write_trace(0, H);
+  if (lat) {
+    lat->len = len;
+    lat->nodes.assign(1, H);
+    lat->arcs.clear();
+  }
   double margin = std::numeric_limits<double>::infinity();
   std::vector<double> logp;
   out.frame_margin.assign(len, std::numeric_limits<double>::infinity());
@@ -187,12 +213,12 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     for (int i = 0; i < (int)H.size(); ++i) {
       const Tup& x = H[i];
       const double* lp = &logp[row_of(x.ctx) * V];
-      cands.push_back(Cand{x.s, x.ctx, x.score + lp[0], i, -1, 0, -1});
+      cands.push_back(Cand{x.s, x.ctx, x.score + lp[0], i, -1, 0, -1, lp[0]});
       const int64_t bprev = x.ctx % V;
       for (int j = g.rp[x.s]; j < g.rp[x.s + 1]; ++j) {
         const int c = g.label[j];
         cands.push_back(Cand{g.dest[j], bprev * V + c, x.score + (double)g.q[j] + lp[c], i,
-                             j - g.rp[x.s], c, j});
+                             j - g.rp[x.s], c, j, (double)g.q[j] + lp[c]});
       }
     }
 
@@ -272,6 +298,24 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     });
     out.frame_margin[t] = fmar;
     margin = std::min(margin, fmar);
+    if (lat) {
+      // lattice arcs of frame t: the candidates whose (state, context) survived;
+      // cands are in (source, arc position) order, blank first
+      std::vector<std::vector<LatArc>> into(nH.size());
+      for (const Cand& c : cands) {
+        auto it = std::lower_bound(nH.begin(), nH.end(), c, [](const Tup& x, const Cand& y) {
+          if (x.ctx != y.ctx) return x.ctx < y.ctx;
+          return x.s < y.s;
+        });
+        if (it == nH.end() || it->ctx != c.ctx || it->s != c.s) continue;
+        const int j = (int)(it - nH.begin());
+        into[j].push_back(LatArc{c.parent, j, c.label, c.arc, c.w});
+      }
+      std::vector<LatArc> fa;
+      for (auto& v : into) fa.insert(fa.end(), v.begin(), v.end());
+      lat->arcs.push_back(std::move(fa));
+      lat->nodes.push_back(nH);
+    }
     hist.push_back(nH);
     H.swap(nH);
     write_trace(t + 1, H);
@@ -297,6 +341,14 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     out.status = pass;
   }
   out.final_margin = second != kNegInf ? pick_v - second : std::numeric_limits<double>::infinity();
+  if (lat) {
+    // final weights of the lattice: those of the graph, or 0 for every node of
+    // the last frame when none of them is final (the same fallback as above)
+    lat->fw.assign(H.size(), 0.0);
+    lat->status = out.status;
+    if (g.fin && out.status == 0)
+      for (size_t i = 0; i < H.size(); ++i) lat->fw[i] = (double)g.fin[H[i].s];
+  }
   margin = std::min(margin, out.final_margin);
   out.score = pick_v;
   out.margin = margin;
@@ -313,6 +365,92 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
   }
   std::reverse(out.tokens.begin(), out.tokens.end());
 }
+
+// log(exp(a) + exp(b)) without overflow.
+double log_add(double a, double b) {
+  if (a == kNegInf) return b;
+  if (b == kNegInf) return a;
+  const double hi = std::max(a, b), lo = std::min(a, b);
+  return hi + std::log1p(std::exp(lo - hi));
+}
+
+// Forward scores of a lattice in the log semiring: alpha[f][j] = log of the sum,
+// over lattice paths from the initial node to node j of frame f, of exp(path
+// weight); returns the total over complete paths with final weights.
+double lattice_forward(const Lattice& L, std::vector<std::vector<double>>& alpha) {
+  alpha.assign(L.len + 1, {});
+  alpha[0].assign(L.nodes[0].size(), kNegInf);
+  alpha[0][0] = 0.0;
+  for (int f = 0; f < L.len; ++f) {
+    alpha[f + 1].assign(L.nodes[f + 1].size(), kNegInf);
+    for (const LatArc& a : L.arcs[f])
+      alpha[f + 1][a.dst] = log_add(alpha[f + 1][a.dst], alpha[f][a.src] + a.w);
+  }
+  double tot = kNegInf;
+  for (size_t j = 0; j < L.nodes[L.len].size(); ++j)
+    tot = log_add(tot, alpha[L.len][j] + L.fw[j]);
+  return tot;
+}
+
+// Picks one of K items with probabilities proportional to exp(v[k]) by
+// inversion: the first item whose running sum of exp(v - max) exceeds u times
+// the full sum (u in [0, 1)).  margin: the distance of u * sum from the nearest
+// boundary between two items, as a fraction of the sum (+inf for one item).
+int pick_by_inversion(const std::vector<double>& v, double u, double* margin) {
+  double mx = kNegInf;
+  for (double x : v) mx = std::max(mx, x);
+  std::vector<double> cum(v.size());
+  double sum = 0.0;
+  for (size_t k = 0; k < v.size(); ++k) {
+    sum += v[k] == kNegInf ? 0.0 : std::exp(v[k] - mx);
+    cum[k] = sum;
+  }
+  const double target = u * sum;
+  int pick = -1;
+  for (size_t k = 0; k < v.size(); ++k)
+    if (cum[k] > target) {
+      pick = (int)k;
+      break;
+    }
+  if (pick < 0)  // rounding: the last item with a nonzero share
+    for (size_t k = v.size(); k-- > 0;)
+      if (v[k] != kNegInf) {
+        pick = (int)k;
+        break;
+      }
+  double m = std::numeric_limits<double>::infinity();
+  for (size_t k = 0; k + 1 < v.size(); ++k) m = std::min(m, std::fabs(cum[k] - target) / sum);
+  *margin = m;
+  return pick;
+}
+
+// Total probability (log) of the label sequence y[0..n) in the lattice: the
+// lattice composed with the linear acceptor of y, blanks as epsilon, summed over
+// every path (Sec. 2.5, label sequence with the highest probability).  Dense
+// recursion over (node, labels of y consumed).
+double lattice_sequence_score(const Lattice& L, const int* y, int n) {
+  std::vector<std::vector<double>> cur(L.nodes[0].size(), std::vector<double>(n + 1, kNegInf));
+  cur[0][0] = 0.0;
+  for (int f = 0; f < L.len; ++f) {
+    std::vector<std::vector<double>> nxt(L.nodes[f + 1].size(),
+                                         std::vector<double>(n + 1, kNegInf));
+    for (const LatArc& a : L.arcs[f])
+      for (int k = 0; k <= n; ++k) {
+        if (a.label == 0)
+          nxt[a.dst][k] = log_add(nxt[a.dst][k], cur[a.src][k] + a.w);
+        else if (k >= 1 && y[k - 1] == a.label)
+          nxt[a.dst][k] = log_add(nxt[a.dst][k], cur[a.src][k - 1] + a.w);
+      }
+    cur.swap(nxt);
+  }
+  double tot = kNegInf;
+  for (size_t j = 0; j < cur.size(); ++j) tot = log_add(tot, cur[j][n] + L.fw[j]);
+  return tot;
+}
+
+struct Decoded {
+  std::vector<Lattice> lat;
+};
 
 }  // namespace
 
@@ -415,6 +553,151 @@ int oracle_rescore(int C, int V, int len, const float* enc, const int* arcs, con
   }
   *score_out = score;
   return 0;
+}
+
+// Lattices of a batch (same arguments as oracle_decode): returns a handle for
+// the functions below, or null.  frame_margins [B][T+1] or null as in oracle_decode.
+void* oracle_lattice(int B, int T, int C, int V, const float* enc, const int* lengths,
+                     const float* E, const float* conv, const float* W, const float* bias,
+                     int bf16, int S, int start, const int* rp, const int* dest,
+                     const int* label, const float* q, const float* fin, double beam, int Ns,
+                     int Nc, int nthreads, double* frame_margins) {
+  Model m{V, C, E, conv, W, bias, bf16};
+  Graph g{S, start, rp, dest, label, q, fin};
+  Params p{beam, Ns, Nc};
+  Decoded* D = new Decoded();
+  D->lat.resize(B);
+  std::atomic<int> next{0};
+  auto work = [&]() {
+    for (;;) {
+      int b = next.fetch_add(1);
+      if (b >= B) break;
+      StreamOut o;
+      decode_stream(m, g, p, enc + (size_t)b * T * C, T, lengths[b], o, nullptr, 0, &D->lat[b]);
+      if (frame_margins) {
+        double* fm = frame_margins + (size_t)b * (T + 1);
+        for (int t = 0; t <= T; ++t) fm[t] = std::numeric_limits<double>::infinity();
+        for (int t = 0; t < lengths[b]; ++t) fm[t] = o.frame_margin[t];
+        fm[T] = o.final_margin;
+      }
+    }
+  };
+  int nt = nthreads > 0 ? nthreads : (int)std::thread::hardware_concurrency();
+  if (nt < 1) nt = 1;
+  if (nt > B) nt = B > 0 ? B : 1;
+  std::vector<std::thread> pool;
+  for (int i = 1; i < nt; ++i) pool.emplace_back(work);
+  work();
+  for (auto& th : pool) th.join();
+  return D;
+}
+
+void oracle_lattice_free(void* h) { delete static_cast<Decoded*>(h); }
+
+// Sizes of stream b's lattice: *len, nnodes[len+1] (nodes per frame), narcs[len].
+int oracle_lattice_sizes(void* h, int b, int* len, int* nnodes, int* narcs) {
+  const Lattice& L = static_cast<Decoded*>(h)->lat[b];
+  *len = L.len;
+  if (nnodes)
+    for (int f = 0; f <= L.len; ++f) nnodes[f] = (int)L.nodes[f].size();
+  if (narcs)
+    for (int f = 0; f < L.len; ++f) narcs[f] = (int)L.arcs[f].size();
+  return 0;
+}
+
+// Stream b's lattice: nodes [sum nnodes][4] (ctx, state, parent, label), arcs
+// [sum narcs][4] (src, dst, label, graph arc), w [sum narcs], fw [nnodes[len]],
+// alpha [sum nnodes] (forward scores), *total, *status.
+int oracle_lattice_get(void* h, int b, int* nodes, int* arcs, double* w, double* fw,
+                       double* alpha, double* total, int* status) {
+  const Lattice& L = static_cast<Decoded*>(h)->lat[b];
+  size_t n = 0, a = 0;
+  for (int f = 0; f <= L.len; ++f)
+    for (const Tup& x : L.nodes[f]) {
+      nodes[4 * n + 0] = (int)x.ctx;
+      nodes[4 * n + 1] = x.s;
+      nodes[4 * n + 2] = x.parent;
+      nodes[4 * n + 3] = x.label;
+      ++n;
+    }
+  for (int f = 0; f < L.len; ++f)
+    for (const LatArc& x : L.arcs[f]) {
+      arcs[4 * a + 0] = x.src;
+      arcs[4 * a + 1] = x.dst;
+      arcs[4 * a + 2] = x.label;
+      arcs[4 * a + 3] = x.arc;
+      w[a] = x.w;
+      ++a;
+    }
+  for (size_t j = 0; j < L.fw.size(); ++j) fw[j] = L.fw[j];
+  std::vector<std::vector<double>> al;
+  *total = lattice_forward(L, al);
+  size_t k = 0;
+  for (auto& v : al)
+    for (double x : v) alpha[k++] = x;
+  *status = L.status;
+  return 0;
+}
+
+// n-best label-sequence search on stream b's lattice (Sec. 2.5): sample n paths
+// (u [n][len+1]: entry f < len picks the arc into the path's node of frame f+1,
+// going backwards from the end; entry len picks the final node first), take the
+// distinct blank-free label sequences in order of first occurrence, score each
+// by its total probability in the lattice and pick the best (first on ties).
+// paths [n][len+1]: local arc index within frame f for f < len, final node at
+// len; margins [n][len+1]: the inversion margin of each pick; first [n]: the
+// path index of each distinct sequence; uscore [n]: its log probability.
+// Returns the number of distinct sequences; *best: index of the best among them.
+int oracle_lattice_nbest(void* h, int b, int n, const double* u, int* paths, double* margins,
+                         int* first, double* uscore, int* best) {
+  const Lattice& L = static_cast<Decoded*>(h)->lat[b];
+  std::vector<std::vector<double>> alpha;
+  lattice_forward(L, alpha);
+  const int len = L.len;
+  std::vector<std::vector<int>> seqs(n);
+  for (int p = 0; p < n; ++p) {
+    const double* up = u + (size_t)p * (len + 1);
+    int* pp = paths + (size_t)p * (len + 1);
+    double* mp = margins + (size_t)p * (len + 1);
+    std::vector<double> v;
+    for (size_t j = 0; j < L.nodes[len].size(); ++j) v.push_back(alpha[len][j] + L.fw[j]);
+    int node = pick_by_inversion(v, up[len], &mp[len]);
+    pp[len] = node;
+    std::vector<int> labs;
+    for (int f = len - 1; f >= 0; --f) {
+      std::vector<int> ids;
+      v.clear();
+      for (size_t k = 0; k < L.arcs[f].size(); ++k)
+        if (L.arcs[f][k].dst == node) {
+          ids.push_back((int)k);
+          v.push_back(alpha[f][L.arcs[f][k].src] + L.arcs[f][k].w);
+        }
+      const int k = ids[pick_by_inversion(v, up[f], &mp[f])];
+      pp[f] = k;
+      if (L.arcs[f][k].label > 0) labs.push_back(L.arcs[f][k].label);
+      node = L.arcs[f][k].src;
+    }
+    std::reverse(labs.begin(), labs.end());
+    seqs[p] = labs;
+  }
+  int nu = 0;
+  for (int p = 0; p < n; ++p) {
+    bool seen = false;
+    for (int k = 0; k < nu && !seen; ++k) seen = seqs[first[k]] == seqs[p];
+    if (!seen) first[nu++] = p;
+  }
+  *best = 0;
+  for (int k = 0; k < nu; ++k) {
+    const std::vector<int>& y = seqs[first[k]];
+    uscore[k] = lattice_sequence_score(L, y.data(), (int)y.size());
+    if (uscore[k] > uscore[*best]) *best = k;
+  }
+  return nu;
+}
+
+// Total probability (log) of label sequence y [n] in stream b's lattice.
+double oracle_lattice_seqscore(void* h, int b, const int* y, int n) {
+  return lattice_sequence_score(static_cast<Decoded*>(h)->lat[b], y, n);
 }
 
 }  // extern "C"

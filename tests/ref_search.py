@@ -210,3 +210,51 @@ def beam_search_sorted(joiner, graph, enc, length, beam, max_states, max_context
             tokens.append(c)
         i = par
     return best_v, tokens[::-1], trace
+
+
+def all_alignments(joiner, graph, enc, length):
+    """Every alignment of ``length`` frames (one label or blank per frame, the labels a
+    graph path from the start state): list of (score, frame labels, arcs, final weight or
+    None for a non-final end state)."""
+    V = joiner.V
+    lp = _logp_fn(joiner, enc)
+    rp, dest, lab, q = graph.row_ptr, graph.dest, graph.label, graph.score
+    out = []
+
+    def rec(t, ctx, s, score, labels, arcs):
+        if t == length:
+            out.append((score, tuple(labels), tuple(arcs), _final(graph, s)))
+            return
+        p = lp(t, ctx)
+        rec(t + 1, ctx, s, score + p[0], labels + [0], arcs + [-1])
+        for j in range(rp[s], rp[s + 1]):
+            c = int(lab[j])
+            rec(t + 1, (ctx % V) * V + c, int(dest[j]), score + float(q[j]) + p[c],
+                labels + [c], arcs + [j])
+
+    rec(0, 0, graph.start, 0.0, [], [])
+    return out
+
+
+def _logsumexp(xs):
+    xs = [x for x in xs if x != -math.inf]
+    if not xs:
+        return -math.inf
+    m = max(xs)
+    return m + math.log(sum(math.exp(x - m) for x in xs))
+
+
+def sequence_totals(joiner, graph, enc, length):
+    """Exhaustive LogAdd merge: {blank-free label sequence: log of the summed probability of
+    its alignments}, final weights included; alignments ending in non-final states count
+    (with weight 0) only if no alignment ends in a final state.  Also returns the total."""
+    al = all_alignments(joiner, graph, enc, length)
+    any_final = any(f is not None for _, _, _, f in al)
+    terms = {}
+    for score, labels, _, f in al:
+        if any_final and f is None:
+            continue
+        y = tuple(c for c in labels if c)
+        terms.setdefault(y, []).append(score + (f if any_final else 0.0))
+    totals = {y: _logsumexp(v) for y, v in terms.items()}
+    return totals, _logsumexp([v for vs in terms.values() for v in vs])
