@@ -231,6 +231,78 @@ tbs_status tbs_state_finish(tbs_state *state, int32_t *out_tokens, int32_t *out_
 void tbs_state_destroy(tbs_state *state);
 
 /*
+ * Lattice output and label-sequence search (Sec. 2.5: the search's output is a lattice,
+ * an FSA, from which the label sequence with the highest total probability is found by
+ * sampling n paths, removing blanks, keeping the distinct sequences and scoring each by
+ * composing it with the lattice -- the "LogAdd" rows of Tables 3 and 6).
+ *
+ * tbs_lattice_create
+ *   Runs the search of tbs_decode (same arguments, schedule and kernels; B >= 1), then
+ *   builds on the device, per stream, the lattice:
+ *     nodes  the survivors of each frame f = 0..len_b (the survivor trace of tbs_decode);
+ *     arcs   for each frame f < len_b, every expansion of a frame-f survivor -- blank, or
+ *            a graph arc -- whose (state, context) survived frame f+1, whatever candidate
+ *            won the max-merge; weight q + log P(label | context, f) (blank: log P(blank))
+ *            in fp32, from the joiner and log-softmax recomputed for the survivors'
+ *            contexts; ordered by (destination, source, arc position), blank first;
+ *     final  per last-frame node the graph's final weight, or 0 for all of them if none
+ *            is final (then status = 1, as out_status of tbs_decode).
+ *   Forward scores and totals are computed in fp64.  Synchronises hip_stream once (the
+ *   arc count sizes the arc arrays); the rest is enqueued.  The lattice keeps its own
+ *   copies of everything it needs (the model and graphs must outlive it).  Errors as for
+ *   tbs_decode; TBS_EINVAL for B < 1.
+ * tbs_lattice_create_graphs: the same with one graph per stream (as tbs_decode_graphs).
+ * tbs_lattice_num_arcs: total arcs A over all streams (host).
+ * tbs_lattice_export: device copies (each pointer may be NULL):
+ *   frame_off  int64 [B*T+1]: the arcs of frame f of stream b are
+ *              [frame_off[b*T+f], frame_off[b*T+f+1]) (empty for f >= len_b);
+ *   arcs       int32 [A][4]: (source node index within frame f, destination node index
+ *              within frame f+1, label (0 = blank), graph arc id or -1);
+ *   weights    float [A];
+ *   nodes      int32 [T+1][B][max_states][4], the trace layout of tbs_decode;
+ *   alpha      double [B][T+1][max_states]: log of the summed weight of the paths from
+ *              the initial node to each node (-inf for empty slots and frames > len_b);
+ *   final_w    double [B][max_states]; total double [B]: log of the summed weight of all
+ *              complete paths, final weights included; status int32 [B].
+ * tbs_lattice_nbest
+ *   num_paths >= 1 paths per stream are sampled from the lattice's path distribution
+ *   (probability proportional to exp(path weight + final weight)) by inversion, going
+ *   backwards: uniforms (DEVICE double [B][num_paths][T+1], each in [0, 1)) entry len_b
+ *   picks the final node, entry f < len_b the arc into the path's node of frame f+1;
+ *   among K items of log weight v_k, the pick is the first k whose running sum of
+ *   exp(v - max v) exceeds u times the full sum.  The blank-free label sequences of the
+ *   paths, without repeats, in order of first occurrence, are each scored by the log of
+ *   their total probability in the lattice (all paths with that label sequence, final
+ *   weights included); the best (the first on ties) is returned:
+ *   out_tokens int32 [B][T] (-1 padded), out_num_tokens [B], out_scores double [B];
+ *   optional: out_num_unique int32 [B], out_unique_scores double [B][num_paths] and
+ *   out_unique_first int32 [B][num_paths] (the sampled path that first gave each
+ *   sequence; -inf / -1 padded), out_paths int32 [B][num_paths][T+1] (per path: the
+ *   arc taken on frame f as an index within frame f's arcs, the final node at len_b,
+ *   -1 after).  Scratch for num_paths is kept in the lattice.  Calls on one lattice are
+ *   stream-ordered across streams.
+ */
+typedef struct tbs_lattice tbs_lattice;
+
+tbs_status tbs_lattice_create(const tbs_model *model, const tbs_graph *graph,
+                              const tbs_beam_params *params, const float *encoder_out,
+                              const int32_t *lengths, int32_t B, int32_t T, void *hip_stream,
+                              tbs_lattice **out);
+tbs_status tbs_lattice_create_graphs(const tbs_model *model, const tbs_graph *const *graphs,
+                                     const tbs_beam_params *params, const float *encoder_out,
+                                     const int32_t *lengths, int32_t B, int32_t T,
+                                     void *hip_stream, tbs_lattice **out);
+tbs_status tbs_lattice_num_arcs(const tbs_lattice *lattice, int64_t *out);
+tbs_status tbs_lattice_export(const tbs_lattice *lattice, int64_t *frame_off, int32_t *arcs,
+                              float *weights, int32_t *nodes, double *alpha, double *final_w,
+                              double *total, int32_t *status, void *hip_stream);
+tbs_status tbs_lattice_nbest(tbs_lattice *lattice, int32_t num_paths, const double *uniforms,
+                             int32_t *out_tokens, int32_t *out_num_tokens, double *out_scores,
+                             int32_t *out_num_unique, double *out_unique_scores,
+                             int32_t *out_unique_first, int32_t *out_paths, void *hip_stream);
+void tbs_lattice_destroy(tbs_lattice *lattice);
+
+/*
  * How tbs_decode drives the frame loop of Algorithm 1 (all schedules compute
  * the same search; results agree within the fp32 rounding of the joiner):
  *   TBS_SCHEDULE_FRAME   two kernels per frame over the whole batch: a joiner

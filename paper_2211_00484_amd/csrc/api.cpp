@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdarg>
@@ -847,6 +848,189 @@ tbs_status state_create_impl(const tbs_model* model, const tbs_graph* graph,
 
 }  // namespace
 
+struct tbs_lattice {
+  tbs_model* m = nullptr;
+  GraphDev gd{};
+  int B = 0, T = 0, Ns = 0, Nc = 0;
+  long long A = 0;                  // arcs
+  int* len = nullptr;               // [B]
+  int* trace = nullptr;             // [T+1][B][Ns][4] survivors (the lattice nodes)
+  int* tokens = nullptr;            // best path of the search (needed by the decode call)
+  int* ntok = nullptr;
+  double* scores = nullptr;
+  int* dstatus = nullptr;
+  GraphDev* gtab = nullptr;         // [B] per-stream graphs, or null
+  int* nn = nullptr;
+  int* cnt = nullptr;
+  long long* off = nullptr;
+  int* dptr = nullptr;
+  int4* arcs = nullptr;
+  float* w = nullptr;
+  int* rowctx = nullptr;
+  double* alpha = nullptr;
+  double* fw = nullptr;
+  double* total = nullptr;
+  int* status = nullptr;
+  void* h = nullptr;                // joiner rows of one chunk of streams
+  float* logits = nullptr;
+  float2* stats = nullptr;
+  // n-best scratch, for up to ncap paths
+  int ncap = 0;
+  int* seq = nullptr;
+  int* pntok = nullptr;
+  unsigned long long* hash = nullptr;
+  int* first = nullptr;
+  int* nuniq = nullptr;
+  double* uscore = nullptr;
+  double* dp = nullptr;
+  size_t dp_lds = 0;
+  int dp_grid = 0;
+  hipEvent_t done = nullptr;        // the lattice's latest device work
+  bool pending = false;
+
+  LatticeDev dev() const {
+    LatticeDev L;
+    L.B = B;
+    L.T = T;
+    L.Ns = Ns;
+    L.Nc = Nc;
+    L.V = m->V;
+    L.len = len;
+    L.nodes = trace;
+    L.graphs = gtab;
+    L.nn = nn;
+    L.cnt = cnt;
+    L.off = off;
+    L.dptr = dptr;
+    L.arcs = arcs;
+    L.w = w;
+    L.rowctx = rowctx;
+    L.alpha = alpha;
+    L.fw = fw;
+    L.total = total;
+    L.status = status;
+    return L;
+  }
+  void free_nbest() {
+    hipFree(seq); hipFree(pntok); hipFree(hash); hipFree(first); hipFree(nuniq);
+    hipFree(uscore); hipFree(dp);
+    seq = pntok = first = nuniq = nullptr;
+    hash = nullptr;
+    uscore = dp = nullptr;
+    ncap = 0;
+  }
+  void release() {
+    if (done && pending) hipEventSynchronize(done);
+    free_nbest();
+    hipFree(len); hipFree(trace); hipFree(tokens); hipFree(ntok); hipFree(scores);
+    hipFree(dstatus); hipFree(gtab); hipFree(nn); hipFree(cnt); hipFree(off); hipFree(dptr);
+    hipFree(arcs); hipFree(w); hipFree(rowctx); hipFree(alpha); hipFree(fw); hipFree(total);
+    hipFree(status); hipFree(h); hipFree(logits); hipFree(stats);
+    if (done) hipEventDestroy(done);
+  }
+};
+
+namespace {
+
+// Builds the lattice of a decode (tbs_lattice_create / tbs_lattice_create_graphs).
+tbs_status lattice_create_impl(const tbs_model* model, const tbs_graph* graph,
+                               const tbs_graph* const* graphs, const tbs_beam_params* params,
+                               const float* encoder_out, const int32_t* lengths, int32_t B,
+                               int32_t T, void* hip_stream, tbs_lattice** out, const char* who) {
+  if (!out) return fail(TBS_EINVAL, "%s: out is NULL", who);
+  *out = nullptr;
+  if (B < 1 || T < 0) return fail(TBS_EINVAL, "%s: B must be >= 1 and T >= 0", who);
+  GraphDev gd;
+  tbs_status s = graph_set(model, graph, graphs, B, params, who, &gd);
+  if (s != TBS_OK) return s;
+  if (!lengths) return fail(TBS_EINVAL, "%s: lengths is NULL", who);
+  for (int b = 0; b < B; ++b)
+    if (lengths[b] < 0 || lengths[b] > T)
+      return fail(TBS_EINVAL, "%s: lengths[%d] = %d outside [0, %d]", who, b, lengths[b], T);
+  tbs_model* m = const_cast<tbs_model*>(model);
+  hipStream_t st = (hipStream_t)hip_stream;
+  tbs_lattice* L = new tbs_lattice();
+  L->m = m;
+  L->gd = gd;
+  L->B = B;
+  L->T = T;
+  L->Ns = params->max_states;
+  L->Nc = params->max_contexts < L->Ns ? params->max_contexts : L->Ns;
+  const size_t BN = (size_t)B * L->Ns, BT = (size_t)B * T;
+  const int nvt = m->Vpad / kJoinerBN;
+  const size_t esz = m->bf16 ? 2 : 4;
+  // joiner rows per chunk of streams: whole streams, logits of at most 512 MiB
+  const size_t per_stream = (size_t)T * L->Nc;
+  size_t cap_rows = ((size_t)512 << 20) / ((size_t)m->Vpad * 4);
+  if (cap_rows < per_stream) cap_rows = per_stream;
+  const int chunk = per_stream == 0 ? B : (int)std::min<size_t>(B, cap_rows / per_stream);
+  const size_t rows = per_stream * (size_t)chunk;
+  auto cleanup = [&](tbs_status st_) {
+    L->release();
+    delete L;
+    return st_;
+  };
+  hipError_t e = hipSuccess;
+#define LAT_ALLOC(expr) \
+  if (e == hipSuccess) e = (expr)
+  LAT_ALLOC(dalloc(&L->len, B));
+  LAT_ALLOC(dalloc(&L->trace, (size_t)(T + 1) * BN * 4));
+  LAT_ALLOC(dalloc(&L->tokens, BT));
+  LAT_ALLOC(dalloc(&L->ntok, B));
+  LAT_ALLOC(dalloc(&L->scores, B));
+  LAT_ALLOC(dalloc(&L->dstatus, B));
+  if (graphs) LAT_ALLOC(dalloc(&L->gtab, B));
+  LAT_ALLOC(dalloc(&L->nn, (size_t)B * (T + 1)));
+  LAT_ALLOC(dalloc(&L->cnt, BT));
+  LAT_ALLOC(dalloc(&L->off, BT + 1));
+  LAT_ALLOC(dalloc(&L->dptr, BT * (L->Ns + 1)));
+  LAT_ALLOC(dalloc(&L->rowctx, BT * L->Nc));
+  LAT_ALLOC(dalloc(&L->alpha, (size_t)(T + 1) * BN));
+  LAT_ALLOC(dalloc(&L->fw, BN));
+  LAT_ALLOC(dalloc(&L->total, B));
+  LAT_ALLOC(dalloc(&L->status, B));
+  LAT_ALLOC(dalloc((char**)&L->h, rows * m->Kpad * esz));
+  LAT_ALLOC(dalloc(&L->logits, rows * m->Vpad));
+  LAT_ALLOC(dalloc(&L->stats, rows * nvt));
+  LAT_ALLOC(hipEventCreateWithFlags(&L->done, hipEventDisableTiming));
+#undef LAT_ALLOC
+  if (e != hipSuccess) return cleanup(hip_fail(e, who));
+  if (graphs) {
+    std::vector<GraphDev> tab(B);
+    for (int b = 0; b < B; ++b) tab[b] = graph_dev(graphs[b]);
+    e = hipMemcpy(L->gtab, tab.data(), (size_t)B * sizeof(GraphDev), hipMemcpyHostToDevice);
+  }
+  if (e == hipSuccess) e = hipMemcpy(L->len, lengths, (size_t)B * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return cleanup(hip_fail(e, who));
+  // the search, with its survivor trace as the lattice nodes
+  s = decode_impl(model, graph, graphs, params, encoder_out, lengths, B, T, L->tokens, L->ntok,
+                  L->scores, L->dstatus, nullptr, L->trace, hip_stream, who);
+  if (s != TBS_OK) return cleanup(s);
+  const LatticeDev d0 = L->dev();
+  e = launch_lattice_count(d0, gd, st);
+  if (e == hipSuccess) e = launch_lattice_scan(d0, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(&L->A, L->off + BT, sizeof(long long), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = dalloc(&L->arcs, (size_t)L->A);
+  if (e == hipSuccess) e = dalloc(&L->w, (size_t)L->A);
+  if (e != hipSuccess) return cleanup(hip_fail(e, who));
+  const LatticeDev d = L->dev();
+  const ModelDev md = model_dev(m);
+  e = launch_lattice_fill(d, gd, st);
+  for (int b0 = 0; e == hipSuccess && b0 < B; b0 += chunk)
+    e = launch_lattice_weights(md, d, gd, encoder_out, b0, std::min(B, b0 + chunk), L->h,
+                               L->logits, L->stats, m->ncu, st);
+  if (e == hipSuccess) e = launch_lattice_forward(d, gd, st);
+  if (e == hipSuccess) e = hipEventRecord(L->done, st);
+  if (e != hipSuccess) return cleanup(hip_fail(e, who));
+  L->pending = true;
+  *out = L;
+  return TBS_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 tbs_status tbs_decode(const tbs_model* model, const tbs_graph* graph,
@@ -1045,6 +1229,128 @@ tbs_status tbs_model_read_profile(tbs_model* model, tbs_kernel_time* out) {
   prof_drop(model);
   for (int k = 0; k < TBS_KERNEL_COUNT; ++k) out[k] = model->prof_acc[k];
   return TBS_OK;
+}
+
+
+tbs_status tbs_lattice_create(const tbs_model* model, const tbs_graph* graph,
+                              const tbs_beam_params* params, const float* encoder_out,
+                              const int32_t* lengths, int32_t B, int32_t T, void* hip_stream,
+                              tbs_lattice** out) {
+  if (!graph) {
+    if (out) *out = nullptr;
+    return fail(TBS_EINVAL, "tbs_lattice_create: graph is NULL");
+  }
+  return lattice_create_impl(model, graph, nullptr, params, encoder_out, lengths, B, T,
+                             hip_stream, out, "tbs_lattice_create");
+}
+
+tbs_status tbs_lattice_create_graphs(const tbs_model* model, const tbs_graph* const* graphs,
+                                     const tbs_beam_params* params, const float* encoder_out,
+                                     const int32_t* lengths, int32_t B, int32_t T,
+                                     void* hip_stream, tbs_lattice** out) {
+  if (!graphs || !model || !params) {
+    if (out) *out = nullptr;
+    return fail(TBS_EINVAL, "tbs_lattice_create_graphs: NULL model/graphs/params");
+  }
+  return lattice_create_impl(model, nullptr, graphs, params, encoder_out, lengths, B, T,
+                             hip_stream, out, "tbs_lattice_create_graphs");
+}
+
+tbs_status tbs_lattice_num_arcs(const tbs_lattice* lat, int64_t* out) {
+  if (!lat || !out) return fail(TBS_EINVAL, "tbs_lattice_num_arcs: NULL argument");
+  *out = lat->A;
+  return TBS_OK;
+}
+
+tbs_status tbs_lattice_export(const tbs_lattice* lat, int64_t* frame_off, int32_t* arcs,
+                              float* weights, int32_t* nodes, double* alpha, double* final_w,
+                              double* total, int32_t* status, void* hip_stream) {
+  if (!lat) return fail(TBS_EINVAL, "tbs_lattice_export: lattice is NULL");
+  tbs_lattice* L = const_cast<tbs_lattice*>(lat);
+  std::lock_guard<std::mutex> lk(L->m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  if (L->pending) HIP_TRY(hipStreamWaitEvent(st, L->done, 0), "hipStreamWaitEvent");
+  const size_t BT = (size_t)L->B * L->T, BN = (size_t)L->B * L->Ns;
+  auto cp = [&](void* dst, const void* src, size_t bytes) {
+    return dst && bytes ? hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, st)
+                        : hipSuccess;
+  };
+  HIP_TRY(cp(frame_off, L->off, (BT + 1) * 8), "tbs_lattice_export");
+  HIP_TRY(cp(arcs, L->arcs, (size_t)L->A * 16), "tbs_lattice_export");
+  HIP_TRY(cp(weights, L->w, (size_t)L->A * 4), "tbs_lattice_export");
+  HIP_TRY(cp(nodes, L->trace, (size_t)(L->T + 1) * BN * 16), "tbs_lattice_export");
+  HIP_TRY(cp(alpha, L->alpha, (size_t)(L->T + 1) * BN * 8), "tbs_lattice_export");
+  HIP_TRY(cp(final_w, L->fw, BN * 8), "tbs_lattice_export");
+  HIP_TRY(cp(total, L->total, (size_t)L->B * 8), "tbs_lattice_export");
+  HIP_TRY(cp(status, L->status, (size_t)L->B * 4), "tbs_lattice_export");
+  HIP_TRY(hipEventRecord(L->done, st), "hipEventRecord");
+  L->pending = true;
+  return TBS_OK;
+}
+
+tbs_status tbs_lattice_nbest(tbs_lattice* lat, int32_t num_paths, const double* uniforms,
+                             int32_t* out_tokens, int32_t* out_num_tokens, double* out_scores,
+                             int32_t* out_num_unique, double* out_unique_scores,
+                             int32_t* out_unique_first, int32_t* out_paths, void* hip_stream) {
+  if (!lat) return fail(TBS_EINVAL, "tbs_lattice_nbest: lattice is NULL");
+  if (num_paths < 1) return fail(TBS_EINVAL, "tbs_lattice_nbest: num_paths must be >= 1");
+  if (!uniforms || !out_num_tokens || !out_scores || (lat->T > 0 && !out_tokens))
+    return fail(TBS_EINVAL, "tbs_lattice_nbest: NULL uniforms or output pointer");
+  tbs_lattice* L = lat;
+  std::lock_guard<std::mutex> lk(L->m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  const int B = L->B, T = L->T, Ns = L->Ns;
+  const size_t Bn = (size_t)B * num_paths;
+  const int W = T / 2 + 1;  // widest band of the sequence DP
+  const size_t lds = (size_t)2 * Ns * W * 8;
+  if (num_paths > L->ncap) {
+    if (L->pending) HIP_TRY(hipEventSynchronize(L->done), "hipEventSynchronize");
+    L->free_nbest();
+    hipError_t e = dalloc(&L->seq, Bn * (T > 0 ? T : 1));
+    if (e == hipSuccess) e = dalloc(&L->pntok, Bn);
+    if (e == hipSuccess) e = dalloc(&L->hash, Bn);
+    if (e == hipSuccess) e = dalloc(&L->first, Bn);
+    if (e == hipSuccess) e = dalloc(&L->nuniq, (size_t)B);
+    if (e == hipSuccess) e = dalloc(&L->uscore, Bn);
+    // the DP's two band buffers live in LDS when they fit, else in global memory
+    L->dp_lds = lds <= (64u << 10) ? lds : 0;
+    L->dp_grid = (int)std::min<size_t>(Bn, L->dp_lds ? 65535 : 1024);
+    if (e == hipSuccess && !L->dp_lds) e = dalloc(&L->dp, (size_t)L->dp_grid * 2 * Ns * W);
+    if (e != hipSuccess) {
+      L->free_nbest();
+      return hip_fail(e, "tbs_lattice_nbest");
+    }
+    L->ncap = num_paths;
+  }
+  NBestDev N;
+  N.n = num_paths;
+  N.u = uniforms;
+  N.paths = out_paths;
+  N.seq = L->seq;
+  N.ntok = L->pntok;
+  N.hash = L->hash;
+  N.first = L->first;
+  N.nuniq = L->nuniq;
+  N.score = L->uscore;
+  N.dp = L->dp;
+  N.dp_stride = W;
+  if (L->pending) HIP_TRY(hipStreamWaitEvent(st, L->done, 0), "hipStreamWaitEvent");
+  const int grid = (int)std::min<size_t>(Bn, (size_t)L->dp_grid);
+  HIP_TRY(launch_nbest(L->dev(), N, out_tokens, out_num_tokens, out_scores, out_num_unique,
+                       out_unique_scores, out_unique_first, grid, L->dp_lds, st),
+          "launch(nbest)");
+  HIP_TRY(hipEventRecord(L->done, st), "hipEventRecord");
+  L->pending = true;
+  return TBS_OK;
+}
+
+void tbs_lattice_destroy(tbs_lattice* lat) {
+  if (!lat) return;
+  {
+    std::lock_guard<std::mutex> lk(lat->m->mu);
+    lat->release();
+  }
+  delete lat;
 }
 
 }  // extern "C"

@@ -132,4 +132,60 @@ hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const in
                               void* h, float* logits, float2* stats, float* out_logp, int ncu,
                               hipStream_t st);
 
+// Lattice of a batch (the search's output FSA): nodes are the survivors of each frame
+// (the survivor trace, [T+1][B][Ns][4] = (ctx, state, parent, label), -1 padded); the
+// arcs of frame f of stream b run from its frame-f survivors into its frame-(f+1)
+// survivors, ordered by (destination, source, arc position) with blank first.
+struct LatticeDev {
+  int B, T, Ns, Nc, V;
+  const int* len;           // [B]
+  const int* nodes;         // survivor trace
+  const GraphDev* graphs;   // [B] per-stream graphs, or null
+  int* nn;                  // [B][T+1] nodes per frame (written by the forward pass)
+  int* cnt;                 // [B*T] arcs of (b, f)
+  long long* off;           // [B*T+1] first arc of (b, f)
+  int* dptr;                // [B*T][Ns+1] local offset of each destination's first arc
+  int4* arcs;               // [A] (src, dst, label, graph arc or -1)
+  float* w;                 // [A] weight: q + log P(label), blank: log P(blank)
+  int* rowctx;              // [B*T*Nc] context of joiner row (b, f, r), -1 = none
+  double* alpha;            // [B][T+1][Ns] forward log scores (-inf for absent nodes)
+  double* fw;               // [B][Ns] final weights of the last frame's nodes
+  double* total;            // [B]
+  int* status;              // [B] 1: no survivor of the last frame is final
+};
+
+// n-best scratch of a lattice for n paths.
+struct NBestDev {
+  int n;
+  const double* u;          // [B][n][T+1]
+  int* paths;               // [B][n][T+1] or null
+  int* seq;                 // [B][n][T] blank-free label sequences
+  int* ntok;                // [B][n]
+  unsigned long long* hash; // [B][n]
+  int* first;               // [B][n] path of each distinct sequence
+  int* nuniq;               // [B]
+  double* score;            // [B][n] total log probability of each distinct sequence
+  double* dp;               // DP scratch in global memory, or null (LDS)
+  int dp_stride;            // doubles per DP buffer row: band width cap
+};
+
+hipError_t launch_lattice_count(const LatticeDev& L, const GraphDev& g, hipStream_t st);
+hipError_t launch_lattice_scan(const LatticeDev& L, hipStream_t st);
+hipError_t launch_lattice_fill(const LatticeDev& L, const GraphDev& g, hipStream_t st);
+// Joiner rows of streams [b0, b1) (dense (b, f, r) rows, ctx from L.rowctx): h rows,
+// logits and per-tile softmax statistics, then the arc weights of those streams.
+hipError_t launch_lattice_weights(const ModelDev& m, const LatticeDev& L, const GraphDev& g,
+                                  const float* enc, int b0, int b1, void* h, float* logits,
+                                  float2* stats, int ncu, hipStream_t st);
+hipError_t launch_lattice_forward(const LatticeDev& L, const GraphDev& g, hipStream_t st);
+hipError_t launch_nbest(const LatticeDev& L, const NBestDev& N, int* out_tokens, int* out_ntok,
+                        double* out_scores, int* out_nuniq, double* out_uscores,
+                        int* out_ufirst, int dp_grid, size_t dp_lds, hipStream_t st);
+
+// joiner rows of a dense row table: row r of the batch is table row row0 + r, with
+// context ctx[row0 + r] (-1: no row, h = 0) and encoder row (row0 + r) / per_enc
+hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, const int* ctx, long long row0,
+                               int per_enc, int R, void* h, float* logits, float2* stats, int ncu,
+                               hipStream_t st);
+
 }  // namespace tbs

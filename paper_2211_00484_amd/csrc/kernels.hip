@@ -276,6 +276,34 @@ __global__ __launch_bounds__(256) void k_h_rows(ModelDev m, const float* __restr
                     reinterpret_cast<char*>(h) + (size_t)r * m.Kpad * esz, m.Kpad, threadIdx.x);
 }
 
+// Rows of a dense (encoder row, context) table: batch row r is table row row0 + r,
+// with context ctx[row0 + r] (-1: an empty slot, written as zeros) and encoder row
+// (row0 + r) / per_enc.
+__global__ __launch_bounds__(256) void k_h_rows_dense(ModelDev m, const float* __restrict__ enc,
+                                                      const int* __restrict__ ctx, long long row0,
+                                                      int per_enc, void* __restrict__ h) {
+  __shared__ int2 off;
+  const long long g = row0 + blockIdx.x;
+  const int c = ctx[g];
+  const size_t esz = m.bf16 ? 2 : 4;
+  char* hrow = reinterpret_cast<char*>(h) + (size_t)blockIdx.x * m.Kpad * esz;
+  if (c < 0) {
+    for (int k = threadIdx.x; k < m.Kpad; k += blockDim.x) {
+      if (m.bf16)
+        reinterpret_cast<uint16_t*>(hrow)[k] = 0;
+      else
+        reinterpret_cast<float*>(hrow)[k] = 0.f;
+    }
+    return;
+  }
+  if (threadIdx.x == 0) {
+    const int a = c / m.V;
+    off = make_int2(a * m.Kpad, (c - a * m.V) * m.Kpad);
+  }
+  __syncthreads();
+  write_h_rows<256>(m, enc + (size_t)(g / per_enc) * m.C, 0, &off, 1, hrow, m.Kpad, threadIdx.x);
+}
+
 // ---------------------------------------------------------------------------
 // joiner
 
@@ -2992,6 +3020,26 @@ hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, 
   launch_k(k_final, dim3(d.B), dim3(256), 0, st, g, d, out_tokens, out_ntok, out_scores,
                      out_status, out_arcs, exchange_err);
   return hipGetLastError();
+}
+
+hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, const int* ctx, long long row0,
+                               int per_enc, int R, void* h, float* logits, float2* stats, int ncu,
+                               hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_h_rows_dense, dim3(R), dim3(256), 0, st, m, enc, ctx, row0, per_enc, h);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const JoinerPlan p = plan_joiner(R, m.Vpad, m.Kpad, m.bf16, ncu);
+  JoinArgs a{};
+  a.h = h;
+  a.logits = logits;
+  a.stats = stats;
+  a.R = R;
+  a.n_rt = p.n_rt;
+  a.n_ct = p.n_ct;
+  a.nvt = m.Vpad / kJoinerBN;
+  a.rows_mode = 1;
+  return launch_joiner(m, a, p, false, st);
 }
 
 hipError_t launch_joiner_rows(const ModelDev& m, const float* enc_rows, const int* ctx, int R,

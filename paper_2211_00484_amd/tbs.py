@@ -98,6 +98,20 @@ def lib():
     L.tbs_state_create_graphs.restype = _I32
     L.tbs_state_create_graphs.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _I32, _I32, _P,
                                           ctypes.POINTER(_P)]
+    L.tbs_lattice_create.restype = _I32
+    L.tbs_lattice_create.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32, _P,
+                                     ctypes.POINTER(_P)]
+    L.tbs_lattice_create_graphs.restype = _I32
+    L.tbs_lattice_create_graphs.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32,
+                                            _I32, _P, ctypes.POINTER(_P)]
+    L.tbs_lattice_num_arcs.restype = _I32
+    L.tbs_lattice_num_arcs.argtypes = [_P, ctypes.POINTER(ctypes.c_int64)]
+    L.tbs_lattice_export.restype = _I32
+    L.tbs_lattice_export.argtypes = [_P] + [_P] * 8 + [_P]
+    L.tbs_lattice_nbest.restype = _I32
+    L.tbs_lattice_nbest.argtypes = [_P, _I32, _P] + [_P] * 7 + [_P]
+    L.tbs_lattice_destroy.restype = None
+    L.tbs_lattice_destroy.argtypes = [_P]
     L.tbs_decode_chunk.restype = _I32
     L.tbs_decode_chunk.argtypes = [_P, _P, _P, _I32, _P, _P]
     L.tbs_state_finish.restype = _I32
@@ -352,6 +366,106 @@ class DecodeState:
     def close(self):
         if self._h is not None and _lib is not None:
             _lib.tbs_state_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        self.close()
+
+
+@dataclass
+class NBestOutput:
+    tokens: "object"         # int32 [B, T] device: the best label sequence, -1 padded
+    num_tokens: "object"     # int32 [B]
+    scores: "object"         # float64 [B]: its total log probability in the lattice
+    num_unique: "object"     # int32 [B]: distinct sequences among the sampled paths
+    unique_scores: "object"  # float64 [B, n]
+    unique_first: "object"   # int32 [B, n]: the path that first gave each sequence
+    paths: "object"          # int32 [B, n, T+1] or None
+
+    def token_lists(self):
+        tok = self.tokens.cpu().numpy()
+        n = self.num_tokens.cpu().numpy()
+        return [list(tok[b, : n[b]]) for b in range(tok.shape[0])]
+
+
+class Lattice:
+    """The search's lattice (tbs_lattice_create) and the n-best label-sequence search on it
+    (tbs_lattice_nbest).  ``graph``: one Graph, or a list of one Graph per stream."""
+
+    def __init__(self, model: Model, graph, encoder_out, lengths, beam: float = math.inf,
+                 max_states: int = 4, max_contexts: int = 4, stream=None):
+        self._h = None
+        lens = np.ascontiguousarray(np.asarray(lengths), dtype=np.int32)
+        B, T = int(encoder_out.shape[0]), int(encoder_out.shape[1])
+        if encoder_out.dim() != 3 or encoder_out.shape[2] != model.dim:
+            raise ValueError("encoder_out must be [B, T, dim]")
+        if lens.shape != (B,):
+            raise ValueError("lengths must have shape [B]")
+        params = BeamParams(float(math.inf if beam is None else beam), int(max_states),
+                            int(max_contexts))
+        h = _P()
+        if isinstance(graph, Graph):
+            fn, gh = lib().tbs_lattice_create, graph._h
+        else:
+            graph = list(graph)
+            fn, gh = lib().tbs_lattice_create_graphs, _graph_table(graph, B)
+        _check(fn(model._h, gh, ctypes.byref(params), _dev_ptr(encoder_out.contiguous()),
+                  _host_ptr(lens), B, T, _stream_ptr(stream), ctypes.byref(h)))
+        self._h = h
+        self._refs = (model, graph)
+        self.device = encoder_out.device
+        self.B, self.T, self.max_states = B, T, int(max_states)
+        self.lengths = lens
+
+    def num_arcs(self) -> int:
+        n = ctypes.c_int64(0)
+        _check(lib().tbs_lattice_num_arcs(self._h, ctypes.byref(n)))
+        return int(n.value)
+
+    def export(self, stream=None) -> dict:
+        """Device tensors: frame_off [B*T+1], arcs [A, 4] (src, dst, label, graph arc),
+        weights [A], nodes [T+1, B, Ns, 4], alpha [B, T+1, Ns], final_w [B, Ns], total [B],
+        status [B]."""
+        import torch
+        A, B, T, Ns, dev = self.num_arcs(), self.B, self.T, self.max_states, self.device
+        out = {"frame_off": torch.empty(B * T + 1, dtype=torch.int64, device=dev),
+               "arcs": torch.empty((A, 4), dtype=torch.int32, device=dev),
+               "weights": torch.empty(A, dtype=torch.float32, device=dev),
+               "nodes": torch.empty((T + 1, B, Ns, 4), dtype=torch.int32, device=dev),
+               "alpha": torch.empty((B, T + 1, Ns), dtype=torch.float64, device=dev),
+               "final_w": torch.empty((B, Ns), dtype=torch.float64, device=dev),
+               "total": torch.empty(B, dtype=torch.float64, device=dev),
+               "status": torch.empty(B, dtype=torch.int32, device=dev)}
+        _check(lib().tbs_lattice_export(self._h, *[_dev_ptr(out[k]) for k in (
+            "frame_off", "arcs", "weights", "nodes", "alpha", "final_w", "total", "status")],
+            _stream_ptr(stream)))
+        return out
+
+    def nbest(self, num_paths: int, uniforms, want_paths: bool = False,
+              stream=None) -> NBestOutput:
+        """n-best label-sequence search; uniforms: float64 [B, num_paths, T+1] on the
+        device, each in [0, 1)."""
+        import torch
+        B, T, n, dev = self.B, self.T, int(num_paths), self.device
+        if tuple(uniforms.shape) != (B, n, T + 1) or uniforms.dtype != torch.float64:
+            raise ValueError(f"uniforms must be float64 [{B}, {n}, {T + 1}]")
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = NBestOutput(tokens=torch.empty((B, T), **i32), num_tokens=torch.empty(B, **i32),
+                          scores=torch.empty(B, dtype=torch.float64, device=dev),
+                          num_unique=torch.empty(B, **i32),
+                          unique_scores=torch.empty((B, n), dtype=torch.float64, device=dev),
+                          unique_first=torch.empty((B, n), **i32),
+                          paths=torch.empty((B, n, T + 1), **i32) if want_paths else None)
+        _check(lib().tbs_lattice_nbest(self._h, n, _dev_ptr(uniforms.contiguous()),
+                                       _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
+                                       _dev_ptr(out.scores), _dev_ptr(out.num_unique),
+                                       _dev_ptr(out.unique_scores), _dev_ptr(out.unique_first),
+                                       _dev_ptr(out.paths), _stream_ptr(stream)))
+        return out
+
+    def close(self):
+        if self._h is not None and _lib is not None:
+            _lib.tbs_lattice_destroy(self._h)
         self._h = None
 
     def __del__(self):
