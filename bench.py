@@ -220,6 +220,96 @@ def scaled_microbench(dtype: str, steps: int):
     print(json.dumps(line), flush=True)
 
 
+def logadd_cpu_baseline(w, inputs, model_np, graph_np, dtype, n, threads=None,
+                        min_seconds=10.0, max_seconds=30.0):
+    """The oracle's lattice + n-best search on whole streams, timed on the host."""
+    import oracle
+    threads = threads or os.cpu_count() or 1
+    rng = np.random.default_rng(1)
+    t0 = time.perf_counter()
+    frames = 0
+    done = 0
+    order = list(range(inputs.B))
+    while time.perf_counter() - t0 < min_seconds and done < inputs.B:
+        streams = order[done:done + threads]
+        lat = oracle.lattice(model_np, graph_np, inputs.encoder_out, inputs.lengths, w.beam,
+                             w.max_states, w.max_contexts, bf16=(dtype == "bf16"),
+                             nthreads=threads, streams=streams)
+        for k, b in enumerate(streams):
+            L = int(inputs.lengths[b])
+            lat.nbest(k, rng.uniform(size=(n, L + 1)))
+            frames += L
+        done += len(streams)
+        if time.perf_counter() - t0 > max_seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": frames / dt, "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of {inputs.B} streams ({frames} frames): lattice search on "
+                      f"{threads} threads, then the n-best search ({n} paths) per stream on "
+                      "one thread"}
+
+
+def logadd_bench(args, w, inputs, model_np, graph_np, model, graph, enc, dtype, K, W, work):
+    """One step: tbs_lattice_create (the search, then the lattice) + tbs_lattice_nbest with
+    N paths + destroy, on the whole batch."""
+    import torch
+    from paper_2211_00484_amd import tbs
+    n = args.logadd
+    B, T = inputs.B, inputs.T
+    frames = int(inputs.lengths.sum())
+    u = torch.from_numpy(np.random.default_rng(1).uniform(size=(B, n, T + 1))).cuda()
+
+    def step(times=None):
+        t0 = time.perf_counter()
+        lat = tbs.Lattice(model, graph, enc, inputs.lengths, beam=w.beam,
+                          max_states=w.max_states, max_contexts=w.max_contexts)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        out = lat.nbest(n, u)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        arcs = lat.num_arcs()
+        lat.close()
+        if times is not None:
+            times.append((t1 - t0, t2 - t1, arcs, float(out.num_unique.float().mean())))
+        return out
+
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    phases = []
+    for _ in range(K):
+        step(phases)
+    ms_step = (t1 - t0) * 1e3 / K
+    line = {
+        "metric": METRIC + " (LogAdd: lattice + n-best label-sequence search)",
+        "value": frames * K / (t1 - t0), "unit": "frames/s", "n_gpus": 1, "steps": K,
+        "warmup": W, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 search and arc weights, f64 lattice scores" if dtype == "fp32"
+                 else "bf16 joiner operands, f32 search and arc weights, f64 lattice scores",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}+logadd{n}", "description": w.description, "B": B,
+                   "T_max": T, "frames": frames, "num_paths": n, "joiner": dtype,
+                   "beam": "inf" if math.isinf(w.beam) else w.beam,
+                   "max_states": w.max_states, "max_contexts": w.max_contexts},
+        "phases_ms": {"search_and_lattice": 1e3 * float(np.mean([p[0] for p in phases])),
+                      "nbest": 1e3 * float(np.mean([p[1] for p in phases]))},
+        "lattice_arcs": phases[0][2],
+        "distinct_sequences_per_stream": float(np.mean([p[3] for p in phases])),
+        "work_per_step": work,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = logadd_cpu_baseline(w, inputs, model_np, graph_np, dtype, n,
+                                                   threads=args.cpu_threads)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -232,6 +322,9 @@ def main():
                          "workgroup per stream (auto picks per shape)")
     ap.add_argument("--joiner-dtype", choices=["fp32", "bf16"], default=None,
                     help="override the workload's joiner dtype (e.g. Large in bf16)")
+    ap.add_argument("--logadd", type=int, default=0, metavar="N",
+                    help="time the LogAdd path instead: lattice of the search plus the n-best "
+                         "label-sequence search with N sampled paths per stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="threads for the oracle baseline (default: all host threads)")
@@ -276,6 +369,10 @@ def main():
     work = algorithmic_work(tr_out.trace.cpu().numpy(), inputs.lengths, graph_np, w.V, w.C, nvt,
                             w.max_states)
     del tr_out
+
+    if args.logadd:
+        logadd_bench(args, w, inputs, model_np, graph_np, model, graph, enc, dtype, K, W, work)
+        return
 
     out = tbs.allocate_outputs(B, T, w.max_states, status=True)
     for _ in range(W):

@@ -866,6 +866,7 @@ struct tbs_lattice {
   int* dptr = nullptr;
   int4* arcs = nullptr;
   float* w = nullptr;
+  double* pc = nullptr;
   int* rowctx = nullptr;
   double* alpha = nullptr;
   double* fw = nullptr;
@@ -904,6 +905,7 @@ struct tbs_lattice {
     L.dptr = dptr;
     L.arcs = arcs;
     L.w = w;
+    L.pc = pc;
     L.rowctx = rowctx;
     L.alpha = alpha;
     L.fw = fw;
@@ -924,7 +926,7 @@ struct tbs_lattice {
     free_nbest();
     hipFree(len); hipFree(trace); hipFree(tokens); hipFree(ntok); hipFree(scores);
     hipFree(dstatus); hipFree(gtab); hipFree(nn); hipFree(cnt); hipFree(off); hipFree(dptr);
-    hipFree(arcs); hipFree(w); hipFree(rowctx); hipFree(alpha); hipFree(fw); hipFree(total);
+    hipFree(arcs); hipFree(w); hipFree(pc); hipFree(rowctx); hipFree(alpha); hipFree(fw); hipFree(total);
     hipFree(status); hipFree(h); hipFree(logits); hipFree(stats);
     if (done) hipEventDestroy(done);
   }
@@ -1007,13 +1009,15 @@ tbs_status lattice_create_impl(const tbs_model* model, const tbs_graph* graph,
                   L->scores, L->dstatus, nullptr, L->trace, hip_stream, who);
   if (s != TBS_OK) return cleanup(s);
   const LatticeDev d0 = L->dev();
-  e = launch_lattice_count(d0, gd, st);
+  // node counts: the count pass writes them; with no frames only the initial node exists
+  e = T == 0 ? launch_fill_i32(L->nn, B, 1, st) : launch_lattice_count(d0, gd, st);
   if (e == hipSuccess) e = launch_lattice_scan(d0, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(&L->A, L->off + BT, sizeof(long long), hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e == hipSuccess) e = dalloc(&L->arcs, (size_t)L->A);
   if (e == hipSuccess) e = dalloc(&L->w, (size_t)L->A);
+  if (e == hipSuccess) e = dalloc(&L->pc, (size_t)L->A);
   if (e != hipSuccess) return cleanup(hip_fail(e, who));
   const LatticeDev d = L->dev();
   const ModelDev md = model_dev(m);
@@ -1302,7 +1306,6 @@ tbs_status tbs_lattice_nbest(tbs_lattice* lat, int32_t num_paths, const double* 
   const int B = L->B, T = L->T, Ns = L->Ns;
   const size_t Bn = (size_t)B * num_paths;
   const int W = T / 2 + 1;  // widest band of the sequence DP
-  const size_t lds = (size_t)2 * Ns * W * 8;
   if (num_paths > L->ncap) {
     if (L->pending) HIP_TRY(hipEventSynchronize(L->done), "hipEventSynchronize");
     L->free_nbest();
@@ -1312,10 +1315,16 @@ tbs_status tbs_lattice_nbest(tbs_lattice* lat, int32_t num_paths, const double* 
     if (e == hipSuccess) e = dalloc(&L->first, Bn);
     if (e == hipSuccess) e = dalloc(&L->nuniq, (size_t)B);
     if (e == hipSuccess) e = dalloc(&L->uscore, Bn);
-    // the DP's two band buffers live in LDS when they fit, else in global memory
-    L->dp_lds = lds <= (64u << 10) ? lds : 0;
-    L->dp_grid = (int)std::min<size_t>(Bn, L->dp_lds ? 65535 : 1024);
-    if (e == hipSuccess && !L->dp_lds) e = dalloc(&L->dp, (size_t)L->dp_grid * 2 * Ns * W);
+    // the DP's two band buffers per sequence (four sequences per workgroup) live in LDS
+    // (768 doubles per sequence) when the band fits; for shapes where a band may not
+    // fit, a global scratch slice per sequence slot is allotted and the workgroups per
+    // stream are capped at 1024 in all (grid-strided)
+    const bool may_spill = 2 * (size_t)Ns * W > 768;
+    L->dp_lds = may_spill ? 0 : 1;
+    const int groups = (num_paths + 3) / 4;
+    L->dp_grid = may_spill ? std::max(1, std::min(groups, 1024 / B)) : groups;
+    if (e == hipSuccess && may_spill)
+      e = dalloc(&L->dp, (size_t)L->dp_grid * B * 4 * 2 * Ns * W);
     if (e != hipSuccess) {
       L->free_nbest();
       return hip_fail(e, "tbs_lattice_nbest");
@@ -1335,7 +1344,7 @@ tbs_status tbs_lattice_nbest(tbs_lattice* lat, int32_t num_paths, const double* 
   N.dp = L->dp;
   N.dp_stride = W;
   if (L->pending) HIP_TRY(hipStreamWaitEvent(st, L->done, 0), "hipStreamWaitEvent");
-  const int grid = (int)std::min<size_t>(Bn, (size_t)L->dp_grid);
+  const int grid = std::min((num_paths + 3) / 4, L->dp_grid);
   HIP_TRY(launch_nbest(L->dev(), N, out_tokens, out_num_tokens, out_scores, out_num_unique,
                        out_unique_scores, out_unique_first, grid, L->dp_lds, st),
           "launch(nbest)");

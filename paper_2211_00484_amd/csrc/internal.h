@@ -147,6 +147,8 @@ struct LatticeDev {
   int* dptr;                // [B*T][Ns+1] local offset of each destination's first arc
   int4* arcs;               // [A] (src, dst, label, graph arc or -1)
   float* w;                 // [A] weight: q + log P(label), blank: log P(blank)
+  double* pc;               // [A] exp(alpha[src] + w - alpha[dst]): the arc's share of its
+                            // destination's forward score (backward sampling)
   int* rowctx;              // [B*T*Nc] context of joiner row (b, f, r), -1 = none
   double* alpha;            // [B][T+1][Ns] forward log scores (-inf for absent nodes)
   double* fw;               // [B][Ns] final weights of the last frame's nodes

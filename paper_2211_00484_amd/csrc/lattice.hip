@@ -19,7 +19,9 @@
 //   k_lat_frame<true>   write the arcs and the per-destination offsets
 //   joiner GEMM over the dense (stream, frame, context) rows, then k_lat_weights
 //   k_lat_forward       forward log scores, final weights, totals (one workgroup per stream)
+// The last three walk the frames from LDS stages of consecutive frames (stage_frames).
 //   k_lat_sample        one thread per sampled path: backward sampling by inversion
+//                       (one workgroup per stream)
 //   k_lat_unique        distinct blank-free sequences in order of first occurrence
 //   k_lat_seqscore      one workgroup per distinct sequence: composition with the lattice
 //   k_lat_best          the best distinct sequence per stream
@@ -36,6 +38,14 @@ namespace {
 constexpr int kLT = 256;  // threads per workgroup
 
 __device__ __forceinline__ double neg_inf() { return -__builtin_inf(); }
+
+// Workgroup barrier that orders LDS accesses only: global stores issued before it may
+// still be in flight (they are read by later kernels only).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 // Exclusive prefix sum over a 256-thread workgroup; *total receives the sum.
 __device__ int block_exclusive_scan(int v, int* s_w, int* total) {
@@ -132,6 +142,7 @@ __global__ __launch_bounds__(kLT) void k_lat_frame(LatticeDev L, GraphDev g0) {
   if (f >= L.len[b]) {
     if (!FILL) {
       if (tid == 0) L.cnt[fi] = 0;
+      if (tid == 0 && f == 0) L.nn[(size_t)b * (L.T + 1)] = 1;  // the initial node
       for (int r = tid; r < L.Nc; r += kLT) L.rowctx[fi * L.Nc + r] = -1;
     }
     return;
@@ -140,6 +151,10 @@ __global__ __launch_bounds__(kLT) void k_lat_frame(LatticeDev L, GraphDev g0) {
   load_frame_nodes(L, b, f, s);
   const int n0 = s.n0, n1 = s.n1, V = L.V;
   if (!FILL) {
+    if (tid == 0) {
+      L.nn[(size_t)b * (L.T + 1) + f + 1] = n1;
+      if (f == 0) L.nn[(size_t)b * (L.T + 1)] = n0;
+    }
     // the frame's joiner rows: its distinct contexts in ascending order
     for (int r = tid; r < L.Nc; r += kLT) L.rowctx[fi * L.Nc + r] = -1;
     __syncthreads();
@@ -254,66 +269,221 @@ __global__ __launch_bounds__(kLT) void k_lat_weights(LatticeDev L, GraphDev g0,
   }
 }
 
-// Log of the sum of exp(alpha[src] + w) over the arcs [a0, a1).
-__device__ double arcs_logsum(const LatticeDev& L, const double* alpha_f, long long a0,
-                              long long a1) {
-  double m = neg_inf();
-  for (long long a = a0; a < a1; ++a) m = fmax(m, alpha_f[L.arcs[a].x] + (double)L.w[a]);
-  if (m == neg_inf()) return m;
-  double sum = 0.0;
-  for (long long a = a0; a < a1; ++a) sum += exp(alpha_f[L.arcs[a].x] + (double)L.w[a] - m);
-  return m + log(sum);
+// ---------------------------------------------------------------------------
+// Frame-chunk staging.  The kernels that walk a stream's frames in order (forward
+// scores, path sampling, sequence scoring) first copy the arcs (source, label,
+// weight), per-destination offsets, node counts and, if asked, forward scores of a run
+// of consecutive frames into LDS with coalesced loads, then walk those frames from LDS:
+// the walk's dependent loads hit LDS instead of global memory.  A single frame larger
+// than the stage is read from global memory.
+
+constexpr int kStageF = kLT;  // frames per stage at most (one candidate per thread)
+
+template <int ACAP, int DCAP, int XCAP>
+struct Stage {
+  int src[ACAP];
+  int lab[ACAP];
+  float w[ACAP];
+  int dp[DCAP];                     // [frames][Ns+1]
+  double pc[XCAP > 0 ? ACAP : 1];   // arc shares (XCAP > 0)
+  int fo[kStageF + 1];              // first arc of each frame, relative to a0
+  int nn1[kStageF];                 // nodes of frame f+1
+  long long a0;
+  int lo, hi, staged;
+};
+
+struct FrameView {
+  const int* dp;   // [Ns+1] offsets of each destination's arcs within the frame
+  const int* src;  // arc k: src[k * stride], lab[k * stride]
+  const int* lab;
+  int stride;
+  const float* w;
+  const double* pc;  // arc shares of the destination's score (XCAP > 0 only)
+  int n1;            // nodes of frame f+1
+};
+
+// Stages frames [lo, hi) of stream b: forward from f (lo = f, hi <= fend), or backward
+// (hi = f, lo >= fend).  Every thread must call it; it begins and ends with a barrier.
+template <int ACAP, int DCAP, int XCAP>
+__device__ void stage_frames(const LatticeDev& L, Stage<ACAP, DCAP, XCAP>& s, int b, int f,
+                             bool backward, int fend) {
+  const int tid = threadIdx.x, Ns = L.Ns, T = L.T;
+  const long long* off = L.off + (size_t)b * T;
+  __syncthreads();  // the previous stage is no longer read
+  // thread t tries t + 1 frames; the valid counts form a prefix 1..m
+  const int nf = tid + 1;
+  bool ok = backward ? f - nf >= fend : f + nf <= fend;
+  if (ok) {
+    const int lo = backward ? f - nf : f, hi = lo + nf;
+    ok = off[hi] - off[lo] <= ACAP && nf * (Ns + 1) <= DCAP;
+  }
+  const int m = __syncthreads_count(ok);
+  const int nfr = m > 0 ? m : 1;
+  const int lo = backward ? f - nfr : f, hi = lo + nfr;
+  if (tid == 0) {
+    s.lo = lo;
+    s.hi = hi;
+    s.staged = m > 0;
+    s.a0 = off[lo];
+  }
+  if (m > 0) {
+    const long long a0 = off[lo];
+    const int na = (int)(off[hi] - a0);
+    for (int i = tid; i < na; i += kLT) {
+      const int4 x = L.arcs[a0 + i];
+      s.src[i] = x.x;
+      s.lab[i] = x.z;
+      s.w[i] = L.w[a0 + i];
+      if (XCAP > 0) s.pc[i] = L.pc[a0 + i];
+    }
+    const int* dsrc = L.dptr + ((size_t)b * T + lo) * (Ns + 1);
+    for (int i = tid; i < nfr * (Ns + 1); i += kLT) s.dp[i] = dsrc[i];
+    for (int i = tid; i <= nfr; i += kLT) s.fo[i] = (int)(off[lo + i] - a0);
+    for (int i = tid; i < nfr; i += kLT) s.nn1[i] = L.nn[(size_t)b * (T + 1) + lo + i + 1];
+  }
+  __syncthreads();
+}
+
+template <int ACAP, int DCAP, int XCAP>
+__device__ FrameView frame_view(const LatticeDev& L, const Stage<ACAP, DCAP, XCAP>& s, int b,
+                                int f) {
+  const int Ns = L.Ns, T = L.T;
+  FrameView v;
+  if (s.staged) {
+    const int i = f - s.lo, a = s.fo[i];
+    v.dp = s.dp + i * (Ns + 1);
+    v.src = s.src + a;
+    v.lab = s.lab + a;
+    v.stride = 1;
+    v.w = s.w + a;
+    v.pc = XCAP > 0 ? s.pc + a : nullptr;
+    v.n1 = s.nn1[i];
+  } else {
+    const size_t fi = (size_t)b * T + f;
+    const long long a = L.off[fi];
+    v.dp = L.dptr + fi * (Ns + 1);
+    v.src = reinterpret_cast<const int*>(L.arcs + a);
+    v.lab = v.src + 2;
+    v.stride = 4;
+    v.w = L.w + a;
+    v.pc = L.pc + a;
+    v.n1 = L.nn[(size_t)b * (T + 1) + f + 1];
+  }
+  return v;
 }
 
 // Forward scores, final weights and totals; one workgroup per stream.
 __global__ __launch_bounds__(kLT) void k_lat_forward(LatticeDev L, GraphDev g0) {
+  __shared__ Stage<1024, 1024, 0> s;
+  __shared__ double s_al[2][kMaxStates];
   const int b = blockIdx.x, tid = threadIdx.x, Ns = L.Ns, T = L.T;
   const int len = L.len[b];
   const GraphDev g = L.graphs ? L.graphs[b] : g0;
   double* al = L.alpha + (size_t)b * (T + 1) * Ns;
-  if (tid < Ns) al[tid] = tid == 0 ? 0.0 : neg_inf();
-  if (tid == 0) L.nn[(size_t)b * (T + 1)] = 1;
-  __syncthreads();
-  for (int f = 0; f < len; ++f) {
-    const size_t fi = (size_t)b * T + f;
-    const int* p1 = L.nodes + ((size_t)(f + 1) * L.B + b) * Ns * 4;
-    const bool here = tid < Ns && p1[4 * tid] >= 0;
-    const int n1 = __syncthreads_count(here);
-    if (tid == 0) L.nn[(size_t)b * (T + 1) + f + 1] = n1;
-    if (tid < Ns) {
-      double v = neg_inf();
-      if (here) {
-        const int* dp = L.dptr + fi * (Ns + 1);
-        const long long o = L.off[fi];
-        v = arcs_logsum(L, al + (size_t)f * Ns, o + dp[tid], o + dp[tid + 1]);
+  if (tid < Ns) {
+    const double v = tid == 0 ? 0.0 : neg_inf();
+    s_al[0][tid] = v;
+    al[tid] = v;
+  }
+  int cur = 0;
+  for (int f0 = 0; f0 < len; f0 = s.hi) {
+    stage_frames(L, s, b, f0, false, len);
+    for (int f = s.lo; f < s.hi; ++f) {
+      const FrameView v = frame_view(L, s, b, f);
+      if (tid < Ns) {
+        double x = neg_inf();
+        if (tid < v.n1) {
+          const int k0 = v.dp[tid], k1 = v.dp[tid + 1];
+          // each arc's share of the destination's score (sampling, sequence scores)
+          double* pc = L.pc + s.a0 + (s.staged ? s.fo[f - s.lo] : L.off[(size_t)b * T + f] - s.a0);
+          if (k1 - k0 <= 8) {
+            // few arcs: their terms stay in registers, one exp each
+            double e[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+              e[i] = k0 + i < k1 ? s_al[cur][v.src[(k0 + i) * v.stride]] + (double)v.w[k0 + i]
+                                 : neg_inf();
+#pragma unroll
+            for (int i = 0; i < 8; ++i) x = fmax(x, e[i]);
+            if (x != neg_inf()) {
+              // the terms relative to the largest, in fp32 (relative error ~1e-7 per
+              // frame); the scores accumulate in fp64
+              float ef[8], sum = 0.f;
+#pragma unroll
+              for (int i = 0; i < 8; ++i) {
+                ef[i] = e[i] == neg_inf() ? 0.f : __expf((float)(e[i] - x));
+                sum += ef[i];
+              }
+              x += (double)__logf(sum);
+              const float inv = 1.f / sum;
+#pragma unroll
+              for (int i = 0; i < 8; ++i)
+                if (k0 + i < k1) pc[k0 + i] = (double)(ef[i] * inv);
+            }
+          } else {
+            for (int k = k0; k < k1; ++k)
+              x = fmax(x, s_al[cur][v.src[k * v.stride]] + (double)v.w[k]);
+            if (x != neg_inf()) {
+              double sum = 0.0;
+              for (int k = k0; k < k1; ++k)
+                sum += exp(s_al[cur][v.src[k * v.stride]] + (double)v.w[k] - x);
+              x += log(sum);
+              for (int k = k0; k < k1; ++k)
+                pc[k] = exp(s_al[cur][v.src[k * v.stride]] + (double)v.w[k] - x);
+            }
+          }
+        }
+        s_al[cur ^ 1][tid] = x;
+        al[(size_t)(f + 1) * Ns + tid] = x;
       }
-      al[(size_t)(f + 1) * Ns + tid] = v;
+      lds_barrier();  // the next frame reads s_al only
+      cur ^= 1;
     }
-    __syncthreads();
   }
   // final weights: the graph's, or 0 for every node if none of them is final
+  const int nl = L.nn[(size_t)b * (T + 1) + len];
   const int* pl = L.nodes + ((size_t)len * L.B + b) * Ns * 4;
-  const bool node = tid < Ns && pl[4 * tid] >= 0;
+  const bool node = tid < nl;
   const double fin = node ? (g.fin ? (double)g.fin[pl[4 * tid + 1]] : 0.0) : neg_inf();
   const int nfinal = __syncthreads_count(node && fin != neg_inf());
   if (tid < Ns) L.fw[(size_t)b * Ns + tid] = node ? (nfinal > 0 ? fin : 0.0) : neg_inf();
   __syncthreads();
   if (tid == 0) {
     const double* fw = L.fw + (size_t)b * Ns;
-    const double* a = al + (size_t)len * Ns;
     double m = neg_inf();
-    for (int j = 0; j < Ns; ++j) m = fmax(m, a[j] + fw[j]);
+    for (int j = 0; j < nl; ++j) m = fmax(m, s_al[cur][j] + fw[j]);
     double sum = 0.0;
     if (m != neg_inf())
-      for (int j = 0; j < Ns; ++j) sum += a[j] + fw[j] == neg_inf() ? 0.0 : exp(a[j] + fw[j] - m);
+      for (int j = 0; j < nl; ++j) {
+        const double x = s_al[cur][j] + fw[j];
+        if (x != neg_inf()) sum += exp(x - m);
+      }
     L.total[b] = m == neg_inf() ? m : m + log(sum);
     L.status[b] = nfinal > 0 ? 0 : 1;
   }
 }
 
-// Inversion pick among K items of log weight v(k): the first item whose running sum of
-// exp(v - max) exceeds u times the full sum; if rounding leaves none, the last item
+// Inversion pick among K items with nonnegative shares p(k): the first item whose
+// running sum exceeds u times the full sum; if rounding leaves none, the last item
 // with a nonzero share.
+template <class F>
+__device__ int pick_by_share(int K, double u, F p) {
+  double sum = 0.0;
+  for (int k = 0; k < K; ++k) sum += p(k);
+  const double target = u * sum;
+  double cum = 0.0;
+  int last = -1;
+  for (int k = 0; k < K; ++k) {
+    const double x = p(k);
+    if (x == 0.0) continue;
+    cum += x;
+    last = k;
+    if (cum > target) return k;
+  }
+  return last;
+}
+
+// The same with log weights v(k): shares exp(v - max v).
 template <class F>
 __device__ int pick_by_inversion(int K, double u, F v) {
   double m = neg_inf();
@@ -336,72 +506,122 @@ __device__ int pick_by_inversion(int K, double u, F v) {
   return last;
 }
 
-// One thread per (stream, path): the final node, then backwards the arc into the path's
-// node of each frame, picked by inversion with the path's uniforms.
-__global__ __launch_bounds__(64) void k_lat_sample(LatticeDev L, NBestDev N) {
-  const int b = blockIdx.y, p = blockIdx.x * 64 + threadIdx.x;
-  if (p >= N.n) return;
-  const int Ns = L.Ns, T = L.T, len = L.len[b];
-  const size_t pi = (size_t)b * N.n + p;
-  const double* up = N.u + pi * (T + 1);
-  int* pp = N.paths ? N.paths + pi * (T + 1) : nullptr;
+// One thread per path, kLT paths per workgroup (grid: path groups x streams): the final
+// node, then backwards the arc into the path's node of each frame, picked by inversion
+// with the path's uniforms (arc shares from the forward pass); the paths of a
+// workgroup walk the staged frames together.
+__global__ __launch_bounds__(kLT) void k_lat_sample(LatticeDev L, NBestDev N) {
+  __shared__ Stage<2048, 1024, 1> s;
+  const int b = blockIdx.y, tid = threadIdx.x;
+  const int Ns = L.Ns, T = L.T, len = L.len[b], n = N.n;
   const double* al = L.alpha + (size_t)b * (T + 1) * Ns;
   const double* fw = L.fw + (size_t)b * Ns;
   const int nl = L.nn[(size_t)b * (T + 1) + len];
-  int node = pick_by_inversion(nl, up[len],
+  {
+    const int p = blockIdx.x * kLT + tid;
+    const bool act = p < n;
+    const size_t pi = (size_t)b * n + (act ? p : 0);
+    const double* up = N.u + pi * (T + 1);
+    int* pp = act && N.paths ? N.paths + pi * (T + 1) : nullptr;
+    int* seq = N.seq + pi * T;
+    int node = -1, nt = 0;
+    if (act) {
+      node = pick_by_inversion(nl, up[len],
                                [&](int j) { return al[(size_t)len * Ns + j] + fw[j]; });
-  if (pp) {
-    pp[len] = node;
-    for (int f = len + 1; f <= T; ++f) pp[f] = -1;
+      if (pp) {
+        pp[len] = node;
+        for (int f = len + 1; f <= T; ++f) pp[f] = -1;
+      }
+    }
+    // the uniforms of the next four frames are loaded ahead of their use
+    double q0 = 0.0, q1 = 0.0, q2 = 0.0, q3 = 0.0;
+    if (act) {
+      if (len - 1 >= 0) q0 = up[len - 1];
+      if (len - 2 >= 0) q1 = up[len - 2];
+      if (len - 3 >= 0) q2 = up[len - 3];
+      if (len - 4 >= 0) q3 = up[len - 4];
+    }
+    for (int f1 = len; f1 > 0; f1 = s.lo) {
+      stage_frames(L, s, b, f1, true, 0);
+      for (int f = s.hi - 1; f >= s.lo; --f) {
+        const double uf = q0;
+        q0 = q1;
+        q1 = q2;
+        q2 = q3;
+        q3 = act && f - 4 >= 0 ? up[f - 4] : 0.0;
+        if (!act || node < 0) continue;
+        const FrameView v = frame_view(L, s, b, f);
+        const int a0 = v.dp[node], K = v.dp[node + 1] - a0;
+        const int k = pick_by_share(K, uf, [&](int kk) { return v.pc[a0 + kk]; });
+        if (k < 0) {  // no arc with a nonzero share (not reached: every node has one)
+          node = -1;
+          continue;
+        }
+        if (pp) pp[f] = a0 + k;
+        const int lab = v.lab[(a0 + k) * v.stride];
+        if (lab > 0) seq[T - 1 - nt++] = lab;  // labels arrive last first
+        node = v.src[(a0 + k) * v.stride];
+      }
+    }
+    if (act) {
+      // move the sequence to the front in forward order and hash it (FNV-1a, 64-bit)
+      unsigned long long h = 1469598103934665603ull;
+      for (int k = 0; k < nt; ++k) {
+        const int y = seq[T - nt + k];
+        seq[k] = y;
+        h = (h ^ (unsigned)y) * 1099511628211ull;
+      }
+      N.ntok[pi] = nt;
+      N.hash[pi] = h ^ (unsigned long long)nt;
+    }
   }
-  int* seq = N.seq + pi * T;
-  int nt = 0;
-  for (int f = len - 1; f >= 0 && node >= 0; --f) {
-    const size_t fi = (size_t)b * T + f;
-    const int* dp = L.dptr + fi * (Ns + 1);
-    const long long a0 = L.off[fi] + dp[node];
-    const int K = dp[node + 1] - dp[node];
-    const double* af = al + (size_t)f * Ns;
-    const int k = pick_by_inversion(K, up[f], [&](int kk) {
-      return af[L.arcs[a0 + kk].x] + (double)L.w[a0 + kk];
-    });
-    if (k < 0) break;  // no arc with a nonzero share (not reached: every node has one)
-    const int4 x = L.arcs[a0 + k];
-    if (pp) pp[f] = dp[node] + k;
-    if (x.z > 0) seq[T - 1 - nt++] = x.z;  // labels arrive last first
-    node = x.x;
-  }
-  // move the sequence to the front in forward order and hash it (FNV-1a, 64-bit)
-  unsigned long long h = 1469598103934665603ull;
-  for (int k = 0; k < nt; ++k) {
-    const int y = seq[T - nt + k];
-    seq[k] = y;
-    h = (h ^ (unsigned)y) * 1099511628211ull;
-  }
-  N.ntok[pi] = nt;
-  N.hash[pi] = h ^ (unsigned long long)nt;
 }
 
 // Distinct sequences of each stream, in order of first occurrence.
+constexpr int kUniqStage = 2048;
+
 __global__ __launch_bounds__(kLT) void k_lat_unique(LatticeDev L, NBestDev N) {
   __shared__ int s_w[kLT / 64];
+  __shared__ unsigned long long s_h[kUniqStage];
+  __shared__ int s_n[kUniqStage];
   const int b = blockIdx.x, tid = threadIdx.x, n = N.n, T = L.T;
   const size_t b0 = (size_t)b * n;
+  const bool staged = n <= kUniqStage;
+  if (staged)
+    for (int p = tid; p < n; p += kLT) {
+      s_h[p] = N.hash[b0 + p];
+      s_n[p] = N.ntok[b0 + p];
+    }
+  __syncthreads();
+  const unsigned long long* hh = staged ? s_h : N.hash + b0;
+  const int* nn = staged ? s_n : N.ntok + b0;
   int base = 0;
   for (int p0 = 0; p0 < n; p0 += kLT) {
     const int p = p0 + tid;
     int is_first = 0;
     if (p < n) {
       is_first = 1;
-      const unsigned long long h = N.hash[b0 + p];
-      const int nt = N.ntok[b0 + p];
+      const unsigned long long h = hh[p];
+      const int nt = nn[p];
       const int* sp = N.seq + (b0 + p) * T;
       for (int q = 0; q < p && is_first; ++q) {
-        if (N.hash[b0 + q] != h || N.ntok[b0 + q] != nt) continue;
+        if (hh[q] != h || nn[q] != nt) continue;
         const int* sq = N.seq + (b0 + q) * T;
+        // compare 16 labels per step (independent loads in flight together)
+        bool eq = true;
         int k = 0;
-        while (k < nt && sq[k] == sp[k]) ++k;
-        if (k == nt) is_first = 0;
+        for (; eq && k + 16 <= nt; k += 16) {
+          int x[16], y[16];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            x[i] = sq[k + i];
+            y[i] = sp[k + i];
+          }
+#pragma unroll
+          for (int i = 0; i < 16; ++i) eq = eq && x[i] == y[i];
+        }
+        for (; eq && k < nt; ++k) eq = sq[k] == sp[k];
+        if (eq) is_first = 0;
       }
     }
     int tot;
@@ -415,77 +635,146 @@ __global__ __launch_bounds__(kLT) void k_lat_unique(LatticeDev L, NBestDev N) {
 // Total probability of each distinct sequence y: the lattice composed with the linear
 // acceptor of y (blanks as epsilon), summed over paths.  State (node, k): k labels of y
 // consumed; at frame f only k in [max(0, |y| - (len - f)), min(f, |y|)] can reach the
-// end, and the DP keeps that band.  One workgroup per (stream, sequence), grid-strided.
+// end, and the DP keeps that band.  The DP runs on ratios to the forward scores,
+// R_f(j, k) = A_f(j, k) / exp(alpha_f(j)) in [0, 1], so that one frame is
+// R_{f+1}(j, k) = sum over arcs a into j of R_f(src, k') * share(a), with the arc
+// shares of the forward pass (no exp or log per arc); each frame is rescaled by its
+// largest ratio, whose log is accumulated.  One wave per sequence; the four waves of a
+// workgroup take four sequences of one stream and walk its staged frames together
+// (grid: sequence groups x streams, grid-strided over the groups).
+constexpr int kYStage = 512;
+constexpr int kSeqWaves = kLT / 64;
+
+__device__ __forceinline__ double wave_max_f64(double x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmax(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+// DP buffers: per wave kSeqLds doubles of LDS (small enough for three workgroups per
+// compute unit), used when the sequence's band fits
+// (2 * Ns * band width); otherwise the wave's slice of the global scratch.
+constexpr int kSeqLds = 768;
+
 __global__ __launch_bounds__(kLT) void k_lat_seqscore(LatticeDev L, NBestDev N) {
-  extern __shared__ double dyn[];
-  const int tid = threadIdx.x, Ns = L.Ns, T = L.T, n = N.n;
-  const int W = N.dp_stride;  // band width capacity
-  double* A0 = N.dp ? N.dp + (size_t)blockIdx.x * 2 * Ns * W : dyn;
-  double* A1 = A0 + (size_t)Ns * W;
-  for (long long item = blockIdx.x; item < (long long)L.B * n; item += gridDim.x) {
-    const int b = (int)(item / n), u = (int)(item - (long long)b * n);
-    if (u >= N.nuniq[b]) continue;  // uniform over the workgroup
-    const int len = L.len[b];
-    const size_t pi = (size_t)b * n + N.first[(size_t)b * n + u];
-    const int Ly = N.ntok[pi];
-    const int* y = N.seq + pi * T;
-    double* cur = A0;
-    double* nxt = A1;
-    // frame 0: the initial node with nothing consumed (band [lo, hi] = [max(0, Ly - len), 0])
-    int lo = Ly - len > 0 ? Ly - len : 0, hi = 0;
-    if (tid == 0) cur[0] = lo == 0 ? 0.0 : neg_inf();
-    __syncthreads();
-    for (int f = 0; f < len; ++f) {
-      const int lo1 = Ly - (len - f - 1) > 0 ? Ly - (len - f - 1) : 0;
-      const int hi1 = f + 1 < Ly ? f + 1 : Ly;
-      const int w1 = hi1 - lo1 + 1;
-      const size_t fi = (size_t)b * T + f;
-      const int* dp = L.dptr + fi * (Ns + 1);
-      const long long o = L.off[fi];
-      const int n1 = L.nn[(size_t)b * (T + 1) + f + 1];
-      for (int q = tid; q < n1 * w1; q += kLT) {
-        const int j = q / w1, k = lo1 + (q - j * w1);
-        const long long a0 = o + dp[j], a1 = o + dp[j + 1];
-        double m = neg_inf();
-        for (int pass = 0; pass < 2; ++pass) {
-          double sum = 0.0;
-          for (long long a = a0; a < a1; ++a) {
-            const int4 x = L.arcs[a];
-            const int kk = x.z == 0 ? k : (k >= 1 && y[k - 1] == x.z ? k - 1 : -1);
-            if (kk < lo || kk > hi) continue;
-            const double v = cur[(size_t)x.x * W + (kk - lo)] + (double)L.w[a];
-            if (pass == 0)
-              m = fmax(m, v);
-            else if (v != neg_inf())
-              sum += exp(v - m);
-          }
-          if (pass == 0 && m == neg_inf()) break;
-          if (pass == 1) m = m + log(sum);
-        }
-        nxt[(size_t)j * W + (k - lo1)] = m;
-      }
-      __syncthreads();
-      double* t = cur;
-      cur = nxt;
-      nxt = t;
-      lo = lo1;
-      hi = hi1;
+  __shared__ Stage<512, 512, 1> s;
+  __shared__ int s_y[kSeqWaves][kYStage];
+  __shared__ double s_dp[kSeqWaves][kSeqLds];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int Ns = L.Ns, T = L.T, n = N.n, b = blockIdx.y;
+  const size_t blk = (size_t)blockIdx.y * gridDim.x + blockIdx.x;
+  double* gdp = N.dp ? N.dp + (blk * kSeqWaves + wv) * 2 * (size_t)Ns * N.dp_stride : nullptr;
+  const int len = L.len[b], nu = N.nuniq[b];
+  const double* fw = L.fw + (size_t)b * Ns;
+  const double* al_len = L.alpha + ((size_t)b * (T + 1) + len) * Ns;
+  const int nl = L.nn[(size_t)b * (T + 1) + len];
+  for (int u0 = blockIdx.x * kSeqWaves; u0 < nu; u0 += gridDim.x * kSeqWaves) {
+    const int u = u0 + wv;
+    const bool act = u < nu;
+    int Ly = 0;
+    const int* y = s_y[wv];
+    // band width of this sequence: min(|y|, len - |y|) + 1
+    int W = 1;
+    bool in_lds = true;
+    double* A0 = s_dp[wv];
+    if (act) {
+      const size_t pi = (size_t)b * n + N.first[(size_t)b * n + u];
+      Ly = N.ntok[pi];
+      const int* yg = N.seq + pi * T;
+      if (Ly <= kYStage)
+        for (int k = lane; k < Ly; k += 64) s_y[wv][k] = yg[k];
+      else
+        y = yg;
+      W = (Ly < len - Ly ? Ly : len - Ly) + 1;
+      in_lds = 2 * Ns * W <= kSeqLds;
+      if (!in_lds) A0 = gdp;  // the host allots it whenever a band may not fit
+      if (lane == 0) A0[0] = 1.0;  // frame 0: the initial node, nothing consumed
     }
-    if (tid == 0) {
-      // band at the last frame is [Ly, Ly]
-      const double* fw = L.fw + (size_t)b * Ns;
-      const int nl = L.nn[(size_t)b * (T + 1) + len];
+    double* cur = A0;
+    double* nxt = A0 + (size_t)Ns * W;
+    double logscale = 0.0;
+    int lo = 0, hi = 0;
+    for (int f0 = 0; f0 < len; f0 = s.hi) {
+      stage_frames(L, s, b, f0, false, len);  // also orders the writes above
+      for (int f = s.lo; f < s.hi; ++f) {
+        if (act) {
+          const int lo1 = Ly - (len - f - 1) > 0 ? Ly - (len - f - 1) : 0;
+          const int hi1 = f + 1 < Ly ? f + 1 : Ly;
+          const int w1 = hi1 - lo1 + 1;
+          const FrameView v = frame_view(L, s, b, f);
+          double mx = 0.0;
+          for (int q = lane; q < v.n1 * w1; q += 64) {
+            const int j = q / w1, k = lo1 + (q - j * w1);
+            const int a0 = v.dp[j], a1 = v.dp[j + 1];
+            const int yk = k >= 1 ? y[k - 1] : -1;
+            double r = 0.0;
+            if (a1 - a0 <= 8) {
+              // few arcs: all their loads in flight together
+              int sr[8], lb[8];
+              double pcv[8];
+#pragma unroll
+              for (int i = 0; i < 8; ++i) {
+                const bool in = a0 + i < a1;
+                sr[i] = in ? v.src[(a0 + i) * v.stride] : 0;
+                lb[i] = in ? v.lab[(a0 + i) * v.stride] : -2;
+                pcv[i] = in ? v.pc[a0 + i] : 0.0;
+              }
+#pragma unroll
+              for (int i = 0; i < 8; ++i) {
+                const int kk = lb[i] == 0 ? k : (lb[i] == yk ? k - 1 : -1);
+                if (kk >= lo && kk <= hi) r += cur[(size_t)sr[i] * W + (kk - lo)] * pcv[i];
+              }
+            } else {
+              for (int a = a0; a < a1; ++a) {
+                const int lab = v.lab[a * v.stride];
+                const int kk = lab == 0 ? k : (lab == yk ? k - 1 : -1);
+                if (kk < lo || kk > hi) continue;
+                r += cur[(size_t)v.src[a * v.stride] * W + (kk - lo)] * v.pc[a];
+              }
+            }
+            nxt[(size_t)j * W + (k - lo1)] = r;
+            mx = fmax(mx, r);
+          }
+          // every 8 frames, rescale by the largest ratio (no underflow on long streams)
+          if ((f & 7) == 7) {
+            mx = wave_max_f64(mx);
+            if (mx > 0.0) {
+              const double inv = 1.0 / mx;
+              for (int q = lane; q < v.n1 * w1; q += 64) {
+                const int j = q / w1, k = lo1 + (q - j * w1);
+                nxt[(size_t)j * W + (k - lo1)] *= inv;
+              }
+              logscale += log(mx);
+            }
+          }
+          lo = lo1;
+          hi = hi1;
+          double* t = cur;
+          cur = nxt;
+          nxt = t;
+        }
+        // the wave's next frame reads what its lanes wrote for this one: a wave's
+        // memory operations are performed in order, so a wavefront-scope fence
+        // (ordering only) suffices, for LDS and global buffers alike
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
+    if (act && lane == 0) {
+      // band at the last frame is [Ly, Ly]: log sum_j R(j, Ly) exp(alpha(j) + final(j))
       double m = neg_inf();
-      for (int j = 0; j < nl; ++j) m = fmax(m, cur[(size_t)j * W] + fw[j]);
+      for (int j = 0; j < nl; ++j)
+        if (cur[(size_t)j * W] > 0.0) m = fmax(m, log(cur[(size_t)j * W]) + al_len[j] + fw[j]);
       double sum = 0.0;
       if (m != neg_inf())
-        for (int j = 0; j < nl; ++j) {
-          const double v = cur[(size_t)j * W] + fw[j];
-          if (v != neg_inf()) sum += exp(v - m);
-        }
-      N.score[(size_t)b * n + u] = m == neg_inf() ? m : m + log(sum);
+        for (int j = 0; j < nl; ++j)
+          if (cur[(size_t)j * W] > 0.0) {
+            const double x = log(cur[(size_t)j * W]) + al_len[j] + fw[j];
+            if (x != neg_inf()) sum += exp(x - m);
+          }
+      N.score[(size_t)b * n + u] = m == neg_inf() ? m : m + log(sum) + logscale;
     }
-    __syncthreads();
+    __syncthreads();  // s_y and the DP buffers are reused by the next group
   }
 }
 
@@ -561,17 +850,13 @@ hipError_t launch_nbest(const LatticeDev& L, const NBestDev& N, int* out_tokens,
                         double* out_scores, int* out_nuniq, double* out_uscores,
                         int* out_ufirst, int dp_grid, size_t dp_lds, hipStream_t st) {
   if (L.B == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_lat_sample, dim3((N.n + 63) / 64, L.B), dim3(64), 0, st, L, N);
+  hipLaunchKernelGGL(k_lat_sample, dim3((N.n + kLT - 1) / kLT, L.B), dim3(kLT), 0, st, L, N);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_lat_unique, dim3(L.B), dim3(kLT), 0, st, L, N);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (dp_lds > 0) {
-    e = hipFuncSetAttribute((const void*)k_lat_seqscore,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)dp_lds);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(k_lat_seqscore, dim3(dp_grid), dim3(kLT), dp_lds, st, L, N);
+  (void)dp_lds;
+  hipLaunchKernelGGL(k_lat_seqscore, dim3(dp_grid, L.B), dim3(kLT), 0, st, L, N);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(k_lat_best, dim3(L.B), dim3(kLT), 0, st, L, N, out_tokens, out_ntok,
                      out_scores, out_nuniq, out_uscores, out_ufirst);
