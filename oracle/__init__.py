@@ -17,6 +17,12 @@ best label sequence are pinned against exhaustive enumeration of alignments; pat
 sampling against the exact path posteriors of small lattices.  Which expansions a pruned
 lattice keeps (every arc into a surviving tuple) is this implementation's reading and is
 pinned by invariants only.
+
+Full-sequence beam search (Table 5's comparison search): with a beam wide enough to keep
+every sequence it is pinned against exhaustive enumeration (max merge: the best path;
+log-add merge: the sequence with the highest total probability); with one hypothesis
+against per-frame argmax greedy search; pruned, against an independent Python
+implementation over tuples.
 """
 from __future__ import annotations
 
@@ -63,6 +69,9 @@ def _load():
         lib.oracle_rescore.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I,
                                        _P, _P, _P, _P, _P, _P]
         lib.oracle_rescore.restype = _I
+        lib.oracle_hyps.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I]
+                                    + [_P] * 5)
+        lib.oracle_hyps.restype = _I
         lib.oracle_lattice.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I,
                                         _I, _I, _P, _P, _P, _P, _P, _D, _I, _I, _I, _P])
         lib.oracle_lattice.restype = _P
@@ -294,3 +303,32 @@ def lattice(model, graph, encoder_out: np.ndarray, lengths: np.ndarray, beam: fl
                            _ptr(rp), _ptr(dest), _ptr(lab), _ptr(q), _ptr(fin), beam_v,
                            int(max_states), int(max_contexts), int(nthreads), _ptr(fm))
     return Lattice(h, B, T, fm, list(range(B)) if streams is None else list(streams))
+
+
+def hyp_search(model, encoder_out: np.ndarray, lengths: np.ndarray, beam_size: int,
+               logadd: bool, bf16: bool = False, nthreads: int = 0, streams=None):
+    """Full-sequence beam search (Table 5's comparison search); see tbs_oracle.cpp.
+    Returns an OracleResult with trace [T+1, B, N, 2] (parent rank, label)."""
+    lib = _load()
+    enc = _f32(encoder_out)
+    lens = _i32(lengths)
+    if streams is not None:
+        idx = np.asarray(streams, dtype=np.int64)
+        enc = np.ascontiguousarray(enc[idx])
+        lens = np.ascontiguousarray(lens[idx])
+    B, T, C = enc.shape
+    N = int(beam_size)
+    if N < 1:
+        raise ValueError("beam_size must be >= 1")
+    E, conv, W = _f32(model.embed), _f32(model.conv), _f32(model.w_out)
+    bias = None if model.b_out is None else _f32(model.b_out)
+    tokens = np.empty((B, T), dtype=np.int32)
+    ntok = np.empty(B, dtype=np.int32)
+    scores = np.empty(B, dtype=np.float64)
+    trace = np.empty((T + 1, B, N, 2), dtype=np.int32)
+    fm = np.empty((B, T + 1), dtype=np.float64)
+    lib.oracle_hyps(B, T, C, model.vocab_size, _ptr(enc), _ptr(lens), _ptr(E), _ptr(conv),
+                    _ptr(W), _ptr(bias), int(bf16), N, int(bool(logadd)), int(nthreads),
+                    _ptr(tokens), _ptr(ntok), _ptr(scores), _ptr(trace), _ptr(fm))
+    return OracleResult(tokens, ntok, scores, np.zeros(B, dtype=np.int32), None, trace,
+                        fm.min(axis=1), fm)

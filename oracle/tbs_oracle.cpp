@@ -452,6 +452,94 @@ struct Decoded {
   std::vector<Lattice> lat;
 };
 
+// Beam search over full label sequences, the comparison search of Table 5 ("beam
+// search", max-symbols 1; Sec. 2.2 footnote: the state space is the whole sequence
+// y).  A hypothesis is a distinct blank-free sequence with a score.  On each frame
+// every hypothesis expands to blank (y kept) and to every label a (y + a), with
+// weight log P(label | last two labels of y, t) and no blank factor (as R5); equal
+// sequences merge by max or by log-add (Table 3's two merge operations); the N best
+// by (score desc, first candidate index asc) are kept, in that order.  A candidate's
+// index is hyp_rank * V + label (blank = 0).  The result is the first hypothesis.
+struct HypOut {
+  std::vector<int> tokens;
+  double score = 0.0;
+  std::vector<double> frame_margin;  // per frame: gap at the N-best cut (+inf if none)
+  double final_margin = std::numeric_limits<double>::infinity();
+};
+
+void hyp_stream(const Model& m, const float* enc, int len, int N, bool logadd, HypOut& out,
+                int* trace, int trace_stride_frame) {
+  const int V = m.V, C = m.C;
+  struct Hyp {
+    std::vector<int> y;
+    double score;
+  };
+  std::vector<Hyp> H{Hyp{{}, 0.0}};
+  if (trace) {
+    trace[0] = -1;
+    trace[1] = -1;
+  }
+  out.frame_margin.assign(len, std::numeric_limits<double>::infinity());
+  std::vector<double> lp(V);
+  for (int t = 0; t < len; ++t) {
+    struct Group {
+      double score;
+      int first;             // smallest candidate index of the group
+      int rep;               // candidate index of the best member (ties: smaller index)
+      double rep_score;
+      int parent, label;
+    };
+    std::map<std::vector<int>, Group> groups;
+    for (int i = 0; i < (int)H.size(); ++i) {
+      const std::vector<int>& y = H[i].y;
+      const int a = y.size() >= 2 ? y[y.size() - 2] : 0;
+      const int b = y.size() >= 1 ? y[y.size() - 1] : 0;
+      joiner_logp(m, enc + (size_t)t * C, a, b, lp.data());
+      for (int c = 0; c < V; ++c) {
+        std::vector<int> z = y;
+        if (c > 0) z.push_back(c);
+        const double sc = H[i].score + lp[c];
+        const int idx = i * V + c;
+        auto it = groups.find(z);
+        if (it == groups.end()) {
+          groups.emplace(std::move(z), Group{sc, idx, idx, sc, i, c});
+          continue;
+        }
+        Group& g = it->second;
+        g.score = logadd ? log_add(g.score, sc) : std::max(g.score, sc);
+        if (sc > g.rep_score) {  // candidates arrive in index order: ties keep the first
+          g.rep = idx;
+          g.rep_score = sc;
+          g.parent = i;
+          g.label = c;
+        }
+        g.first = std::min(g.first, idx);
+      }
+    }
+    std::vector<std::pair<const std::vector<int>*, const Group*>> order;
+    for (auto& kv : groups) order.push_back({&kv.first, &kv.second});
+    std::sort(order.begin(), order.end(), [](const auto& x, const auto& y) {
+      if (x.second->score != y.second->score) return x.second->score > y.second->score;
+      return x.second->first < y.second->first;
+    });
+    if ((int)order.size() > N)
+      out.frame_margin[t] = order[N - 1].second->score - order[N].second->score;
+    std::vector<Hyp> nH;
+    for (int k = 0; k < (int)order.size() && k < N; ++k) {
+      nH.push_back(Hyp{*order[k].first, order[k].second->score});
+      if (trace) {
+        int* p = trace + (size_t)(t + 1) * trace_stride_frame + 2 * k;
+        p[0] = order[k].second->parent;
+        p[1] = order[k].second->label;
+      }
+    }
+    H.swap(nH);
+  }
+  out.tokens = H[0].y;
+  out.score = H[0].score;
+  if (H.size() > 1) out.final_margin = H[0].score - H[1].score;
+}
+
 }  // namespace
 
 extern "C" {
@@ -698,6 +786,48 @@ int oracle_lattice_nbest(void* h, int b, int n, const double* u, int* paths, dou
 // Total probability (log) of label sequence y [n] in stream b's lattice.
 double oracle_lattice_seqscore(void* h, int b, const int* y, int n) {
   return lattice_sequence_score(static_cast<Decoded*>(h)->lat[b], y, n);
+}
+
+
+// Full-sequence beam search (see hyp_stream) over a batch: tokens [B][T] (-1 padded),
+// ntok [B], scores [B]; trace [T+1][B][N][2] or null: per frame the kept hypotheses'
+// (parent rank, label), -1 padded; frame_margins [B][T+1] or null (entry T: the gap
+// between the best two final hypotheses).
+int oracle_hyps(int B, int T, int C, int V, const float* enc, const int* lengths,
+                const float* E, const float* conv, const float* W, const float* bias, int bf16,
+                int N, int logadd, int nthreads, int* tokens, int* ntok, double* scores,
+                int* trace, double* frame_margins) {
+  Model m{V, C, E, conv, W, bias, bf16};
+  for (size_t i = 0; i < (size_t)B * T; ++i) tokens[i] = -1;
+  if (trace)
+    for (size_t i = 0; i < (size_t)(T + 1) * B * N * 2; ++i) trace[i] = -1;
+  std::atomic<int> next{0};
+  auto work = [&]() {
+    for (;;) {
+      int b = next.fetch_add(1);
+      if (b >= B) break;
+      HypOut o;
+      hyp_stream(m, enc + (size_t)b * T * C, lengths[b], N, logadd != 0, o,
+                 trace ? trace + (size_t)b * N * 2 : nullptr, B * N * 2);
+      for (size_t k = 0; k < o.tokens.size(); ++k) tokens[(size_t)b * T + k] = o.tokens[k];
+      ntok[b] = (int)o.tokens.size();
+      scores[b] = o.score;
+      if (frame_margins) {
+        double* fm = frame_margins + (size_t)b * (T + 1);
+        for (int t = 0; t <= T; ++t) fm[t] = std::numeric_limits<double>::infinity();
+        for (int t = 0; t < lengths[b]; ++t) fm[t] = o.frame_margin[t];
+        fm[T] = o.final_margin;
+      }
+    }
+  };
+  int nt = nthreads > 0 ? nthreads : (int)std::thread::hardware_concurrency();
+  if (nt < 1) nt = 1;
+  if (nt > B) nt = B > 0 ? B : 1;
+  std::vector<std::thread> pool;
+  for (int i = 1; i < nt; ++i) pool.emplace_back(work);
+  work();
+  for (auto& th : pool) th.join();
+  return 0;
 }
 
 }  // extern "C"

@@ -258,3 +258,30 @@ def sequence_totals(joiner, graph, enc, length):
         terms.setdefault(y, []).append(score + (f if any_final else 0.0))
     totals = {y: _logsumexp(v) for y, v in terms.items()}
     return totals, _logsumexp([v for vs in terms.values() for v in vs])
+
+
+def hyp_beam_search(joiner, enc, length, beam_size, logadd):
+    """Full-sequence beam search with max-symbols 1 over tuples of labels (Table 5's
+    comparison search), written independently of the oracle: expand every hypothesis by
+    blank and every label, merge equal tuples (max or log-add), keep the best
+    ``beam_size`` by (score desc, first candidate index asc).  Returns (tokens, score)."""
+    V = joiner.V
+    hyps = [((), 0.0)]
+    for t in range(length):
+        groups = {}
+        for i, (y, sc) in enumerate(hyps):
+            a = y[-2] if len(y) >= 2 else 0
+            b = y[-1] if len(y) >= 1 else 0
+            p = joiner(enc[t], a, b)
+            for c in range(V):
+                z = y + (c,) if c else y
+                v = sc + float(p[c])
+                idx = i * V + c
+                if z in groups:
+                    old, first = groups[z]
+                    groups[z] = (_logsumexp([old, v]) if logadd else max(old, v), min(first, idx))
+                else:
+                    groups[z] = (v, idx)
+        ranked = sorted(groups.items(), key=lambda kv: (-kv[1][0], kv[1][1]))
+        hyps = [(z, v) for z, (v, _) in ranked[:beam_size]]
+    return list(hyps[0][0]), hyps[0][1]
