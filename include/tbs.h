@@ -303,6 +303,37 @@ tbs_status tbs_lattice_nbest(tbs_lattice *lattice, int32_t num_paths, const doub
 void tbs_lattice_destroy(tbs_lattice *lattice);
 
 /*
+ * Full-sequence beam search with max-symbols 1: the comparison search of Table 5
+ * ("beam search"), whose hypotheses are whole label sequences (footnote to Sec. 2.2)
+ * instead of (context, graph state) tuples; no decoding graph.  On each frame every
+ * hypothesis y expands to blank (y kept) and to every label c (y + c), weighted by
+ * log P(label | last two labels of y, frame) with no blank factor; equal sequences
+ * merge by max or by log-add (Table 3); the beam_size best by (score desc, first
+ * candidate index asc) are kept, where candidate (i, c) of the i-th hypothesis has
+ * index i * vocab_size + c (blank c = 0).  The result is the best hypothesis after
+ * each stream's last frame.
+ *   beam_size  in [1, 16] (TBS_ECAPACITY above); merge TBS_MERGE_MAX or TBS_MERGE_LOGADD.
+ *   encoder_out, lengths, B, T, out_tokens, out_num_tokens, out_scores as tbs_decode
+ *   (out_scores: the hypothesis score, fp64).
+ *   trace  DEVICE int32 [T+1][B][beam_size][2] or NULL: per frame f >= 1 the kept
+ *          hypotheses' (rank of the parent on frame f-1, label; 0 = blank), -1 padded.
+ * Sequences are identified by 64-bit hashes (of y and of y without its last label)
+ * plus their length; two distinct sequences with equal hashes would be merged.  The
+ * workspace is cached in the model; calls on a model are serialised.
+ */
+typedef enum { TBS_MERGE_MAX = 0, TBS_MERGE_LOGADD = 1 } tbs_merge_op;
+
+typedef struct {
+  int32_t beam_size;
+  int32_t merge;  /* tbs_merge_op */
+} tbs_hyp_params;
+
+tbs_status tbs_hyp_search(const tbs_model *model, const tbs_hyp_params *params,
+                          const float *encoder_out, const int32_t *lengths, int32_t B, int32_t T,
+                          int32_t *out_tokens, int32_t *out_num_tokens, double *out_scores,
+                          int32_t *trace, void *hip_stream);
+
+/*
  * How tbs_decode drives the frame loop of Algorithm 1 (all schedules compute
  * the same search; results agree within the fp32 rounding of the joiner):
  *   TBS_SCHEDULE_FRAME   two kernels per frame over the whole batch: a joiner

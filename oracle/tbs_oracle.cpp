@@ -463,7 +463,9 @@ struct Decoded {
 struct HypOut {
   std::vector<int> tokens;
   double score = 0.0;
-  std::vector<double> frame_margin;  // per frame: gap at the N-best cut (+inf if none)
+  std::vector<double> frame_margin;  // per frame: smallest gap between neighbouring ranks up
+                                     // to the N-best cut, or between the two best members
+                                     // of a kept merged sequence
   double final_margin = std::numeric_limits<double>::infinity();
 };
 
@@ -488,6 +490,7 @@ void hyp_stream(const Model& m, const float* enc, int len, int N, bool logadd, H
       int rep;               // candidate index of the best member (ties: smaller index)
       double rep_score;
       int parent, label;
+      double second;         // best score among the other members (-inf: none)
     };
     std::map<std::vector<int>, Group> groups;
     for (int i = 0; i < (int)H.size(); ++i) {
@@ -502,16 +505,19 @@ void hyp_stream(const Model& m, const float* enc, int len, int N, bool logadd, H
         const int idx = i * V + c;
         auto it = groups.find(z);
         if (it == groups.end()) {
-          groups.emplace(std::move(z), Group{sc, idx, idx, sc, i, c});
+          groups.emplace(std::move(z), Group{sc, idx, idx, sc, i, c, kNegInf});
           continue;
         }
         Group& g = it->second;
         g.score = logadd ? log_add(g.score, sc) : std::max(g.score, sc);
         if (sc > g.rep_score) {  // candidates arrive in index order: ties keep the first
+          g.second = g.rep_score;
           g.rep = idx;
           g.rep_score = sc;
           g.parent = i;
           g.label = c;
+        } else {
+          g.second = std::max(g.second, sc);
         }
         g.first = std::min(g.first, idx);
       }
@@ -522,10 +528,17 @@ void hyp_stream(const Model& m, const float* enc, int len, int N, bool logadd, H
       if (x.second->score != y.second->score) return x.second->score > y.second->score;
       return x.second->first < y.second->first;
     });
-    if ((int)order.size() > N)
-      out.frame_margin[t] = order[N - 1].second->score - order[N].second->score;
+    // the kept hypotheses are stored in rank order, so every gap between neighbours up
+    // to the cut is a decision
+    for (int k = 0; k + 1 < (int)order.size() && k < N; ++k)
+      out.frame_margin[t] = std::min(out.frame_margin[t],
+                                     order[k].second->score - order[k + 1].second->score);
     std::vector<Hyp> nH;
     for (int k = 0; k < (int)order.size() && k < N; ++k) {
+      // the back-pointer of a merged sequence is its best member: a decision too
+      const Group& g = *order[k].second;
+      if (g.second != kNegInf)
+        out.frame_margin[t] = std::min(out.frame_margin[t], g.rep_score - g.second);
       nH.push_back(Hyp{*order[k].first, order[k].second->score});
       if (trace) {
         int* p = trace + (size_t)(t + 1) * trace_stride_frame + 2 * k;

@@ -91,6 +91,47 @@ struct Workspace {
   }
 };
 
+// Workspace of the full-sequence beam search (tbs_hyp_search), cached in the model.
+struct HypWork {
+  int B = 0, T = 0, N = 0;
+  int* len = nullptr;
+  unsigned long long* hash[2] = {nullptr, nullptr};
+  unsigned long long* phash[2] = {nullptr, nullptr};
+  int* n[2] = {nullptr, nullptr};
+  int* ctx[2] = {nullptr, nullptr};
+  double* score[2] = {nullptr, nullptr};
+  int* nh[2] = {nullptr, nullptr};
+  int* rowctx = nullptr;
+  int* hrow = nullptr;
+  int* hist = nullptr;
+  void* h = nullptr;
+  float* logits = nullptr;
+  float2* stats = nullptr;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+
+  void release() {
+    if (done && pending) (void)hipEventSynchronize(done);
+    for (int i = 0; i < 2; ++i) {
+      (void)hipFree(hash[i]);
+      (void)hipFree(phash[i]);
+      (void)hipFree(n[i]);
+      (void)hipFree(ctx[i]);
+      (void)hipFree(score[i]);
+      (void)hipFree(nh[i]);
+    }
+    (void)hipFree(len);
+    (void)hipFree(rowctx);
+    (void)hipFree(hrow);
+    (void)hipFree(hist);
+    (void)hipFree(h);
+    (void)hipFree(logits);
+    (void)hipFree(stats);
+    if (done) (void)hipEventDestroy(done);
+    *this = HypWork();
+  }
+};
+
 }  // namespace
 
 struct tbs_graph {
@@ -133,6 +174,7 @@ struct tbs_model {
   int schedule = TBS_SCHEDULE_AUTO;
   std::mutex mu;
   Workspace ws;
+  HypWork hw;
   // device work of every decode and chunk on this model is serialised on this event
   // (they share the exchange buffer and, for tbs_decode, the workspace)
   hipEvent_t busy = nullptr;
@@ -690,6 +732,7 @@ void tbs_model_destroy(tbs_model* m) {
     std::lock_guard<std::mutex> lk(m->mu);
     if (m->ws.done && m->ws.pending) hipEventSynchronize(m->ws.done);
     m->ws.release();
+    m->hw.release();
   }
   prof_drop(m);
   for (hipEvent_t e : m->prof_pool) hipEventDestroy(e);
@@ -1360,6 +1403,103 @@ void tbs_lattice_destroy(tbs_lattice* lat) {
     lat->release();
   }
   delete lat;
+}
+
+
+tbs_status tbs_hyp_search(const tbs_model* model, const tbs_hyp_params* params,
+                          const float* encoder_out, const int32_t* lengths, int32_t B, int32_t T,
+                          int32_t* out_tokens, int32_t* out_num_tokens, double* out_scores,
+                          int32_t* trace, void* hip_stream) {
+  if (!model || !params) return fail(TBS_EINVAL, "tbs_hyp_search: NULL model/params");
+  const int N = params->beam_size;
+  if (N < 1 || N > kMaxHyps)
+    return fail(N < 1 ? TBS_EINVAL : TBS_ECAPACITY,
+                "tbs_hyp_search: beam_size %d outside [1, %d]", N, kMaxHyps);
+  if (params->merge != TBS_MERGE_MAX && params->merge != TBS_MERGE_LOGADD)
+    return fail(TBS_EINVAL, "tbs_hyp_search: unknown merge %d", (int)params->merge);
+  if (B < 0 || T < 0) return fail(TBS_EINVAL, "tbs_hyp_search: B and T must be >= 0");
+  if (B == 0) return TBS_OK;
+  if (!lengths) return fail(TBS_EINVAL, "tbs_hyp_search: lengths is NULL");
+  int maxlen = 0;
+  for (int b = 0; b < B; ++b) {
+    if (lengths[b] < 0 || lengths[b] > T)
+      return fail(TBS_EINVAL, "tbs_hyp_search: lengths[%d] = %d outside [0, %d]", b, lengths[b],
+                  T);
+    if (lengths[b] > maxlen) maxlen = lengths[b];
+  }
+  if (maxlen > 0 && !encoder_out) return fail(TBS_EINVAL, "tbs_hyp_search: encoder_out is NULL");
+  if (!out_num_tokens || !out_scores || (T > 0 && !out_tokens))
+    return fail(TBS_EINVAL, "tbs_hyp_search: NULL output pointer");
+  tbs_model* m = const_cast<tbs_model*>(model);
+  std::lock_guard<std::mutex> lk(m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  HypWork& w = m->hw;
+  if (!(w.done && w.B >= B && w.T >= T && w.N == N)) {
+    w.release();
+    const size_t BN = (size_t)B * N;
+    const int nvt = m->Vpad / kJoinerBN;
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+      e = dalloc(&w.hash[i], BN);
+      if (e == hipSuccess) e = dalloc(&w.phash[i], BN);
+      if (e == hipSuccess) e = dalloc(&w.n[i], BN);
+      if (e == hipSuccess) e = dalloc(&w.ctx[i], BN);
+      if (e == hipSuccess) e = dalloc(&w.score[i], BN);
+      if (e == hipSuccess) e = dalloc(&w.nh[i], (size_t)B);
+    }
+    if (e == hipSuccess) e = dalloc(&w.len, (size_t)B);
+    if (e == hipSuccess) e = dalloc(&w.rowctx, BN);
+    if (e == hipSuccess) e = dalloc(&w.hrow, BN);
+    if (e == hipSuccess) e = dalloc(&w.hist, (size_t)T * BN);
+    if (e == hipSuccess) e = dalloc((char**)&w.h, BN * m->Kpad * (m->bf16 ? 2 : 4));
+    if (e == hipSuccess) e = dalloc(&w.logits, BN * m->Vpad);
+    if (e == hipSuccess) e = dalloc(&w.stats, BN * nvt);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&w.done, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      w.release();
+      return hip_fail(e, "tbs_hyp_search");
+    }
+    w.B = B;
+    w.T = T;
+    w.N = N;
+  }
+  HIP_TRY(model_wait(m, st), "hipStreamWaitEvent");
+  if (w.pending) HIP_TRY(hipStreamWaitEvent(st, w.done, 0), "hipStreamWaitEvent");
+  HIP_TRY(hipMemcpyAsync(w.len, lengths, (size_t)B * 4, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(lengths)");
+  HypDev d;
+  d.B = B;
+  d.T = T;
+  d.N = N;
+  d.merge_logadd = params->merge == TBS_MERGE_LOGADD;
+  d.len = w.len;
+  for (int i = 0; i < 2; ++i) {
+    d.hash[i] = w.hash[i];
+    d.phash[i] = w.phash[i];
+    d.n[i] = w.n[i];
+    d.ctx[i] = w.ctx[i];
+    d.score[i] = w.score[i];
+    d.nh[i] = w.nh[i];
+  }
+  d.rowctx = w.rowctx;
+  d.hrow = w.hrow;
+  d.hist = w.hist;
+  const ModelDev md = model_dev(m);
+  if (trace)
+    HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * N * 2, -1, st), "fill(trace)");
+  HIP_TRY(launch_hyp_init(d, trace, st), "launch(hyp init)");
+  for (int t = 0; t < maxlen; ++t) {
+    HIP_TRY(launch_hyp_rows(d, t, st), "launch(hyp rows)");
+    HIP_TRY(launch_joiner_dense(md, encoder_out + (size_t)t * m->C, (long long)T * m->C,
+                                w.rowctx, 0, N, B * N, w.h, w.logits, w.stats, m->ncu, st),
+            "launch(joiner)");
+    HIP_TRY(launch_hyp_step(md, d, t, w.logits, w.stats, trace, st), "launch(hyp step)");
+  }
+  HIP_TRY(launch_hyp_final(d, out_tokens, out_num_tokens, out_scores, st), "launch(hyp final)");
+  HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
+  w.pending = true;
+  HIP_TRY(model_mark(m, st), "hipEventRecord");
+  return TBS_OK;
 }
 
 }  // extern "C"

@@ -22,6 +22,7 @@ constexpr int kStatStage = kHashSlots;  // softmax partials staged in LDS (in hk
 constexpr int kTopkStage = 2 * (kChunk + kMaxStates);  // trivial-graph label lists staged in LDS (in uk)
 constexpr size_t kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
 constexpr int kStreamMaxV = 512;     // per-stream kernel: vocabulary limit (8 logits per lane)
+constexpr int kMaxHyps = 16;         // full-sequence beam search: hypotheses per stream
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -185,9 +186,31 @@ hipError_t launch_nbest(const LatticeDev& L, const NBestDev& N, int* out_tokens,
                         int* out_ufirst, int dp_grid, size_t dp_lds, hipStream_t st);
 
 // joiner rows of a dense row table: row r of the batch is table row row0 + r, with
-// context ctx[row0 + r] (-1: no row, h = 0) and encoder row (row0 + r) / per_enc
-hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, const int* ctx, long long row0,
-                               int per_enc, int R, void* h, float* logits, float2* stats, int ncu,
-                               hipStream_t st);
+// context ctx[row0 + r] (-1: no row, h = 0) and encoder row
+// enc + ((row0 + r) / per_enc) * enc_stride
+hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, long long enc_stride,
+                               const int* ctx, long long row0, int per_enc, int R, void* h,
+                               float* logits, float2* stats, int ncu, hipStream_t st);
+
+// Full-sequence beam search (the comparison search of Table 5), frame schedule.
+struct HypDev {
+  int B, T, N, merge_logadd;
+  const int* len;                     // [B]
+  unsigned long long* hash[2];        // [B][N] per frame parity: hash of the sequence
+  unsigned long long* phash[2];       // hash of the sequence without its last label
+  int* n[2];                          // sequence length
+  int* ctx[2];                        // last two labels a * V + b
+  double* score[2];
+  int* nh[2];                         // [B] hypotheses
+  int* rowctx;                        // [B*N] joiner row contexts (-1: none)
+  int* hrow;                          // [B*N] joiner row of each hypothesis
+  int* hist;                          // [T][B][N] parent << 16 | label
+};
+hipError_t launch_hyp_init(const HypDev& d, int* trace, hipStream_t st);
+hipError_t launch_hyp_rows(const HypDev& d, int t, hipStream_t st);
+hipError_t launch_hyp_step(const ModelDev& m, const HypDev& d, int t, const float* logits,
+                           const float2* stats, int* trace, hipStream_t st);
+hipError_t launch_hyp_final(const HypDev& d, int* out_tokens, int* out_ntok, double* out_scores,
+                            hipStream_t st);
 
 }  // namespace tbs

@@ -278,10 +278,11 @@ __global__ __launch_bounds__(256) void k_h_rows(ModelDev m, const float* __restr
 
 // Rows of a dense (encoder row, context) table: batch row r is table row row0 + r,
 // with context ctx[row0 + r] (-1: an empty slot, written as zeros) and encoder row
-// (row0 + r) / per_enc.
+// enc + ((row0 + r) / per_enc) * enc_stride.
 __global__ __launch_bounds__(256) void k_h_rows_dense(ModelDev m, const float* __restrict__ enc,
                                                       const int* __restrict__ ctx, long long row0,
-                                                      int per_enc, void* __restrict__ h) {
+                                                      int per_enc, long long enc_stride,
+                                                      void* __restrict__ h) {
   __shared__ int2 off;
   const long long g = row0 + blockIdx.x;
   const int c = ctx[g];
@@ -301,7 +302,8 @@ __global__ __launch_bounds__(256) void k_h_rows_dense(ModelDev m, const float* _
     off = make_int2(a * m.Kpad, (c - a * m.V) * m.Kpad);
   }
   __syncthreads();
-  write_h_rows<256>(m, enc + (size_t)(g / per_enc) * m.C, 0, &off, 1, hrow, m.Kpad, threadIdx.x);
+  write_h_rows<256>(m, enc + (size_t)(g / per_enc) * enc_stride, 0, &off, 1, hrow, m.Kpad,
+                    threadIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -3022,11 +3024,12 @@ hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, 
   return hipGetLastError();
 }
 
-hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, const int* ctx, long long row0,
-                               int per_enc, int R, void* h, float* logits, float2* stats, int ncu,
-                               hipStream_t st) {
+hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, long long enc_stride,
+                               const int* ctx, long long row0, int per_enc, int R, void* h,
+                               float* logits, float2* stats, int ncu, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_h_rows_dense, dim3(R), dim3(256), 0, st, m, enc, ctx, row0, per_enc, h);
+  hipLaunchKernelGGL(k_h_rows_dense, dim3(R), dim3(256), 0, st, m, enc, ctx, row0, per_enc,
+                     enc_stride, h);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const JoinerPlan p = plan_joiner(R, m.Vpad, m.Kpad, m.bf16, ncu);

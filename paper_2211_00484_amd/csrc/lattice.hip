@@ -833,7 +833,7 @@ hipError_t launch_lattice_weights(const ModelDev& m, const LatticeDev& L, const 
   const long long row0 = (long long)b0 * L.T * L.Nc;
   const int R = (b1 - b0) * L.T * L.Nc;
   hipError_t e =
-      launch_joiner_dense(m, enc, L.rowctx, row0, L.Nc, R, h, logits, stats, ncu, st);
+      launch_joiner_dense(m, enc, m.C, L.rowctx, row0, L.Nc, R, h, logits, stats, ncu, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_lat_weights, dim3(L.T, b1 - b0), dim3(kLT), 0, st, L, g, logits, stats,
                      m.Vpad / kJoinerBN, m.Vpad, b0);

@@ -98,6 +98,9 @@ def lib():
     L.tbs_state_create_graphs.restype = _I32
     L.tbs_state_create_graphs.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _I32, _I32, _P,
                                           ctypes.POINTER(_P)]
+    L.tbs_hyp_search.restype = _I32
+    L.tbs_hyp_search.argtypes = [_P, ctypes.POINTER(HypParams), _P, _P, _I32, _I32, _P, _P, _P,
+                                 _P, _P]
     L.tbs_lattice_create.restype = _I32
     L.tbs_lattice_create.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32, _P,
                                      ctypes.POINTER(_P)]
@@ -470,3 +473,36 @@ class Lattice:
 
     def __del__(self):
         self.close()
+
+
+class HypParams(ctypes.Structure):
+    _fields_ = [("beam_size", _I32), ("merge", _I32)]
+
+
+MERGES = {"max": 0, "logadd": 1}
+
+
+def hyp_search(model: Model, encoder_out, lengths, beam_size: int = 4, merge: str = "logadd",
+               want_trace: bool = False, stream=None) -> DecodeOutput:
+    """Full-sequence beam search with max-symbols 1 (tbs_hyp_search, Table 5's comparison
+    search); outputs on the device; trace [T+1, B, beam_size, 2] (parent rank, label)."""
+    import torch
+    lens = np.ascontiguousarray(np.asarray(lengths), dtype=np.int32)
+    B, T = int(encoder_out.shape[0]), int(encoder_out.shape[1])
+    if encoder_out.dim() != 3 or encoder_out.shape[2] != model.dim:
+        raise ValueError("encoder_out must be [B, T, dim]")
+    if lens.shape != (B,):
+        raise ValueError("lengths must have shape [B]")
+    dev = encoder_out.device
+    i32 = dict(dtype=torch.int32, device=dev)
+    out = DecodeOutput(tokens=torch.empty((B, T), **i32), num_tokens=torch.empty(B, **i32),
+                       scores=torch.empty(B, dtype=torch.float64, device=dev), status=None,
+                       arcs=None,
+                       trace=torch.empty((T + 1, B, int(beam_size), 2), **i32) if want_trace
+                       else None)
+    params = HypParams(int(beam_size), MERGES[merge])
+    _check(lib().tbs_hyp_search(model._h, ctypes.byref(params),
+                                _dev_ptr(encoder_out.contiguous()), _host_ptr(lens), B, T,
+                                _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
+                                _dev_ptr(out.scores), _dev_ptr(out.trace), _stream_ptr(stream)))
+    return out

@@ -84,6 +84,9 @@ def test_decode_null_handles():
     assert L.tbs_state_create_graphs(None, None, ctypes.byref(p), 1, 1, None,
                                      ctypes.byref(h)) == EINVAL
     assert h.value is None
+    hp = tbs.HypParams(4, 1)
+    assert L.tbs_hyp_search(None, ctypes.byref(hp), None, None, 1, 1, None, None, None, None,
+                            None) == EINVAL
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
