@@ -276,6 +276,107 @@ def decode_roofline(prof, K, work, dtype):
     return kernels, roofline, schedule, j_tflops, s_gbps, peak_j
 
 
+def hyps_bench(args, w, inputs, model_np, model, graph, enc, dtype, K, W):
+    """One step: tbs_hyp_search over the whole batch (beam_size hypotheses, max-symbols 1),
+    with the FSA-based search of the same workload timed beside it."""
+    import torch
+    from paper_2211_00484_amd import tbs
+    N, merge = args.beam_size, args.merge
+    B, T = inputs.B, inputs.T
+    frames = int(inputs.lengths.sum())
+    run = lambda **kw: tbs.hyp_search(model, enc, inputs.lengths, beam_size=N, merge=merge, **kw)
+    # algorithmic work from the hypotheses' back-pointers of one untimed run: the joiner
+    # rows are the distinct contexts of each stream's hypotheses on each frame
+    tr = run(want_trace=True).trace.cpu().numpy()
+    V = w.V
+    rows = 0
+    for b in range(B):
+        ctx = [0]
+        for f in range(int(inputs.lengths[b])):
+            rows += len(set(ctx))
+            nxt = []
+            for k in range(N):
+                par, lab = tr[f + 1, b, k]
+                if par < 0:
+                    break
+                c = ctx[par]
+                nxt.append(c if lab == 0 else (c % V) * V + int(lab))
+            ctx = nxt
+    flop = 2.0 * w.C * V * rows
+    for _ in range(W):
+        run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        run()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    model.set_profiling(True)
+    for _ in range(K):
+        run()
+    torch.cuda.synchronize()
+    prof = model.read_profile()
+    model.set_profiling(False)
+    kernels = {n: {"launches_per_step": c / K, "avg_us": 1e3 * ms / max(c, 1),
+                   "ms_per_step": ms / K} for n, (c, ms) in prof.items() if c}
+    peak_j = PEAK["bf16_mfma_tflops"] if dtype == "bf16" else PEAK["fp32_mfma_tflops"]
+    j = kernels["joiner"]
+    j_tflops = flop / j["launches_per_step"] / (j["avg_us"] * 1e-6) / 1e12
+    # the step kernel reads each joiner row's logits and statistics once per selection
+    # round at most; algorithmic bytes: each row's logits and statistics once
+    st_bytes = rows * (w.V * 4 + ((w.V + 63) // 64) * 8)
+    sk = kernels["hyp_step"]
+    st_gbps = st_bytes / sk["launches_per_step"] / (sk["avg_us"] * 1e-6) / 1e9
+    if j["ms_per_step"] >= sk["ms_per_step"]:
+        roofline = {"kernel": "k_joiner", "bound": "mfma", "achieved": j_tflops, "peak": peak_j,
+                    "unit": "TFLOP/s", "frac": j_tflops / peak_j}
+    else:
+        roofline = {"kernel": "k_hyp_step", "bound": "hbm", "achieved": st_gbps,
+                    "peak": PEAK["hbm_gbps"], "unit": "GB/s", "frac": st_gbps / PEAK["hbm_gbps"]}
+    roofline["traffic"] = None
+    # the FSA-based search on the same inputs (the paper's comparison, Table 5)
+    out = tbs.allocate_outputs(B, T, w.max_states, status=True)
+    for _ in range(W):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(K):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+    value = frames * K / (t1 - t0)
+    fsa = frames * K / (t3 - t2)
+    line = {
+        "metric": METRIC + " (full-sequence beam search, the comparison search of Table 5)",
+        "value": value, "unit": "frames/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": (t1 - t0) * 1e3 / K, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if dtype == "fp32" else "bf16 joiner operands",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}+hyps{N}-{merge}", "description": w.description,
+                   "B": B, "T_max": T, "frames": frames, "beam_size": N, "merge": merge,
+                   "joiner": dtype},
+        "roofline": roofline,
+        "kernels": kernels,
+        "joiner_rows_per_step": rows,
+        "fsa_search_frames_per_s": fsa,
+        "fsa_speedup_over_hyps": fsa / value,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        t4 = time.perf_counter()
+        sample = list(range(min(B, 8)))
+        oracle.hyp_search(model_np, inputs.encoder_out, inputs.lengths, N, merge == "logadd",
+                          bf16=(dtype == "bf16"), nthreads=args.cpu_threads or os.cpu_count(),
+                          streams=sample)
+        dt = time.perf_counter() - t4
+        nf = int(inputs.lengths[sample].sum())
+        line["cpu_baseline"] = {"value": nf / dt, "unit": "frames/s",
+                                "cores": min(len(sample), args.cpu_threads or os.cpu_count()),
+                                "kind": "oracle",
+                                "sample": f"{len(sample)} of {B} streams ({nf} frames)"}
+    print(json.dumps(line), flush=True)
+
+
 def logadd_cpu_baseline(w, inputs, model_np, graph_np, dtype, n, threads=None,
                         min_seconds=10.0, max_seconds=30.0):
     """The oracle's lattice + n-best search on whole streams, timed on the host."""
@@ -391,6 +492,12 @@ def main():
     ap.add_argument("--logadd", type=int, default=0, metavar="N",
                     help="time the LogAdd path instead: lattice of the search plus the n-best "
                          "label-sequence search with N sampled paths per stream")
+    ap.add_argument("--search", choices=["fsa", "hyps"], default="fsa",
+                    help="fsa: the FSA-based search (default); hyps: the full-sequence beam "
+                         "search of Table 5 (trivial graph only), timed beside the FSA search")
+    ap.add_argument("--beam-size", type=int, default=4, help="hypotheses for --search hyps")
+    ap.add_argument("--merge", choices=["max", "logadd"], default="logadd",
+                    help="merge of equal sequences for --search hyps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="threads for the oracle baseline (default: all host threads)")
@@ -436,6 +543,9 @@ def main():
                             w.max_states)
     del tr_out
 
+    if args.search == "hyps":
+        hyps_bench(args, w, inputs, model_np, model, graph, enc, dtype, K, W)
+        return
     if args.logadd:
         logadd_bench(args, w, inputs, model_np, graph_np, model, graph, enc, dtype, K, W, work)
         return

@@ -401,7 +401,8 @@ typedef enum {
   TBS_KERNEL_FINAL = 2,
   TBS_KERNEL_STREAM = 3, /* the persistent kernel, one workgroup per stream */
   TBS_KERNEL_STREAM_GROUP = 4, /* the persistent kernel, several workgroups per stream */
-  TBS_KERNEL_COUNT = 5
+  TBS_KERNEL_HYP_STEP = 5, /* tbs_hyp_search: merge and selection of one frame */
+  TBS_KERNEL_COUNT = 6
 } tbs_kernel_id;
 
 typedef struct {

@@ -1490,10 +1490,18 @@ tbs_status tbs_hyp_search(const tbs_model* model, const tbs_hyp_params* params,
   HIP_TRY(launch_hyp_init(d, trace, st), "launch(hyp init)");
   for (int t = 0; t < maxlen; ++t) {
     HIP_TRY(launch_hyp_rows(d, t, st), "launch(hyp rows)");
-    HIP_TRY(launch_joiner_dense(md, encoder_out + (size_t)t * m->C, (long long)T * m->C,
-                                w.rowctx, 0, N, B * N, w.h, w.logits, w.stats, m->ncu, st),
+    HIP_TRY(launch_h_rows_dense(md, encoder_out + (size_t)t * m->C, (long long)T * m->C,
+                                w.rowctx, 0, N, B * N, w.h, st),
+            "launch(joiner rows)");
+    HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
+                         [&] {
+                           return launch_joiner_gemm(md, w.h, B * N, w.logits, w.stats, m->ncu,
+                                                     st);
+                         }),
             "launch(joiner)");
-    HIP_TRY(launch_hyp_step(md, d, t, w.logits, w.stats, trace, st), "launch(hyp step)");
+    HIP_TRY(timed_launch(m, TBS_KERNEL_HYP_STEP, st,
+                         [&] { return launch_hyp_step(md, d, t, w.logits, w.stats, trace, st); }),
+            "launch(hyp step)");
   }
   HIP_TRY(launch_hyp_final(d, out_tokens, out_num_tokens, out_scores, st), "launch(hyp final)");
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");

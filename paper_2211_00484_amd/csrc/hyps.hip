@@ -15,6 +15,7 @@
 // Frame schedule, three launches per frame: k_hyp_rows (each hypothesis's context,
 // distinct contexts to joiner rows), the dense joiner GEMM, k_hyp_step (merge and
 // top-N selection, one workgroup per stream).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -25,6 +26,7 @@ namespace tbs {
 namespace {
 
 constexpr int kHT = 256;
+constexpr int kHypCache = 16;  // candidates per thread scored once into registers
 constexpr unsigned long long kHashInit = 0x9e3779b97f4a7c15ull;  // hash of the empty sequence
 constexpr unsigned long long kHashMul = 0x100000001b3ull;       // odd multiplier
 
@@ -97,7 +99,8 @@ __global__ __launch_bounds__(kHT) void k_hyp_step(ModelDev m, HypDev d, int t,
                                                   const float2* __restrict__ stats, int* trace) {
   __shared__ double s_lse[kMaxHyps], s_sc[kMaxHyps], s_gs[kMaxHyps];
   __shared__ int s_gfirst[kMaxHyps], s_rpar[kMaxHyps], s_rlab[kMaxHyps], s_mj[kMaxHyps];
-  __shared__ int s_last[kMaxHyps], s_row[kMaxHyps];
+  __shared__ int s_last[kMaxHyps], s_row[kMaxHyps], s_n[kMaxHyps];
+  __shared__ unsigned long long s_h[kMaxHyps];
   __shared__ Cand s_w[kHT / 64];
   __shared__ Cand s_win[kMaxHyps];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -119,6 +122,8 @@ __global__ __launch_bounds__(kHT) void k_hyp_step(ModelDev m, HypDev d, int t,
     s_row[tid] = row;
     const int nn = d.n[cur][o + tid];
     s_last[tid] = nn > 0 ? d.ctx[cur][o + tid] % V : -1;
+    s_n[tid] = nn;
+    s_h[tid] = d.hash[cur][o + tid];
   }
   __syncthreads();
   auto logp = [&](int i, int c) {
@@ -131,11 +136,11 @@ __global__ __launch_bounds__(kHT) void k_hyp_step(ModelDev m, HypDev d, int t,
     const double a = s_sc[i] + logp(i, 0);
     double gs = a;
     int gfirst = i * V, rpar = i, rlab = 0, mj = -1;
-    const int ni = d.n[cur][o + i];
+    const int ni = s_n[i];
     if (ni > 0) {
       const unsigned long long ph = d.phash[cur][o + i];
       for (int j = 0; j < nh; ++j)
-        if (d.hash[cur][o + j] == ph && d.n[cur][o + j] == ni - 1) mj = j;
+        if (s_h[j] == ph && s_n[j] == ni - 1) mj = j;
     }
     if (mj >= 0) {
       const int c = s_last[i];
@@ -156,26 +161,52 @@ __global__ __launch_bounds__(kHT) void k_hyp_step(ModelDev m, HypDev d, int t,
     s_mj[i] = mj;
   }
   __syncthreads();
-  // top-N: rounds of a workgroup argmax over the candidates not taken yet
+  // top-N: rounds of a workgroup argmax over the candidates not taken yet.  Up to
+  // kHypCache candidates per thread are scored once into registers (all their logit
+  // loads in flight together); larger sets are rescored every round.
   const int total = nh * V;
+  auto score_of = [&](int idx, Cand& x) {
+    const int i = idx / V, c = idx - i * V;
+    if (c == 0) {
+      x = Cand{s_gs[i], s_gfirst[i], idx};
+      return true;
+    }
+    bool merged = false;  // label c of y_i is the blank group of some y_k
+    for (int k = 0; k < nh; ++k) merged = merged || (s_mj[k] == i && s_last[k] == c);
+    if (merged) return false;
+    x = Cand{s_sc[i] + logp(i, c), idx, idx};
+    return true;
+  };
+  const bool cached = total <= kHypCache * kHT;
+  double cs[kHypCache];
+  int cf[kHypCache];
+  if (cached) {
+#pragma unroll
+    for (int q = 0; q < kHypCache; ++q) {
+      const int idx = tid + q * kHT;
+      Cand x{neg_inf_d(), 0x7fffffff, idx};
+      if (idx >= total || !score_of(idx, x)) x.score = neg_inf_d();
+      cs[q] = x.score;
+      cf[q] = x.first;
+    }
+  }
   int kept = 0;
   for (int r = 0; r < N; ++r) {
     Cand best{neg_inf_d(), 0x7fffffff, -1};
-    for (int idx = tid; idx < total; idx += kHT) {
-      bool taken = false;
-      for (int q = 0; q < r; ++q) taken = taken || s_win[q].slot == idx;
-      if (taken) continue;
-      const int i = idx / V, c = idx - i * V;
-      Cand x;
-      if (c == 0) {
-        x = Cand{s_gs[i], s_gfirst[i], idx};
-      } else {
-        bool merged = false;  // label c of y_i is the blank group of some y_k
-        for (int k = 0; k < nh; ++k) merged = merged || (s_mj[k] == i && s_last[k] == c);
-        if (merged) continue;
-        x = Cand{s_sc[i] + logp(i, c), idx, idx};
+    if (cached) {
+#pragma unroll
+      for (int q = 0; q < kHypCache; ++q) {
+        const Cand x{cs[q], cf[q], tid + q * kHT};
+        if (x.score != neg_inf_d() && (best.slot < 0 || cand_before(x, best))) best = x;
       }
-      if (x.score != neg_inf_d() && (best.slot < 0 || cand_before(x, best))) best = x;
+    } else {
+      for (int idx = tid; idx < total; idx += kHT) {
+        bool taken = false;
+        for (int q = 0; q < r; ++q) taken = taken || s_win[q].slot == idx;
+        Cand x;
+        if (taken || !score_of(idx, x)) continue;
+        if (x.score != neg_inf_d() && (best.slot < 0 || cand_before(x, best))) best = x;
+      }
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
@@ -194,8 +225,14 @@ __global__ __launch_bounds__(kHT) void k_hyp_step(ModelDev m, HypDev d, int t,
       s_win[r] = w;
     }
     __syncthreads();
-    if (s_win[r].slot < 0) break;  // uniform: no candidate left
+    const int ws = s_win[r].slot;
+    if (ws < 0) break;  // uniform: no candidate left
     kept = r + 1;
+    if (cached && ws % kHT == tid) {
+#pragma unroll
+      for (int q = 0; q < kHypCache; ++q)
+        if (tid + q * kHT == ws) cs[q] = neg_inf_d();  // taken
+    }
   }
   // the kept hypotheses, in rank order, and their back-pointers
   if (tid < kept) {
@@ -274,7 +311,12 @@ hipError_t launch_hyp_rows(const HypDev& d, int t, hipStream_t st) {
 
 hipError_t launch_hyp_step(const ModelDev& m, const HypDev& d, int t, const float* logits,
                            const float2* stats, int* trace, hipStream_t st) {
-  hipLaunchKernelGGL(k_hyp_step, dim3(d.B), dim3(kHT), 0, st, m, d, t, logits, stats, trace);
+  hipEvent_t ea, eb;
+  if (take_launch_events(&ea, &eb))  // per-kernel profiling: events in the dispatch packet
+    hipExtLaunchKernelGGL(k_hyp_step, dim3(d.B), dim3(kHT), 0, st, ea, eb, 0u, m, d, t, logits,
+                          stats, trace);
+  else
+    hipLaunchKernelGGL(k_hyp_step, dim3(d.B), dim3(kHT), 0, st, m, d, t, logits, stats, trace);
   return hipGetLastError();
 }
 

@@ -89,6 +89,8 @@ JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu);
 // that launch's dispatch packet (per-kernel profiling); pending until a launch takes them.
 void set_launch_events(hipEvent_t start, hipEvent_t stop);
 bool launch_events_pending();
+// Takes the pending events (for a launch made outside kernels.hip); false if none.
+bool take_launch_events(hipEvent_t* start, hipEvent_t* stop);
 
 // Per-stream kernel (one workgroup runs every frame of one stream).
 struct StreamPlan {
@@ -191,6 +193,13 @@ hipError_t launch_nbest(const LatticeDev& L, const NBestDev& N, int* out_tokens,
 hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, long long enc_stride,
                                const int* ctx, long long row0, int per_enc, int R, void* h,
                                float* logits, float2* stats, int ncu, hipStream_t st);
+
+// the two halves of launch_joiner_dense: h rows, then the GEMM over R rows of h
+hipError_t launch_h_rows_dense(const ModelDev& m, const float* enc, long long enc_stride,
+                               const int* ctx, long long row0, int per_enc, int R, void* h,
+                               hipStream_t st);
+hipError_t launch_joiner_gemm(const ModelDev& m, const void* h, int R, float* logits,
+                              float2* stats, int ncu, hipStream_t st);
 
 // Full-sequence beam search (the comparison search of Table 5), frame schedule.
 struct HypDev {

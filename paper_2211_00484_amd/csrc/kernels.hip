@@ -2793,6 +2793,14 @@ void set_launch_events(hipEvent_t start, hipEvent_t stop) {
 
 bool launch_events_pending() { return g_ev_start != nullptr; }
 
+bool take_launch_events(hipEvent_t* start, hipEvent_t* stop) {
+  if (!g_ev_start) return false;
+  *start = g_ev_start;
+  *stop = g_ev_stop;
+  g_ev_start = g_ev_stop = nullptr;
+  return true;
+}
+
 JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu) {
   JoinerPlan p;
   const int esz = bf16 ? 2 : 4;
@@ -3024,14 +3032,27 @@ hipError_t launch_final(const GraphDev& g, const DecodeDev& d, int* out_tokens, 
   return hipGetLastError();
 }
 
+hipError_t launch_h_rows_dense(const ModelDev& m, const float* enc, long long enc_stride,
+                               const int* ctx, long long row0, int per_enc, int R, void* h,
+                               hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_h_rows_dense, dim3(R), dim3(256), 0, st, m, enc, ctx, row0, per_enc,
+                     enc_stride, h);
+  return hipGetLastError();
+}
+
 hipError_t launch_joiner_dense(const ModelDev& m, const float* enc, long long enc_stride,
                                const int* ctx, long long row0, int per_enc, int R, void* h,
                                float* logits, float2* stats, int ncu, hipStream_t st) {
   if (R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_h_rows_dense, dim3(R), dim3(256), 0, st, m, enc, ctx, row0, per_enc,
-                     enc_stride, h);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_h_rows_dense(m, enc, enc_stride, ctx, row0, per_enc, R, h, st);
   if (e != hipSuccess) return e;
+  return launch_joiner_gemm(m, h, R, logits, stats, ncu, st);
+}
+
+hipError_t launch_joiner_gemm(const ModelDev& m, const void* h, int R, float* logits,
+                              float2* stats, int ncu, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
   const JoinerPlan p = plan_joiner(R, m.Vpad, m.Kpad, m.bf16, ncu);
   JoinArgs a{};
   a.h = h;

@@ -37,7 +37,7 @@ class KernelTime(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
 
 
-KERNEL_NAMES = ("joiner", "search", "final", "stream", "stream_group")
+KERNEL_NAMES = ("joiner", "search", "final", "stream", "stream_group", "hyp_step")
 SCHEDULES = {"auto": 0, "frame": 1, "stream": 2, "stream1": 3}
 
 
