@@ -18,6 +18,9 @@ sampling against the exact path posteriors of small lattices.  Which expansions 
 lattice keeps (every arc into a surviving tuple) is this implementation's reading and is
 pinned by invariants only.
 
+Transducer forward recursions (Sec. 3, eq. 1-3): pinned against exhaustive enumeration
+of the alignments of small grids and against path-count closed forms.
+
 Full-sequence beam search (Table 5's comparison search): with a beam wide enough to keep
 every sequence it is pinned against exhaustive enumeration (max merge: the best path;
 log-add merge: the sequence with the highest total probability); with one hypothesis
@@ -69,6 +72,8 @@ def _load():
         lib.oracle_rescore.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I,
                                        _P, _P, _P, _P, _P, _P]
         lib.oracle_rescore.restype = _I
+        lib.oracle_transducer_forward.argtypes = [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P]
+        lib.oracle_transducer_forward.restype = _I
         lib.oracle_hyps.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I]
                                     + [_P] * 5)
         lib.oracle_hyps.restype = _I
@@ -332,3 +337,26 @@ def hyp_search(model, encoder_out: np.ndarray, lengths: np.ndarray, beam_size: i
                     _ptr(tokens), _ptr(ntok), _ptr(scores), _ptr(trace), _ptr(fm))
     return OracleResult(tokens, ntok, scores, np.zeros(B, dtype=np.int32), None, trace,
                         fm.min(axis=1), fm)
+
+
+TRANSDUCER_KINDS = {"standard": 0, "modified": 1, "constrained": 2}
+
+
+def transducer_forward(kind: str, blank: np.ndarray, label: np.ndarray, frames, labels):
+    """Forward recursion of the standard (eq. 1), modified (eq. 2) or constrained (eq. 3)
+    transducer on log-probabilities blank [B, T, U+1] and label [B, T, U].
+    Returns (total [B], alpha [B, T+1, U+1]), fp64."""
+    lib = _load()
+    blank, label = _f32(blank), _f32(label)
+    B, T, U1 = blank.shape
+    U = U1 - 1
+    if label.shape != (B, T, U):
+        raise ValueError("label must be [B, T, U]")
+    fr, lb = _i32(frames), _i32(labels)
+    if (fr < 1).any() or (fr > T).any() or (lb < 0).any() or (lb > U).any():
+        raise ValueError("frames must be in [1, T] and labels in [0, U]")
+    alpha = np.empty((B, T + 1, U + 1), dtype=np.float64)
+    total = np.empty(B, dtype=np.float64)
+    lib.oracle_transducer_forward(TRANSDUCER_KINDS[kind], B, T, U, _ptr(blank), _ptr(label),
+                                  _ptr(fr), _ptr(lb), _ptr(alpha), _ptr(total))
+    return total, alpha

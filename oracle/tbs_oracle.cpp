@@ -843,4 +843,55 @@ int oracle_hyps(int B, int T, int C, int V, const float* enc, const int* lengths
   return 0;
 }
 
+
+// Forward recursions of the transducer losses over the (t, u) grid (Sec. 3), on given
+// log-probabilities: blank [B][T][U+1] = log P(blank | frame t, u labels emitted),
+// label [B][T][U] = log P(label u+1 | frame t, u labels emitted).  kind 0: the standard
+// recursion, eq. (1), likelihood alpha(T_b - 1, U_b) + blank(T_b - 1, U_b); kind 1: the
+// modified transducer, eq. (2), where a label also moves to the next frame; kind 2: the
+// constrained transducer, eq. (3), where a label is followed by the blank of the new
+// context on the same frame; both with likelihood alpha(T_b, U_b).  frames [B] and
+// labels [B] are each utterance's T_b >= 1 and U_b.  alpha [B][T+1][U+1] (or null)
+// receives every cell, -inf where no path reaches; total [B].
+int oracle_transducer_forward(int kind, int B, int T, int U, const float* blank,
+                              const float* label, const int* frames, const int* labels,
+                              double* alpha, double* total) {
+  for (int b = 0; b < B; ++b) {
+    const int Tb = frames[b], Ub = labels[b];
+    const float* bl = blank + (size_t)b * T * (U + 1);
+    const float* lb = label + (size_t)b * T * U;
+    auto BL = [&](int t, int u) { return (double)bl[(size_t)t * (U + 1) + u]; };
+    auto LB = [&](int t, int u) { return (double)lb[(size_t)t * U + u]; };
+    std::vector<double> a((size_t)(T + 1) * (U + 1), kNegInf);
+    auto A = [&](int t, int u) -> double& { return a[(size_t)t * (U + 1) + u]; };
+    A(0, 0) = 0.0;
+    if (kind == 0) {
+      for (int t = 0; t < Tb; ++t)
+        for (int u = 0; u <= Ub; ++u) {
+          if (t == 0 && u == 0) continue;
+          double v = kNegInf;
+          if (t > 0) v = log_add(v, A(t - 1, u) + BL(t - 1, u));
+          if (u > 0) v = log_add(v, A(t, u - 1) + LB(t, u - 1));
+          A(t, u) = v;
+        }
+      total[b] = A(Tb - 1, Ub) + BL(Tb - 1, Ub);
+    } else {
+      for (int t = 1; t <= Tb; ++t)
+        for (int u = 0; u <= Ub; ++u) {
+          double v = A(t - 1, u) + BL(t - 1, u);
+          if (u > 0) {
+            double w = A(t - 1, u - 1) + LB(t - 1, u - 1);
+            if (kind == 2) w += BL(t - 1, u);
+            v = log_add(v, w);
+          }
+          A(t, u) = v;
+        }
+      total[b] = A(Tb, Ub);
+    }
+    if (alpha)
+      std::copy(a.begin(), a.end(), alpha + (size_t)b * (T + 1) * (U + 1));
+  }
+  return 0;
+}
+
 }  // extern "C"
