@@ -334,6 +334,41 @@ tbs_status tbs_hyp_search(const tbs_model *model, const tbs_hyp_params *params,
                           int32_t *trace, void *hip_stream);
 
 /*
+ * Forward recursions of the transducer losses over the (frame t, labels emitted u) grid
+ * (Sec. 3), on given log-probabilities:
+ *   blank   DEVICE float [B][T][U+1]: log P(blank | frame t, u labels emitted);
+ *   label   DEVICE float [B][T][U]: log P(label u+1 of the utterance | frame t, u labels);
+ *   lengths DEVICE int32 [B][2]: each utterance's frames T_b in [1, T] and labels U_b in
+ *           [0, U] (cells beyond them are not read);
+ *   kind    TBS_TRANSDUCER_STANDARD, eq. (1): alpha(t, u) = log_add(alpha(t-1, u) +
+ *             blank(t-1, u), alpha(t, u-1) + label(t, u-1)), likelihood
+ *             alpha(T_b - 1, U_b) + blank(T_b - 1, U_b);
+ *           TBS_TRANSDUCER_MODIFIED, eq. (2): a label also moves to the next frame,
+ *             alpha(t, u) = log_add(alpha(t-1, u) + blank(t-1, u), alpha(t-1, u-1) +
+ *             label(t-1, u-1)), likelihood alpha(T_b, U_b);
+ *           TBS_TRANSDUCER_CONSTRAINED, eq. (3): as (2) with blank(t-1, u) added to the
+ *             label term, likelihood alpha(T_b, U_b); alpha(0, 0) = 0 in all three.
+ *   out_total  DEVICE double [B]: the log-likelihood (-inf if no path, e.g. U_b > T_b for
+ *              (2) and (3)); NaN for an utterance whose lengths are out of range;
+ *   out_alpha  DEVICE float [B][T+1][U+1] or NULL: alpha of the rows the recursion visits
+ *              (t <= T_b for (2) and (3), t < T_b for (1)), -inf for u > U_b; other rows
+ *              are not written;
+ *   out_status DEVICE int32 [B] or NULL: 0, or 1 for out-of-range lengths.
+ * Scores accumulate in fp64.  Errors: TBS_EINVAL (kind, sizes, NULL), TBS_ECAPACITY for
+ * U > 1023.
+ */
+typedef enum {
+  TBS_TRANSDUCER_STANDARD = 0,
+  TBS_TRANSDUCER_MODIFIED = 1,
+  TBS_TRANSDUCER_CONSTRAINED = 2
+} tbs_transducer_kind;
+
+tbs_status tbs_transducer_forward(int32_t kind, const float *blank, const float *label,
+                                  const int32_t *lengths, int32_t B, int32_t T, int32_t U,
+                                  double *out_total, float *out_alpha, int32_t *out_status,
+                                  void *hip_stream);
+
+/*
  * How tbs_decode drives the frame loop of Algorithm 1 (all schedules compute
  * the same search; results agree within the fp32 rounding of the joiner):
  *   TBS_SCHEDULE_FRAME   two kernels per frame over the whole batch: a joiner

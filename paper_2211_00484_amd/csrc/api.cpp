@@ -1510,4 +1510,26 @@ tbs_status tbs_hyp_search(const tbs_model* model, const tbs_hyp_params* params,
   return TBS_OK;
 }
 
+
+tbs_status tbs_transducer_forward(int32_t kind, const float* blank, const float* label,
+                                  const int32_t* lengths, int32_t B, int32_t T, int32_t U,
+                                  double* out_total, float* out_alpha, int32_t* out_status,
+                                  void* hip_stream) {
+  if (kind != TBS_TRANSDUCER_STANDARD && kind != TBS_TRANSDUCER_MODIFIED &&
+      kind != TBS_TRANSDUCER_CONSTRAINED)
+    return fail(TBS_EINVAL, "tbs_transducer_forward: unknown kind %d", (int)kind);
+  if (B < 0 || T < 1 || U < 0)
+    return fail(TBS_EINVAL, "tbs_transducer_forward: need B >= 0, T >= 1, U >= 0");
+  if (U + 1 > 64 * kTransducerMaxK)
+    return fail(TBS_ECAPACITY, "tbs_transducer_forward: U = %d exceeds the limit %d", (int)U,
+                64 * kTransducerMaxK - 1);
+  if (B == 0) return TBS_OK;
+  if (!blank || (U > 0 && !label) || !lengths || !out_total)
+    return fail(TBS_EINVAL, "tbs_transducer_forward: NULL pointer");
+  HIP_TRY(launch_transducer_forward(kind, blank, label, lengths, B, T, U, out_total, out_alpha,
+                                    out_status, (hipStream_t)hip_stream),
+          "launch(transducer)");
+  return TBS_OK;
+}
+
 }  // extern "C"

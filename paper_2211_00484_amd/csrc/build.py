@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libtbs.so")
-SOURCES = ["api.cpp", "kernels.hip", "lattice.hip", "hyps.hip"]
+SOURCES = ["api.cpp", "kernels.hip", "lattice.hip", "hyps.hip", "transducer.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed-fp32 VALU forms are kept out of the generated code on purpose.

@@ -23,6 +23,7 @@ constexpr int kTopkStage = 2 * (kChunk + kMaxStates);  // trivial-graph label li
 constexpr size_t kMaxLds = 160 * 1024;  // LDS per workgroup on gfx950
 constexpr int kStreamMaxV = 512;     // per-stream kernel: vocabulary limit (8 logits per lane)
 constexpr int kMaxHyps = 16;         // full-sequence beam search: hypotheses per stream
+constexpr int kTransducerMaxK = 16;  // transducer recursions: cells per lane (U + 1 <= 1024)
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -221,5 +222,11 @@ hipError_t launch_hyp_step(const ModelDev& m, const HypDev& d, int t, const floa
                            const float2* stats, int* trace, hipStream_t st);
 hipError_t launch_hyp_final(const HypDev& d, int* out_tokens, int* out_ntok, double* out_scores,
                             hipStream_t st);
+
+// Transducer forward recursions (kind 0: eq. 1, 1: eq. 2, 2: eq. 3); one wave per
+// utterance.  lengths: DEVICE [B][2] (frames, labels).
+hipError_t launch_transducer_forward(int kind, const float* blank, const float* label,
+                                     const int* lengths, int B, int T, int U, double* total,
+                                     float* alpha, int* status, hipStream_t st);
 
 }  // namespace tbs

@@ -98,6 +98,8 @@ def lib():
     L.tbs_state_create_graphs.restype = _I32
     L.tbs_state_create_graphs.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _I32, _I32, _P,
                                           ctypes.POINTER(_P)]
+    L.tbs_transducer_forward.restype = _I32
+    L.tbs_transducer_forward.argtypes = [_I32, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P]
     L.tbs_hyp_search.restype = _I32
     L.tbs_hyp_search.argtypes = [_P, ctypes.POINTER(HypParams), _P, _P, _I32, _I32, _P, _P, _P,
                                  _P, _P]
@@ -506,3 +508,29 @@ def hyp_search(model: Model, encoder_out, lengths, beam_size: int = 4, merge: st
                                 _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
                                 _dev_ptr(out.scores), _dev_ptr(out.trace), _stream_ptr(stream)))
     return out
+
+
+TRANSDUCER_KINDS = {"standard": 0, "modified": 1, "constrained": 2}
+
+
+def transducer_forward(kind: str, blank, label, lengths, want_alpha: bool = False,
+                       stream=None):
+    """Forward recursion of the standard (eq. 1), modified (eq. 2) or constrained (eq. 3)
+    transducer (tbs_transducer_forward).  blank [B, T, U+1] and label [B, T, U] float32 on
+    the device; lengths [B, 2] int32 (frames, labels).  Returns (total [B] float64,
+    alpha [B, T+1, U+1] float32 or None, status [B] int32)."""
+    import torch
+    B, T, U1 = (int(x) for x in blank.shape)
+    U = U1 - 1
+    if tuple(label.shape) != (B, T, U):
+        raise ValueError("label must be [B, T, U]")
+    dev = blank.device
+    lengths = torch.as_tensor(lengths, dtype=torch.int32).reshape(B, 2).to(dev).contiguous()
+    total = torch.empty(B, dtype=torch.float64, device=dev)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    alpha = torch.empty((B, T + 1, U1), dtype=torch.float32, device=dev) if want_alpha else None
+    _check(lib().tbs_transducer_forward(TRANSDUCER_KINDS[kind], _dev_ptr(blank.contiguous()),
+                                        _dev_ptr(label.contiguous()) if U > 0 else None,
+                                        _dev_ptr(lengths), B, T, U, _dev_ptr(total),
+                                        _dev_ptr(alpha), _dev_ptr(status), _stream_ptr(stream)))
+    return total, alpha, status

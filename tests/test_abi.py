@@ -84,6 +84,10 @@ def test_decode_null_handles():
     assert L.tbs_state_create_graphs(None, None, ctypes.byref(p), 1, 1, None,
                                      ctypes.byref(h)) == EINVAL
     assert h.value is None
+    assert L.tbs_transducer_forward(7, None, None, None, 1, 1, 1, None, None, None,
+                                    None) == EINVAL
+    assert L.tbs_transducer_forward(0, None, None, None, 1, 1, 1024, None, None, None,
+                                    None) == -4
     hp = tbs.HypParams(4, 1)
     assert L.tbs_hyp_search(None, ctypes.byref(hp), None, None, 1, 1, None, None, None, None,
                             None) == EINVAL
