@@ -276,6 +276,66 @@ def decode_roofline(prof, K, work, dtype):
     return kernels, roofline, schedule, j_tflops, s_gbps, peak_j
 
 
+def transducer_bench(args):
+    """One step: tbs_transducer_forward over a batch of random log-probabilities."""
+    import torch
+    from paper_2211_00484_amd import tbs
+    B, T, U = (int(x) for x in args.tr_shape.split(","))
+    kind = args.transducer
+    rng = np.random.default_rng(0)
+    blank_np = np.log(rng.uniform(0.01, 1.0, size=(B, T, U + 1))).astype(np.float32)
+    label_np = np.log(rng.uniform(0.01, 1.0, size=(B, T, U))).astype(np.float32)
+    lens = np.stack([np.full(B, T), np.full(B, min(U, T) if kind != "standard" else U)],
+                    axis=1).astype(np.int32)
+    blank, label = torch.from_numpy(blank_np).cuda(), torch.from_numpy(label_np).cuda()
+    lens_d = torch.from_numpy(lens).cuda()
+    K = args.steps or 50
+    W = args.warmup
+    for _ in range(W):
+        tbs.transducer_forward(kind, blank, label, lens_d)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        tbs.transducer_forward(kind, blank, label, lens_d)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    # the kernel is the call's only launch: events on the launch stream bracket it
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(K)]
+    for a, b in ev:
+        a.record()
+        tbs.transducer_forward(kind, blank, label, lens_d)
+        b.record()
+    torch.cuda.synchronize()
+    avg_s = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e-3
+    cells = B * T * (U + 1)
+    nbytes = 4 * B * T * (2 * U + 1)  # each log-probability read once
+    gbps = nbytes / avg_s / 1e9
+    line = {
+        "metric": f"transducer forward recursion ({kind}, eq. {dict(standard=1, modified=2, constrained=3)[kind]}) grid cells/s",
+        "value": cells * K / (t1 - t0), "unit": "cells/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": (t1 - t0) * 1e3 / K, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32 inputs, f64 scores", "data": "synthetic",
+        "config": {"workload": f"transducer-{kind}", "B": B, "T": T, "U": U,
+                   "inputs": "log U(0.01, 1) per cell"},
+        "roofline": {"kernel": "k_transducer", "bound": "hbm", "achieved": gbps,
+                     "peak": PEAK["hbm_gbps"], "unit": "GB/s", "frac": gbps / PEAK["hbm_gbps"],
+                     "traffic": None},
+        "kernel_avg_us": avg_s * 1e6,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        n = 0
+        t2 = time.perf_counter()
+        while time.perf_counter() - t2 < 3.0:
+            oracle.transducer_forward(kind, blank_np, label_np, lens[:, 0], lens[:, 1])
+            n += 1
+        dt = time.perf_counter() - t2
+        line["cpu_baseline"] = {"value": cells * n / dt, "unit": "cells/s", "cores": 1,
+                                "kind": "oracle", "sample": f"the whole batch, {n} passes"}
+    print(json.dumps(line), flush=True)
+
+
 def hyps_bench(args, w, inputs, model_np, model, graph, enc, dtype, K, W):
     """One step: tbs_hyp_search over the whole batch (beam_size hypotheses, max-symbols 1),
     with the FSA-based search of the same workload timed beside it."""
@@ -498,6 +558,13 @@ def main():
     ap.add_argument("--beam-size", type=int, default=4, help="hypotheses for --search hyps")
     ap.add_argument("--merge", choices=["max", "logadd"], default="logadd",
                     help="merge of equal sequences for --search hyps")
+    ap.add_argument("--transducer", choices=["standard", "modified", "constrained"],
+                    default=None,
+                    help="time the transducer forward recursion (eq. 1, 2 or 3) instead, on "
+                         "random log-probabilities of B utterances of T frames and U labels")
+    ap.add_argument("--tr-shape", default="32,250,80", metavar="B,T,U",
+                    help="shape for --transducer (default: a training batch of 10 s "
+                         "utterances at 25 frames/s with 80 labels)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="threads for the oracle baseline (default: all host threads)")
@@ -522,6 +589,9 @@ def main():
         return
     if args.scaled_microbench:
         scaled_microbench(args.joiner_dtype or "fp32", args.steps or 3)
+        return
+    if args.transducer:
+        transducer_bench(args)
         return
     w, inputs, model_np, graph_np = synth.make_workload(args.workload, seed=0)
     K = args.steps if args.steps is not None else DEFAULT_STEPS[w.name]
