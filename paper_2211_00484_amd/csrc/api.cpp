@@ -134,6 +134,8 @@ struct HypWork {
 
 }  // namespace
 
+void lattice_free(tbs_lattice* L);  // release and delete (defined with tbs_lattice)
+
 struct tbs_graph {
   int S = 0, start = 0, V = 0, A = 0, maxdeg = 0;
   int trivial = 0;  // one state, 0-weight loops 1..V-1 in label order, final weight 0
@@ -175,6 +177,7 @@ struct tbs_model {
   std::mutex mu;
   Workspace ws;
   HypWork hw;
+  tbs_lattice* lat_cache = nullptr;  // buffers of the last destroyed lattice, for the next
   // device work of every decode and chunk on this model is serialised on this event
   // (they share the exchange buffer and, for tbs_decode, the workspace)
   hipEvent_t busy = nullptr;
@@ -733,6 +736,8 @@ void tbs_model_destroy(tbs_model* m) {
     if (m->ws.done && m->ws.pending) hipEventSynchronize(m->ws.done);
     m->ws.release();
     m->hw.release();
+    if (m->lat_cache) lattice_free(m->lat_cache);
+    m->lat_cache = nullptr;
   }
   prof_drop(m);
   for (hipEvent_t e : m->prof_pool) hipEventDestroy(e);
@@ -896,13 +901,20 @@ struct tbs_lattice {
   GraphDev gd{};
   int B = 0, T = 0, Ns = 0, Nc = 0;
   long long A = 0;                  // arcs
+  // allocated capacity (a destroyed lattice's buffers serve the model's next one)
+  int capB = 0, capT = 0, capNs = 0, capNc = 0;
+  long long capA = 0;
+  size_t cap_rows = 0;
+  int* len_host = nullptr;          // pinned staging: lengths [capB]
+  GraphDev* gtab_host = nullptr;    // pinned staging: per-stream graphs [capB]
   int* len = nullptr;               // [B]
   int* trace = nullptr;             // [T+1][B][Ns][4] survivors (the lattice nodes)
   int* tokens = nullptr;            // best path of the search (needed by the decode call)
   int* ntok = nullptr;
   double* scores = nullptr;
   int* dstatus = nullptr;
-  GraphDev* gtab = nullptr;         // [B] per-stream graphs, or null
+  GraphDev* gtab = nullptr;         // [B] per-stream graphs
+  bool per_graph = false;           // gtab in use
   int* nn = nullptr;
   int* cnt = nullptr;
   long long* off = nullptr;
@@ -941,7 +953,7 @@ struct tbs_lattice {
     L.V = m->V;
     L.len = len;
     L.nodes = trace;
-    L.graphs = gtab;
+    L.graphs = per_graph ? gtab : nullptr;
     L.nn = nn;
     L.cnt = cnt;
     L.off = off;
@@ -971,9 +983,16 @@ struct tbs_lattice {
     hipFree(dstatus); hipFree(gtab); hipFree(nn); hipFree(cnt); hipFree(off); hipFree(dptr);
     hipFree(arcs); hipFree(w); hipFree(pc); hipFree(rowctx); hipFree(alpha); hipFree(fw); hipFree(total);
     hipFree(status); hipFree(h); hipFree(logits); hipFree(stats);
+    if (len_host) hipHostFree(len_host);
+    if (gtab_host) hipHostFree(gtab_host);
     if (done) hipEventDestroy(done);
   }
 };
+
+void lattice_free(tbs_lattice* L) {
+  L->release();
+  delete L;
+}
 
 namespace {
 
@@ -994,59 +1013,89 @@ tbs_status lattice_create_impl(const tbs_model* model, const tbs_graph* graph,
       return fail(TBS_EINVAL, "%s: lengths[%d] = %d outside [0, %d]", who, b, lengths[b], T);
   tbs_model* m = const_cast<tbs_model*>(model);
   hipStream_t st = (hipStream_t)hip_stream;
-  tbs_lattice* L = new tbs_lattice();
-  L->m = m;
-  L->gd = gd;
-  L->B = B;
-  L->T = T;
-  L->Ns = params->max_states;
-  L->Nc = params->max_contexts < L->Ns ? params->max_contexts : L->Ns;
-  const size_t BN = (size_t)B * L->Ns, BT = (size_t)B * T;
+  const int Ns = params->max_states;
+  const int Nc = params->max_contexts < Ns ? params->max_contexts : Ns;
+  const size_t BN = (size_t)B * Ns, BT = (size_t)B * T;
   const int nvt = m->Vpad / kJoinerBN;
   const size_t esz = m->bf16 ? 2 : 4;
   // joiner rows per chunk of streams: whole streams, logits of at most 512 MiB
-  const size_t per_stream = (size_t)T * L->Nc;
+  const size_t per_stream = (size_t)T * Nc;
   size_t cap_rows = ((size_t)512 << 20) / ((size_t)m->Vpad * 4);
   if (cap_rows < per_stream) cap_rows = per_stream;
   const int chunk = per_stream == 0 ? B : (int)std::min<size_t>(B, cap_rows / per_stream);
   const size_t rows = per_stream * (size_t)chunk;
+  // the buffers of the model's last destroyed lattice, when they are large enough
+  tbs_lattice* L = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(m->mu);
+    L = m->lat_cache;
+    m->lat_cache = nullptr;
+  }
+  if (L && !(B <= L->capB && T <= L->capT && Ns == L->capNs && Nc == L->capNc &&
+             rows <= L->cap_rows)) {
+    L->release();
+    delete L;
+    L = nullptr;
+  }
   auto cleanup = [&](tbs_status st_) {
     L->release();
     delete L;
     return st_;
   };
   hipError_t e = hipSuccess;
+  if (!L) {
+    L = new tbs_lattice();
 #define LAT_ALLOC(expr) \
   if (e == hipSuccess) e = (expr)
-  LAT_ALLOC(dalloc(&L->len, B));
-  LAT_ALLOC(dalloc(&L->trace, (size_t)(T + 1) * BN * 4));
-  LAT_ALLOC(dalloc(&L->tokens, BT));
-  LAT_ALLOC(dalloc(&L->ntok, B));
-  LAT_ALLOC(dalloc(&L->scores, B));
-  LAT_ALLOC(dalloc(&L->dstatus, B));
-  if (graphs) LAT_ALLOC(dalloc(&L->gtab, B));
-  LAT_ALLOC(dalloc(&L->nn, (size_t)B * (T + 1)));
-  LAT_ALLOC(dalloc(&L->cnt, BT));
-  LAT_ALLOC(dalloc(&L->off, BT + 1));
-  LAT_ALLOC(dalloc(&L->dptr, BT * (L->Ns + 1)));
-  LAT_ALLOC(dalloc(&L->rowctx, BT * L->Nc));
-  LAT_ALLOC(dalloc(&L->alpha, (size_t)(T + 1) * BN));
-  LAT_ALLOC(dalloc(&L->fw, BN));
-  LAT_ALLOC(dalloc(&L->total, B));
-  LAT_ALLOC(dalloc(&L->status, B));
-  LAT_ALLOC(dalloc((char**)&L->h, rows * m->Kpad * esz));
-  LAT_ALLOC(dalloc(&L->logits, rows * m->Vpad));
-  LAT_ALLOC(dalloc(&L->stats, rows * nvt));
-  LAT_ALLOC(hipEventCreateWithFlags(&L->done, hipEventDisableTiming));
+    LAT_ALLOC(dalloc(&L->len, B));
+    LAT_ALLOC(dalloc(&L->trace, (size_t)(T + 1) * BN * 4));
+    LAT_ALLOC(dalloc(&L->tokens, BT));
+    LAT_ALLOC(dalloc(&L->ntok, B));
+    LAT_ALLOC(dalloc(&L->scores, B));
+    LAT_ALLOC(dalloc(&L->dstatus, B));
+    LAT_ALLOC(dalloc(&L->gtab, B));
+    LAT_ALLOC(dalloc(&L->nn, (size_t)B * (T + 1)));
+    LAT_ALLOC(dalloc(&L->cnt, BT));
+    LAT_ALLOC(dalloc(&L->off, BT + 1));
+    LAT_ALLOC(dalloc(&L->dptr, BT * (Ns + 1)));
+    LAT_ALLOC(dalloc(&L->rowctx, BT * Nc));
+    LAT_ALLOC(dalloc(&L->alpha, (size_t)(T + 1) * BN));
+    LAT_ALLOC(dalloc(&L->fw, BN));
+    LAT_ALLOC(dalloc(&L->total, B));
+    LAT_ALLOC(dalloc(&L->status, B));
+    LAT_ALLOC(dalloc((char**)&L->h, rows * m->Kpad * esz));
+    LAT_ALLOC(dalloc(&L->logits, rows * m->Vpad));
+    LAT_ALLOC(dalloc(&L->stats, rows * nvt));
+    LAT_ALLOC(hipHostMalloc((void**)&L->len_host, (size_t)B * 4, hipHostMallocDefault));
+    LAT_ALLOC(hipHostMalloc((void**)&L->gtab_host, (size_t)B * sizeof(GraphDev),
+                            hipHostMallocDefault));
+    LAT_ALLOC(hipEventCreateWithFlags(&L->done, hipEventDisableTiming));
 #undef LAT_ALLOC
-  if (e != hipSuccess) return cleanup(hip_fail(e, who));
-  if (graphs) {
-    std::vector<GraphDev> tab(B);
-    for (int b = 0; b < B; ++b) tab[b] = graph_dev(graphs[b]);
-    e = hipMemcpy(L->gtab, tab.data(), (size_t)B * sizeof(GraphDev), hipMemcpyHostToDevice);
+    L->capB = B;
+    L->capT = T;
+    L->capNs = Ns;
+    L->capNc = Nc;
+    L->cap_rows = rows;
+    if (e != hipSuccess) return cleanup(hip_fail(e, who));
   }
-  if (e == hipSuccess) e = hipMemcpy(L->len, lengths, (size_t)B * 4, hipMemcpyHostToDevice);
+  L->m = m;
+  L->gd = gd;
+  L->B = B;
+  L->T = T;
+  L->Ns = Ns;
+  L->Nc = Nc;
+  L->A = 0;
+  L->pending = false;
+  std::memcpy(L->len_host, lengths, (size_t)B * 4);
+  e = hipMemcpyAsync(L->len, L->len_host, (size_t)B * 4, hipMemcpyHostToDevice, st);
+  if (graphs) {
+    for (int b = 0; b < B; ++b) L->gtab_host[b] = graph_dev(graphs[b]);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(L->gtab, L->gtab_host, (size_t)B * sizeof(GraphDev),
+                         hipMemcpyHostToDevice, st);
+  }
   if (e != hipSuccess) return cleanup(hip_fail(e, who));
+  L->per_graph = graphs != nullptr;
   // the search, with its survivor trace as the lattice nodes
   s = decode_impl(model, graph, graphs, params, encoder_out, lengths, B, T, L->tokens, L->ntok,
                   L->scores, L->dstatus, nullptr, L->trace, hip_stream, who);
@@ -1058,9 +1107,19 @@ tbs_status lattice_create_impl(const tbs_model* model, const tbs_graph* graph,
   if (e == hipSuccess)
     e = hipMemcpyAsync(&L->A, L->off + BT, sizeof(long long), hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
-  if (e == hipSuccess) e = dalloc(&L->arcs, (size_t)L->A);
-  if (e == hipSuccess) e = dalloc(&L->w, (size_t)L->A);
-  if (e == hipSuccess) e = dalloc(&L->pc, (size_t)L->A);
+  if (e == hipSuccess && L->A > L->capA) {
+    (void)hipFree(L->arcs);
+    (void)hipFree(L->w);
+    (void)hipFree(L->pc);
+    L->arcs = nullptr;
+    L->w = nullptr;
+    L->pc = nullptr;
+    L->capA = 0;
+    e = dalloc(&L->arcs, (size_t)L->A);
+    if (e == hipSuccess) e = dalloc(&L->w, (size_t)L->A);
+    if (e == hipSuccess) e = dalloc(&L->pc, (size_t)L->A);
+    if (e == hipSuccess) L->capA = L->A;
+  }
   if (e != hipSuccess) return cleanup(hip_fail(e, who));
   const LatticeDev d = L->dev();
   const ModelDev md = model_dev(m);
@@ -1398,10 +1457,15 @@ tbs_status tbs_lattice_nbest(tbs_lattice* lat, int32_t num_paths, const double* 
 
 void tbs_lattice_destroy(tbs_lattice* lat) {
   if (!lat) return;
-  {
-    std::lock_guard<std::mutex> lk(lat->m->mu);
-    lat->release();
+  tbs_model* m = lat->m;
+  std::lock_guard<std::mutex> lk(m->mu);
+  if (lat->done && lat->pending) (void)hipEventSynchronize(lat->done);
+  lat->pending = false;
+  if (!m->lat_cache) {
+    m->lat_cache = lat;  // its buffers serve the model's next lattice
+    return;
   }
+  lat->release();
   delete lat;
 }
 
