@@ -281,6 +281,9 @@ void tbs_state_destroy(tbs_state *state);
  *   arc taken on frame f as an index within frame f's arcs, the final node at len_b,
  *   -1 after).  Scratch for num_paths is kept in the lattice.  Calls on one lattice are
  *   stream-ordered across streams.
+ * tbs_lattice_destroy waits for the lattice's device work; its buffers then serve the
+ *   model's next tbs_lattice_create when they are large enough (no allocation), and are
+ *   freed with the model or when a larger lattice needs new ones.
  */
 typedef struct tbs_lattice tbs_lattice;
 

@@ -440,6 +440,8 @@ __global__ __launch_bounds__(kLT) void k_lat_forward(LatticeDev L, GraphDev g0) 
       cur ^= 1;
     }
   }
+  // frames after the stream's end hold no nodes
+  for (size_t i = (size_t)(len + 1) * Ns + tid; i < (size_t)(T + 1) * Ns; i += kLT) al[i] = neg_inf();
   // final weights: the graph's, or 0 for every node if none of them is final
   const int nl = L.nn[(size_t)b * (T + 1) + len];
   const int* pl = L.nodes + ((size_t)len * L.B + b) * Ns * 4;

@@ -324,3 +324,35 @@ def test_nbest_arguments():
         out = lat.nbest(n, u)
         torch.cuda.synchronize()
         assert (_np(out.num_unique) >= 1).all() and (_np(out.num_unique) <= n).all()
+
+
+def test_buffer_reuse_across_sizes():
+    """Lattices built one after another on one model (smaller, equal, larger than the
+    last destroyed one) equal lattices built on fresh models."""
+    import torch
+    from paper_2211_00484_amd import tbs
+    w, inputs, model_np, graph_np = synth.make_workload("graph", B=6)
+    enc = torch.from_numpy(inputs.encoder_out).cuda()
+    u = torch.from_numpy(np.random.default_rng(2).uniform(size=(6, 24, inputs.T + 1))).cuda()
+
+    def build(model, B, T):
+        lat = tbs.Lattice(model, tbs.Graph.from_synth(graph_np), enc[:B, :T].contiguous(),
+                          np.minimum(inputs.lengths[:B], T), beam=4.0, max_states=32,
+                          max_contexts=8)
+        ex = {k: _np(v) for k, v in lat.export().items()}
+        nb = lat.nbest(24, u[:B, :, :T + 1].contiguous(), want_paths=True)
+        res = (ex, _np(nb.tokens), _np(nb.scores), _np(nb.paths))
+        torch.cuda.synchronize()
+        lat.close()
+        return res
+
+    shared = tbs.Model.from_synth(model_np)
+    shared.set_schedule("frame")
+    for B, T in ((6, inputs.T), (3, inputs.T // 2), (3, inputs.T // 2), (6, inputs.T)):
+        fresh = tbs.Model.from_synth(model_np)
+        fresh.set_schedule("frame")
+        a, b = build(shared, B, T), build(fresh, B, T)
+        for k in a[0]:
+            assert np.array_equal(a[0][k], b[0][k]), (B, T, k)
+        for x, y in zip(a[1:], b[1:]):
+            assert np.array_equal(x, y), (B, T)
