@@ -1548,15 +1548,13 @@ tbs_status tbs_hyp_search(const tbs_model* model, const tbs_hyp_params* params,
   d.rowctx = w.rowctx;
   d.hrow = w.hrow;
   d.hist = w.hist;
+  d.enc = encoder_out;
+  d.h = w.h;
   const ModelDev md = model_dev(m);
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * N * 2, -1, st), "fill(trace)");
-  HIP_TRY(launch_hyp_init(d, trace, st), "launch(hyp init)");
+  HIP_TRY(launch_hyp_init(md, d, st), "launch(hyp init)");
   for (int t = 0; t < maxlen; ++t) {
-    HIP_TRY(launch_hyp_rows(d, t, st), "launch(hyp rows)");
-    HIP_TRY(launch_h_rows_dense(md, encoder_out + (size_t)t * m->C, (long long)T * m->C,
-                                w.rowctx, 0, N, B * N, w.h, st),
-            "launch(joiner rows)");
     HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
                          [&] {
                            return launch_joiner_gemm(md, w.h, B * N, w.logits, w.stats, m->ncu,

@@ -12,9 +12,9 @@
 // last label, so sequences are carried as 64-bit hashes (of y and of y without its last
 // label) plus their length; equal hashes are taken as equal sequences.
 //
-// Frame schedule, three launches per frame: k_hyp_rows (each hypothesis's context,
-// distinct contexts to joiner rows), the dense joiner GEMM, k_hyp_step (merge and
-// top-N selection, one workgroup per stream).
+// Frame schedule, two launches per frame: the joiner GEMM over the rows of every
+// stream's distinct hypothesis contexts, then k_hyp_step (one workgroup per stream:
+// merge, top-N selection, and the next frame's joiner rows).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -36,33 +36,19 @@ __device__ __forceinline__ unsigned long long hash_push(unsigned long long h, in
 
 __device__ __forceinline__ double neg_inf_d() { return -__builtin_inf(); }
 
-__global__ void k_hyp_init(HypDev d) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= d.B) return;
-  const size_t o = (size_t)b * d.N;
-  d.nh[0][b] = 1;
-  d.hash[0][o] = kHashInit;
-  d.phash[0][o] = 0;
-  d.n[0][o] = 0;
-  d.ctx[0][o] = 0;
-  d.score[0][o] = 0.0;
-}
-
-// Joiner rows of frame t: the distinct contexts of each stream's hypotheses, one row each
-// at b * N + rank (ascending), -1 for the unused slots; hrow maps hypotheses to rows.
-__global__ __launch_bounds__(64) void k_hyp_rows(HypDev d, int t) {
-  __shared__ int s_c[kMaxHyps];
-  const int b = blockIdx.x, lane = threadIdx.x, N = d.N;
+// Joiner rows of frame t for stream b from the hypotheses in buffer buf: the distinct
+// contexts, ascending, go to rows b * N + r (rowctx, hrow), and each row's input
+// h = tanh(enc[b][t] + ReLU(P0[a] + P1[c])) for context (a, c), fp32 or bf16 (RNE).
+// Every thread of the workgroup calls it.
+__device__ void hyp_rows(const ModelDev& m, const HypDev& d, int b, int t, int buf, int* s_c,
+                         int* s_rc, int* s_nd) {
+  const int tid = threadIdx.x, N = d.N;
   const size_t o = (size_t)b * N;
-  if (t >= d.len[b]) {
-    if (lane < N) d.rowctx[o + lane] = -1;
-    return;
-  }
-  const int cur = t & 1, nh = d.nh[cur][b];
-  const int c = lane < nh ? d.ctx[cur][o + lane] : -1;
-  if (lane < N) s_c[lane] = c;
+  const int nh = d.nh[buf][b];
+  if (tid < N) s_c[tid] = tid < nh ? d.ctx[buf][o + tid] : -1;
   __syncthreads();
-  if (lane < N) {
+  if (tid < N) {
+    const int c = s_c[tid];
     int rank = 0, first = 1, nd = 0;
     for (int j = 0; j < nh; ++j) {
       const int cj = s_c[j];
@@ -72,14 +58,50 @@ __global__ __launch_bounds__(64) void k_hyp_rows(HypDev d, int t) {
         ++nd;
         if (cj < c) ++rank;
       }
-      if (j < lane && cj == c) first = 0;
+      if (j < tid && cj == c) first = 0;
     }
-    if (lane < nh) {
-      d.hrow[o + lane] = rank;
-      if (first) d.rowctx[o + rank] = c;
+    if (tid < nh) {
+      d.hrow[o + tid] = rank;
+      if (first) {
+        d.rowctx[o + rank] = c;
+        s_rc[rank] = c;
+      }
     }
-    if (lane >= nd) d.rowctx[o + lane] = -1;
+    if (tid >= nd) d.rowctx[o + tid] = -1;
+    if (tid == 0) *s_nd = nd;
   }
+  __syncthreads();
+  const int nd = *s_nd, C = m.C, Kpad = m.Kpad, V = m.V;
+  const float* e = d.enc + ((size_t)b * d.T + t) * C;
+  for (int i = tid; i < nd * Kpad; i += blockDim.x) {
+    const int r = i / Kpad, k = i - r * Kpad;
+    const int c = s_rc[r], a = c / V, cc = c - a * V;
+    const float x = k < C ? tanh_fast(e[k] + fmaxf(m.P0[(size_t)a * Kpad + k] +
+                                                   m.P1[(size_t)cc * Kpad + k], 0.f))
+                          : 0.f;
+    const size_t q = (o + r) * Kpad + k;
+    if (m.bf16)
+      reinterpret_cast<uint16_t*>(d.h)[q] = f32_to_bf16_rne(x);
+    else
+      reinterpret_cast<float*>(d.h)[q] = x;
+  }
+}
+
+// The empty hypothesis of every stream and its joiner row for frame 0.
+__global__ __launch_bounds__(256) void k_hyp_init(ModelDev m, HypDev d) {
+  __shared__ int s_c[kMaxHyps], s_rc[kMaxHyps], s_nd;
+  const int b = blockIdx.x;
+  const size_t o = (size_t)b * d.N;
+  if (threadIdx.x == 0) {
+    d.nh[0][b] = 1;
+    d.hash[0][o] = kHashInit;
+    d.phash[0][o] = 0;
+    d.n[0][o] = 0;
+    d.ctx[0][o] = 0;
+    d.score[0][o] = 0.0;
+  }
+  __syncthreads();
+  if (d.len[b] > 0) hyp_rows(m, d, b, 0, 0, s_c, s_rc, &s_nd);
 }
 
 // (score, first, slot) ordered by score desc, then first asc.
@@ -103,6 +125,7 @@ __global__ __launch_bounds__(kHT) void k_hyp_step(ModelDev m, HypDev d, int t,
   __shared__ unsigned long long s_h[kMaxHyps];
   __shared__ Cand s_w[kHT / 64];
   __shared__ Cand s_win[kMaxHyps];
+  __shared__ int s_hc[kMaxHyps], s_hrc[kMaxHyps], s_hnd;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (t >= d.len[b]) return;
   const int N = d.N, V = m.V, Vpad = m.Vpad, nvt = m.Vpad / kJoinerBN;
@@ -264,6 +287,11 @@ __global__ __launch_bounds__(kHT) void k_hyp_step(ModelDev m, HypDev d, int t,
     }
   }
   if (tid == 0) d.nh[nx][b] = kept;
+  if (t + 1 < d.len[b]) {  // uniform: the next frame's joiner rows
+    __syncthreads();  // the kept hypotheses (and their count) are written
+    __threadfence_block();
+    hyp_rows(m, d, b, t + 1, nx, s_hc, s_hrc, &s_hnd);
+  }
 }
 
 // Result: the first hypothesis after the stream's last frame, traced back.
@@ -298,14 +326,8 @@ __global__ __launch_bounds__(64) void k_hyp_final(HypDev d, int* out_tokens, int
 
 }  // namespace
 
-hipError_t launch_hyp_init(const HypDev& d, int* trace, hipStream_t st) {
-  (void)trace;
-  hipLaunchKernelGGL(k_hyp_init, dim3((d.B + 63) / 64), dim3(64), 0, st, d);
-  return hipGetLastError();
-}
-
-hipError_t launch_hyp_rows(const HypDev& d, int t, hipStream_t st) {
-  hipLaunchKernelGGL(k_hyp_rows, dim3(d.B), dim3(64), 0, st, d, t);
+hipError_t launch_hyp_init(const ModelDev& m, const HypDev& d, hipStream_t st) {
+  hipLaunchKernelGGL(k_hyp_init, dim3(d.B), dim3(256), 0, st, m, d);
   return hipGetLastError();
 }
 

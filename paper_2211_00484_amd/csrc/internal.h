@@ -27,6 +27,21 @@ constexpr int kTransducerMaxK = 16;  // transducer recursions: cells per lane (U
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
+// Round to the nearest bfloat16, ties to even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// tanh for the joiner input: (e - 1) / (e + 1), e = exp(2x), with x clamped to [-9, 9]
+// (|tanh(9)| rounds to 1 in fp32), the hardware exp and reciprocal.
+__device__ __forceinline__ float tanh_fast(float x) {
+  const float xc = fminf(fmaxf(x, -9.f), 9.f);
+  const float e = __expf(2.f * xc);
+  return (e - 1.f) * __builtin_amdgcn_rcpf(e + 1.f);
+}
+
 // Device-side model tables (padded: rows to Vpad, columns to Kpad, zeros).
 struct ModelDev {
   int V, C, Kpad, Vpad;
@@ -206,6 +221,8 @@ hipError_t launch_joiner_gemm(const ModelDev& m, const void* h, int R, float* lo
 struct HypDev {
   int B, T, N, merge_logadd;
   const int* len;                     // [B]
+  const float* enc;                   // [B][T][C] encoder output
+  void* h;                            // [B*N][Kpad] joiner rows of the next frame
   unsigned long long* hash[2];        // [B][N] per frame parity: hash of the sequence
   unsigned long long* phash[2];       // hash of the sequence without its last label
   int* n[2];                          // sequence length
@@ -216,8 +233,7 @@ struct HypDev {
   int* hrow;                          // [B*N] joiner row of each hypothesis
   int* hist;                          // [T][B][N] parent << 16 | label
 };
-hipError_t launch_hyp_init(const HypDev& d, int* trace, hipStream_t st);
-hipError_t launch_hyp_rows(const HypDev& d, int t, hipStream_t st);
+hipError_t launch_hyp_init(const ModelDev& m, const HypDev& d, hipStream_t st);
 hipError_t launch_hyp_step(const ModelDev& m, const HypDev& d, int t, const float* logits,
                            const float2* stats, int* trace, hipStream_t st);
 hipError_t launch_hyp_final(const HypDev& d, int* out_tokens, int* out_ntok, double* out_scores,

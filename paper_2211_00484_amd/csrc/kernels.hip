@@ -34,11 +34,6 @@ constexpr unsigned long long kEmpty = ~0ull;
 // ---------------------------------------------------------------------------
 // small helpers
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest, ties to even (finite inputs)
-  return (uint16_t)(u >> 16);
-}
 
 // Order-preserving map float -> uint32 (larger float -> larger code).
 __device__ __forceinline__ uint32_t f2ord(float f) {
@@ -199,15 +194,8 @@ __global__ void k_fill_i32(int* p, long long n, int v) {
 }
 
 // ---------------------------------------------------------------------------
-// tanh from the hardware exp and reciprocal: (e - 1) / (e + 1), e = exp(2x), with
-// x clamped to [-9, 9] (|tanh(9)| rounds to 1 in fp32); the quotient takes the
-// hardware reciprocal (1 ulp).  Absolute error ~2e-7, which moves a joiner logit
-// by at most ~C * max|W| * 2e-7.
-__device__ __forceinline__ float tanh_fast(float x) {
-  const float xc = fminf(fmaxf(x, -9.f), 9.f);
-  const float e = __expf(2.f * xc);
-  return (e - 1.f) * __builtin_amdgcn_rcpf(e + 1.f);
-}
+// tanh_fast (internal.h) has absolute error ~2e-7, which moves a joiner logit by at
+// most ~C * max|W| * 2e-7.
 
 // Joiner input rows (Algorithm 1: decoder, IndexSelect of the encoder frame):
 // h[k] = tanh(enc[k] + ReLU(P0[a][k] + P1[b][k])) for k < C, 0 for C <= k < Kpad,
