@@ -46,8 +46,10 @@ def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles, Ns, frames=None):
     one logit per arc.  Trivial graph: arcs are implicit (every label); the joiner
     keeps each row's best Ns labels per 16-column sub-tile, and the search reads those
     lists (value + label) and the blank logit instead."""
-    trivial = graph.num_states == 1 and graph.num_arcs == V - 1
-    deg = np.diff(graph.row_ptr).astype(np.int64)
+    graphs = list(graph) if isinstance(graph, (list, tuple)) else None
+    g0 = graphs[0] if graphs else graph
+    trivial = not graphs and g0.num_states == 1 and g0.num_arcs == V - 1
+    degs = [np.diff(g.row_ptr).astype(np.int64) for g in (graphs or [g0])]
     rows = 0
     cands = 0
     arcs = 0
@@ -55,6 +57,7 @@ def algorithmic_work(trace, lengths, graph, V, C, Vpad_tiles, Ns, frames=None):
     survivors_out = 0
     for b in range(trace.shape[1]):
         L = int(lengths[b])
+        deg = degs[b] if graphs else degs[0]
         for f in (range(L) if frames is None else range(frames[0], min(frames[1], L))):
             cur = trace[f, b]
             n = int((cur[:, 0] >= 0).sum())
@@ -274,6 +277,70 @@ def decode_roofline(prof, K, work, dtype):
                         "peak": PEAK["hbm_gbps"], "unit": "GB/s",
                         "frac": s_gbps / PEAK["hbm_gbps"]}
     return kernels, roofline, schedule, j_tflops, s_gbps, peak_j
+
+
+def chunked_bench(args, w, inputs, model_np, graph_np, model, graph, enc, dtype, K, W):
+    """One step: a decode state for the batch, its frames in chunks of N (every stream
+    advances by up to N frames per chunk), then finish."""
+    import torch
+    from paper_2211_00484_amd import tbs
+    N = args.chunk
+    B, T = inputs.B, inputs.T
+    lens = inputs.lengths
+    frames = int(lens.sum())
+    chunks = []
+    for c0 in range(0, T, N):
+        piece = np.clip(lens - c0, 0, N).astype(np.int32)
+        if piece.max() == 0:
+            break
+        chunks.append((enc[:, c0:c0 + int(piece.max())].contiguous(), piece))
+    tr_out = tbs.decode(model, graph, enc, lens, beam=w.beam, max_states=w.max_states,
+                        max_contexts=w.max_contexts, want_trace=True)
+    torch.cuda.synchronize()
+    work = algorithmic_work(tr_out.trace.cpu().numpy(), lens, graph_np, w.V, w.C,
+                            (w.V + 63) // 64, w.max_states)
+    del tr_out
+
+    def step():
+        st = tbs.DecodeState(model, graph, B, T, beam=w.beam, max_states=w.max_states,
+                             max_contexts=w.max_contexts)
+        for x, piece in chunks:
+            st.chunk(x, piece)
+        out = st.finish()
+        st.close()
+        return out
+
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    model.set_profiling(True)
+    for _ in range(K):
+        step()
+    torch.cuda.synchronize()
+    prof = model.read_profile()
+    model.set_profiling(False)
+    kernels, roofline, schedule, j_tflops, s_gbps, peak_j = decode_roofline(prof, K, work, dtype)
+    roofline["traffic"] = None  # counters are taken for the one-shot decode
+    line = {
+        "metric": METRIC + " (streaming: chunked decode)", "value": frames * K / (t1 - t0),
+        "unit": "frames/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": (t1 - t0) * 1e3 / K, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if dtype == "fp32" else "bf16 joiner operands",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}+chunk{N}", "description": w.description, "B": B,
+                   "T_max": T, "frames": frames, "chunk_frames": N, "chunks": len(chunks),
+                   "per_stream_graphs": "2 alternating" if args.alt_graphs else None,
+                   "schedule": schedule},
+        "roofline": roofline,
+        "kernels": kernels,
+        "per_chunk_ms": (t1 - t0) * 1e3 / K / max(len(chunks), 1),
+    }
+    print(json.dumps(line), flush=True)
 
 
 def transducer_bench(args):
@@ -565,6 +632,12 @@ def main():
     ap.add_argument("--tr-shape", default="32,250,80", metavar="B,T,U",
                     help="shape for --transducer (default: a training batch of 10 s "
                          "utterances at 25 frames/s with 80 labels)")
+    ap.add_argument("--chunk", type=int, default=0, metavar="N",
+                    help="streaming decode: every step decodes the batch in chunks of N "
+                         "frames (tbs_state_create / tbs_decode_chunk / tbs_state_finish)")
+    ap.add_argument("--alt-graphs", action="store_true",
+                    help="one graph per stream: the workload's graph and a second graph of "
+                         "the same kind (seed 2) alternate over the batch (tbs_decode_graphs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="threads for the oracle baseline (default: all host threads)")
@@ -603,6 +676,17 @@ def main():
     enc = torch.from_numpy(inputs.encoder_out).cuda()
     B, T = inputs.B, inputs.T
     frames = int(inputs.lengths.sum())
+    if args.alt_graphs:
+        if w.graph == "trivial":
+            sys.exit("--alt-graphs needs a workload with a general graph (graph, large)")
+        g2_np = synth.power_law_graph(1_000_000, 5_000_000, w.V, seed=2) \
+            if w.graph == "powerlaw1m" else synth.uniform_random_graph(5000, 100_000, w.V, seed=2)
+        g2 = tbs.Graph.from_synth(g2_np)
+        graph = [graph if b % 2 == 0 else g2 for b in range(B)]
+        graph_np = [graph_np if b % 2 == 0 else g2_np for b in range(B)]
+    if args.chunk:
+        chunked_bench(args, w, inputs, model_np, graph_np, model, graph, enc, dtype, K, W)
+        return
 
     # untimed decode with the survivor trace: algorithmic work of one step
     tr_out = tbs.decode(model, graph, enc, inputs.lengths, beam=w.beam, max_states=w.max_states,
@@ -611,6 +695,7 @@ def main():
     nvt = (w.V + 63) // 64
     work = algorithmic_work(tr_out.trace.cpu().numpy(), inputs.lengths, graph_np, w.V, w.C, nvt,
                             w.max_states)
+    g_desc = graph_np[0] if isinstance(graph_np, list) else graph_np
     del tr_out
 
     if args.search == "hyps":
@@ -662,7 +747,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "B": B, "T_max": T,
                    "frames": frames, "C": w.C, "V": w.V, "graph": w.graph,
-                   "graph_states": graph_np.num_states, "graph_arcs": graph_np.num_arcs,
+                   "graph_states": g_desc.num_states, "graph_arcs": g_desc.num_arcs,
+                   "per_stream_graphs": "2 alternating" if args.alt_graphs else None,
                    "beam": "inf" if math.isinf(w.beam) else w.beam,
                    "max_states": w.max_states, "max_contexts": w.max_contexts,
                    "joiner": dtype, "schedule": schedule},
