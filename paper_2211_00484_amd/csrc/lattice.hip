@@ -670,6 +670,11 @@ __global__ __launch_bounds__(kLT) void k_lat_seqscore(LatticeDev L, NBestDev N) 
   const double* fw = L.fw + (size_t)b * Ns;
   const double* al_len = L.alpha + ((size_t)b * (T + 1) + len) * Ns;
   const int nl = L.nn[(size_t)b * (T + 1) + len];
+  // the stream's largest node count sizes the DP buffers (usually far below Ns)
+  int nmax = 1;
+  for (int f = lane; f <= len; f += 64) nmax = max(nmax, L.nn[(size_t)b * (T + 1) + f]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) nmax = max(nmax, __shfl_xor(nmax, o, 64));
   for (int u0 = blockIdx.x * kSeqWaves; u0 < nu; u0 += gridDim.x * kSeqWaves) {
     const int u = u0 + wv;
     const bool act = u < nu;
@@ -688,12 +693,12 @@ __global__ __launch_bounds__(kLT) void k_lat_seqscore(LatticeDev L, NBestDev N) 
       else
         y = yg;
       W = (Ly < len - Ly ? Ly : len - Ly) + 1;
-      in_lds = 2 * Ns * W <= kSeqLds;
+      in_lds = 2 * nmax * W <= kSeqLds;
       if (!in_lds) A0 = gdp;  // the host allots it whenever a band may not fit
       if (lane == 0) A0[0] = 1.0;  // frame 0: the initial node, nothing consumed
     }
     double* cur = A0;
-    double* nxt = A0 + (size_t)Ns * W;
+    double* nxt = A0 + (size_t)nmax * W;
     double logscale = 0.0;
     int lo = 0, hi = 0;
     for (int f0 = 0; f0 < len; f0 = s.hi) {
