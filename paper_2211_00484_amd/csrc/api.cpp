@@ -79,14 +79,14 @@ struct Workspace {
   bool pending = false;
 
   void release() {
-    hipFree(len); hipFree(nsurv); hipFree(surv_ctx); hipFree(surv_state); hipFree(surv_score);
-    hipFree(surv_row); hipFree(nctx); hipFree(ctx_list); hipFree(offset); hipFree(h);
-    hipFree(logits); hipFree(stats); hipFree(tk_z); hipFree(tk_c); hipFree(z0);
-    hipFree(hist_pl); hipFree(hist_arc); hipFree(path_lab);
-    hipFree(gtab);
-    if (len_host) hipHostFree(len_host);
-    if (gtab_host) hipHostFree(gtab_host);
-    if (done) hipEventDestroy(done);
+    (void)hipFree(len); (void)hipFree(nsurv); (void)hipFree(surv_ctx); (void)hipFree(surv_state); (void)hipFree(surv_score);
+    (void)hipFree(surv_row); (void)hipFree(nctx); (void)hipFree(ctx_list); (void)hipFree(offset); (void)hipFree(h);
+    (void)hipFree(logits); (void)hipFree(stats); (void)hipFree(tk_z); (void)hipFree(tk_c); (void)hipFree(z0);
+    (void)hipFree(hist_pl); (void)hipFree(hist_arc); (void)hipFree(path_lab);
+    (void)hipFree(gtab);
+    if (len_host) (void)hipHostFree(len_host);
+    if (gtab_host) (void)hipHostFree(gtab_host);
+    if (done) (void)hipEventDestroy(done);
     *this = Workspace();
   }
 };
@@ -252,11 +252,11 @@ tbs_status graph_upload(tbs_graph* g, const int32_t* row_ptr, const int32_t* des
 
 void graph_free(tbs_graph* g) {
   if (!g) return;
-  hipFree(g->rp);
-  hipFree(g->dest);
-  hipFree(g->label);
-  hipFree(g->q);
-  hipFree(g->fin);
+  (void)hipFree(g->rp);
+  (void)hipFree(g->dest);
+  (void)hipFree(g->label);
+  (void)hipFree(g->q);
+  (void)hipFree(g->fin);
   delete g;
 }
 
@@ -301,7 +301,7 @@ hipError_t timed_launch(tbs_model* m, int kernel, hipStream_t st, F fn) {
 
 void prof_drop(tbs_model* m) {
   for (auto& x : m->prof_pending) {
-    hipEventSynchronize(x.stop);
+    (void)hipEventSynchronize(x.stop);
     m->prof_pool.push_back(x.start);
     m->prof_pool.push_back(x.stop);
   }
@@ -359,7 +359,7 @@ tbs_status ensure_workspace(tbs_model* m, int B, int T, int Ns, int Nc, int KT,
       (w.has_logits || !need_logits))
     return TBS_OK;
   if (w.done) {
-    if (w.pending) hipEventSynchronize(w.done);
+    if (w.pending) (void)hipEventSynchronize(w.done);
     w.release();
   }
   tbs_status st = alloc_workspace(m, w, B, T, Ns, Nc, KT, need_logits);
@@ -733,32 +733,32 @@ void tbs_model_destroy(tbs_model* m) {
   if (!m) return;
   {
     std::lock_guard<std::mutex> lk(m->mu);
-    if (m->ws.done && m->ws.pending) hipEventSynchronize(m->ws.done);
+    if (m->ws.done && m->ws.pending) (void)hipEventSynchronize(m->ws.done);
     m->ws.release();
     m->hw.release();
     if (m->lat_cache) lattice_free(m->lat_cache);
     m->lat_cache = nullptr;
   }
   prof_drop(m);
-  for (hipEvent_t e : m->prof_pool) hipEventDestroy(e);
-  hipFree(m->P0);
-  hipFree(m->P1);
-  hipFree(m->Wf);
-  hipFree(m->Wb);
-  hipFree(m->Wi);
-  hipFree(m->bias);
-  hipFree(m->xerr);
+  for (hipEvent_t e : m->prof_pool) (void)hipEventDestroy(e);
+  (void)hipFree(m->P0);
+  (void)hipFree(m->P1);
+  (void)hipFree(m->Wf);
+  (void)hipFree(m->Wb);
+  (void)hipFree(m->Wi);
+  (void)hipFree(m->bias);
+  (void)hipFree(m->xerr);
   if (m->busy) {
-    if (m->busy_pending) hipEventSynchronize(m->busy);
-    hipEventDestroy(m->busy);
+    if (m->busy_pending) (void)hipEventSynchronize(m->busy);
+    (void)hipEventDestroy(m->busy);
   }
   if (m->xbuf.p) {
     std::lock_guard<std::mutex> xl(g_xmu);
     g_xfree.push_back(m->xbuf);
   }
-  hipFree(m->rows_h);
-  hipFree(m->rows_logits);
-  hipFree(m->rows_stats);
+  (void)hipFree(m->rows_h);
+  (void)hipFree(m->rows_logits);
+  (void)hipFree(m->rows_stats);
   delete m;
 }
 
@@ -884,9 +884,9 @@ tbs_status state_create_impl(const tbs_model* model, const tbs_graph* graph,
     if (e != hipSuccess) s = hip_fail(e, who);
   }
   if (s != TBS_OK) {
-    if (S->w.pending) hipEventSynchronize(S->w.done);
+    if (S->w.pending) (void)hipEventSynchronize(S->w.done);
     S->w.release();
-    hipFree(S->xerr);
+    (void)hipFree(S->xerr);
     delete S;
     return s;
   }
@@ -969,23 +969,23 @@ struct tbs_lattice {
     return L;
   }
   void free_nbest() {
-    hipFree(seq); hipFree(pntok); hipFree(hash); hipFree(first); hipFree(nuniq);
-    hipFree(uscore); hipFree(dp);
+    (void)hipFree(seq); (void)hipFree(pntok); (void)hipFree(hash); (void)hipFree(first); (void)hipFree(nuniq);
+    (void)hipFree(uscore); (void)hipFree(dp);
     seq = pntok = first = nuniq = nullptr;
     hash = nullptr;
     uscore = dp = nullptr;
     ncap = 0;
   }
   void release() {
-    if (done && pending) hipEventSynchronize(done);
+    if (done && pending) (void)hipEventSynchronize(done);
     free_nbest();
-    hipFree(len); hipFree(trace); hipFree(tokens); hipFree(ntok); hipFree(scores);
-    hipFree(dstatus); hipFree(gtab); hipFree(nn); hipFree(cnt); hipFree(off); hipFree(dptr);
-    hipFree(arcs); hipFree(w); hipFree(pc); hipFree(rowctx); hipFree(alpha); hipFree(fw); hipFree(total);
-    hipFree(status); hipFree(h); hipFree(logits); hipFree(stats);
-    if (len_host) hipHostFree(len_host);
-    if (gtab_host) hipHostFree(gtab_host);
-    if (done) hipEventDestroy(done);
+    (void)hipFree(len); (void)hipFree(trace); (void)hipFree(tokens); (void)hipFree(ntok); (void)hipFree(scores);
+    (void)hipFree(dstatus); (void)hipFree(gtab); (void)hipFree(nn); (void)hipFree(cnt); (void)hipFree(off); (void)hipFree(dptr);
+    (void)hipFree(arcs); (void)hipFree(w); (void)hipFree(pc); (void)hipFree(rowctx); (void)hipFree(alpha); (void)hipFree(fw); (void)hipFree(total);
+    (void)hipFree(status); (void)hipFree(h); (void)hipFree(logits); (void)hipFree(stats);
+    if (len_host) (void)hipHostFree(len_host);
+    if (gtab_host) (void)hipHostFree(gtab_host);
+    if (done) (void)hipEventDestroy(done);
   }
 };
 
@@ -1264,10 +1264,10 @@ void tbs_state_destroy(tbs_state* S) {
   if (!S) return;
   {
     std::lock_guard<std::mutex> lk(S->m->mu);
-    if (S->w.pending) hipEventSynchronize(S->w.done);
+    if (S->w.pending) (void)hipEventSynchronize(S->w.done);
     S->w.release();
   }
-  hipFree(S->xerr);
+  (void)hipFree(S->xerr);
   delete S;
 }
 
@@ -1284,9 +1284,9 @@ tbs_status tbs_joiner_logp(const tbs_model* model, const float* enc_rows, const 
   const int Rpad = round_up(R, 64);
   if (Rpad > m->rows_cap) {
     HIP_TRY(hipStreamSynchronize(st), "hipStreamSynchronize");
-    hipFree(m->rows_h);
-    hipFree(m->rows_logits);
-    hipFree(m->rows_stats);
+    (void)hipFree(m->rows_h);
+    (void)hipFree(m->rows_logits);
+    (void)hipFree(m->rows_stats);
     m->rows_h = nullptr;
     m->rows_logits = nullptr;
     m->rows_stats = nullptr;
