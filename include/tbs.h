@@ -393,8 +393,8 @@ tbs_status tbs_transducer_forward(int32_t kind, const float *blank, const float 
  *                        vocabulary columns), G workgroups share each stream:
  *                        each computes its columns of the joiner, they exchange
  *                        per-row normaliser terms and best labels every frame
- *                        through tagged words in uncached device memory
- *                        (cooperative launch), and all run the same search.
+ *                        through tagged words in device memory (device-scope
+ *                        atomics; cooperative launch), and all run the same search.
  *                        out_status[b] = 2 reports an exchange wait that timed
  *                        out (results of that decode are then not valid);
  *   TBS_SCHEDULE_AUTO    (default) STREAM when it fits, the joiner weight

@@ -146,11 +146,11 @@ struct tbs_graph {
   float* fin = nullptr;
 };
 
-// Exchange buffers of the grouped per-stream kernel: uncached device memory, which
-// must not be freed once a kernel has read it, so a destroyed model returns its
-// buffer to a per-process free list for later models instead.  Words carry a
-// 16-bit decode epoch; when the process-wide epoch wraps, a buffer is cleared
-// before its next use.
+// Exchange buffers of the grouped per-stream kernel (device memory, accessed with
+// device-scope atomics).  A destroyed model returns its buffer to a per-process free
+// list for later models, which then skip the allocation and the clear.  Words carry a
+// 16-bit decode epoch; when the process-wide epoch wraps, a buffer is cleared before
+// its next use.
 struct XBuf {
   int dev = -1;
   unsigned long long* p = nullptr;
@@ -388,7 +388,7 @@ hipError_t ensure_xbuf(tbs_model* m, size_t words, hipStream_t st) {
     XBuf x;
     x.dev = m->dev;
     x.words = words;
-    hipError_t e = hipExtMallocWithFlags((void**)&x.p, words * 8, hipDeviceMallocUncached);
+    hipError_t e = hipMalloc((void**)&x.p, words * 8);
     if (e != hipSuccess) return e;
     x.wrap = ~0u;  // cleared below
     m->xbuf = x;

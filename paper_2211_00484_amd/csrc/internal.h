@@ -122,7 +122,7 @@ StreamPlan plan_stream(const ModelDev& m, int Nc, int KT, int trivial);
 
 // Grouped per-stream kernel (trivial graph, fp32): G workgroups per stream, each with
 // Vpad / 64 / G (1 or 2) column groups; cooperative launch of B * G workgroups.
-// xbuf: uncached device memory of at least B * G * 2 * group_words(Nc, KT) words.
+// xbuf: device memory of at least B * G * 2 * group_words(Nc, KT) words.
 int group_words(int Nc, int KT);
 hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
                                int* trace, const StreamPlan& p, unsigned long long* xbuf, int G,

@@ -2076,7 +2076,8 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
 // Member g computes the joiner for its NCG 64-column groups starting at cg0 = g NCG,
 // and every member runs the same search on the same data, so they stay identical;
 // per frame they exchange each row's (max, sum exp), best KT labels and blank logit
-// through tagged 64-bit words in uncached memory.
+// through tagged 64-bit words: relaxed device-scope atomic stores and loads, coherent
+// across the compute units and L2 caches of every XCD.
 
 constexpr int kResSlices = kKStep / 16;  // 16-byte k slices per wave of a resident W slice
 
@@ -2174,7 +2175,7 @@ static_assert(offsetof(SearchSmem, uv) == offsetof(SearchSmem, uk) + sizeof(Sear
 
 // Exchange slot of (stream b, member g, frame parity): Nc rows of RW words.
 struct GroupX {
-  unsigned long long* buf;  // uncached device memory
+  unsigned long long* buf;  // device memory (device-scope atomics only)
   int G, xwords;            // members per stream; words per slot
   unsigned epoch;           // decode number (16 bits), tags are epoch << 16 | frame
   unsigned spin_limit;      // polls before a wait is abandoned (recorded in err)
@@ -2369,17 +2370,17 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         unsigned long long* w = slot + (size_t)j * RW;
         const unsigned long long tg = (unsigned long long)tag << 32;
         if (lane == 0) {
-          __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-          __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           const float z0 = cg0 == 0 ? z[0] : 0.f;  // lane 0 of the first member holds label 0
           __hip_atomic_store(w + 2 + 2 * KT, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_SYSTEM);
+                             __HIP_MEMORY_SCOPE_AGENT);
         }
         if (lane < KT) {
           __hip_atomic_store(w + 2 + 2 * lane, tg | __float_as_uint(my_z), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_SYSTEM);
+                             __HIP_MEMORY_SCOPE_AGENT);
           __hip_atomic_store(w + 3 + 2 * lane, tg | (unsigned)my_c, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_SYSTEM);
+                             __HIP_MEMORY_SCOPE_AGENT);
         }
       }
     }
@@ -2390,14 +2391,14 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
       for (int idx = tid; idx < total; idx += blockDim.x) {
         const int g2 = idx / per, rest = idx - g2 * per;
         const unsigned long long* w = group_slot(x, b, g2, t) + rest;
-        unsigned long long v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        unsigned long long v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         unsigned n = 0;
         while ((unsigned)(v >> 32) != tag) {
           if (++n > x.spin_limit) {
             atomicAdd(x.err, 1u);
             break;
           }
-          v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         xs[idx] = (unsigned)v;
       }
