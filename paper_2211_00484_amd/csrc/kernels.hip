@@ -22,6 +22,7 @@
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
+#include <type_traits>
 
 namespace tbs {
 namespace {
@@ -528,11 +529,14 @@ __global__ __launch_bounds__(256) void k_joiner_small(ModelDev m, JoinArgs a) {
   joiner_tile_small<BF16, MB, TOPK>(m, a, ct, rt, smem, js);
 }
 
+constexpr float kLog2e = 1.44269504088896341f;
+
 // Joiner GEMM tile: 128 rows x 128 vocabulary columns, four waves in a 2 x 2 grid,
 // each wave 64 rows x 64 columns (4 x 4 MFMA blocks of 16 x 16).  Both operands go
 // through LDS in K slices of 128 bytes per row (64 bf16 or 32 fp32 values), two
-// buffers deep: while the waves run the MFMAs of slice s, slice s + 1 is fetched
-// into registers and then written to the other buffer (one barrier per slice).  A
+// buffers deep: while the waves run the MFMAs of slice s, slices s + 1 and s + 2
+// are in flight to registers, and slice s + 1 then goes to the other buffer (one
+// barrier per slice).  A
 // wave's 64 columns are one vocabulary tile, so its epilogue produces that tile's
 // (max, sum exp) per row and either the logits or each row's best labels per
 // 16-column sub-tile.
@@ -568,25 +572,35 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
   const char* hsrc = reinterpret_cast<const char*>(a.h);
   const char* wsrc = BF16 ? reinterpret_cast<const char*>(m.Wb) : reinterpret_cast<const char*>(m.Wf);
   const size_t rowb = (size_t)Kpad * ESZ;
-  uint4 ra[4], rb[4];
-  auto gload = [&](int s) {
+  // two slices in flight: register sets 0 and 1
+  uint4 ra0[4], rb0[4], ra1[4], rb1[4];
+  auto gload = [&](int s, int set) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = tid + 256 * u, row = c >> 3, part = c & 7;
       const size_t off = (size_t)s * kJSlice + part * 16;
-      ra[u] = r0 + row < a.R ? *reinterpret_cast<const uint4*>(hsrc + (size_t)(r0 + row) * rowb + off)
-                             : make_uint4(0, 0, 0, 0);
-      rb[u] = c0 + row < Vpad ? *reinterpret_cast<const uint4*>(wsrc + (size_t)(c0 + row) * rowb + off)
-                              : make_uint4(0, 0, 0, 0);
+      // Rows past the batch or the padded vocabulary read the last valid row: their
+      // products land only in rows and columns the epilogue never writes.  (No
+      // branches around the loads, so their waits stay exact.)
+      const int hr = min(r0 + row, a.R - 1), wr_ = min(c0 + row, Vpad - 1);
+      const uint4 va = *reinterpret_cast<const uint4*>(hsrc + (size_t)hr * rowb + off);
+      const uint4 vb = *reinterpret_cast<const uint4*>(wsrc + (size_t)wr_ * rowb + off);
+      if (set == 0) {
+        ra0[u] = va;
+        rb0[u] = vb;
+      } else {
+        ra1[u] = va;
+        rb1[u] = vb;
+      }
     }
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](int buf, int set) {
     unsigned char* base = smem + (size_t)buf * kJStage;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = tid + 256 * u, row = c >> 3, part = c & 7;
-      *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + part * 16) = ra[u];
-      *reinterpret_cast<uint4*>(base + (size_t)(kJBM + row) * kJRow + part * 16) = rb[u];
+      *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + part * 16) = set == 0 ? ra0[u] : ra1[u];
+      *reinterpret_cast<uint4*>(base + (size_t)(kJBM + row) * kJRow + part * 16) = set == 0 ? rb0[u] : rb1[u];
     }
   };
   f32x4 acc[4][4];
@@ -630,75 +644,103 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
       }
     }
   };
-  const int nsl = (int)(rowb / kJSlice);  // Kpad is a multiple of 512: 8 (bf16) or 16 (fp32) per 512
-  gload(0);
-  lstore(0);
+  // Slice s + 2 is requested before the MFMAs of slice s, so each fetch has two
+  // slices of MFMAs to land; slice s + 1 goes to the other LDS buffer after them.
+  const int nsl = (int)(rowb / kJSlice);  // Kpad is a multiple of 512: 8 (bf16) or 16 (fp32) per 512 (even)
+  gload(0, 0);
+  gload(1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  lstore(0, 0);
   __syncthreads();
-  for (int s = 0; s < nsl; ++s) {
-    if (s + 1 < nsl) gload(s + 1);
-    compute(s & 1);
-    if (s + 1 < nsl) lstore((s + 1) & 1);
+  // (the scheduling barriers keep each fetch ahead of the MFMAs and LDS writes
+  // that follow it, where the compiler would otherwise sink it)
+  for (int s = 0; s + 2 < nsl; s += 2) {
+    gload(s + 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(0);
+    lstore(1, 1);
+    __syncthreads();
+    gload(s + 3, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1);
+    lstore(0, 0);
     __syncthreads();
   }
+  compute(0);  // the last two slices
+  lstore(1, 1);
+  __syncthreads();
+  compute(1);
 
   // epilogue of this wave's vocabulary tile (none beyond the padded vocabulary)
   if (vt >= nvt) return;
-  float bias[4];
-  bool cvalid[4];
-#pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
-    const int col = 64 * vt + 16 * nb + lr;
-    cvalid[nb] = col < V;
-    bias[nb] = cvalid[nb] ? m.bias[col] : 0.f;
-  }
   const int nsub = nvt * (kJoinerBN / 16);
+  // FULL: every column of the tile is a label (all but the last tile), so no
+  // per-column validity selects
+  auto epilogue = [&](auto full_tag) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    float bias[4];
+    bool cvalid[4];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) {
+    for (int nb = 0; nb < 4; ++nb) {
+      const int col = 64 * vt + 16 * nb + lr;
+      cvalid[nb] = FULL || col < V;
+      bias[nb] = cvalid[nb] ? m.bias[col] : 0.f;
+    }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = 64 * wr + 16 * mb + 4 * lg + i;  // the 16 lanes of a DPP row share it
-      const bool ract = s_act[row];
-      float z[4];
-      float mx = -INFINITY;
+    for (int mb = 0; mb < 4; ++mb) {
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        z[nb] = cvalid[nb] ? acc[mb][nb][i] + bias[nb] : -INFINITY;
-        mx = fmaxf(mx, z[nb]);
-      }
-      const float M = row16_max(mx);
-      float e = 0.f;
+      for (int i = 0; i < 4; ++i) {
+        const int row = 64 * wr + 16 * mb + 4 * lg + i;  // the 16 lanes of a DPP row share it
+        const bool ract = s_act[row];
+        float z[4];
+        float mx = -INFINITY;
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) e += cvalid[nb] ? expf(z[nb] - M) : 0.f;
-      const float S = row16_sum(e);
-      if (ract && lr == 0) a.stats[(size_t)(r0 + row) * nvt + vt] = make_float2(M, S);
+        for (int nb = 0; nb < 4; ++nb) {
+          z[nb] = cvalid[nb] ? acc[mb][nb][i] + bias[nb] : -INFINITY;
+          mx = fmaxf(mx, z[nb]);
+        }
+        const float M = row16_max(mx);
+        // sum of e^(z - M) on the base-2 exponential: (z - M) log2(e) <= 0, and its
+        // rounding moves a term by a few ulp at most
+        float e = 0.f;
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const int col = 64 * vt + 16 * nb + lr;
-        if (!TOPK) {
-          if (ract && cvalid[nb]) a.logits[(size_t)(r0 + row) * (nvt * kJoinerBN) + col] = z[nb];
-        } else {
-          // each row's best KT labels of this 16-column sub-tile (DPP row reductions)
-          unsigned long long key = (cvalid[nb] && col >= 1)
-                                       ? ((unsigned long long)f2ord(z[nb]) << 32) | (0xffffffffu - (unsigned)col)
-                                       : 0ull;
-          const size_t ob = ((size_t)(r0 + row) * nsub + vt * (kJoinerBN / 16) + nb) * a.KT;
-          for (int q = 0; q < a.KT; ++q) {
-            const unsigned long long best = row16_max_u64(key);
-            if (ract && best != 0ull && key == best) {
-              a.tk_z[ob + q] = z[nb];
-              a.tk_c[ob + q] = col;
+        for (int nb = 0; nb < 4; ++nb)
+          e += cvalid[nb] ? __builtin_amdgcn_exp2f((z[nb] - M) * kLog2e) : 0.f;
+        const float S = row16_sum(e);
+        if (ract && lr == 0) a.stats[(size_t)(r0 + row) * nvt + vt] = make_float2(M, S);
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+          const int col = 64 * vt + 16 * nb + lr;
+          if (!TOPK) {
+            if (ract && cvalid[nb]) a.logits[(size_t)(r0 + row) * (nvt * kJoinerBN) + col] = z[nb];
+          } else {
+            // each row's best KT labels of this 16-column sub-tile (DPP row reductions)
+            unsigned long long key = (cvalid[nb] && col >= 1)
+                                         ? ((unsigned long long)f2ord(z[nb]) << 32) | (0xffffffffu - (unsigned)col)
+                                         : 0ull;
+            const size_t ob = ((size_t)(r0 + row) * nsub + vt * (kJoinerBN / 16) + nb) * a.KT;
+            for (int q = 0; q < a.KT; ++q) {
+              const unsigned long long best = row16_max_u64(key);
+              if (ract && best != 0ull && key == best) {
+                a.tk_z[ob + q] = z[nb];
+                a.tk_c[ob + q] = col;
+              }
+              if (ract && best == 0ull && lr == 0) {
+                a.tk_z[ob + q] = -INFINITY;
+                a.tk_c[ob + q] = -1;
+              }
+              if (key == best) key = 0ull;
             }
-            if (ract && best == 0ull && lr == 0) {
-              a.tk_z[ob + q] = -INFINITY;
-              a.tk_c[ob + q] = -1;
-            }
-            if (key == best) key = 0ull;
           }
         }
+        if (TOPK && ract && vt == 0 && lr == 0) a.z0[r0 + row] = z[0];
       }
-      if (TOPK && ract && vt == 0 && lr == 0) a.z0[r0 + row] = z[0];
     }
-  }
+  };
+  if (64 * vt + 64 <= V)
+    epilogue(std::true_type{});
+  else
+    epilogue(std::false_type{});
 }
 
 __global__ void k_logp_rows(const float* __restrict__ logits, const float2* __restrict__ stats,
