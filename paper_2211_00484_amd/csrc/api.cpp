@@ -506,7 +506,7 @@ tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
                          [&] { return launch_stream(md, gd, d, beam, trace, splan, st); }),
             "launch(stream)");
   if (!per_stream) {
-    const JoinerPlan plan = plan_joiner(d.B * d.Nc, m->Vpad, m->Kpad, m->bf16, m->ncu);
+    const JoinerPlan plan = plan_joiner(d.B * d.Nc, m->Vpad, m->Kpad, m->bf16, m->ncu, d.KT > 0);
     for (int t = 0; t < maxlen; ++t) {
       HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
                            [&] { return launch_joiner_frame(md, d, plan, t, st); }),

@@ -93,13 +93,15 @@ struct DecodeDev {
 };
 
 struct JoinerPlan {
-  int MB;                   // 0: 128 x 128 GEMM tiles; else 16 MB x 64 tiles
+  int MB;                   // 0: GEMM tiles (128 x 128, or 256 x 256 if wide); else 16 MB x 64 tiles
+  int wide;                 // 1: 256 x 256 GEMM tiles (bf16)
   int n_rt, n_ct;           // row and column tiles
   int grid;                 // workgroups (XCD-interleaved tile order)
   size_t lds;               // dynamic LDS bytes
 };
 
-JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu);
+// topk: the joiner writes each row's best labels (trivial graph) instead of logits
+JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu, bool topk = false);
 
 // Events for the next non-cooperative kernel launch of the calling thread, recorded in
 // that launch's dispatch packet (per-kernel profiling); pending until a launch takes them.

@@ -531,60 +531,84 @@ __global__ __launch_bounds__(256) void k_joiner_small(ModelDev m, JoinArgs a) {
 
 constexpr float kLog2e = 1.44269504088896341f;
 
-// Joiner GEMM tile: 128 rows x 128 vocabulary columns, four waves in a 2 x 2 grid,
-// each wave 64 rows x 64 columns (4 x 4 MFMA blocks of 16 x 16).  Both operands go
-// through LDS in K slices of 128 bytes per row (64 bf16 or 32 fp32 values), two
-// buffers deep: while the waves run the MFMAs of slice s, slices s + 1 and s + 2
-// are in flight to registers, and slice s + 1 then goes to the other buffer (one
-// barrier per slice).  A
-// wave's 64 columns are one vocabulary tile, so its epilogue produces that tile's
-// (max, sum exp) per row and either the logits or each row's best labels per
-// 16-column sub-tile.
-constexpr int kJBM = 128, kJBN = 128;          // tile rows, columns
+// Joiner GEMM tile: BM = 32 MBW rows x BN = 64 WN vocabulary columns, 2 x WN waves,
+// each wave 16 MBW rows x 64 columns (MBW x 4 MFMA blocks of 16 x 16):
+//  - 128 x 128 (MBW = 4, WN = 2; four waves), for batches that give every compute
+//    unit a tile of that size;
+//  - 256 x 256 (MBW = 8, WN = 4; eight waves), for bf16 batches with several such
+//    tiles per compute unit: half the operand bytes per product of the 128 tile, and
+//    a quarter fewer LDS fragment reads per MFMA.
+// Both operands go through LDS in K slices of 128 bytes per row (64 bf16 or 32 fp32
+// values), two buffers deep, one barrier per slice.  The 128 tile keeps slices s + 1
+// and s + 2 in flight to registers during the MFMAs of slice s; the 256 tile, whose
+// slices hold twice the MFMAs, keeps slice s + 1.  A wave's 64 columns are one
+// vocabulary tile, so its epilogue produces that tile's (max, sum exp) per row and
+// either the logits or each row's best labels per 16-column sub-tile.
+constexpr int kJBM = 128, kJBN = 128;          // the 128 tile: rows, columns
 constexpr int kJSlice = 128;                   // bytes of K per row and slice
 constexpr int kJRow = kJSlice + 16;            // LDS row stride (pad: conflict-free fragment reads)
 constexpr int kJStage = (kJBM + kJBN) * kJRow; // bytes per buffer: A rows, then B rows
 constexpr size_t kJLds = 2 * (size_t)kJStage;  // 73,728 bytes
+constexpr int kJWideBM = 256, kJWideBN = 256;  // the 256 tile
+constexpr size_t kJWideLds = 2 * (size_t)(kJWideBM + kJWideBN) * kJRow;  // 147,456 bytes
 
-template <bool BF16, bool TOPK>
-__global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
+template <bool BF16, bool TOPK, int WN, int MBW>
+__global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
+  constexpr int NT = 128 * WN, BM = 32 * MBW, BN = 64 * WN;
+  constexpr int STAGE = (BM + BN) * kJRow;
+  constexpr bool DEEP = MBW == 4;  // two slices in flight (else one)
+  static_assert(BM == NT / 2 && BN == NT / 2, "slice loads: 4 chunks per thread and operand");
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int s_act[kJBM];
-  // Workgroup i runs on XCD i mod 8.  XCD x owns the column tiles x, x + 8, ...
-  // and walks row tiles in order, its column tiles fastest: its W columns stay
-  // in its L2 while each h row tile is read once per XCD.
+  __shared__ int s_act[BM];
   const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
-  const int ncx = (a.n_ct + 7) >> 3;
-  const int rt = slot / ncx, ct = xcd + 8 * (slot - rt * ncx);
-  if (ct >= a.n_ct) return;
+  int rt, ct;
+  if (WN == 2) {
+    // Workgroup i runs on XCD i mod 8.  XCD x owns the column tiles x, x + 8, ...
+    // and walks row tiles in order, its column tiles fastest: its W columns stay
+    // in its L2 while each h row tile is read once per XCD.
+    const int ncx = (a.n_ct + 7) >> 3;
+    rt = slot / ncx;
+    ct = xcd + 8 * (slot - rt * ncx);
+    if (ct >= a.n_ct) return;
+  } else {
+    // Tiles in row-major order, tile q on XCD q mod 8: with a column-tile count that
+    // is not a multiple of 8, each XCD still gets an equal share, and sees only the
+    // column tiles congruent to its index modulo gcd(n_ct, 8).
+    const int q = xcd + 8 * slot;
+    rt = q / a.n_ct;
+    ct = q - rt * a.n_ct;
+    if (rt >= a.n_rt) return;
+  }
   constexpr int ESZ = BF16 ? 2 : 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / WN, wc = wave % WN;
   const int lr = lane & 15, lg = lane >> 4;
-  const int r0 = rt * kJBM, c0 = ct * kJBN;
+  const int r0 = rt * BM, c0 = ct * BN;
   const int Kpad = m.Kpad, V = m.V, Vpad = m.Vpad, nvt = a.nvt;
-  const int vt = 2 * ct + wc;  // this wave's vocabulary tile
-  const int act = tid < kJBM ? (int)joiner_row_active(a, r0 + tid) : 0;
-  if (tid < kJBM) s_act[tid] = act;
+  const int vt = WN * ct + wc;  // this wave's vocabulary tile
+  const int act = tid < BM ? (int)joiner_row_active(a, r0 + tid) : 0;
+  if (tid < BM) s_act[tid] = act;
   if (!__syncthreads_or(act)) return;  // uniform: no active row in this tile
 
-  // slice loads: 4 chunks of 16 bytes per thread for each operand (128 rows x 8 chunks)
+  // slice loads: 4 chunks of 16 bytes per thread for each operand (BM or BN rows x 8 chunks)
   const char* hsrc = reinterpret_cast<const char*>(a.h);
   const char* wsrc = BF16 ? reinterpret_cast<const char*>(m.Wb) : reinterpret_cast<const char*>(m.Wf);
   const size_t rowb = (size_t)Kpad * ESZ;
-  // two slices in flight: register sets 0 and 1
+  const unsigned rowb32 = (unsigned)rowb;  // h and W each stay below 4 GiB (checked at launch)
+  // slices in flight: register sets 0 and 1 (set 1 only with DEEP)
   uint4 ra0[4], rb0[4], ra1[4], rb1[4];
   auto gload = [&](int s, int set) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int c = tid + 256 * u, row = c >> 3, part = c & 7;
+      const int c = tid + NT * u, row = c >> 3, part = c & 7;
       const size_t off = (size_t)s * kJSlice + part * 16;
       // Rows past the batch or the padded vocabulary read the last valid row: their
       // products land only in rows and columns the epilogue never writes.  (No
       // branches around the loads, so their waits stay exact.)
+      // (32-bit offsets from the uniform bases: one register per load address)
       const int hr = min(r0 + row, a.R - 1), wr_ = min(c0 + row, Vpad - 1);
-      const uint4 va = *reinterpret_cast<const uint4*>(hsrc + (size_t)hr * rowb + off);
-      const uint4 vb = *reinterpret_cast<const uint4*>(wsrc + (size_t)wr_ * rowb + off);
+      const uint4 va = *reinterpret_cast<const uint4*>(hsrc + ((unsigned)hr * rowb32 + (unsigned)off));
+      const uint4 vb = *reinterpret_cast<const uint4*>(wsrc + ((unsigned)wr_ * rowb32 + (unsigned)off));
       if (set == 0) {
         ra0[u] = va;
         rb0[u] = vb;
@@ -595,46 +619,55 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
     }
   };
   auto lstore = [&](int buf, int set) {
-    unsigned char* base = smem + (size_t)buf * kJStage;
+    unsigned char* base = smem + (size_t)buf * STAGE;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int c = tid + 256 * u, row = c >> 3, part = c & 7;
+      const int c = tid + NT * u, row = c >> 3, part = c & 7;
       *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + part * 16) = set == 0 ? ra0[u] : ra1[u];
-      *reinterpret_cast<uint4*>(base + (size_t)(kJBM + row) * kJRow + part * 16) = set == 0 ? rb0[u] : rb1[u];
+      *reinterpret_cast<uint4*>(base + (size_t)(BM + row) * kJRow + part * 16) = set == 0 ? rb0[u] : rb1[u];
     }
   };
-  f32x4 acc[4][4];
+  f32x4 acc[MBW][4];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   // one slice of MFMAs from LDS buffer buf; fragments: lane (lr, lg) reads 16 bytes
   // of row lr of a block at byte 64 j + 16 lg of the slice (bf16: k-step j of 32;
   // fp32: group j of 16, the four values feeding four k-steps)
   auto compute = [&](int buf) {
-    const unsigned char* base = smem + (size_t)buf * kJStage;
-    const unsigned char* abase = base + (size_t)(64 * wr + lr) * kJRow + 16 * lg;
-    const unsigned char* bbase = base + (size_t)(kJBM + 64 * wc + lr) * kJRow + 16 * lg;
+    const unsigned char* base = smem + (size_t)buf * STAGE;
+    const unsigned char* abase = base + (size_t)(16 * MBW * wr + lr) * kJRow + 16 * lg;
+    const unsigned char* bbase = base + (size_t)(BM + 64 * wc + lr) * kJRow + 16 * lg;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      uint4 fa[4], fb[4];
+      uint4 fa[MBW], fb[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + 64 * j);
-        fb[q] = *reinterpret_cast<const uint4*>(bbase + (size_t)16 * q * kJRow + 64 * j);
-      }
+      for (int q = 0; q < 4; ++q) fb[q] = *reinterpret_cast<const uint4*>(bbase + (size_t)16 * q * kJRow + 64 * j);
       if (BF16) {
+        // row blocks in groups of 4: with 8 row blocks, the fragments of the second
+        // group are read after the first group's MFMAs (fewer live registers)
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
+        for (int g = 0; g < MBW; g += 4) {
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[mb]), as_bf16x8(fb[nb]),
-                                                                  acc[mb][nb], 0, 0, 0);
+          for (int q = g; q < g + 4; ++q)
+            fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + 64 * j);
+#pragma unroll
+          for (int mb = g; mb < g + 4; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[mb]), as_bf16x8(fb[nb]),
+                                                                    acc[mb][nb], 0, 0, 0);
+          if (MBW > 4) __builtin_amdgcn_sched_barrier(0);
+        }
       } else {
+#pragma unroll
+        for (int q = 0; q < MBW; ++q)
+          fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + 64 * j);
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int mb = 0; mb < 4; ++mb)
+          for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
               const float av = __uint_as_float(u == 0 ? fa[mb].x : u == 1 ? fa[mb].y : u == 2 ? fa[mb].z : fa[mb].w);
@@ -644,32 +677,50 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
       }
     }
   };
-  // Slice s + 2 is requested before the MFMAs of slice s, so each fetch has two
-  // slices of MFMAs to land; slice s + 1 goes to the other LDS buffer after them.
   const int nsl = (int)(rowb / kJSlice);  // Kpad is a multiple of 512: 8 (bf16) or 16 (fp32) per 512 (even)
-  gload(0, 0);
-  gload(1, 1);
-  __builtin_amdgcn_sched_barrier(0);
-  lstore(0, 0);
-  __syncthreads();
-  // (the scheduling barriers keep each fetch ahead of the MFMAs and LDS writes
-  // that follow it, where the compiler would otherwise sink it)
-  for (int s = 0; s + 2 < nsl; s += 2) {
-    gload(s + 2, 0);
+  if constexpr (DEEP) {
+    // Slice s + 2 is requested before the MFMAs of slice s, so each fetch has two
+    // slices of MFMAs to land; slice s + 1 goes to the other LDS buffer after them.
+    // (The scheduling barriers keep each fetch ahead of the MFMAs and LDS writes that
+    // follow it, where the compiler would otherwise sink it.)
+    gload(0, 0);
+    gload(1, 1);
     __builtin_amdgcn_sched_barrier(0);
-    compute(0);
-    lstore(1, 1);
-    __syncthreads();
-    gload(s + 3, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(1);
     lstore(0, 0);
     __syncthreads();
+    for (int s = 0; s + 2 < nsl; s += 2) {
+      gload(s + 2, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      lstore(1, 1);
+      __syncthreads();
+      gload(s + 3, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      lstore(0, 0);
+      __syncthreads();
+    }
+    compute(0);  // the last two slices
+    lstore(1, 1);
+    __syncthreads();
+    compute(1);
+  } else {
+    gload(0, 0);
+    lstore(0, 0);
+    __syncthreads();
+    for (int s = 0; s < nsl; s += 2) {
+      if (s + 1 < nsl) gload(s + 1, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      if (s + 1 < nsl) lstore(1, 0);
+      __syncthreads();
+      if (s + 2 < nsl) gload(s + 2, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      if (s + 2 < nsl) lstore(0, 0);
+      __syncthreads();
+    }
   }
-  compute(0);  // the last two slices
-  lstore(1, 1);
-  __syncthreads();
-  compute(1);
 
   // epilogue of this wave's vocabulary tile (none beyond the padded vocabulary)
   if (vt >= nvt) return;
@@ -687,10 +738,10 @@ __global__ __launch_bounds__(256) void k_joiner(ModelDev m, JoinArgs a) {
       bias[nb] = cvalid[nb] ? m.bias[col] : 0.f;
     }
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
+    for (int mb = 0; mb < MBW; ++mb) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 64 * wr + 16 * mb + 4 * lg + i;  // the 16 lanes of a DPP row share it
+        const int row = 16 * MBW * wr + 16 * mb + 4 * lg + i;  // the 16 lanes of a DPP row share it
         const bool ract = s_act[row];
         float z[4];
         float mx = -INFINITY;
@@ -2765,17 +2816,17 @@ inline int grid_for(long long n, int threads, int cap = 4096) {
   return (int)g;
 }
 
-template <bool BF16, bool TOPK>
+template <bool BF16, bool TOPK, int WN, int MBW>
 hipError_t launch_joiner_t(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p,
                            hipStream_t st) {
   static size_t attr = 0;  // dynamic LDS limit granted so far (kernel default: 64 KiB)
   if (p.lds > 65536 && p.lds > attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_joiner<BF16, TOPK>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_joiner<BF16, TOPK, WN, MBW>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
     if (e != hipSuccess) return e;
     attr = p.lds;
   }
-  launch_k((k_joiner<BF16, TOPK>), dim3(p.grid), dim3(256), p.lds, st, m, a);
+  launch_k((k_joiner<BF16, TOPK, WN, MBW>), dim3(p.grid), dim3(128 * WN), p.lds, st, m, a);
   return hipGetLastError();
 }
 
@@ -2805,10 +2856,21 @@ hipError_t launch_joiner_small(const ModelDev& m, const JoinArgs& a, const Joine
 
 hipError_t launch_joiner(const ModelDev& m, const JoinArgs& a, const JoinerPlan& p, bool topk,
                          hipStream_t st) {
+  if (p.MB == 0) {  // the GEMM tiles address h and W with 32-bit byte offsets
+    const unsigned long long rowb = (unsigned long long)m.Kpad * (m.bf16 ? 2 : 4);
+    if ((unsigned long long)a.R * rowb >= (1ull << 32) || (unsigned long long)m.Vpad * rowb >= (1ull << 32))
+      return hipErrorInvalidValue;
+  }
+  if (p.MB == 0 && p.wide) {  // bf16 logits only
+    if (!m.bf16 || topk) return hipErrorInvalidValue;
+    return launch_joiner_t<true, false, 4, 8>(m, a, p, st);
+  }
   if (p.MB == 0) {
     if (m.bf16)
-      return topk ? launch_joiner_t<true, true>(m, a, p, st) : launch_joiner_t<true, false>(m, a, p, st);
-    return topk ? launch_joiner_t<false, true>(m, a, p, st) : launch_joiner_t<false, false>(m, a, p, st);
+      return topk ? launch_joiner_t<true, true, 2, 4>(m, a, p, st)
+                  : launch_joiner_t<true, false, 2, 4>(m, a, p, st);
+    return topk ? launch_joiner_t<false, true, 2, 4>(m, a, p, st)
+                : launch_joiner_t<false, false, 2, 4>(m, a, p, st);
   }
   if (m.bf16)
     return topk ? launch_joiner_small<true, true>(m, a, p, st) : launch_joiner_small<true, false>(m, a, p, st);
@@ -2832,10 +2894,24 @@ bool take_launch_events(hipEvent_t* start, hipEvent_t* stop) {
   return true;
 }
 
-JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu) {
+JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu, bool topk) {
   JoinerPlan p;
+  p.wide = 0;
   const int esz = bf16 ? 2 : 4;
   const int nvt = Vpad / kJoinerBN;
+  // bf16 logits: 256 x 256 GEMM tiles when they give every compute unit several
+  if (bf16 && !topk) {
+    p.n_rt = (rows + kJWideBM - 1) / kJWideBM;
+    p.n_ct = (nvt * kJoinerBN + kJWideBN - 1) / kJWideBN;
+    const long long tiles = (long long)p.n_rt * p.n_ct;
+    if (tiles >= 4LL * ncu) {
+      p.MB = 0;
+      p.wide = 1;
+      p.grid = (int)(8 * ((tiles + 7) / 8));
+      p.lds = kJWideLds;
+      return p;
+    }
+  }
   // 128 x 128 GEMM tiles when they give every compute unit one (MB = 0)
   p.n_rt = (rows + kJBM - 1) / kJBM;
   p.n_ct = (nvt + 1) / 2;
