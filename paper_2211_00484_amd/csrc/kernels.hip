@@ -546,11 +546,16 @@ constexpr float kLog2e = 1.44269504088896341f;
 // either the logits or each row's best labels per 16-column sub-tile.
 constexpr int kJBM = 128, kJBN = 128;          // the 128 tile: rows, columns
 constexpr int kJSlice = 128;                   // bytes of K per row and slice
-constexpr int kJRow = kJSlice + 16;            // LDS row stride (pad: conflict-free fragment reads)
+constexpr int kJRow = kJSlice;                 // LDS row stride (16-byte chunks swizzled per row)
 constexpr int kJStage = (kJBM + kJBN) * kJRow; // bytes per buffer: A rows, then B rows
-constexpr size_t kJLds = 2 * (size_t)kJStage;  // 73,728 bytes
+constexpr size_t kJLds = 2 * (size_t)kJStage;  // 65,536 bytes
 constexpr int kJWideBM = 256, kJWideBN = 256;  // the 256 tile
-constexpr size_t kJWideLds = 2 * (size_t)(kJWideBM + kJWideBN) * kJRow;  // 147,456 bytes
+constexpr size_t kJWideLds = 2 * (size_t)(kJWideBM + kJWideBN) * kJRow;  // 131,072 bytes
+// LDS chunk swizzle: chunk k of a row with index r mod 16 = l sits at slot k ^ jswz(l).
+// A fragment read (16 rows of a block, one chunk each) then touches 16 distinct 4-bank
+// groups whether the LDS serves 8 lanes from 32 banks or 16 lanes from 64 banks per
+// cycle, and so does a slice write (8 lanes per row, two rows per 16 lanes).
+__device__ __forceinline__ int jswz(int l) { return (l & 7) ^ ((l >> 3) & 1); }
 
 template <bool BF16, bool TOPK, int WN, int MBW>
 __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
@@ -623,8 +628,9 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = tid + NT * u, row = c >> 3, part = c & 7;
-      *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + part * 16) = set == 0 ? ra0[u] : ra1[u];
-      *reinterpret_cast<uint4*>(base + (size_t)(BM + row) * kJRow + part * 16) = set == 0 ? rb0[u] : rb1[u];
+      const int slot = (part ^ jswz(row & 15)) * 16;
+      *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + slot) = set == 0 ? ra0[u] : ra1[u];
+      *reinterpret_cast<uint4*>(base + (size_t)(BM + row) * kJRow + slot) = set == 0 ? rb0[u] : rb1[u];
     }
   };
   f32x4 acc[MBW][4];
@@ -637,13 +643,14 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
   // fp32: group j of 16, the four values feeding four k-steps)
   auto compute = [&](int buf) {
     const unsigned char* base = smem + (size_t)buf * STAGE;
-    const unsigned char* abase = base + (size_t)(16 * MBW * wr + lr) * kJRow + 16 * lg;
-    const unsigned char* bbase = base + (size_t)(BM + 64 * wc + lr) * kJRow + 16 * lg;
+    const unsigned char* abase = base + (size_t)(16 * MBW * wr + lr) * kJRow;
+    const unsigned char* bbase = base + (size_t)(BM + 64 * wc + lr) * kJRow;
+    const int cs = (lg ^ jswz(lr)) * 16;  // chunk lg (j = 0) or 4 + lg (j = 1), swizzled
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       uint4 fa[MBW], fb[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) fb[q] = *reinterpret_cast<const uint4*>(bbase + (size_t)16 * q * kJRow + 64 * j);
+      for (int q = 0; q < 4; ++q) fb[q] = *reinterpret_cast<const uint4*>(bbase + (size_t)16 * q * kJRow + (cs ^ (64 * j)));
       if (BF16) {
         // row blocks in groups of 4: with 8 row blocks, the fragments of the second
         // group are read after the first group's MFMAs (fewer live registers)
@@ -651,7 +658,7 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
         for (int g = 0; g < MBW; g += 4) {
 #pragma unroll
           for (int q = g; q < g + 4; ++q)
-            fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + 64 * j);
+            fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + (cs ^ (64 * j)));
 #pragma unroll
           for (int mb = g; mb < g + 4; ++mb)
 #pragma unroll
@@ -663,7 +670,7 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
       } else {
 #pragma unroll
         for (int q = 0; q < MBW; ++q)
-          fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + 64 * j);
+          fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + (cs ^ (64 * j)));
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
