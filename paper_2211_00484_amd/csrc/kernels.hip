@@ -222,15 +222,13 @@ __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_ro
       const int k = tid + j * NT;
       ro[u] = r;
       ko[u] = k;
-      e[u] = 0.f;
-      p0[u] = 0.f;
-      p1[u] = 0.f;
-      if (r < nrows && k < C) {
-        const int2 off = rowoff[r];
-        e[u] = enc_rows[(size_t)r * enc_stride + k];
-        p0[u] = P0[(size_t)off.x + k];
-        p1[u] = P1[(size_t)off.y + k];
-      }
+      // past the last row or column: load a valid element and drop the result, so
+      // that no branch separates the loads (all of them in flight at once)
+      const int rc = min(r, nrows - 1), kc = min(k, C - 1);
+      const int2 off = rowoff[rc];
+      e[u] = enc_rows[(size_t)rc * enc_stride + kc];
+      p0[u] = P0[(size_t)off.x + kc];
+      p1[u] = P1[(size_t)off.y + kc];
       if (++j == cols) {
         j = 0;
         ++r;
@@ -246,6 +244,57 @@ __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_ro
         reinterpret_cast<uint16_t*>(hbase)[o] = f32_to_bf16_rne(h);
       else
         reinterpret_cast<float*>(hbase)[o] = h;
+    }
+  }
+}
+
+// The same rows for an even C, two adjacent columns per item: thread tid owns the
+// column pairs (2 tid, 2 tid + 1), (2 tid + 2 NT, ...), ... of every row, so a batch
+// of U items issues U 8-byte loads of P0 and of P1 (all in flight at once) and U
+// 8-byte (fp32) or 4-byte (bf16) stores.  enc is one frame shared by every row.
+template <int NT, int U = 16>
+__device__ void write_h_rows_pairs(const ModelDev& m, const float* __restrict__ enc,
+                                   const int2* rowoff, int nrows, void* __restrict__ hbase,
+                                   int hstride, int tid) {
+  const int C = m.C, Kpad = m.Kpad;
+  const float* __restrict__ P0 = m.P0;
+  const float* __restrict__ P1 = m.P1;
+  const int cols = Kpad / (2 * NT);  // column pairs per thread per row
+  int r = 0, j = 0;                  // (row, pair slot) of the next item
+  while (r < nrows) {
+    float2 p0[U], p1[U];
+    int ro[U], ko[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = 2 * (tid + j * NT);
+      ro[u] = r;
+      ko[u] = k;
+      // past the last row or column: load a valid pair and drop the result (no
+      // branch separates the loads)
+      const int rc = min(r, nrows - 1), kc = min(k, C - 2);
+      const int2 off = rowoff[rc];
+      p0[u] = *reinterpret_cast<const float2*>(P0 + (size_t)off.x + kc);
+      p1[u] = *reinterpret_cast<const float2*>(P1 + (size_t)off.y + kc);
+      if (++j == cols) {
+        j = 0;
+        ++r;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (ro[u] >= nrows) continue;
+      const int k = ko[u];
+      float h0 = 0.f, h1 = 0.f;
+      if (k < C) {
+        h0 = tanh_fast(enc[k] + fmaxf(p0[u].x + p1[u].x, 0.f));
+        h1 = tanh_fast(enc[k + 1] + fmaxf(p0[u].y + p1[u].y, 0.f));
+      }
+      const size_t o = (size_t)ro[u] * hstride + k;
+      if (m.bf16)
+        *reinterpret_cast<unsigned*>(reinterpret_cast<uint16_t*>(hbase) + o) =
+            (unsigned)f32_to_bf16_rne(h0) | ((unsigned)f32_to_bf16_rne(h1) << 16);
+      else
+        *reinterpret_cast<float2*>(reinterpret_cast<float*>(hbase) + o) = make_float2(h0, h1);
     }
   }
 }
@@ -1492,11 +1541,72 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   if (N > kSmallCands && beam < INFINITY && N <= kChunk + kMaxStates) {
     float lmax = -INFINITY;
     __syncthreads();  // trivial graph: uk/uv held the staged tile lists until here
-    for (int c = tid; c < N; c += blockDim.x) {
-      const ulonglong2 kv = make_cand(c);
-      s.uk[c] = kv.x;
-      s.uv[c] = kv.y;
-      if (kv.x != kEmpty) lmax = fmaxf(lmax, ord2f((unsigned)(kv.y >> 32)));
+    if (TRIV) {
+      for (int c = tid; c < N; c += blockDim.x) {
+        const ulonglong2 kv = make_cand(c);
+        s.uk[c] = kv.x;
+        s.uv[c] = kv.y;
+        if (kv.x != kEmpty) lmax = fmaxf(lmax, ord2f((unsigned)(kv.y >> 32)));
+      }
+    } else {
+      // make_cand for PF candidates per thread at a time, with each step's loads in
+      // flight together: the arcs' (label, score, destination), then the logits they
+      // select.  A blank candidate (or one past N) reads arc 0, which every graph
+      // buffer holds, and drops it.
+      constexpr int PF = 4;
+      for (int c0 = tid; c0 < N; c0 += PF * kSearchThreads) {
+        int ci[PF], cpos[PF], crow[PF], cj[PF];
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+          const int c = c0 + u * kSearchThreads;
+          int i = 0, pos = -1;
+          if (c < N) locate(c, i, pos);
+          ci[u] = i;
+          cpos[u] = pos;
+          crow[u] = s.s_row[i];
+          cj[u] = pos < 0 ? 0 : s.s_base[i] + pos;
+        }
+        int clab[PF], cdst[PF];
+        float cq[PF];
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+          clab[u] = g.label[cj[u]];
+          cq[u] = g.q[cj[u]];
+          cdst[u] = g.dest[cj[u]];
+        }
+        float cz[PF];
+#pragma unroll
+        for (int u = 0; u < PF; ++u)
+          cz[u] = zbase[(size_t)crow[u] * m.Vpad + (cpos[u] < 0 ? 0 : clab[u])];
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+          const int c = c0 + u * kSearchThreads;
+          if (c < N) {
+            const int i = ci[u], pos = cpos[u];
+            const double lse = s.s_lse[crow[u]];
+            float sc;
+            unsigned nctx;
+            int nst, tbpos;
+            if (pos < 0) {
+              sc = s.s_score[i] + logp_of(cz[u], lse);
+              nctx = (unsigned)s.s_ctx[i];
+              nst = s.s_state[i];
+              tbpos = 0;
+            } else {
+              sc = (s.s_score[i] + cq[u]) + logp_of(cz[u], lse);
+              nctx = (unsigned)s.s_bprev[i] * (unsigned)V + (unsigned)clab[u];
+              nst = cdst[u];
+              tbpos = pos + 1;
+            }
+            const unsigned tb = (unsigned)i * stride_tb + (unsigned)tbpos;
+            const unsigned long long k = ((unsigned long long)(unsigned)nst << 32) | nctx;
+            const unsigned long long v = ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - tb);
+            s.uk[c] = k;
+            s.uv[c] = v;
+            lmax = fmaxf(lmax, ord2f((unsigned)(v >> 32)));
+          }
+        }
+      }
     }
     lmax = wave_max_f(lmax);
     if (lane == 0) s.wmax[wave] = lmax;
@@ -1877,11 +1987,13 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     } else if (FUSED) {
       write_h_rows<kSearchThreads>(m, s.enc_next, 0, s.n_rowoff, nC, hl, hstride, tid);
     } else {
-      // (32 elements per thread: the gathers of up to 16 rows of K = 512 in one batch)
+      // (the gathers of up to 16 rows of K = 512 in one batch)
       const size_t esz = m.bf16 ? 2 : 4;
-      write_h_rows<kSearchThreads, 32>(m, s.enc_next, 0, s.n_rowoff, nC,
-                                       reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz,
-                                       m.Kpad, tid);
+      char* hrows = reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz;
+      if ((m.C & 1) == 0)
+        write_h_rows_pairs<kSearchThreads, 16>(m, s.enc_next, s.n_rowoff, nC, hrows, m.Kpad, tid);
+      else
+        write_h_rows<kSearchThreads, 32>(m, s.enc_next, 0, s.n_rowoff, nC, hrows, m.Kpad, tid);
     }
   }
   const bool store_surv = writer && (!FUSED || t + 1 == L);
