@@ -1264,6 +1264,15 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   }
   __syncthreads();
   const int ns = s.ns, nc = s.nc;
+  // general graph: the arc ranges of the survivors' states, requested before the
+  // normalisers so that their round trip overlaps them (one survivor per thread)
+  static_assert(kMaxStates <= kSearchThreads, "one survivor per thread");
+  int rp_lo = 0, rp_hi = 0;
+  if (!TRIV && tid < ns) {
+    const int st = s.s_state[tid];
+    rp_lo = g.rp[st];
+    rp_hi = g.rp[st + 1];
+  }
   // log-softmax normaliser of each context row: 16 threads (one DPP row) per row,
   // 16 rows at a time
   for (int j0 = 0; !FUSED && j0 < nc; j0 += kSearchThreads / 16) {
@@ -1383,14 +1392,10 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
         prev = best ? best : 1ull;
       }
     }
-  } else {
-    for (int i = tid; i < ns; i += blockDim.x) {
-      const int st = s.s_state[i];
-      const int lo = g.rp[st], hi = g.rp[st + 1];
-      s.s_bprev[i] = s.s_ctx[i] % V;
-      s.s_base[i] = lo;
-      s.s_off[i + 1] = hi - lo;
-    }
+  } else if (tid < ns) {
+    s.s_bprev[tid] = s.s_ctx[tid] % V;
+    s.s_base[tid] = rp_lo;
+    s.s_off[tid + 1] = rp_hi - rp_lo;
   }
   if (tid == 0) {
     s.s_off[0] = 0;
