@@ -93,8 +93,8 @@ struct DecodeDev {
 };
 
 struct JoinerPlan {
-  int MB;                   // 0: GEMM tiles (128 x 128, or 256 x 256 if wide); else 16 MB x 64 tiles
-  int wide;                 // 1: 256 x 256 GEMM tiles (bf16)
+  int MB;                   // 0: GEMM tiles (shape); else 16 MB x 64 tiles
+  int shape;                // GEMM tiles: 0 = 128 x 128, 1 = 256 x 256 (bf16), 2 = 64 x 128 (fp32)
   int n_rt, n_ct;           // row and column tiles
   int grid;                 // workgroups (XCD-interleaved tile order)
   size_t lds;               // dynamic LDS bytes

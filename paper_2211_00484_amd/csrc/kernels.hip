@@ -598,6 +598,8 @@ constexpr int kJSlice = 128;                   // bytes of K per row and slice
 constexpr int kJRow = kJSlice;                 // LDS row stride (16-byte chunks swizzled per row)
 constexpr int kJStage = (kJBM + kJBN) * kJRow; // bytes per buffer: A rows, then B rows
 constexpr size_t kJLds = 2 * (size_t)kJStage;  // 65,536 bytes
+constexpr int kJHalfBM = 64;                   // the 64 x 128 tile
+constexpr size_t kJHalfLds = 2 * (size_t)(kJHalfBM + kJBN) * kJRow;  // 49,152 bytes
 constexpr int kJWideBM = 256, kJWideBN = 256;  // the 256 tile
 constexpr size_t kJWideLds = 2 * (size_t)(kJWideBM + kJWideBN) * kJRow;  // 131,072 bytes
 // LDS chunk swizzle: chunk k of a row with index r mod 16 = l sits at slot k ^ jswz(l).
@@ -610,8 +612,9 @@ template <bool BF16, bool TOPK, int WN, int MBW>
 __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
   constexpr int NT = 128 * WN, BM = 32 * MBW, BN = 64 * WN;
   constexpr int STAGE = (BM + BN) * kJRow;
-  constexpr bool DEEP = MBW == 4;  // two slices in flight (else one)
-  static_assert(BM == NT / 2 && BN == NT / 2, "slice loads: 4 chunks per thread and operand");
+  constexpr bool DEEP = MBW <= 4;  // two slices in flight (else one)
+  constexpr int UA = BM * 8 / NT, UB = BN * 8 / NT;  // 16-byte chunks per thread and slice
+  static_assert(UA * NT == BM * 8 && UB * NT == BN * 8 && UA <= UB, "slice loads");
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_act[BM];
   const int bid = blockIdx.x, xcd = bid & 7, slot = bid >> 3;
@@ -650,10 +653,10 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
   const size_t rowb = (size_t)Kpad * ESZ;
   const unsigned rowb32 = (unsigned)rowb;  // h and W each stay below 4 GiB (checked at launch)
   // slices in flight: register sets 0 and 1 (set 1 only with DEEP)
-  uint4 ra0[4], rb0[4], ra1[4], rb1[4];
+  uint4 ra0[UA], rb0[UB], ra1[UA], rb1[UB];
   auto gload = [&](int s, int set) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < UB; ++u) {
       const int c = tid + NT * u, row = c >> 3, part = c & 7;
       const size_t off = (size_t)s * kJSlice + part * 16;
       // Rows past the batch or the padded vocabulary read the last valid row: their
@@ -661,24 +664,29 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
       // branches around the loads, so their waits stay exact.)
       // (32-bit offsets from the uniform bases: one register per load address)
       const int hr = min(r0 + row, a.R - 1), wr_ = min(c0 + row, Vpad - 1);
-      const uint4 va = *reinterpret_cast<const uint4*>(hsrc + ((unsigned)hr * rowb32 + (unsigned)off));
       const uint4 vb = *reinterpret_cast<const uint4*>(wsrc + ((unsigned)wr_ * rowb32 + (unsigned)off));
-      if (set == 0) {
-        ra0[u] = va;
+      if (set == 0)
         rb0[u] = vb;
-      } else {
-        ra1[u] = va;
+      else
         rb1[u] = vb;
+      if (u < UA) {
+        const uint4 va = *reinterpret_cast<const uint4*>(hsrc + ((unsigned)hr * rowb32 + (unsigned)off));
+        if (set == 0)
+          ra0[u < UA ? u : 0] = va;
+        else
+          ra1[u < UA ? u : 0] = va;
       }
     }
   };
   auto lstore = [&](int buf, int set) {
     unsigned char* base = smem + (size_t)buf * STAGE;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < UB; ++u) {
       const int c = tid + NT * u, row = c >> 3, part = c & 7;
       const int slot = (part ^ jswz(row & 15)) * 16;
-      *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + slot) = set == 0 ? ra0[u] : ra1[u];
+      if (u < UA)
+        *reinterpret_cast<uint4*>(base + (size_t)row * kJRow + slot) =
+            set == 0 ? ra0[u < UA ? u : 0] : ra1[u < UA ? u : 0];
       *reinterpret_cast<uint4*>(base + (size_t)(BM + row) * kJRow + slot) = set == 0 ? rb0[u] : rb1[u];
     }
   };
@@ -703,13 +711,14 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
       if (BF16) {
         // row blocks in groups of 4: with 8 row blocks, the fragments of the second
         // group are read after the first group's MFMAs (fewer live registers)
+        constexpr int GB = MBW < 4 ? MBW : 4;
 #pragma unroll
-        for (int g = 0; g < MBW; g += 4) {
+        for (int g = 0; g < MBW; g += GB) {
 #pragma unroll
-          for (int q = g; q < g + 4; ++q)
+          for (int q = g; q < g + GB; ++q)
             fa[q] = *reinterpret_cast<const uint4*>(abase + (size_t)16 * q * kJRow + (cs ^ (64 * j)));
 #pragma unroll
-          for (int mb = g; mb < g + 4; ++mb)
+          for (int mb = g; mb < g + GB; ++mb)
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb)
               acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[mb]), as_bf16x8(fb[nb]),
@@ -2985,9 +2994,14 @@ hipError_t launch_joiner(const ModelDev& m, const JoinArgs& a, const JoinerPlan&
     if ((unsigned long long)a.R * rowb >= (1ull << 32) || (unsigned long long)m.Vpad * rowb >= (1ull << 32))
       return hipErrorInvalidValue;
   }
-  if (p.MB == 0 && p.wide) {  // bf16 logits only
+  if (p.MB == 0 && p.shape == 1) {  // bf16 logits only
     if (!m.bf16 || topk) return hipErrorInvalidValue;
     return launch_joiner_t<true, false, 4, 8>(m, a, p, st);
+  }
+  if (p.MB == 0 && p.shape == 2) {  // fp32 only
+    if (m.bf16) return hipErrorInvalidValue;
+    return topk ? launch_joiner_t<false, true, 2, 2>(m, a, p, st)
+                : launch_joiner_t<false, false, 2, 2>(m, a, p, st);
   }
   if (p.MB == 0) {
     if (m.bf16)
@@ -3020,7 +3034,7 @@ bool take_launch_events(hipEvent_t* start, hipEvent_t* stop) {
 
 JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu, bool topk) {
   JoinerPlan p;
-  p.wide = 0;
+  p.shape = 0;
   const int esz = bf16 ? 2 : 4;
   const int nvt = Vpad / kJoinerBN;
   // bf16 logits: 256 x 256 GEMM tiles when they give every compute unit several
@@ -3030,7 +3044,7 @@ JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu, bool top
     const long long tiles = (long long)p.n_rt * p.n_ct;
     if (tiles >= 4LL * ncu) {
       p.MB = 0;
-      p.wide = 1;
+      p.shape = 1;
       p.grid = (int)(8 * ((tiles + 7) / 8));
       p.lds = kJWideLds;
       return p;
@@ -3041,8 +3055,16 @@ JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu, bool top
   p.n_ct = (nvt + 1) / 2;
   if ((long long)p.n_rt * p.n_ct >= ncu) {
     p.MB = 0;
+    if (!bf16 && (long long)p.n_rt * p.n_ct < 4LL * ncu) {
+      // fp32 with a few 128 x 128 tiles per CU: 64 x 128 tiles (three workgroups per CU),
+      // which spread the work over the CUs in finer and more even parts
+      p.shape = 2;
+      p.n_rt = (rows + kJHalfBM - 1) / kJHalfBM;
+      p.lds = kJHalfLds;
+    } else {
+      p.lds = kJLds;
+    }
     p.grid = 8 * ((p.n_ct + 7) / 8) * p.n_rt;
-    p.lds = kJLds;
     return p;
   }
   // Otherwise small tiles: the largest row block (4 or 2 MFMA blocks, else 1) whose h
