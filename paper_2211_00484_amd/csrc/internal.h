@@ -94,7 +94,7 @@ struct DecodeDev {
 
 struct JoinerPlan {
   int MB;                   // 0: GEMM tiles (shape); else 16 MB x 64 tiles
-  int shape;                // GEMM tiles: 0 = 128 x 128, 1 = 256 x 256 (bf16), 2 = 64 x 128 (fp32)
+  int shape;                // GEMM tiles: 0 = 128 x 128, 1 = 256 x 256 (bf16), 2 = 64 x 128
   int n_rt, n_ct;           // row and column tiles
   int grid;                 // workgroups (XCD-interleaved tile order)
   size_t lds;               // dynamic LDS bytes

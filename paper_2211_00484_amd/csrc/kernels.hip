@@ -2998,8 +2998,10 @@ hipError_t launch_joiner(const ModelDev& m, const JoinArgs& a, const JoinerPlan&
     if (!m.bf16 || topk) return hipErrorInvalidValue;
     return launch_joiner_t<true, false, 4, 8>(m, a, p, st);
   }
-  if (p.MB == 0 && p.shape == 2) {  // fp32 only
-    if (m.bf16) return hipErrorInvalidValue;
+  if (p.MB == 0 && p.shape == 2) {
+    if (m.bf16)
+      return topk ? launch_joiner_t<true, true, 2, 2>(m, a, p, st)
+                  : launch_joiner_t<true, false, 2, 2>(m, a, p, st);
     return topk ? launch_joiner_t<false, true, 2, 2>(m, a, p, st)
                 : launch_joiner_t<false, false, 2, 2>(m, a, p, st);
   }
@@ -3055,9 +3057,9 @@ JoinerPlan plan_joiner(int rows, int Vpad, int Kpad, int bf16, int ncu, bool top
   p.n_ct = (nvt + 1) / 2;
   if ((long long)p.n_rt * p.n_ct >= ncu) {
     p.MB = 0;
-    if (!bf16 && (long long)p.n_rt * p.n_ct < 4LL * ncu) {
-      // fp32 with a few 128 x 128 tiles per CU: 64 x 128 tiles (three workgroups per CU),
-      // which spread the work over the CUs in finer and more even parts
+    if ((long long)p.n_rt * p.n_ct < 4LL * ncu) {
+      // a few 128 x 128 tiles per CU: 64 x 128 tiles (three workgroups per CU), which
+      // spread the work over the CUs in finer and more even parts
       p.shape = 2;
       p.n_rt = (rows + kJHalfBM - 1) / kJHalfBM;
       p.lds = kJHalfLds;
