@@ -165,15 +165,17 @@ def test_throughput_sampled(schedule):
          schedule=schedule)
 
 
+@pytest.mark.parametrize("B", [256, 1024])
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_trivial_wide_frame_joiner(dtype):
-    # trivial graph on the frame schedule with enough joiner rows (B = 256, 8 contexts)
-    # and columns (V = 2,000) for the 128 x 128 GEMM tiles: their top-label epilogue
+def test_trivial_wide_frame_joiner(dtype, B):
+    # trivial graph on the frame schedule with enough joiner rows (B streams, 8 contexts)
+    # and columns (V = 2,000) for the GEMM tiles' top-label epilogue: B = 256 gives one
+    # 128 x 128 tile per CU (the 64 x 128 tiles run), B = 1,024 four (the 128 x 128 tiles)
     rng = np.random.default_rng(11)
     model = synth.make_model(rng, 2000, 256, 0.05)
-    inputs = synth.make_inputs(rng, 256, 6, 256, length_range=(0, 6))
+    inputs = synth.make_inputs(rng, B, 6, 256, length_range=(0, 6))
     _run((inputs, model, synth.trivial_graph(2000)), math.inf, 8, 8, dtype=dtype,
-         streams=range(0, 256, 32), schedule="frame")
+         streams=range(0, B, B // 8), schedule="frame")
 
 
 def test_large_sampled():
