@@ -582,15 +582,18 @@ constexpr float kLog2e = 1.44269504088896341f;
 
 // Joiner GEMM tile: BM = 32 MBW rows x BN = 64 WN vocabulary columns, 2 x WN waves,
 // each wave 16 MBW rows x 64 columns (MBW x 4 MFMA blocks of 16 x 16):
-//  - 128 x 128 (MBW = 4, WN = 2; four waves), for batches that give every compute
-//    unit a tile of that size;
+//  - 128 x 128 (MBW = 4, WN = 2; four waves), for batches with at least four such
+//    tiles per compute unit;
+//  - 64 x 128 (MBW = 2, WN = 2; four waves, three workgroups per compute unit), for
+//    batches with one to four 128 x 128 tiles per compute unit, which it splits into
+//    finer, more evenly spread parts;
 //  - 256 x 256 (MBW = 8, WN = 4; eight waves), for bf16 batches with several such
 //    tiles per compute unit: half the operand bytes per product of the 128 tile, and
 //    a quarter fewer LDS fragment reads per MFMA.
 // Both operands go through LDS in K slices of 128 bytes per row (64 bf16 or 32 fp32
-// values), two buffers deep, one barrier per slice.  The 128 tile keeps slices s + 1
-// and s + 2 in flight to registers during the MFMAs of slice s; the 256 tile, whose
-// slices hold twice the MFMAs, keeps slice s + 1.  A wave's 64 columns are one
+// values), two buffers deep, one barrier per slice.  The 128 and 64 tiles keep slices
+// s + 1 and s + 2 in flight to registers during the MFMAs of slice s; the 256 tile,
+// whose slices hold twice the MFMAs, keeps slice s + 1.  A wave's 64 columns are one
 // vocabulary tile, so its epilogue produces that tile's (max, sum exp) per row and
 // either the logits or each row's best labels per 16-column sub-tile.
 constexpr int kJBM = 128, kJBN = 128;          // the 128 tile: rows, columns
