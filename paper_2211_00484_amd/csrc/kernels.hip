@@ -78,6 +78,24 @@ __device__ __forceinline__ float row16_sum(float v) {
   v += dpp_f<kRor2>(v);
   return v + dpp_f<kRor1>(v);
 }
+// v of lane (this lane xor M), M a power of two up to 32, in the cheapest form for M:
+// DPP within 16-lane rows (1, 2: quad permutations; 4: half-row mirror then quad
+// reversal; 8: row mirror then half-row mirror), a swizzle across the halves of 32
+// lanes (16), and a permute through LDS only across the wave's halves (32).
+__device__ __forceinline__ int xor_lane(int v, int M) {
+  switch (M) {
+    case 1: return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xf, 0xf, false);
+    case 2: return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xf, 0xf, false);
+    case 4:
+      return __builtin_amdgcn_update_dpp(0, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xf, 0xf, false),
+                                         0x1B, 0xf, 0xf, false);
+    case 8:
+      return __builtin_amdgcn_update_dpp(0, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xf, 0xf, false),
+                                         0x141, 0xf, 0xf, false);
+    case 16: return __builtin_amdgcn_ds_swizzle(v, 0x401F);  // and 31, or 0, xor 16
+    default: return __shfl_xor(v, M, 64);
+  }
+}
 __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
   return a > b ? a : b;
 }
@@ -1813,12 +1831,15 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     // of ballots, because the sorted order is the canonical one.
     if (wave == 0) {
       auto xor64 = [](unsigned long long v, int m) {
-        const int lo = __shfl_xor((int)(unsigned)v, m), hi = __shfl_xor((int)(unsigned)(v >> 32), m);
+        const int lo = xor_lane((int)(unsigned)v, m), hi = xor_lane((int)(unsigned)(v >> 32), m);
         return ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo;
       };
       unsigned long long sk = tid < K ? ((unsigned long long)my_ci << 32) | my_st : ~0ull;  // sentinels last
       unsigned long long sv = tid < K ? my_v : 0ull;
+      // (fully unrolled, so that each stage's exchange distance is a constant)
+#pragma unroll
       for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
         for (int j = k >> 1; j > 0; j >>= 1) {
           const unsigned long long pk = xor64(sk, j), pv = xor64(sv, j);
           const bool up = (lane & k) == 0, lower = (lane & j) == 0;
