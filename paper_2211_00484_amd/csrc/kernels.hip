@@ -668,7 +668,7 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
   if (tid < BM) s_act[tid] = act;
   if (!__syncthreads_or(act)) return;  // uniform: no active row in this tile
 
-  // slice loads: 4 chunks of 16 bytes per thread for each operand (BM or BN rows x 8 chunks)
+  // slice loads: UA (h) and UB (W) chunks of 16 bytes per thread (BM and BN rows x 8 chunks)
   const char* hsrc = reinterpret_cast<const char*>(a.h);
   const char* wsrc = BF16 ? reinterpret_cast<const char*>(m.Wb) : reinterpret_cast<const char*>(m.Wf);
   const size_t rowb = (size_t)Kpad * ESZ;
