@@ -1843,10 +1843,11 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
         for (int j = k >> 1; j > 0; j >>= 1) {
           const unsigned long long pk = xor64(sk, j), pv = xor64(sv, j);
           const bool up = (lane & k) == 0, lower = (lane & j) == 0;
-          if (lower == up ? pk < sk : pk > sk) {
-            sk = pk;
-            sv = pv;
-          }
+          // (selects rather than a branch: each stage stays a short dependent chain)
+          const bool lt = pk < sk, gt = pk > sk, asc = lower == up;
+          const bool take = (asc & lt) | (!asc & gt);
+          sk = take ? pk : sk;
+          sv = take ? pv : sv;
         }
       const bool valid = sk != ~0ull;
       const unsigned ci = (unsigned)(sk >> 32), stt = (unsigned)sk;
