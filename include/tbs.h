@@ -53,7 +53,8 @@ typedef struct tbs_model tbs_model;
  * device and the caller may free them when the call returns.
  *   num_states   S >= 1
  *   start_state  in [0, S)
- *   vocab_size   V in [2, 65535] (blank = 0 included)
+ *   vocab_size   V in [2, 46340] (blank = 0 included; a context (a, b) is the
+ *                int32 a * V + b, so V * V must stay below 2^31)
  *   row_ptr      host int32 [S+1]: row_ptr[0] = 0, non-decreasing; A = row_ptr[S]
  *   dest         host int32 [A]: destination state of each arc, in [0, S)
  *   label        host int32 [A]: label of each arc, in [1, V-1] (label 0 is
@@ -91,7 +92,8 @@ typedef enum { TBS_JOINER_FP32 = 0, TBS_JOINER_BF16 = 1 } tbs_joiner_dtype;
  *                      label a; no bias);
  *   joiner             logits = w_out . tanh(enc + dec) + b_out, then log-softmax
  *                      over all V outputs, blank included.
- *   vocab_size V in [2, 65535]; dim C in [1, 2048]; context_size must be 2
+ *   vocab_size V in [2, 46340] (contexts a * V + b are int32); dim C in [1, 2048];
+ *   context_size must be 2
  *   (TBS_EUNSUPPORTED otherwise).
  *   embed  DEVICE float [V][C];  conv DEVICE float [C][2];
  *   w_out  DEVICE float [V][C] (torch Linear layout);  b_out DEVICE float [V] or NULL (= 0).

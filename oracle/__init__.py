@@ -69,6 +69,9 @@ def _load():
         lib.oracle_decode.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I,
                                        _I, _I, _P, _P, _P, _P, _P, _D, _I, _I, _I] + [_P] * 8)
         lib.oracle_decode.restype = _I
+        lib.oracle_replay.argtypes = ([_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I,
+                                       _I, _I, _P, _P, _P, _P, _P, _D, _I, _I, _I] + [_P] * 8)
+        lib.oracle_replay.restype = _I
         lib.oracle_rescore.argtypes = [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _I, _I,
                                        _P, _P, _P, _P, _P, _P]
         lib.oracle_rescore.restype = _I
@@ -165,6 +168,55 @@ def decode(model, graph, encoder_out: np.ndarray, lengths: np.ndarray, beam: flo
                       int(nthreads), _ptr(tokens), _ptr(ntok), _ptr(scores), _ptr(status),
                       _ptr(arcs), _ptr(trace), _ptr(margins), _ptr(frame_margins))
     return OracleResult(tokens, ntok, scores, status, arcs, trace, margins, frame_margins)
+
+
+class ReplayResult:
+    """Frame-by-frame replay of a given survivor trace (see ``replay``)."""
+
+    def __init__(self, ref, ref_score, ref_cscore, key_score, cand_score, margins, bounds):
+        self.ref, self.ref_score, self.ref_cscore = ref, ref_score, ref_cscore
+        self.key_score, self.cand_score = key_score, cand_score
+        self.margins, self.bounds = margins, bounds
+
+
+def replay(model, graph, encoder_out: np.ndarray, lengths: np.ndarray, given_trace: np.ndarray,
+           beam: float, max_states: int, max_contexts: int, bf16: bool = False,
+           nthreads: int = 0, streams=None) -> ReplayResult:
+    """Decides every frame again from the survivors of the previous frame as given in
+    ``given_trace`` ([T+1, B, Ns, 4], the layout of ``decode``'s trace), each scored in
+    fp64 along its (state, context); see ``oracle_replay`` in tbs_oracle.cpp.  With
+    ``streams``, the given trace and the outputs hold those streams only."""
+    lib = _load()
+    enc = _f32(encoder_out)
+    lens = _i32(lengths)
+    given = _i32(given_trace)
+    if streams is not None:
+        idx = np.asarray(streams, dtype=np.int64)
+        enc = np.ascontiguousarray(enc[idx])
+        lens = np.ascontiguousarray(lens[idx])
+        given = np.ascontiguousarray(given[:, idx])
+    B, T, C = enc.shape
+    Ns = int(max_states)
+    if given.shape != (T + 1, B, Ns, 4):
+        raise ValueError(f"given trace has shape {given.shape}, expected {(T + 1, B, Ns, 4)}")
+    E, conv, W = _f32(model.embed), _f32(model.conv), _f32(model.w_out)
+    bias = None if model.b_out is None else _f32(model.b_out)
+    rp, dest, lab, q = _i32(graph.row_ptr), _i32(graph.dest), _i32(graph.label), _f32(graph.score)
+    fin = None if graph.final is None else _f32(graph.final)
+    ref = np.empty((T + 1, B, Ns, 4), dtype=np.int32)
+    ref_score = np.empty((T + 1, B, Ns), dtype=np.float64)
+    ref_cscore = np.empty_like(ref_score)
+    key_score = np.empty_like(ref_score)
+    cand_score = np.empty_like(ref_score)
+    margins = np.empty((B, T + 1), dtype=np.float64)
+    bounds = np.empty((B, T, 5), dtype=np.float64)
+    beam_v = float(beam) if beam is not None else math.inf
+    lib.oracle_replay(B, T, C, model.vocab_size, _ptr(enc), _ptr(lens), _ptr(E), _ptr(conv),
+                      _ptr(W), _ptr(bias), int(bf16), graph.num_states, graph.start, _ptr(rp),
+                      _ptr(dest), _ptr(lab), _ptr(q), _ptr(fin), beam_v, Ns, int(max_contexts),
+                      int(nthreads), _ptr(given), _ptr(ref), _ptr(ref_score), _ptr(ref_cscore),
+                      _ptr(key_score), _ptr(cand_score), _ptr(margins), _ptr(bounds))
+    return ReplayResult(ref, ref_score, ref_cscore, key_score, cand_score, margins, bounds)
 
 
 def rescore(model, graph, enc_stream: np.ndarray, arcs: np.ndarray, bf16: bool = False):

@@ -41,6 +41,10 @@ struct Model {
   const float* W;     // [V][C] joiner output weight
   const float* bias;  // [V] or null
   int bf16;           // 1: joiner GEMM operands rounded to bfloat16 (RNE)
+  std::vector<float> Wr;  // bf16 mode: W rounded to bfloat16 once (each value exact in float)
+
+  Model(int V_, int C_, const float* E_, const float* conv_, const float* W_, const float* bias_,
+        int bf16_);
 };
 
 struct Graph {
@@ -69,6 +73,15 @@ double round_bf16(double x) {
   return std::ldexp(r / 256.0, e);
 }
 
+Model::Model(int V_, int C_, const float* E_, const float* conv_, const float* W_,
+             const float* bias_, int bf16_)
+    : V(V_), C(C_), E(E_), conv(conv_), W(W_), bias(bias_), bf16(bf16_) {
+  if (bf16) {
+    Wr.resize((size_t)V * C);
+    for (size_t i = 0; i < Wr.size(); ++i) Wr[i] = (float)round_bf16((double)W[i]);
+  }
+}
+
 // Stateless decoder (Sec. 2.2, Sec. 5.1): embedding of the two most recent
 // labels followed by a kernel-2 convolution, read as depthwise with a ReLU
 // and no bias; then the joiner tanh(enc + dec) -> Linear(V) -> log-softmax
@@ -87,11 +100,8 @@ void joiner_logp(const Model& m, const float* enc_row, int a, int b, double* log
   std::vector<double> z(V);
   for (int v = 0; v < V; ++v) {
     double acc = 0.0;
-    const float* wr = m.W + (size_t)v * C;
-    for (int k = 0; k < C; ++k) {
-      double w = m.bf16 ? round_bf16((double)wr[k]) : (double)wr[k];
-      acc += w * h[k];
-    }
+    const float* wr = (m.bf16 ? m.Wr.data() : m.W) + (size_t)v * C;
+    for (int k = 0; k < C; ++k) acc += (double)wr[k] * h[k];
     if (m.bias) acc += (double)m.bias[v];
     z[v] = acc;
     if (acc > zmax) zmax = acc;
@@ -150,6 +160,145 @@ bool cand_better(const Cand& x, const Cand& y) {
   return x.pos < y.pos;
 }
 
+// A merged (state, context) tuple of one frame: the best candidate reaching it
+// and the best score among its candidates with another (parent, label).
+struct Entry {
+  int s;
+  int64_t ctx;
+  const Cand* best;
+  double runner_up;
+};
+
+// What one frame of the search decides from a list of tuples.
+struct FrameOut {
+  std::vector<Cand> cands;   // every unpruned expansion, in (source, arc position) order
+  std::map<std::pair<int, int64_t>, std::vector<const Cand*>> groups;  // candidates per (state, ctx)
+  std::vector<Entry> ranked; // merged tuples by (score desc, (state, context) asc), unpruned
+  std::vector<Tup> next;     // the survivors, canonical order
+  double margin = std::numeric_limits<double>::infinity();  // smallest decision margin
+  double thr = kNegInf;      // best - beam
+  double s_in = kNegInf, s_out = kNegInf;  // scores at ranks Ns-1 and Ns within the beam
+  double c_in = kNegInf, c_out = kNegInf;  // context scores at ranks Nc-1 and Nc
+  std::map<int64_t, double> cscore;        // context score after beam + max-states
+};
+
+// One frame of Algorithm 1 for one stream, from the tuples H (canonical order):
+// contexts, decoder, joiner and log-softmax once per context, unpruned expansion,
+// merge by max, beam + max-states in one pruning operation, then max-contexts.
+void search_frame(const Model& m, const Graph& g, const Params& p, const float* enc_row,
+                  const std::vector<Tup>& H, FrameOut& fo) {
+  const int V = m.V;
+  double fmar = std::numeric_limits<double>::infinity();
+  // GetContexts: the distinct contexts of the current tuples, ascending.
+  std::vector<int64_t> ctxs;
+  for (const Tup& x : H) ctxs.push_back(x.ctx);
+  std::sort(ctxs.begin(), ctxs.end());
+  ctxs.erase(std::unique(ctxs.begin(), ctxs.end()), ctxs.end());
+  // Decoder + IndexSelect(enc_t) + joiner + log-softmax, once per context.
+  std::vector<double> logp(ctxs.size() * (size_t)V, 0.0);
+  for (size_t r = 0; r < ctxs.size(); ++r)
+    joiner_logp(m, enc_row, (int)(ctxs[r] / V), (int)(ctxs[r] % V), &logp[r * V]);
+  auto row_of = [&](int64_t ctx) {
+    return (size_t)(std::lower_bound(ctxs.begin(), ctxs.end(), ctx) - ctxs.begin());
+  };
+
+  // ExpandArcs without pruning.  Blank keeps context and state; an arc
+  // s -> r with label c and score q moves to ((b, c), t+1, r) with weight
+  // q + log P(c | (a, b), t); with S = 1 no blank factor is added.
+  std::vector<Cand>& cands = fo.cands;
+  for (int i = 0; i < (int)H.size(); ++i) {
+    const Tup& x = H[i];
+    const double* lp = &logp[row_of(x.ctx) * V];
+    cands.push_back(Cand{x.s, x.ctx, x.score + lp[0], i, -1, 0, -1, lp[0]});
+    const int64_t bprev = x.ctx % V;
+    for (int j = g.rp[x.s]; j < g.rp[x.s + 1]; ++j) {
+      const int c = g.label[j];
+      cands.push_back(Cand{g.dest[j], bprev * V + c, x.score + (double)g.q[j] + lp[c], i,
+                           j - g.rp[x.s], c, j, (double)g.q[j] + lp[c]});
+    }
+  }
+
+  // Merge tuples with equal (state, context) by max (Table 3 / Table 6 "Max").
+  std::map<std::pair<int, int64_t>, std::vector<const Cand*>>& groups = fo.groups;
+  for (const Cand& c : cands) groups[{c.s, c.ctx}].push_back(&c);
+  std::vector<Entry>& ents = fo.ranked;
+  ents.reserve(groups.size());
+  for (auto& kv : groups) {
+    const Cand* best = kv.second[0];
+    for (const Cand* c : kv.second)
+      if (cand_better(*c, *best)) best = c;
+    double ru = kNegInf;
+    for (const Cand* c : kv.second)
+      if (!(c->parent == best->parent && c->label == best->label)) ru = std::max(ru, c->score);
+    ents.push_back(Entry{kv.first.first, kv.first.second, best, ru});
+  }
+
+  // Beam and max-states constraints in one pruning operation: keep a tuple
+  // iff its score is within `beam` of the best and it ranks among the first
+  // max_states by (score desc, (state, context) asc).
+  auto ent_before = [](const Entry& x, const Entry& y) {
+    if (x.best->score != y.best->score) return x.best->score > y.best->score;
+    if (x.s != y.s) return x.s < y.s;
+    return x.ctx < y.ctx;
+  };
+  std::sort(ents.begin(), ents.end(), ent_before);
+  const double best = ents[0].best->score;
+  const double thr = best - p.beam;
+  fo.thr = thr;
+  size_t n_in_beam = 0;
+  while (n_in_beam < ents.size() && ents[n_in_beam].best->score >= thr) ++n_in_beam;
+  size_t n1 = std::min(n_in_beam, (size_t)p.Ns);
+  if (n_in_beam >= (size_t)p.Ns) fo.s_in = ents[p.Ns - 1].best->score;
+  if (n_in_beam > (size_t)p.Ns) {
+    fo.s_out = ents[p.Ns].best->score;
+    fmar = std::min(fmar, ents[p.Ns - 1].best->score - ents[p.Ns].best->score);
+  }
+  if (std::isfinite(p.beam)) {
+    // the best tuple is never outside its own beam: its distance (the beam) decides nothing
+    const size_t lim = std::min(ents.size(), (size_t)p.Ns);
+    for (size_t i = 1; i < lim; ++i) fmar = std::min(fmar, std::fabs(ents[i].best->score - thr));
+  }
+
+  // Max-contexts constraint: a context scores the max over its surviving
+  // tuples; keep the max_contexts best by (score desc, context asc) and drop
+  // every tuple of the other contexts.
+  std::map<int64_t, double>& cscore = fo.cscore;
+  for (size_t i = 0; i < n1; ++i) {
+    const Entry& e = ents[i];
+    auto it = cscore.find(e.ctx);
+    if (it == cscore.end() || e.best->score > it->second) cscore[e.ctx] = e.best->score;
+  }
+  std::vector<std::pair<double, int64_t>> cl;
+  for (auto& kv : cscore) cl.push_back({kv.second, kv.first});
+  std::sort(cl.begin(), cl.end(), [](const std::pair<double, int64_t>& x,
+                                      const std::pair<double, int64_t>& y) {
+    if (x.first != y.first) return x.first > y.first;
+    return x.second < y.second;
+  });
+  if (cl.size() >= (size_t)p.Nc) fo.c_in = cl[p.Nc - 1].first;
+  if (cl.size() > (size_t)p.Nc) {
+    fo.c_out = cl[p.Nc].first;
+    fmar = std::min(fmar, cl[p.Nc - 1].first - cl[p.Nc].first);
+  }
+  std::vector<int64_t> kept_ctx;
+  for (size_t i = 0; i < cl.size() && i < (size_t)p.Nc; ++i) kept_ctx.push_back(cl[i].second);
+  std::sort(kept_ctx.begin(), kept_ctx.end());
+
+  // New tuple list in canonical order: (context, state) ascending.
+  std::vector<Tup>& nH = fo.next;
+  for (size_t i = 0; i < n1; ++i) {
+    const Entry& e = ents[i];
+    if (!std::binary_search(kept_ctx.begin(), kept_ctx.end(), e.ctx)) continue;
+    if (e.runner_up != kNegInf) fmar = std::min(fmar, e.best->score - e.runner_up);
+    nH.push_back(Tup{e.ctx, e.s, e.best->score, e.best->parent, e.best->label, e.best->arc});
+  }
+  std::sort(nH.begin(), nH.end(), [](const Tup& x, const Tup& y) {
+    if (x.ctx != y.ctx) return x.ctx < y.ctx;
+    return x.s < y.s;
+  });
+  fo.margin = fmar;
+}
+
 struct StreamOut {
   std::vector<int> tokens;
   std::vector<int> arcs;     // per frame: arc id, -1 blank
@@ -165,7 +314,7 @@ struct StreamOut {
 void decode_stream(const Model& m, const Graph& g, const Params& p, const float* enc, int T,
                    int len, StreamOut& out, int* trace, int trace_stride_frame,
                    Lattice* lat = nullptr) {
-  const int V = m.V, C = m.C;
+  const int C = m.C;
   std::vector<Tup> H;
   H.push_back(Tup{0, g.start, 0.0, -1, -1, -1});  // ((blank, blank), 0, start), Sec. 2.2 / 2.4
   std::vector<std::vector<Tup>> hist;               // survivors after each frame
@@ -187,122 +336,19 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
     lat->arcs.clear();
   }
   double margin = std::numeric_limits<double>::infinity();
-  std::vector<double> logp;
   out.frame_margin.assign(len, std::numeric_limits<double>::infinity());
 
   for (int t = 0; t < len; ++t) {
-    double fmar = std::numeric_limits<double>::infinity();
-    // GetContexts: the distinct contexts of the current tuples, ascending.
-    std::vector<int64_t> ctxs;
-    for (const Tup& x : H) ctxs.push_back(x.ctx);
-    std::sort(ctxs.begin(), ctxs.end());
-    ctxs.erase(std::unique(ctxs.begin(), ctxs.end()), ctxs.end());
-    // Decoder + IndexSelect(enc_t) + joiner + log-softmax, once per context.
-    logp.assign(ctxs.size() * (size_t)V, 0.0);
-    const float* enc_row = enc + (size_t)t * C;
-    for (size_t r = 0; r < ctxs.size(); ++r)
-      joiner_logp(m, enc_row, (int)(ctxs[r] / V), (int)(ctxs[r] % V), &logp[r * V]);
-    auto row_of = [&](int64_t ctx) {
-      return (size_t)(std::lower_bound(ctxs.begin(), ctxs.end(), ctx) - ctxs.begin());
-    };
-
-    // ExpandArcs without pruning.  Blank keeps context and state; an arc
-    // s -> r with label c and score q moves to ((b, c), t+1, r) with weight
-    // q + log P(c | (a, b), t); with S = 1 no blank factor is added.
-    std::vector<Cand> cands;
-    for (int i = 0; i < (int)H.size(); ++i) {
-      const Tup& x = H[i];
-      const double* lp = &logp[row_of(x.ctx) * V];
-      cands.push_back(Cand{x.s, x.ctx, x.score + lp[0], i, -1, 0, -1, lp[0]});
-      const int64_t bprev = x.ctx % V;
-      for (int j = g.rp[x.s]; j < g.rp[x.s + 1]; ++j) {
-        const int c = g.label[j];
-        cands.push_back(Cand{g.dest[j], bprev * V + c, x.score + (double)g.q[j] + lp[c], i,
-                             j - g.rp[x.s], c, j, (double)g.q[j] + lp[c]});
-      }
-    }
-
-    // Merge tuples with equal (state, context) by max (Table 3 / Table 6 "Max").
-    std::map<std::pair<int, int64_t>, std::vector<const Cand*>> groups;
-    for (const Cand& c : cands) groups[{c.s, c.ctx}].push_back(&c);
-    struct Entry {
-      int s;
-      int64_t ctx;
-      const Cand* best;
-      double runner_up;  // best score among candidates with another (parent, label)
-    };
-    std::vector<Entry> ents;
-    ents.reserve(groups.size());
-    for (auto& kv : groups) {
-      const Cand* best = kv.second[0];
-      for (const Cand* c : kv.second)
-        if (cand_better(*c, *best)) best = c;
-      double ru = kNegInf;
-      for (const Cand* c : kv.second)
-        if (!(c->parent == best->parent && c->label == best->label)) ru = std::max(ru, c->score);
-      ents.push_back(Entry{kv.first.first, kv.first.second, best, ru});
-    }
-
-    // Beam and max-states constraints in one pruning operation: keep a tuple
-    // iff its score is within `beam` of the best and it ranks among the first
-    // max_states by (score desc, (state, context) asc).
-    auto ent_before = [](const Entry& x, const Entry& y) {
-      if (x.best->score != y.best->score) return x.best->score > y.best->score;
-      if (x.s != y.s) return x.s < y.s;
-      return x.ctx < y.ctx;
-    };
-    std::sort(ents.begin(), ents.end(), ent_before);
-    const double best = ents[0].best->score;
-    const double thr = best - p.beam;
-    size_t n_in_beam = 0;
-    while (n_in_beam < ents.size() && ents[n_in_beam].best->score >= thr) ++n_in_beam;
-    size_t n1 = std::min(n_in_beam, (size_t)p.Ns);
-    if (n_in_beam > (size_t)p.Ns)
-      fmar = std::min(fmar, ents[p.Ns - 1].best->score - ents[p.Ns].best->score);
-    if (std::isfinite(p.beam)) {
-      const size_t lim = std::min(ents.size(), (size_t)p.Ns);
-      for (size_t i = 0; i < lim; ++i) fmar = std::min(fmar, std::fabs(ents[i].best->score - thr));
-    }
-    ents.resize(n1);
-
-    // Max-contexts constraint: a context scores the max over its surviving
-    // tuples; keep the max_contexts best by (score desc, context asc) and drop
-    // every tuple of the other contexts.
-    std::map<int64_t, double> cscore;
-    for (const Entry& e : ents) {
-      auto it = cscore.find(e.ctx);
-      if (it == cscore.end() || e.best->score > it->second) cscore[e.ctx] = e.best->score;
-    }
-    std::vector<std::pair<double, int64_t>> cl;
-    for (auto& kv : cscore) cl.push_back({kv.second, kv.first});
-    std::sort(cl.begin(), cl.end(), [](const std::pair<double, int64_t>& x,
-                                        const std::pair<double, int64_t>& y) {
-      if (x.first != y.first) return x.first > y.first;
-      return x.second < y.second;
-    });
-    if (cl.size() > (size_t)p.Nc) fmar = std::min(fmar, cl[p.Nc - 1].first - cl[p.Nc].first);
-    std::vector<int64_t> kept_ctx;
-    for (size_t i = 0; i < cl.size() && i < (size_t)p.Nc; ++i) kept_ctx.push_back(cl[i].second);
-    std::sort(kept_ctx.begin(), kept_ctx.end());
-
-    // New tuple list in canonical order: (context, state) ascending.
-    std::vector<Tup> nH;
-    for (const Entry& e : ents) {
-      if (!std::binary_search(kept_ctx.begin(), kept_ctx.end(), e.ctx)) continue;
-      if (e.runner_up != kNegInf) fmar = std::min(fmar, e.best->score - e.runner_up);
-      nH.push_back(Tup{e.ctx, e.s, e.best->score, e.best->parent, e.best->label, e.best->arc});
-    }
-    std::sort(nH.begin(), nH.end(), [](const Tup& x, const Tup& y) {
-      if (x.ctx != y.ctx) return x.ctx < y.ctx;
-      return x.s < y.s;
-    });
-    out.frame_margin[t] = fmar;
-    margin = std::min(margin, fmar);
+    FrameOut fo;
+    search_frame(m, g, p, enc + (size_t)t * C, H, fo);
+    out.frame_margin[t] = fo.margin;
+    margin = std::min(margin, fo.margin);
     if (lat) {
       // lattice arcs of frame t: the candidates whose (state, context) survived;
       // cands are in (source, arc position) order, blank first
+      const std::vector<Tup>& nH = fo.next;
       std::vector<std::vector<LatArc>> into(nH.size());
-      for (const Cand& c : cands) {
+      for (const Cand& c : fo.cands) {
         auto it = std::lower_bound(nH.begin(), nH.end(), c, [](const Tup& x, const Cand& y) {
           if (x.ctx != y.ctx) return x.ctx < y.ctx;
           return x.s < y.s;
@@ -316,8 +362,8 @@ void decode_stream(const Model& m, const Graph& g, const Params& p, const float*
       lat->arcs.push_back(std::move(fa));
       lat->nodes.push_back(nH);
     }
-    hist.push_back(nH);
-    H.swap(nH);
+    hist.push_back(fo.next);
+    H = fo.next;
     write_trace(t + 1, H);
   }
 
@@ -561,7 +607,7 @@ extern "C" {
 int oracle_logp(int C, int V, int R, const float* enc_rows, const int* ctx_a, const int* ctx_b,
                 const float* E, const float* conv, const float* W, const float* bias, int bf16,
                 double* out) {
-  Model m{V, C, E, conv, W, bias, bf16};
+  const Model m(V, C, E, conv, W, bias, bf16);
   for (int r = 0; r < R; ++r)
     joiner_logp(m, enc_rows + (size_t)r * C, ctx_a[r], ctx_b[r], out + (size_t)r * V);
   return 0;
@@ -580,7 +626,7 @@ int oracle_decode(int B, int T, int C, int V, const float* enc, const int* lengt
                   const float* q, const float* fin, double beam, int Ns, int Nc, int nthreads,
                   int* tokens, int* ntok, double* scores, int* status, int* arcs, int* trace,
                   double* margins, double* frame_margins) {
-  Model m{V, C, E, conv, W, bias, bf16};
+  const Model m(V, C, E, conv, W, bias, bf16);
   Graph g{S, start, rp, dest, label, q, fin};
   Params p{beam, Ns, Nc};
   for (size_t i = 0; i < (size_t)B * T; ++i) tokens[i] = -1;
@@ -621,6 +667,103 @@ int oracle_decode(int B, int T, int C, int V, const float* enc, const int* lengt
   return 0;
 }
 
+// Replays a search trace produced elsewhere, frame by frame: the survivors of
+// frame f given in `given` ([T+1][B][Ns][4] (ctx, state, parent, label),
+// canonical order, -1 padded, the layout of oracle_decode's trace) are taken
+// as the tuples of frame f, each with the fp64 score of its (state, context)
+// after the merge of frame f (0 for the initial tuple), and frame f+1 is
+// decided again from them (search_frame).  Per stream b and frame f <= len_b,
+// with the same layouts:
+//   ref [T+1][B][Ns][4]: the survivors decided from the given frame f-1 (f >= 1);
+//   ref_score, ref_cscore [T+1][B][Ns]: their scores and context scores;
+//   key_score [T+1][B][Ns]: the merged score of each given survivor's
+//     (state, context) on its frame, NaN if no candidate reaches it;
+//   cand_score [T+1][B][Ns]: the best score among the candidates with the given
+//     survivor's (state, context, parent, label), NaN if there is none;
+//   margins [B][T+1]: entry f < len_b, the decision margin of frame f;
+//   bounds [B][T][5]: per frame, best - beam, the scores at ranks Ns-1 and Ns
+//     within the beam and the context scores at ranks Nc-1 and Nc (-inf if absent).
+// A stream's replay stops at the first given survivor that is not a candidate.
+int oracle_replay(int B, int T, int C, int V, const float* enc, const int* lengths,
+                  const float* E, const float* conv, const float* W, const float* bias,
+                  int bf16, int S, int start, const int* rp, const int* dest, const int* label,
+                  const float* q, const float* fin, double beam, int Ns, int Nc, int nthreads,
+                  const int* given, int* ref, double* ref_score, double* ref_cscore,
+                  double* key_score, double* cand_score, double* margins, double* bounds) {
+  const Model m(V, C, E, conv, W, bias, bf16);
+  Graph g{S, start, rp, dest, label, q, fin};
+  Params p{beam, Ns, Nc};
+  const double nan = std::numeric_limits<double>::quiet_NaN();
+  const size_t per_frame = (size_t)B * Ns;
+  for (size_t i = 0; i < (size_t)(T + 1) * per_frame * 4; ++i) ref[i] = -1;
+  for (size_t i = 0; i < (size_t)(T + 1) * per_frame; ++i)
+    ref_score[i] = ref_cscore[i] = key_score[i] = cand_score[i] = nan;
+  for (size_t i = 0; i < (size_t)B * (T + 1); ++i) margins[i] = nan;
+  for (size_t i = 0; i < (size_t)B * T * 5; ++i) bounds[i] = nan;
+  std::atomic<int> next{0};
+  auto work = [&]() {
+    for (;;) {
+      const int b = next.fetch_add(1);
+      if (b >= B) break;
+      std::vector<Tup> H;
+      H.push_back(Tup{0, g.start, 0.0, -1, -1, -1});
+      key_score[(size_t)b * Ns] = cand_score[(size_t)b * Ns] = 0.0;
+      for (int t = 0; t < lengths[b]; ++t) {
+        FrameOut fo;
+        search_frame(m, g, p, enc + ((size_t)b * T + t) * C, H, fo);
+        margins[(size_t)b * (T + 1) + t] = fo.margin;
+        double* bd = bounds + ((size_t)b * T + t) * 5;
+        bd[0] = fo.thr;
+        bd[1] = fo.s_in;
+        bd[2] = fo.s_out;
+        bd[3] = fo.c_in;
+        bd[4] = fo.c_out;
+        const size_t o = (size_t)(t + 1) * per_frame + (size_t)b * Ns;
+        for (size_t i = 0; i < fo.next.size() && i < (size_t)Ns; ++i) {
+          const Tup& x = fo.next[i];
+          int* r = ref + 4 * (o + i);
+          r[0] = (int)x.ctx;
+          r[1] = x.s;
+          r[2] = x.parent;
+          r[3] = x.label;
+          ref_score[o + i] = x.score;
+          ref_cscore[o + i] = fo.cscore.at(x.ctx);
+        }
+        // the given survivors of frame t+1, scored by the merge of frame t
+        std::vector<Tup> nH;
+        bool ok = true;
+        for (int i = 0; i < Ns; ++i) {
+          const int* x = given + 4 * (o + i);
+          if (x[0] < 0) break;
+          auto it = fo.groups.find({x[1], (int64_t)x[0]});
+          if (it == fo.groups.end()) {
+            ok = false;
+            break;
+          }
+          double ks = kNegInf, cs = kNegInf;
+          for (const Cand* c : it->second) {
+            ks = std::max(ks, c->score);
+            if (c->parent == x[2] && c->label == x[3]) cs = std::max(cs, c->score);
+          }
+          key_score[o + i] = ks;
+          cand_score[o + i] = cs == kNegInf ? nan : cs;
+          nH.push_back(Tup{(int64_t)x[0], x[1], ks, x[2], x[3], -1});
+        }
+        if (!ok || nH.empty()) break;
+        H.swap(nH);
+      }
+    }
+  };
+  int nt = nthreads > 0 ? nthreads : (int)std::thread::hardware_concurrency();
+  if (nt < 1) nt = 1;
+  if (nt > B) nt = B > 0 ? B : 1;
+  std::vector<std::thread> pool;
+  for (int i = 1; i < nt; ++i) pool.emplace_back(work);
+  work();
+  for (auto& th : pool) th.join();
+  return 0;
+}
+
 // Scores one alignment of one stream: arcs[t] is the graph arc taken at frame
 // t (-1 = blank).  Returns 0 and the fp64 path score (final weight included)
 // if the alignment is a path of the graph from the start state, -1 otherwise.
@@ -628,7 +771,7 @@ int oracle_rescore(int C, int V, int len, const float* enc, const int* arcs, con
                    const float* conv, const float* W, const float* bias, int bf16, int S,
                    int start, const int* rp, const int* dest, const int* label, const float* q,
                    const float* fin, double* score_out) {
-  Model m{V, C, E, conv, W, bias, bf16};
+  const Model m(V, C, E, conv, W, bias, bf16);
   std::vector<double> lp(V);
   int64_t ctx = 0;
   int s = start;
@@ -663,7 +806,7 @@ void* oracle_lattice(int B, int T, int C, int V, const float* enc, const int* le
                      int bf16, int S, int start, const int* rp, const int* dest,
                      const int* label, const float* q, const float* fin, double beam, int Ns,
                      int Nc, int nthreads, double* frame_margins) {
-  Model m{V, C, E, conv, W, bias, bf16};
+  const Model m(V, C, E, conv, W, bias, bf16);
   Graph g{S, start, rp, dest, label, q, fin};
   Params p{beam, Ns, Nc};
   Decoded* D = new Decoded();
@@ -810,7 +953,7 @@ int oracle_hyps(int B, int T, int C, int V, const float* enc, const int* lengths
                 const float* E, const float* conv, const float* W, const float* bias, int bf16,
                 int N, int logadd, int nthreads, int* tokens, int* ntok, double* scores,
                 int* trace, double* frame_margins) {
-  Model m{V, C, E, conv, W, bias, bf16};
+  const Model m(V, C, E, conv, W, bias, bf16);
   for (size_t i = 0; i < (size_t)B * T; ++i) tokens[i] = -1;
   if (trace)
     for (size_t i = 0; i < (size_t)(T + 1) * B * N * 2; ++i) trace[i] = -1;

@@ -611,8 +611,9 @@ tbs_status tbs_graph_create(int32_t num_states, int32_t start_state, int32_t voc
   if (start_state < 0 || start_state >= num_states)
     return fail(TBS_EINVAL, "tbs_graph_create: start_state %d outside [0, %d)", start_state,
                 num_states);
-  if (vocab_size < 2 || vocab_size > 65535)
-    return fail(TBS_EINVAL, "tbs_graph_create: vocab_size %d outside [2, 65535]", vocab_size);
+  if (vocab_size < 2 || vocab_size > kMaxVocab)
+    return fail(TBS_EINVAL, "tbs_graph_create: vocab_size %d outside [2, %d]", vocab_size,
+                kMaxVocab);
   if (!row_ptr) return fail(TBS_EINVAL, "tbs_graph_create: row_ptr is NULL");
   if (row_ptr[0] != 0) return fail(TBS_EINVAL, "tbs_graph_create: row_ptr[0] must be 0");
   int maxdeg = 0;
@@ -666,9 +667,9 @@ tbs_status tbs_graph_create(int32_t num_states, int32_t start_state, int32_t voc
 tbs_status tbs_graph_create_trivial(int32_t vocab_size, tbs_graph** out) {
   if (!out) return fail(TBS_EINVAL, "tbs_graph_create_trivial: out is NULL");
   *out = nullptr;
-  if (vocab_size < 2 || vocab_size > 65535)
-    return fail(TBS_EINVAL, "tbs_graph_create_trivial: vocab_size %d outside [2, 65535]",
-                vocab_size);
+  if (vocab_size < 2 || vocab_size > kMaxVocab)
+    return fail(TBS_EINVAL, "tbs_graph_create_trivial: vocab_size %d outside [2, %d]",
+                vocab_size, kMaxVocab);
   const int A = vocab_size - 1;
   std::vector<int32_t> rp = {0, A}, dest(A, 0), label(A);
   std::vector<float> q(A, 0.f);
@@ -688,8 +689,9 @@ tbs_status tbs_model_create(int32_t vocab_size, int32_t dim, int32_t context_siz
   if (context_size != 2)
     return fail(TBS_EUNSUPPORTED, "tbs_model_create: context_size %d unsupported (must be 2)",
                 context_size);
-  if (vocab_size < 2 || vocab_size > 65535)
-    return fail(TBS_EINVAL, "tbs_model_create: vocab_size %d outside [2, 65535]", vocab_size);
+  if (vocab_size < 2 || vocab_size > kMaxVocab)
+    return fail(TBS_EINVAL, "tbs_model_create: vocab_size %d outside [2, %d]", vocab_size,
+                kMaxVocab);
   if (dim < 1 || dim > kMaxDim)
     return fail(TBS_EINVAL, "tbs_model_create: dim %d outside [1, %d]", dim, kMaxDim);
   if (!embed || !conv || !w_out)

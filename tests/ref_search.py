@@ -285,3 +285,70 @@ def hyp_beam_search(joiner, enc, length, beam_size, logadd):
         ranked = sorted(groups.items(), key=lambda kv: (-kv[1][0], kv[1][1]))
         hyps = [(z, v) for z, (v, _) in ranked[:beam_size]]
     return list(hyps[0][0]), hyps[0][1]
+
+
+def frame_decisions(cands, beam, max_states, max_contexts, delta=None):
+    """The decisions of one frame of the pruned search (Sec. 2.5), stage by stage.
+
+    ``cands``: list of (key, score, (parent, arc position), label) with key = (state,
+    ctx); ``delta``: optional per-candidate score perturbation (same length).  Returns a
+    dict with the merge winners of the kept keys, the set after the beam + max-states
+    pruning, the kept contexts and the kept keys, plus ``terms``: one (gap, lower,
+    raise) triple per decision, where shifting the candidates ``lower`` down and
+    ``raise`` up by just over half the gap changes that decision (None stands for
+    every candidate not in the other list)."""
+    sc = [c[1] + (0.0 if delta is None else float(delta[i])) for i, c in enumerate(cands)]
+    order = sorted(range(len(cands)), key=lambda i: (-sc[i], cands[i][2]))
+    by_key = {}
+    for i in order:                      # candidates of each key, best first
+        by_key.setdefault(cands[i][0], []).append(i)
+    merged = {k: ix[0] for k, ix in by_key.items()}
+    ents = sorted(merged, key=lambda k: (-sc[merged[k]], k))
+    top = sc[merged[ents[0]]]
+    thr = top - beam
+    in_beam = [k for k in ents if sc[merged[k]] >= thr]
+    pre = in_beam[:max_states]
+    terms = []
+    if len(in_beam) > max_states:
+        a, b = in_beam[max_states - 1], in_beam[max_states]
+        terms.append((sc[merged[a]] - sc[merged[b]], by_key[a], by_key[b]))
+    if math.isfinite(beam):
+        # the best tuple is never outside its own beam; the others are inside or
+        # outside by their distance to the threshold (None: every other candidate)
+        for k in ents[1:max_states]:
+            d = sc[merged[k]] - thr
+            terms.append((abs(d), by_key[k], None) if d >= 0 else (abs(d), None, by_key[k]))
+    cbest = {}
+    for k in pre:
+        cbest[k[1]] = max(cbest.get(k[1], -math.inf), sc[merged[k]])
+    cl = sorted(cbest, key=lambda c: (-cbest[c], c))
+    kept_ctx = set(cl[:max_contexts])
+    if len(cl) > max_contexts:
+        a, b = cl[max_contexts - 1], cl[max_contexts]
+        terms.append((cbest[a] - cbest[b],
+                      [i for k in pre if k[1] == a for i in by_key[k]],
+                      [i for k in pre if k[1] == b for i in by_key[k]]))
+    kept = sorted((k for k in pre if k[1] in kept_ctx), key=lambda k: (k[1], k[0]))
+    winners = {}
+    for k in kept:
+        w = merged[k]
+        winners[k] = (cands[w][2][0], cands[w][3])
+        other = [i for i in by_key[k] if (cands[i][2][0], cands[i][3]) != winners[k]]
+        if other:
+            terms.append((sc[w] - sc[other[0]], [w], [other[0]]))
+    return {"winners": winners, "pre": frozenset(pre), "ctx": frozenset(kept_ctx),
+            "kept": kept, "scores": {k: sc[merged[k]] for k in kept}, "terms": terms}
+
+
+def frame_candidates(lp_row, graph, hyps, V):
+    """Unpruned expansion of one frame (blank keeps (ctx, state); arcs move to
+    ((b, c), dest) with q + log P(c)): (key, score, (parent, arc position), label)."""
+    rp, dest, lab, q = graph.row_ptr, graph.dest, graph.label, graph.score
+    cands = []
+    for i, (ctx, s, v) in enumerate(hyps):
+        p = lp_row(ctx)
+        cands.append(((s, ctx), v + p[0], (i, -1), 0))
+        for pos, j in enumerate(range(rp[s], rp[s + 1])):
+            c = int(lab[j])
+            cands.append(((int(dest[j]), (ctx % V) * V + c), v + float(q[j]) + p[c], (i, pos), c))
+    return cands

@@ -41,6 +41,7 @@ def _graph(S, start, V, rp, dest, label, score, final=None):
     (dict(start=3), "start_state"),
     (dict(V=1), "vocab_size"),
     (dict(V=70000), "vocab_size"),
+    (dict(V=46341), "vocab_size"),   # contexts a * V + b would overflow int32
     (dict(rp=[1, 2, 3]), "row_ptr[0]"),
     (dict(rp=[0, 2, 1]), "decreases"),
     (dict(dest=[0, 2]), "dest[1]"),
@@ -67,6 +68,12 @@ def test_model_validation_before_device_work():
     assert L.tbs_model_create(10, 8, 3, None, None, None, None, 0, None, ctypes.byref(h)) == EUNSUPPORTED
     assert L.tbs_model_create(10, 0, 2, None, None, None, None, 0, None, ctypes.byref(h)) == EINVAL
     assert L.tbs_model_create(10, 8, 2, None, None, None, None, 0, None, ctypes.byref(h)) == EINVAL
+    assert "NULL" in L.tbs_last_error().decode()
+    # contexts a * V + b are int32: V = 46,341 would overflow, 46,340 is the limit
+    assert L.tbs_model_create(46341, 8, 2, None, None, None, None, 0, None, ctypes.byref(h)) == EINVAL
+    assert "vocab_size" in L.tbs_last_error().decode()
+    assert L.tbs_graph_create_trivial(46341, ctypes.byref(h)) == EINVAL
+    assert L.tbs_model_create(46340, 8, 2, None, None, None, None, 0, None, ctypes.byref(h)) == EINVAL
     assert "NULL" in L.tbs_last_error().decode()
 
 

@@ -10,7 +10,11 @@ reported and skipped.
 Parity rule (see parity.py): survivor traces identical up to the first frame with a
 decision margin below MARGIN, and over whole streams where no decision is that close;
 tokens, arcs and status identical on such streams; scores within 1e-4 (fp32 joiner) or
-2e-2 (bf16 joiner, against the bf16-operand oracle).  MARGIN (1e-4 for fp32) is tighter
+2e-2 (bf16 joiner, against the bf16-operand oracle).  Then every frame of every checked
+stream is replayed: the oracle decides it again from the HIP path's own survivors of the
+previous frame, and the HIP survivors must equal the oracle's bit for bit wherever that
+frame's margin exceeds MARGIN (a valid selection elsewhere).  Each case asserts a floor
+on the frames compared bit for bit.  MARGIN (1e-4 for fp32) is tighter
 than the 1e-3 the tolerance allows: the fp32 path's per-decision score error is ~1e-6.
 For the bf16 joiner, h rounds to bf16 from an fp32 tanh on the GPU and from an fp64 tanh
 in the oracle; isolated elements then round to neighbouring bf16 values (logit error
@@ -23,7 +27,7 @@ import pytest
 
 import oracle
 from gpu_util import gpu_decode, say
-from parity import check_trace_invariants, compare
+from parity import check_trace_invariants, compare, replay_check
 from paper_2211_00484_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -36,7 +40,11 @@ SCHEDULES = ["frame", "stream"]
 
 
 def _run(name_or_parts, beam, Ns, Nc, dtype="fp32", streams=None, nthreads=0, seed=0, B=None,
-         schedule="frame"):
+         schedule="frame", exact_floor=None):
+    """Decodes on the GPU, compares with the oracle and replays every frame.  Returns
+    (gpu, oracle, report).  exact_floor: the smallest fraction of the
+    checked frames the replay must compare bit for bit (default: half of what the
+    oracle's own margins predict)."""
     from paper_2211_00484_amd import tbs
     if isinstance(name_or_parts, str):
         w, inputs, model, graph = synth.make_workload(name_or_parts, seed=seed, B=B)
@@ -60,6 +68,14 @@ def _run(name_or_parts, beam, Ns, Nc, dtype="fp32", streams=None, nthreads=0, se
     check_trace_invariants(g["trace"], inputs.lengths, graph, model.vocab_size, Ns, min(Nc, Ns),
                            streams)
     say(f"  {rep}")
+    rrep = replay_check(g, model, graph, inputs.encoder_out, inputs.lengths, streams, beam, Ns,
+                        min(Nc, Ns), margin=tol["margin"], tol=tol["score_tol"],
+                        bf16=(dtype == "bf16"), nthreads=nthreads)
+    say(f"  {rrep}")
+    predicted = sum(int((o.frame_margins[k, :inputs.lengths[b]] > tol["margin"]).sum())
+                    for k, b in enumerate(streams))
+    floor = (exact_floor * rrep.frames) if exact_floor is not None else 0.5 * predicted
+    assert rrep.exact >= floor, f"only {rrep.exact} of {rrep.frames} frames compared bit for bit"
     return g, o, rep
 
 
@@ -148,21 +164,28 @@ def test_max_states_limit(schedule):
 
 @pytest.mark.parametrize("schedule", SCHEDULES + ["stream1"])
 def test_standard(schedule):
-    _, _, rep = _run("standard", math.inf, 4, 4, schedule=schedule)
+    # oracle margins: 76% of the frames precede their stream's first contested frame
+    # (18 of 32 streams clean), 99.7% of the frames have a margin above 1e-4
+    _, _, rep = _run("standard", math.inf, 4, 4, schedule=schedule, exact_floor=0.98)
     assert rep.streams == 32
+    assert rep.frames_prefix >= 0.70 * rep.frames and rep.clean >= 14
 
 
 @pytest.mark.parametrize("schedule", SCHEDULES)
 def test_graph(schedule):
-    _, _, rep = _run("graph", 4.0, 32, 8, schedule=schedule)
+    # oracle margins: 54% prefix (7 of 32 streams clean), 99.2% of frames above 1e-4
+    _, _, rep = _run("graph", 4.0, 32, 8, schedule=schedule, exact_floor=0.97)
     assert rep.streams == 32
+    assert rep.frames_prefix >= 0.50 * rep.frames and rep.clean >= 5
 
 
 @pytest.mark.parametrize("schedule", SCHEDULES)
 def test_throughput_sampled(schedule):
-    # full B = 256 on the GPU (the configuration the benchmark times), 16 streams checked
-    _run("throughput", math.inf, 4, 4, dtype="bf16", streams=range(0, 256, 16),
-         schedule=schedule)
+    # full B = 256 on the GPU (the configuration the benchmark times), 64 streams checked;
+    # bf16 margins of 2e-3 leave 94% of their frames above the threshold
+    _, _, rep = _run("throughput", math.inf, 4, 4, dtype="bf16", streams=range(0, 256, 4),
+                     schedule=schedule, exact_floor=0.90)
+    assert rep.streams == 64
 
 
 @pytest.mark.parametrize("B", [256, 1024])
@@ -178,9 +201,25 @@ def test_trivial_wide_frame_joiner(dtype, B):
          streams=range(0, B, B // 8), schedule="frame")
 
 
+LARGE_STREAMS = list(range(0, 128, 8))
+# oracle margins on these streams: fp32 99.6% of frames above 1e-4 (58% prefix, 5 clean
+# streams); bf16 91.9% above 2e-3 (4% prefix, no clean stream: the replay carries it)
+LARGE_FLOOR = {"fp32": 0.97, "bf16": 0.85}
+
+
 def test_large_sampled():
-    # full B = 128 on the GPU, V = 5,000 and the 1M-state power-law graph; 2 streams checked
-    _run("large", 8.0, 64, 16, streams=[3, 77])
+    # full B = 128 on the GPU, V = 5,000 and the 1M-state power-law graph; 16 streams
+    # spread over the batch checked on every frame
+    _, _, rep = _run("large", 8.0, 64, 16, streams=LARGE_STREAMS, exact_floor=LARGE_FLOOR["fp32"])
+    assert rep.streams == 16
+
+
+def test_large_bf16_sampled():
+    # the Large workload with the bf16 joiner (the benchmark's large-bf16 line), the same
+    # 16 streams, against the bf16-operand oracle
+    _, _, rep = _run("large", 8.0, 64, 16, dtype="bf16", streams=LARGE_STREAMS,
+                     exact_floor=LARGE_FLOOR["bf16"])
+    assert rep.streams == 16
 
 
 @pytest.mark.parametrize("schedule", SCHEDULES)
