@@ -6,7 +6,9 @@ on one MI355X, with the dominant kernel's roofline fraction and the CPU oracle's
 
 A step is one tbs_decode of the whole batch (every frame of every stream: joiner,
 expansion, merge, pruning, history, traceback) on inputs already resident in HBM.
-`value` is frames over the wall time of K plain steps.  Per-kernel durations come
+`value` is frames over the median duration of K plain steps (HIP events between
+consecutive steps on the decode stream; the mean wall time is reported beside it).
+Per-kernel durations come
 from K further steps during which the library records HIP events around each launch
 on the decode stream (tbs_model_set_profiling).  Algorithmic work (joiner FLOP,
 search bytes) is counted from the survivor trace of one untimed decode.
@@ -15,6 +17,7 @@ Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import statistics
 import json
 import math
 import os
@@ -31,7 +34,7 @@ METRIC = "decoded frames/sec (B×T) at beam 4; joiner MFMA util %; prune HBM GB/
 # MI355X published peaks: fp32 matrix and fp32 vector are both 157.3 TFLOP/s
 PEAK = {"fp32_mfma_tflops": 157.3, "fp32_vector_tflops": 157.3, "bf16_mfma_tflops": 2500.0,
         "hbm_gbps": 8000.0}
-DEFAULT_STEPS = {"tiny": 50, "standard": 20, "graph": 20, "throughput": 10, "large": 3}
+DEFAULT_STEPS = {"tiny": 50, "standard": 20, "graph": 20, "throughput": 10, "large": 10}
 KERNEL_SRC = os.path.join(ROOT, "paper_2211_00484_amd", "csrc", "kernels.hip")
 TRAFFIC_TABLE = os.path.join(ROOT, "profiles", "traffic.md")
 COPY_BYTES = 256 << 20
@@ -710,13 +713,18 @@ def main():
         tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
     torch.cuda.synchronize()
 
-    # the timed steps: nothing but the decodes on the stream
+    # the timed steps: nothing but the decodes on the stream, with an event between
+    # consecutive steps (a marker, no host synchronisation) for the per-step median
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(K):
+    evs[0].record()
+    for i in range(K):
         tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+        evs[i + 1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(K)]
 
     # the same steps again with HIP events around every kernel launch: per-kernel
     # durations for the roofline (the events add a little time between kernels)
@@ -730,9 +738,10 @@ def main():
     prof = model.read_profile()
     model.set_profiling(False)
 
-    ms_step = (t1 - t0) * 1e3 / K
+    ms_step = statistics.median(step_ms)
+    ms_step_mean_wall = (t1 - t0) * 1e3 / K
     ms_step_events = (t3 - t2) * 1e3 / K
-    value = frames * K / (t1 - t0)
+    value = frames / (ms_step * 1e-3)
 
     kernels, roofline, schedule, j_tflops, s_gbps, peak_j = decode_roofline(prof, K, work, dtype)
     tr = measured_traffic(w.name if dtype == w.dtype else f"{w.name}-{dtype}", roofline["kernel"])
@@ -756,6 +765,7 @@ def main():
         "kernels": kernels,
         "joiner_mfma_util_pct": 100.0 * j_tflops / peak_j,
         "search_hbm_gbps": s_gbps,
+        "ms_per_step_mean_wall": ms_step_mean_wall,
         "ms_per_step_with_kernel_timing_events": ms_step_events,
         "per_frame_latency_us": 1e3 * ms_step / max(int(inputs.lengths.max()), 1),
         "work_per_step": work,
@@ -767,4 +777,9 @@ def main():
 
 
 if __name__ == "__main__":
-    main()
+    try:
+        main()
+    finally:
+        # release the library's handles while the HIP runtime is fully up
+        if "paper_2211_00484_amd.tbs" in sys.modules:
+            sys.modules["paper_2211_00484_amd.tbs"].close_all()

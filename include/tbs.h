@@ -397,8 +397,13 @@ tbs_status tbs_transducer_forward(int32_t kind, const float *blank, const float 
  *                        per-row normaliser terms and best labels every frame
  *                        through tagged words in device memory (device-scope
  *                        atomics; cooperative launch), and all run the same search.
- *                        out_status[b] = 2 reports an exchange wait that timed
- *                        out (results of that decode are then not valid);
+ *                        A wait that exhausts its poll budget (which does not
+ *                        happen while the whole grid is resident, as the
+ *                        cooperative launch guarantees) makes every later wait
+ *                        of the launch give up at once; each stream that gave up
+ *                        returns out_status[b] = 2 and a NaN score (so the
+ *                        failure shows even when out_status is NULL), and its
+ *                        tokens are not valid;
  *   TBS_SCHEDULE_AUTO    (default) STREAM when it fits, the joiner weight
  *                        (V x dim) is at most 4 MiB and the joiner is bf16 or
  *                        max_contexts <= 4; else FRAME.
@@ -413,6 +418,16 @@ typedef enum {
 } tbs_schedule;
 
 tbs_status tbs_model_set_schedule(tbs_model *model, int32_t schedule);
+
+/*
+ * Poll budget of each exchange wait of the grouped per-stream kernel
+ * (TBS_SCHEDULE_STREAM): polls >= 1, or 0 for the default (4,194,304).  A
+ * diagnostic for the timeout path: a tiny budget makes waits give up while
+ * the other workgroups are still busy, so that path can be exercised with
+ * every kernel still finishing normally.  Per model, for later decodes;
+ * polls < 0 returns TBS_EINVAL.
+ */
+tbs_status tbs_model_set_exchange_spin_limit(tbs_model *model, int32_t polls);
 
 /*
  * Decoder + joiner + log-softmax alone (Algorithm 1: Decoder, IndexSelect,

@@ -73,6 +73,7 @@ struct Workspace {
   int* hist_arc = nullptr;
   int* path_lab = nullptr;
   int* len_host = nullptr;  // pinned staging for lengths (and frame bases), [2B]
+  unsigned* xerr = nullptr;  // [1 + B] exchange timeouts of the grouped kernel: any, per stream
   GraphDev* gtab = nullptr;       // [B] per-stream graph table (decodes with one graph per stream)
   GraphDev* gtab_host = nullptr;  // pinned staging for it
   hipEvent_t done = nullptr;
@@ -84,6 +85,7 @@ struct Workspace {
     (void)hipFree(logits); (void)hipFree(stats); (void)hipFree(tk_z); (void)hipFree(tk_c); (void)hipFree(z0);
     (void)hipFree(hist_pl); (void)hipFree(hist_arc); (void)hipFree(path_lab);
     (void)hipFree(gtab);
+    (void)hipFree(xerr);
     if (len_host) (void)hipHostFree(len_host);
     if (gtab_host) (void)hipHostFree(gtab_host);
     if (done) (void)hipEventDestroy(done);
@@ -166,7 +168,7 @@ struct tbs_model {
   int V = 0, C = 0, Kpad = 0, Vpad = 0, bf16 = 0;
   int dev = 0, ncu = 0, coop = 0;   // device, compute units, cooperative launch support
   XBuf xbuf;
-  unsigned* xerr = nullptr;         // exchange timeouts (device counter)
+  unsigned spin_limit = kDefaultSpinLimit;  // polls before a grouped-kernel wait gives up
   float* P0 = nullptr;
   float* P1 = nullptr;
   float* Wf = nullptr;
@@ -337,6 +339,7 @@ tbs_status alloc_workspace(const tbs_model* m, Workspace& w, int B, int T, int N
   HIP_TRY(dalloc(&w.hist_arc, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.path_lab, (size_t)B * T), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.gtab, B), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.xerr, 1 + (size_t)B), "hipMalloc(workspace)");
   HIP_TRY(hipHostMalloc((void**)&w.len_host, (size_t)(B > 0 ? 2 * B : 1) * 4, hipHostMallocDefault),
           "hipHostMalloc(workspace)");
   HIP_TRY(hipHostMalloc((void**)&w.gtab_host, (size_t)(B > 0 ? B : 1) * sizeof(GraphDev),
@@ -476,7 +479,7 @@ DecodeDev decode_dev(const tbs_model* m, const Workspace& w, int B, int T, int N
 
 // Enqueues frames 0 .. maxlen-1 of d: the grouped or single-workgroup persistent
 // kernel, or the joiner and search kernels per frame.  xerr: the exchange-timeout
-// counter the grouped kernel adds to.  *grouped: whether the grouped kernel ran.
+// counters ([1 + B]) the grouped kernel adds to.  *grouped: whether the grouped kernel ran.
 tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
                           const StreamPlan& splan, bool per_stream, const DecodeDev& d,
                           int maxlen, int* trace, unsigned* xerr, hipStream_t st, bool* grouped) {
@@ -490,8 +493,8 @@ tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
     HIP_TRY(ensure_xbuf(m, (size_t)d.B * G * 2 * group_words(d.Nc, d.KT), st), "exchange buffer");
     const unsigned epoch = next_epoch();
     hipError_t e = timed_launch(m, TBS_KERNEL_STREAM_GROUP, st, [&] {
-      return launch_stream_group(md, gd, d, beam, trace, splan, m->xbuf.p, G, epoch, 1u << 22,
-                                 xerr, st);
+      return launch_stream_group(md, gd, d, beam, trace, splan, m->xbuf.p, G, epoch,
+                                 m->spin_limit, xerr, st);
     });
     if (e == hipSuccess) {
       *grouped = true;
@@ -594,7 +597,6 @@ struct tbs_state {
   bool per_stream = false;
   StreamPlan splan{};
   Workspace w;
-  unsigned* xerr = nullptr;  // exchange timeouts over all chunks
   std::vector<int> done;     // frames decoded so far per stream
 };
 
@@ -712,8 +714,6 @@ tbs_status tbs_model_create(int32_t vocab_size, int32_t dim, int32_t context_siz
   if (e == hipSuccess)
     e = hipDeviceGetAttribute(&m->coop, hipDeviceAttributeCooperativeLaunch, m->dev);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&m->busy, hipEventDisableTiming);
-  if (e == hipSuccess) e = dalloc(&m->xerr, 1);
-  if (e == hipSuccess) e = hipMemsetAsync(m->xerr, 0, sizeof(unsigned), st);
   if (e == hipSuccess) e = dalloc(&m->P0, VK);
   if (e == hipSuccess) e = dalloc(&m->P1, VK);
   if (e == hipSuccess) e = m->bf16 ? dalloc(&m->Wb, VpK) : dalloc(&m->Wf, VpK);
@@ -749,7 +749,6 @@ void tbs_model_destroy(tbs_model* m) {
   (void)hipFree(m->Wb);
   (void)hipFree(m->Wi);
   (void)hipFree(m->bias);
-  (void)hipFree(m->xerr);
   if (m->busy) {
     if (m->busy_pending) (void)hipEventSynchronize(m->busy);
     (void)hipEventDestroy(m->busy);
@@ -823,14 +822,14 @@ tbs_status decode_impl(const tbs_model* model, const tbs_graph* graph,
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
-  HIP_TRY(launch_fill_i32((int*)m->xerr, 1, 0, st), "fill(exchange errors)");
+  HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B, 0, st), "fill(exchange errors)");
   bool grouped = false;
-  s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, m->xerr, st, &grouped);
+  s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, w.xerr, st, &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
                          return launch_final(gd, d, out_tokens, out_num_tokens, out_scores,
-                                             out_status, out_arcs, grouped ? m->xerr : nullptr,
+                                             out_status, out_arcs, grouped ? w.xerr : nullptr,
                                              st);
                        }),
           "launch(final)");
@@ -870,8 +869,7 @@ tbs_status state_create_impl(const tbs_model* model, const tbs_graph* graph,
   if (s == TBS_OK) s = alloc_workspace(m, S->w, B, max_frames, S->Ns, S->Nc, S->KT, S->KT == 0);
   hipError_t e = hipSuccess;
   if (s == TBS_OK) {
-    e = dalloc(&S->xerr, 1);
-    if (e == hipSuccess) e = launch_fill_i32((int*)S->xerr, 1, 0, st);
+    e = launch_fill_i32((int*)S->w.xerr, 1 + (long long)B, 0, st);
     // the initial tuple of every stream (k_init with zero lengths writes no joiner row)
     if (e == hipSuccess) e = launch_fill_i32(S->w.len, 2 * (long long)B, 0, st);
     // the graph table stays for the state's lifetime
@@ -888,7 +886,6 @@ tbs_status state_create_impl(const tbs_model* model, const tbs_graph* graph,
   if (s != TBS_OK) {
     if (S->w.pending) (void)hipEventSynchronize(S->w.done);
     S->w.release();
-    (void)hipFree(S->xerr);
     delete S;
     return s;
   }
@@ -1225,7 +1222,7 @@ tbs_status tbs_decode_chunk(tbs_state* S, const float* encoder_chunk,
           "launch(resume)");
   bool grouped = false;
   tbs_status s = enqueue_frames(m, S->gd, S->beam, S->splan, S->per_stream, d, maxlen, trace,
-                                S->xerr, st, &grouped);
+                                S->w.xerr, st, &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
   w.pending = true;
@@ -1254,7 +1251,7 @@ tbs_status tbs_state_finish(tbs_state* S, int32_t* out_tokens, int32_t* out_num_
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
                          return launch_final(S->gd, d, out_tokens, out_num_tokens,
-                                             out_scores, out_status, out_arcs, S->xerr, st);
+                                             out_scores, out_status, out_arcs, S->w.xerr, st);
                        }),
           "launch(final)");
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
@@ -1269,7 +1266,6 @@ void tbs_state_destroy(tbs_state* S) {
     if (S->w.pending) (void)hipEventSynchronize(S->w.done);
     S->w.release();
   }
-  (void)hipFree(S->xerr);
   delete S;
 }
 
@@ -1312,6 +1308,14 @@ tbs_status tbs_model_set_schedule(tbs_model* model, int32_t schedule) {
     return fail(TBS_EINVAL, "tbs_model_set_schedule: unknown schedule %d", schedule);
   std::lock_guard<std::mutex> lk(model->mu);
   model->schedule = schedule;
+  return TBS_OK;
+}
+
+tbs_status tbs_model_set_exchange_spin_limit(tbs_model* model, int32_t polls) {
+  if (!model) return fail(TBS_EINVAL, "tbs_model_set_exchange_spin_limit: model is NULL");
+  if (polls < 0) return fail(TBS_EINVAL, "tbs_model_set_exchange_spin_limit: polls %d < 0", polls);
+  std::lock_guard<std::mutex> lk(model->mu);
+  model->spin_limit = polls == 0 ? kDefaultSpinLimit : (unsigned)polls;
   return TBS_OK;
 }
 

@@ -2430,7 +2430,8 @@ struct GroupX {
   int G, xwords;            // members per stream; words per slot
   unsigned epoch;           // decode number (16 bits), tags are epoch << 16 | frame
   unsigned spin_limit;      // polls before a wait is abandoned (recorded in err)
-  unsigned* err;
+  unsigned* err;            // [1 + B]: timeouts of any stream (checked by every later
+                            // wait, which then gives up at once), then per stream
 };
 
 // LDS layout of the grouped kernel beyond SearchSmem.
@@ -2645,8 +2646,16 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         unsigned long long v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         unsigned n = 0;
         while ((unsigned)(v >> 32) != tag) {
-          if (++n > x.spin_limit) {
-            atomicAdd(x.err, 1u);
+          ++n;
+          if (n > x.spin_limit ||
+              ((n & 255u) == 0 &&
+               __hip_atomic_load(x.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+            __hip_atomic_fetch_add(x.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(x.err + 1 + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // a neutral payload (the word may hold another decode's data): score words
+            // -inf, the exp-sum and label words 0, so nothing stale is selected
+            const int r = rest % RW;
+            v = (r & 1) ? 0ull : 0xff800000ull;
             break;
           }
           v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2895,7 +2904,10 @@ __global__ __launch_bounds__(256) void k_final(GraphDev g, DecodeDev d, int* __r
     const int st = d.surv_state[(size_t)b * Ns + pick];
     const double f = (status == 0 && g.fin) ? (double)g.fin[st] : 0.0;
     out_scores[b] = (double)d.surv_score[(size_t)b * Ns + pick] + d.offset[b] + f;
-    if (xerr && *xerr) status = 2;  // a grouped stream's exchange wait timed out
+    if (xerr && xerr[1 + b]) {  // a grouped stream's exchange wait timed out
+      status = 2;
+      out_scores[b] = __longlong_as_double(0x7ff8000000000000ll);  // NaN
+    }
     if (out_status) out_status[b] = status;
     s_idx = pick;
   }

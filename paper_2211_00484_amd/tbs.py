@@ -6,10 +6,12 @@ the first call does, and raises if ``libtbs.so`` has not been built.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import math
 import os
 import re
+import weakref
 from dataclasses import dataclass
 from typing import Optional
 
@@ -47,6 +49,29 @@ class BeamParams(ctypes.Structure):
 
 
 _lib = None
+# Set when the interpreter starts to exit: handles still open then are left to the
+# process teardown instead of calling into the library (and HIP) from finalizers that
+# may run after the runtime has begun shutting down.  Call close() to release earlier.
+_exiting = False
+
+
+def _at_exit():
+    global _exiting
+    _exiting = True
+
+
+atexit.register(_at_exit)
+
+_live = weakref.WeakSet()  # open handles (graphs, models, decode states, lattices)
+
+
+def close_all():
+    """Releases every handle still open: lattices and decode states first, then models
+    and graphs (a lattice or state refers to its model).  For programs that want the
+    device memory back before the interpreter exits."""
+    order = {"Lattice": 0, "DecodeState": 1, "Model": 2, "Graph": 3}
+    for obj in sorted(list(_live), key=lambda o: order.get(type(o).__name__, 4)):
+        obj.close()
 
 
 def declared_symbols() -> list:
@@ -86,6 +111,8 @@ def lib():
                                     _P, _P, _P, _P, _P, _P, _P]
     L.tbs_model_set_schedule.restype = _I32
     L.tbs_model_set_schedule.argtypes = [_P, _I32]
+    L.tbs_model_set_exchange_spin_limit.restype = _I32
+    L.tbs_model_set_exchange_spin_limit.argtypes = [_P, _I32]
     L.tbs_model_set_profiling.restype = _I32
     L.tbs_model_set_profiling.argtypes = [_P, _I32]
     L.tbs_model_read_profile.restype = _I32
@@ -155,6 +182,7 @@ class Graph:
 
     def __init__(self, handle, num_states: int, vocab_size: int, max_out_degree: int):
         self._h = handle
+        _live.add(self)
         self.num_states, self.vocab_size, self.max_out_degree = num_states, vocab_size, max_out_degree
 
     @classmethod
@@ -183,7 +211,7 @@ class Graph:
                             g.score, g.final)
 
     def close(self):
-        if self._h is not None and _lib is not None:
+        if self._h is not None and _lib is not None and not _exiting:
             _lib.tbs_graph_destroy(self._h)
         self._h = None
 
@@ -214,12 +242,18 @@ class Model:
                                       _dev_ptr(W), _dev_ptr(b), code, _stream_ptr(stream),
                                       ctypes.byref(h)))
         self._h = h
+        _live.add(self)
         self.vocab_size, self.dim, self.dtype = int(vocab_size), int(dim), dtype
 
     def set_schedule(self, schedule: str):
         """Frame-loop schedule for later decodes: "auto", "frame", "stream" (several
         workgroups per stream where possible) or "stream1" (one per stream)."""
         _check(lib().tbs_model_set_schedule(self._h, SCHEDULES[schedule]))
+
+    def set_exchange_spin_limit(self, polls: int):
+        """Poll budget of the grouped kernel's exchange waits (0 = default); a
+        diagnostic for the timeout path."""
+        _check(lib().tbs_model_set_exchange_spin_limit(self._h, int(polls)))
 
     def set_profiling(self, enable: bool):
         _check(lib().tbs_model_set_profiling(self._h, int(bool(enable))))
@@ -235,7 +269,7 @@ class Model:
         return cls(m.vocab_size, m.dim, m.embed, m.conv, m.w_out, m.b_out, dtype=dtype)
 
     def close(self):
-        if self._h is not None and _lib is not None:
+        if self._h is not None and _lib is not None and not _exiting:
             _lib.tbs_model_destroy(self._h)
         self._h = None
 
@@ -347,6 +381,7 @@ class DecodeState:
         _check(fn(model._h, gh, ctypes.byref(params), int(B), int(max_frames),
                   _stream_ptr(stream), ctypes.byref(h)))
         self._h = h
+        _live.add(self)
         self._refs = (model, graph)  # the state must not outlive them
         self.B, self.max_frames, self.max_states = int(B), int(max_frames), int(max_states)
 
@@ -369,7 +404,7 @@ class DecodeState:
         return out
 
     def close(self):
-        if self._h is not None and _lib is not None:
+        if self._h is not None and _lib is not None and not _exiting:
             _lib.tbs_state_destroy(self._h)
         self._h = None
 
@@ -417,6 +452,7 @@ class Lattice:
         _check(fn(model._h, gh, ctypes.byref(params), _dev_ptr(encoder_out.contiguous()),
                   _host_ptr(lens), B, T, _stream_ptr(stream), ctypes.byref(h)))
         self._h = h
+        _live.add(self)
         self._refs = (model, graph)
         self.device = encoder_out.device
         self.B, self.T, self.max_states = B, T, int(max_states)
@@ -469,7 +505,7 @@ class Lattice:
         return out
 
     def close(self):
-        if self._h is not None and _lib is not None:
+        if self._h is not None and _lib is not None and not _exiting:
             _lib.tbs_lattice_destroy(self._h)
         self._h = None
 

@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 from gpu_util import say
-from parity import check_trace_invariants, compare
+from parity import check_trace_invariants, compare, replay_check
 from paper_2211_00484_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -61,6 +61,10 @@ def test_grouped_trivial(V, C, B, Ns, Nc, beam, grouped):
                   margin=1e-4, score_tol=1e-4)
     check_trace_invariants(g["trace"], inputs.lengths, graph_np, V, Ns, min(Nc, Ns), streams)
     say(f"  {rep}")
+    rrep = replay_check(g, model_np, graph_np, inputs.encoder_out, inputs.lengths, streams, beam,
+                        Ns, min(Nc, Ns), margin=1e-4, tol=1e-4)
+    say(f"  {rrep}")
+    assert rrep.exact >= 0.9 * rrep.frames
 
 
 def test_grouped_repeated_decodes_agree():
@@ -81,3 +85,38 @@ def test_grouped_repeated_decodes_agree():
     for a in outs[1:]:
         for x, y in zip(outs[0], a):
             assert np.array_equal(x, y)
+
+
+def test_grouped_timeout_path_reports_and_recovers():
+    # A one-poll budget makes exchange waits give up while other members are still
+    # working (every kernel still finishes: waits are bounded and a timed-out wait takes
+    # a neutral payload).  Streams that gave up report status 2 and a NaN score; with
+    # the default budget restored the next decode is the normal one again.
+    import torch
+    from paper_2211_00484_amd import tbs
+    w, inputs, model_np, graph_np = synth.make_workload("standard")
+    model = tbs.Model.from_synth(model_np)
+    graph = tbs.Graph.from_synth(graph_np)
+    model.set_schedule("stream")
+    enc = torch.from_numpy(inputs.encoder_out).cuda()
+
+    def run():
+        out = tbs.decode(model, graph, enc, inputs.lengths, beam=math.inf, max_states=4,
+                         max_contexts=4, want_trace=True)
+        torch.cuda.synchronize()
+        return (out.status.cpu().numpy(), out.scores.cpu().numpy(), out.tokens.cpu().numpy(),
+                out.trace.cpu().numpy())
+
+    ref = run()
+    assert (ref[0] == 0).all()
+    model.set_exchange_spin_limit(1)
+    st, sc, _, _ = run()
+    say(f"  one-poll budget: {int((st == 2).sum())} of {inputs.B} streams timed out")
+    assert set(np.unique(st).tolist()) <= {0, 2}
+    assert np.array_equal(st == 2, np.isnan(sc))
+    model.set_exchange_spin_limit(0)
+    again = run()
+    for x, y in zip(ref, again):
+        assert np.array_equal(x, y)
+    with pytest.raises(tbs.TbsError, match="EINVAL"):
+        model.set_exchange_spin_limit(-1)
