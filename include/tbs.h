@@ -182,6 +182,33 @@ tbs_status tbs_decode_graphs(const tbs_model *model, const tbs_graph *const *gra
                              int32_t *out_arcs, int32_t *trace, void *hip_stream);
 
 /*
+ * tbs_decode without any allocation, for callers that cannot allocate: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  The decode workspace (survivors, history, joiner rows, softmax
+ * partials, the grouped kernel's exchange words) is carved from a file-scope
+ * device array of 64 MiB that each GPU the library runs on holds until the
+ * process ends; the call makes no hipMalloc, hipFree, host allocation or
+ * event creation, and ignores per-kernel profiling.
+ * Differences from tbs_decode:
+ *   lengths  DEVICE int32 [B] (not host), read on the device and clamped to
+ *            [0, T]; the frame loop runs to T (frames past a stream's length
+ *            do nothing for it).
+ *   one shared graph (no per-stream graphs).
+ * Every call on a GPU shares that GPU's array and leaves its contents behind
+ * (each call clears what must start at zero).  Calls on the same model are
+ * serialised like tbs_decode; calls on different models or threads that
+ * overlap on one GPU race on the array and must be ordered by the caller.
+ * Other arguments, outputs and errors as for tbs_decode; TBS_ECAPACITY when
+ * the workspace of (B, T, max_states, max_contexts, vocabulary) exceeds the
+ * array (nothing is enqueued then).
+ */
+tbs_status tbs_decode_noalloc(const tbs_model *model, const tbs_graph *graph,
+                              const tbs_beam_params *params, const float *encoder_out,
+                              const int32_t *lengths, int32_t B, int32_t T, int32_t *out_tokens,
+                              int32_t *out_num_tokens, double *out_scores, int32_t *out_status,
+                              int32_t *out_arcs, int32_t *trace, void *hip_stream);
+
+/*
  * Streaming decode: tbs_decode split into chunks of frames (the decoding state of
  * Algorithm 1 carried across calls).  A decode state holds, for each of B streams,
  * the surviving tuples, the fp64 score offset and the back-pointers of every frame

@@ -13,11 +13,16 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "internal.h"
 
 using namespace tbs;
+
+// Workspace of tbs_decode_noalloc: one array per device, held until the process ends.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -477,24 +482,38 @@ DecodeDev decode_dev(const tbs_model* m, const Workspace& w, int B, int T, int N
   return d;
 }
 
+// Workgroups per stream the decode of d will take (1: not grouped).
+int decode_group(const tbs_model* m, const GraphDev& gd, const StreamPlan& splan, bool per_stream,
+                 const DecodeDev& d, int maxlen) {
+  return (per_stream && m->schedule != TBS_SCHEDULE_STREAM_SINGLE)
+             ? pick_group(m, splan, d.B, d.KT, maxlen, gd.trivial)
+             : 1;
+}
+
 // Enqueues frames 0 .. maxlen-1 of d: the grouped or single-workgroup persistent
 // kernel, or the joiner and search kernels per frame.  xerr: the exchange-timeout
-// counters ([1 + B]) the grouped kernel adds to.  *grouped: whether the grouped kernel ran.
+// counters ([1 + B]) the grouped kernel adds to.  xbuf: the grouped kernel's exchange
+// words (zeroed), or null for the model's own buffer.  timed: per-kernel timing when
+// profiling is on.  *grouped: whether the grouped kernel ran.
 tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
                           const StreamPlan& splan, bool per_stream, const DecodeDev& d,
-                          int maxlen, int* trace, unsigned* xerr, hipStream_t st, bool* grouped) {
+                          int maxlen, int* trace, unsigned* xerr, unsigned long long* xbuf,
+                          bool timed, hipStream_t st, bool* grouped) {
   *grouped = false;
   if (maxlen <= 0) return TBS_OK;
   const ModelDev md = model_dev(m);
-  const int G = (per_stream && m->schedule != TBS_SCHEDULE_STREAM_SINGLE)
-                    ? pick_group(m, splan, d.B, d.KT, maxlen, gd.trivial)
-                    : 1;
+  const int G = decode_group(m, gd, splan, per_stream, d, maxlen);
+  auto launch = [&](int kernel, auto fn) { return timed ? timed_launch(m, kernel, st, fn) : fn(); };
   if (G > 1) {
-    HIP_TRY(ensure_xbuf(m, (size_t)d.B * G * 2 * group_words(d.Nc, d.KT), st), "exchange buffer");
+    if (!xbuf) {
+      HIP_TRY(ensure_xbuf(m, (size_t)d.B * G * 2 * group_words(d.Nc, d.KT), st),
+              "exchange buffer");
+      xbuf = m->xbuf.p;
+    }
     const unsigned epoch = next_epoch();
-    hipError_t e = timed_launch(m, TBS_KERNEL_STREAM_GROUP, st, [&] {
-      return launch_stream_group(md, gd, d, beam, trace, splan, m->xbuf.p, G, epoch,
-                                 m->spin_limit, xerr, st);
+    hipError_t e = launch(TBS_KERNEL_STREAM_GROUP, [&] {
+      return launch_stream_group(md, gd, d, beam, trace, splan, xbuf, G, epoch, m->spin_limit,
+                                 xerr, st);
     });
     if (e == hipSuccess) {
       *grouped = true;
@@ -505,17 +524,16 @@ tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
     }
   }
   if (per_stream && !*grouped)
-    HIP_TRY(timed_launch(m, TBS_KERNEL_STREAM, st,
-                         [&] { return launch_stream(md, gd, d, beam, trace, splan, st); }),
+    HIP_TRY(launch(TBS_KERNEL_STREAM,
+                   [&] { return launch_stream(md, gd, d, beam, trace, splan, st); }),
             "launch(stream)");
   if (!per_stream) {
     const JoinerPlan plan = plan_joiner(d.B * d.Nc, m->Vpad, m->Kpad, m->bf16, m->ncu, d.KT > 0);
     for (int t = 0; t < maxlen; ++t) {
-      HIP_TRY(timed_launch(m, TBS_KERNEL_JOINER, st,
-                           [&] { return launch_joiner_frame(md, d, plan, t, st); }),
+      HIP_TRY(launch(TBS_KERNEL_JOINER, [&] { return launch_joiner_frame(md, d, plan, t, st); }),
               "launch(joiner)");
-      HIP_TRY(timed_launch(m, TBS_KERNEL_SEARCH, st,
-                           [&] { return launch_search_frame(md, gd, d, beam, t, trace, st); }),
+      HIP_TRY(launch(TBS_KERNEL_SEARCH,
+                     [&] { return launch_search_frame(md, gd, d, beam, t, trace, st); }),
               "launch(search)");
     }
   }
@@ -824,7 +842,8 @@ tbs_status decode_impl(const tbs_model* model, const tbs_graph* graph,
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
   HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B, 0, st), "fill(exchange errors)");
   bool grouped = false;
-  s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, w.xerr, st, &grouped);
+  s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, w.xerr, nullptr, true, st,
+                     &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
@@ -837,6 +856,56 @@ tbs_status decode_impl(const tbs_model* model, const tbs_graph* graph,
   w.pending = true;
   HIP_TRY(model_mark(m, st), "hipEventRecord");
   return TBS_OK;
+}
+
+// Lays out a decode workspace for (B, T, Ns, Nc, KT) at `base` (an address, or 0 to
+// size it only) and returns the bytes it takes: the device arrays tbs_decode allocates
+// (no per-stream graph table, no host staging), then `xwords` exchange words.
+size_t carve_workspace(const tbs_model* m, uintptr_t base, int B, int T, int Ns, int Nc, int KT,
+                       bool need_logits, size_t xwords, Workspace& w,
+                       unsigned long long** xbuf) {
+  size_t off = 0;
+  auto take = [&](auto*& p, size_t n) {
+    p = reinterpret_cast<std::remove_reference_t<decltype(p)>>(base + off);
+    off += (((n ? n : 1) * sizeof(*p)) + 255) & ~(size_t)255;
+  };
+  const int nvt = m->Vpad / kJoinerBN;
+  const size_t BN = (size_t)B * Ns, BC = (size_t)B * Nc;
+  const size_t esz = m->bf16 ? 2 : 4;
+  w = Workspace();
+  take(w.len, (size_t)B);
+  take(w.nsurv, (size_t)B);
+  take(w.surv_ctx, BN);
+  take(w.surv_state, BN);
+  take(w.surv_score, BN);
+  take(w.surv_row, BN);
+  take(w.nctx, (size_t)B);
+  take(w.ctx_list, BC);
+  take(w.offset, (size_t)B);
+  char* h = nullptr;
+  take(h, BC * m->Kpad * esz);
+  w.h = h;
+  if (need_logits) take(w.logits, BC * m->Vpad);
+  take(w.stats, BC * nvt);
+  if (KT > 0) {
+    const size_t nsub = (size_t)nvt * (kJoinerBN / 16);
+    take(w.tk_z, BC * nsub * KT);
+    take(w.tk_c, BC * nsub * KT);
+    take(w.z0, BC);
+  }
+  take(w.hist_pl, (size_t)T * BN);
+  take(w.hist_arc, (size_t)T * BN);
+  take(w.path_lab, (size_t)B * T);
+  take(w.xerr, 1 + (size_t)B);
+  *xbuf = nullptr;
+  if (xwords) take(*xbuf, xwords);
+  w.B = B;
+  w.T = T;
+  w.Ns = Ns;
+  w.Nc = Nc;
+  w.KT = KT;
+  w.has_logits = need_logits;
+  return off;
 }
 
 tbs_status state_create_impl(const tbs_model* model, const tbs_graph* graph,
@@ -1161,6 +1230,84 @@ tbs_status tbs_decode_graphs(const tbs_model* model, const tbs_graph* const* gra
                      "tbs_decode_graphs");
 }
 
+tbs_status tbs_decode_noalloc(const tbs_model* model, const tbs_graph* graph,
+                              const tbs_beam_params* params, const float* encoder_out,
+                              const int32_t* lengths, int32_t B, int32_t T, int32_t* out_tokens,
+                              int32_t* out_num_tokens, double* out_scores, int32_t* out_status,
+                              int32_t* out_arcs, int32_t* trace, void* hip_stream) {
+  const char* who = "tbs_decode_noalloc";
+  if (B < 0 || T < 0) return fail(TBS_EINVAL, "%s: B and T must be >= 0", who);
+  tbs_status s = check_params(model, graph, params, who);
+  if (s != TBS_OK || B == 0) return s;
+  if (!lengths) return fail(TBS_EINVAL, "%s: lengths is NULL", who);
+  if (T > 0 && !encoder_out) return fail(TBS_EINVAL, "%s: encoder_out is NULL", who);
+  if (!out_num_tokens || !out_scores || (T > 0 && !out_tokens))
+    return fail(TBS_EINVAL, "%s: NULL output pointer", who);
+  const GraphDev gd = graph_dev(graph);
+  const float beam = params->beam;
+  const int Ns = params->max_states;
+  const int Nc = params->max_contexts < Ns ? params->max_contexts : Ns;
+  const int KT = (gd.trivial && Ns <= kMaxTopK) ? Ns : 0;
+  tbs_model* m = const_cast<tbs_model*>(model);
+  std::lock_guard<std::mutex> lk(m->mu);
+  hipStream_t st = (hipStream_t)hip_stream;
+  const ModelDev md = model_dev(m);
+  const StreamPlan splan = plan_stream(md, Nc, KT, gd.trivial);
+  bool per_stream = false;
+  s = choose_schedule(m, splan, Ns, Nc, who, &per_stream);
+  if (s != TBS_OK) return s;
+  // the frame loop runs to T: lengths stay in device memory (no host copy)
+  const int G = (per_stream && m->schedule != TBS_SCHEDULE_STREAM_SINGLE)
+                    ? pick_group(m, splan, B, KT, T, gd.trivial)
+                    : 1;
+  const size_t xwords = G > 1 ? (size_t)B * G * 2 * group_words(Nc, KT) : 0;
+  Workspace w;
+  unsigned long long* xbuf = nullptr;
+  const size_t need = carve_workspace(m, 0, B, T, Ns, Nc, KT, KT == 0, xwords, w, &xbuf);
+  if (need > kScratchBytes)
+    return fail(TBS_ECAPACITY,
+                "%s: the workspace of this decode takes %zu bytes, more than the %zu-byte "
+                "scratch array (use tbs_decode)",
+                who, need, kScratchBytes);
+  // the array's device address on this device, looked up once per device
+  unsigned char* base = nullptr;
+  {
+    static std::mutex mu;
+    static std::vector<std::pair<int, unsigned char*>> addr;
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> al(mu);
+    for (auto& a : addr)
+      if (a.first == dev) base = a.second;
+    if (!base) {
+      void* p = nullptr;
+      HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+      base = static_cast<unsigned char*>(p);
+      addr.push_back({dev, base});
+    }
+  }
+  carve_workspace(m, reinterpret_cast<uintptr_t>(base), B, T, Ns, Nc, KT, KT == 0, xwords, w,
+                  &xbuf);
+  HIP_TRY(model_wait(m, st), "hipStreamWaitEvent");
+  HIP_TRY(launch_clamp_lengths(lengths, w.len, B, T, st), "launch(lengths)");
+  const DecodeDev d = decode_dev(m, w, B, T, Ns, Nc, KT, encoder_out, w.len, nullptr, false);
+  if (trace)
+    HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
+  HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
+  HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B, 0, st), "fill(exchange errors)");
+  // the array keeps the last call's contents: the exchange words start at zero
+  if (xbuf) HIP_TRY(launch_fill_i32((int*)xbuf, 2 * (long long)xwords, 0, st), "fill(exchange)");
+  bool grouped = false;
+  s = enqueue_frames(m, gd, beam, splan, per_stream, d, T, trace, w.xerr, xbuf, false, st,
+                     &grouped);
+  if (s != TBS_OK) return s;
+  HIP_TRY(launch_final(gd, d, out_tokens, out_num_tokens, out_scores, out_status, out_arcs,
+                       grouped ? w.xerr : nullptr, st),
+          "launch(final)");
+  HIP_TRY(model_mark(m, st), "hipEventRecord");
+  return TBS_OK;
+}
+
 tbs_status tbs_state_create(const tbs_model* model, const tbs_graph* graph,
                             const tbs_beam_params* params, int32_t B, int32_t max_frames,
                             void* hip_stream, tbs_state** out) {
@@ -1222,7 +1369,7 @@ tbs_status tbs_decode_chunk(tbs_state* S, const float* encoder_chunk,
           "launch(resume)");
   bool grouped = false;
   tbs_status s = enqueue_frames(m, S->gd, S->beam, S->splan, S->per_stream, d, maxlen, trace,
-                                S->w.xerr, st, &grouped);
+                                S->w.xerr, nullptr, true, st, &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
   w.pending = true;

@@ -140,6 +140,8 @@ hipError_t launch_model_setup(const float* embed, const float* conv, const float
                               float* P0, float* P1, float* Wf, uint16_t* Wb, void* Wi,
                               float* bias, hipStream_t st);
 hipError_t launch_fill_i32(int* p, long long n, int v, hipStream_t st);
+// out[b] = min(max(in[b], 0), T) for b < B (device arrays)
+hipError_t launch_clamp_lengths(const int* in, int* out, int B, int T, hipStream_t st);
 hipError_t launch_init(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,
                        hipStream_t st);
 hipError_t launch_resume(const ModelDev& m, const DecodeDev& d, const GraphDev& g, int* trace,

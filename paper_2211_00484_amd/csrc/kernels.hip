@@ -212,6 +212,12 @@ __global__ void k_fill_i32(int* p, long long n, int v) {
     p[i] = v;
 }
 
+// out[b] = in[b] clamped to [0, T] (stream lengths handed over in device memory).
+__global__ void k_clamp_lengths(const int* __restrict__ in, int* __restrict__ out, int B, int T) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) out[b] = min(max(in[b], 0), T);
+}
+
 // ---------------------------------------------------------------------------
 // tanh_fast (internal.h) has absolute error ~2e-7, which moves a joiner logit by at
 // most ~C * max|W| * 2e-7.
@@ -3131,6 +3137,12 @@ hipError_t launch_model_setup(const float* embed, const float* conv, const float
                               float* bias, hipStream_t st) {
   hipLaunchKernelGGL(k_model_setup, dim3(grid_for((long long)Vpad * Kpad, 256)), dim3(256), 0, st,
                      embed, conv, w_out, b_out, V, C, Kpad, Vpad, bf16, P0, P1, Wf, Wb, Wi, bias);
+  return hipGetLastError();
+}
+
+hipError_t launch_clamp_lengths(const int* in, int* out, int B, int T, hipStream_t st) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_clamp_lengths, dim3((B + 255) / 256), dim3(256), 0, st, in, out, B, T);
   return hipGetLastError();
 }
 

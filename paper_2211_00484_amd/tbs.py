@@ -106,6 +106,9 @@ def lib():
     L.tbs_decode.restype = _I32
     L.tbs_decode.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
                              _P, _P, _P, _P, _P, _P, _P]
+    L.tbs_decode_noalloc.restype = _I32
+    L.tbs_decode_noalloc.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
+                                     _P, _P, _P, _P, _P, _P, _P]
     L.tbs_decode_graphs.restype = _I32
     L.tbs_decode_graphs.argtypes = [_P, _P, ctypes.POINTER(BeamParams), _P, _P, _I32, _I32,
                                     _P, _P, _P, _P, _P, _P, _P]
@@ -334,6 +337,26 @@ def decode_into(model: Model, graph, encoder_out, lengths, beam: float, max_stat
               _host_ptr(lens), B, T, _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
               _dev_ptr(out.scores), _dev_ptr(out.status), _dev_ptr(out.arcs),
               _dev_ptr(out.trace), _stream_ptr(stream)))
+    return out
+
+
+def decode_noalloc_into(model: Model, graph: Graph, encoder_out, lengths_dev, beam: float,
+                        max_states: int, max_contexts: int, out: DecodeOutput,
+                        stream=None) -> DecodeOutput:
+    """tbs_decode_noalloc: tbs_decode with its workspace in the library's fixed device
+    array (no allocation); ``lengths_dev`` is a device int32 tensor [B]."""
+    B, T = int(encoder_out.shape[0]), int(encoder_out.shape[1])
+    if encoder_out.dim() != 3 or encoder_out.shape[2] != model.dim:
+        raise ValueError("encoder_out must be [B, T, dim]")
+    if tuple(lengths_dev.shape) != (B,) or str(lengths_dev.dtype) != "torch.int32":
+        raise ValueError("lengths_dev must be a device int32 tensor of shape [B]")
+    params = BeamParams(float(math.inf if beam is None else beam), int(max_states),
+                        int(max_contexts))
+    _check(lib().tbs_decode_noalloc(model._h, graph._h, ctypes.byref(params),
+                                    _dev_ptr(encoder_out), _dev_ptr(lengths_dev), B, T,
+                                    _dev_ptr(out.tokens), _dev_ptr(out.num_tokens),
+                                    _dev_ptr(out.scores), _dev_ptr(out.status),
+                                    _dev_ptr(out.arcs), _dev_ptr(out.trace), _stream_ptr(stream)))
     return out
 
 
