@@ -641,6 +641,9 @@ def main():
     ap.add_argument("--alt-graphs", action="store_true",
                     help="one graph per stream: the workload's graph and a second graph of "
                          "the same kind (seed 2) alternate over the batch (tbs_decode_graphs)")
+    ap.add_argument("--no-graph-capture", action="store_true",
+                    help="frame schedule: launch every frame's kernels from the host instead "
+                         "of replaying the captured frame loop")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="threads for the oracle baseline (default: all host threads)")
@@ -675,6 +678,7 @@ def main():
     dtype = args.joiner_dtype or w.dtype
     model = tbs.Model.from_synth(model_np, dtype=dtype)
     model.set_schedule(args.schedule)
+    model.set_graph_capture(not args.no_graph_capture)
     graph = tbs.Graph.from_synth(graph_np)
     enc = torch.from_numpy(inputs.encoder_out).cuda()
     B, T = inputs.B, inputs.T
@@ -760,7 +764,8 @@ def main():
                    "per_stream_graphs": "2 alternating" if args.alt_graphs else None,
                    "beam": "inf" if math.isinf(w.beam) else w.beam,
                    "max_states": w.max_states, "max_contexts": w.max_contexts,
-                   "joiner": dtype, "schedule": schedule},
+                   "joiner": dtype, "schedule": schedule,
+                   "frame_loop_graph": dict(zip(("captures", "replays"), model.graph_stats()))},
         "roofline": roofline,
         "kernels": kernels,
         "joiner_mfma_util_pct": 100.0 * j_tflops / peak_j,

@@ -447,6 +447,20 @@ typedef enum {
 tbs_status tbs_model_set_schedule(tbs_model *model, int32_t schedule);
 
 /*
+ * Frame loop of TBS_SCHEDULE_FRAME in a HIP graph (Algorithm 1's loop over
+ * frames without a host launch per kernel): when a decode's launch arguments
+ * (graph, params, B, T, the workspace, encoder_out, trace, the longest length)
+ * repeat those of the model's previous decode, the frame loop is captured once
+ * into a HIP graph and replayed from then on; a decode with other arguments
+ * launches directly (and becomes the candidate for the next capture).  Results
+ * are identical either way.  enable = 0 turns capture off for later decodes
+ * (default on); capture is skipped while per-kernel profiling is on.
+ * tbs_model_graph_stats returns the number of captures and replays so far.
+ */
+tbs_status tbs_model_set_graph_capture(tbs_model *model, int32_t enable);
+tbs_status tbs_model_graph_stats(const tbs_model *model, int32_t *captures, int32_t *replays);
+
+/*
  * Poll budget of each exchange wait of the grouped per-stream kernel
  * (TBS_SCHEDULE_STREAM): polls >= 1, or 0 for the default (4,194,304).  A
  * diagnostic for the timeout path: a tiny budget makes waits give up while

@@ -198,6 +198,15 @@ struct tbs_model {
   std::vector<Timed> prof_pending;
   std::vector<hipEvent_t> prof_pool;
   tbs_kernel_time prof_acc[TBS_KERNEL_COUNT] = {};
+  // frame loop of the frame schedule captured in a HIP graph (tbs_model_set_graph_capture):
+  // the key is the bytes of every argument of the captured launches; a loop is captured
+  // the second time its key is seen and replayed while the key repeats
+  bool graphs = true;
+  std::vector<unsigned char> fg_key, fg_seen;
+  hipGraph_t fg_graph = nullptr;
+  hipGraphExec_t fg_exec = nullptr;
+  hipStream_t cap_stream = nullptr;  // capture stream (the caller's may be the null stream)
+  int fg_captures = 0, fg_replays = 0;
   // scratch for tbs_joiner_logp
   int rows_cap = 0;
   void* rows_h = nullptr;
@@ -494,11 +503,12 @@ int decode_group(const tbs_model* m, const GraphDev& gd, const StreamPlan& splan
 // kernel, or the joiner and search kernels per frame.  xerr: the exchange-timeout
 // counters ([1 + B]) the grouped kernel adds to.  xbuf: the grouped kernel's exchange
 // words (zeroed), or null for the model's own buffer.  timed: per-kernel timing when
-// profiling is on.  *grouped: whether the grouped kernel ran.
+// profiling is on.  use_graph: the frame schedule's loop may be captured in a HIP graph
+// (the model's capture setting).  *grouped: whether the grouped kernel ran.
 tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
                           const StreamPlan& splan, bool per_stream, const DecodeDev& d,
                           int maxlen, int* trace, unsigned* xerr, unsigned long long* xbuf,
-                          bool timed, hipStream_t st, bool* grouped) {
+                          bool timed, bool use_graph, hipStream_t st, bool* grouped) {
   *grouped = false;
   if (maxlen <= 0) return TBS_OK;
   const ModelDev md = model_dev(m);
@@ -529,13 +539,68 @@ tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
             "launch(stream)");
   if (!per_stream) {
     const JoinerPlan plan = plan_joiner(d.B * d.Nc, m->Vpad, m->Kpad, m->bf16, m->ncu, d.KT > 0);
-    for (int t = 0; t < maxlen; ++t) {
-      HIP_TRY(launch(TBS_KERNEL_JOINER, [&] { return launch_joiner_frame(md, d, plan, t, st); }),
-              "launch(joiner)");
-      HIP_TRY(launch(TBS_KERNEL_SEARCH,
-                     [&] { return launch_search_frame(md, gd, d, beam, t, trace, st); }),
-              "launch(search)");
+    auto frames = [&](hipStream_t s2) -> hipError_t {
+      for (int t = 0; t < maxlen; ++t) {
+        hipError_t e = launch(TBS_KERNEL_JOINER,
+                              [&] { return launch_joiner_frame(md, d, plan, t, s2); });
+        if (e == hipSuccess)
+          e = launch(TBS_KERNEL_SEARCH,
+                     [&] { return launch_search_frame(md, gd, d, beam, t, trace, s2); });
+        if (e != hipSuccess) return e;
+      }
+      return hipSuccess;
+    };
+    if (!use_graph || (timed && m->prof)) {
+      HIP_TRY(frames(st), "launch(frame loop)");
+      return TBS_OK;
     }
+    // the arguments of the loop's launches that can change between decodes on this
+    // model, as bytes (GraphDev and DecodeDev hold no padding; the model's tables and
+    // the joiner plan follow from the model and d)
+    static_assert(sizeof(GraphDev) == 4 * sizeof(int) + 5 * sizeof(void*) &&
+                      sizeof(DecodeDev) == 6 * sizeof(int) + 21 * sizeof(void*),
+                  "frame-loop key: GraphDev / DecodeDev must have no padding");
+    std::vector<unsigned char> key;
+    auto put = [&](const void* p, size_t n) {
+      const unsigned char* c = static_cast<const unsigned char*>(p);
+      key.insert(key.end(), c, c + n);
+    };
+    put(&gd, sizeof gd);
+    put(&d, sizeof d);
+    put(&beam, sizeof beam);
+    put(&trace, sizeof trace);
+    put(&maxlen, sizeof maxlen);
+    if (m->fg_exec && key == m->fg_key) {
+      HIP_TRY(hipGraphLaunch(m->fg_exec, st), "hipGraphLaunch(frame loop)");
+      ++m->fg_replays;
+      return TBS_OK;
+    }
+    if (key != m->fg_seen) {  // first time: launch directly, capture if it repeats
+      m->fg_seen = key;
+      HIP_TRY(frames(st), "launch(frame loop)");
+      return TBS_OK;
+    }
+    if (!m->cap_stream)
+      HIP_TRY(hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking), "hipStreamCreate");
+    HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal),
+            "hipStreamBeginCapture");
+    hipError_t e = frames(m->cap_stream);
+    hipGraph_t g = nullptr;
+    const hipError_t e2 = hipStreamEndCapture(m->cap_stream, &g);
+    if (e == hipSuccess) e = e2;
+    hipGraphExec_t x = nullptr;
+    if (e == hipSuccess) e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+      if (g) (void)hipGraphDestroy(g);
+      return hip_fail(e, "capture(frame loop)");
+    }
+    if (m->fg_exec) (void)hipGraphExecDestroy(m->fg_exec);
+    if (m->fg_graph) (void)hipGraphDestroy(m->fg_graph);
+    m->fg_exec = x;
+    m->fg_graph = g;
+    m->fg_key = key;
+    ++m->fg_captures;
+    HIP_TRY(hipGraphLaunch(m->fg_exec, st), "hipGraphLaunch(frame loop)");
   }
   return TBS_OK;
 }
@@ -778,6 +843,9 @@ void tbs_model_destroy(tbs_model* m) {
   (void)hipFree(m->rows_h);
   (void)hipFree(m->rows_logits);
   (void)hipFree(m->rows_stats);
+  if (m->fg_exec) (void)hipGraphExecDestroy(m->fg_exec);
+  if (m->fg_graph) (void)hipGraphDestroy(m->fg_graph);
+  if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
   delete m;
 }
 
@@ -842,8 +910,8 @@ tbs_status decode_impl(const tbs_model* model, const tbs_graph* graph,
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
   HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B, 0, st), "fill(exchange errors)");
   bool grouped = false;
-  s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, w.xerr, nullptr, true, st,
-                     &grouped);
+  s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, w.xerr, nullptr, true,
+                     m->graphs, st, &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(timed_launch(m, TBS_KERNEL_FINAL, st,
                        [&] {
@@ -1298,7 +1366,7 @@ tbs_status tbs_decode_noalloc(const tbs_model* model, const tbs_graph* graph,
   // the array keeps the last call's contents: the exchange words start at zero
   if (xbuf) HIP_TRY(launch_fill_i32((int*)xbuf, 2 * (long long)xwords, 0, st), "fill(exchange)");
   bool grouped = false;
-  s = enqueue_frames(m, gd, beam, splan, per_stream, d, T, trace, w.xerr, xbuf, false, st,
+  s = enqueue_frames(m, gd, beam, splan, per_stream, d, T, trace, w.xerr, xbuf, false, false, st,
                      &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(launch_final(gd, d, out_tokens, out_num_tokens, out_scores, out_status, out_arcs,
@@ -1369,7 +1437,7 @@ tbs_status tbs_decode_chunk(tbs_state* S, const float* encoder_chunk,
           "launch(resume)");
   bool grouped = false;
   tbs_status s = enqueue_frames(m, S->gd, S->beam, S->splan, S->per_stream, d, maxlen, trace,
-                                S->w.xerr, nullptr, true, st, &grouped);
+                                S->w.xerr, nullptr, true, m->graphs, st, &grouped);
   if (s != TBS_OK) return s;
   HIP_TRY(hipEventRecord(w.done, st), "hipEventRecord");
   w.pending = true;
@@ -1455,6 +1523,23 @@ tbs_status tbs_model_set_schedule(tbs_model* model, int32_t schedule) {
     return fail(TBS_EINVAL, "tbs_model_set_schedule: unknown schedule %d", schedule);
   std::lock_guard<std::mutex> lk(model->mu);
   model->schedule = schedule;
+  return TBS_OK;
+}
+
+tbs_status tbs_model_set_graph_capture(tbs_model* model, int32_t enable) {
+  if (!model) return fail(TBS_EINVAL, "tbs_model_set_graph_capture: model is NULL");
+  std::lock_guard<std::mutex> lk(model->mu);
+  model->graphs = enable != 0;
+  return TBS_OK;
+}
+
+tbs_status tbs_model_graph_stats(const tbs_model* model, int32_t* captures, int32_t* replays) {
+  if (!model || !captures || !replays)
+    return fail(TBS_EINVAL, "tbs_model_graph_stats: NULL argument");
+  tbs_model* m = const_cast<tbs_model*>(model);
+  std::lock_guard<std::mutex> lk(m->mu);
+  *captures = m->fg_captures;
+  *replays = m->fg_replays;
   return TBS_OK;
 }
 

@@ -114,6 +114,10 @@ def lib():
                                     _P, _P, _P, _P, _P, _P, _P]
     L.tbs_model_set_schedule.restype = _I32
     L.tbs_model_set_schedule.argtypes = [_P, _I32]
+    L.tbs_model_set_graph_capture.restype = _I32
+    L.tbs_model_set_graph_capture.argtypes = [_P, _I32]
+    L.tbs_model_graph_stats.restype = _I32
+    L.tbs_model_graph_stats.argtypes = [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32)]
     L.tbs_model_set_exchange_spin_limit.restype = _I32
     L.tbs_model_set_exchange_spin_limit.argtypes = [_P, _I32]
     L.tbs_model_set_profiling.restype = _I32
@@ -252,6 +256,17 @@ class Model:
         """Frame-loop schedule for later decodes: "auto", "frame", "stream" (several
         workgroups per stream where possible) or "stream1" (one per stream)."""
         _check(lib().tbs_model_set_schedule(self._h, SCHEDULES[schedule]))
+
+    def set_graph_capture(self, enable: bool):
+        """Capture the frame schedule's frame loop in a HIP graph when a decode repeats
+        the previous one's launch arguments (default on)."""
+        _check(lib().tbs_model_set_graph_capture(self._h, int(bool(enable))))
+
+    def graph_stats(self) -> tuple:
+        """(captures, replays) of the frame-loop graph so far."""
+        c, r = _I32(), _I32()
+        _check(lib().tbs_model_graph_stats(self._h, ctypes.byref(c), ctypes.byref(r)))
+        return int(c.value), int(r.value)
 
     def set_exchange_spin_limit(self, polls: int):
         """Poll budget of the grouped kernel's exchange waits (0 = default); a

@@ -309,3 +309,46 @@ def test_invalid_arguments_rejected():
         tbs.decode(model, tbs.Graph.trivial(9), enc, np.array([1, 1], np.int32))
     with pytest.raises(tbs.TbsError, match="EINVAL"):
         tbs.decode(model, graph, enc, np.array([1, 1], np.int32), beam=-1.0)
+
+
+def test_frame_loop_graph_replays_match_eager():
+    # The frame schedule's loop is captured in a HIP graph the second time a decode's
+    # launch arguments repeat, then replayed.  Every decode (direct, capturing, replays,
+    # and after a decode with other inputs) must equal the same decode on a model with
+    # capture off, with host synchronisation and eager work between the replays.
+    import torch
+    from paper_2211_00484_amd import tbs
+    w, inputs, model_np, graph_np = synth.make_workload("graph")
+    rng = np.random.default_rng(77)
+    enc_np2 = rng.standard_normal(inputs.encoder_out.shape).astype(np.float32)
+    lens2 = rng.integers(1, inputs.T + 1, inputs.B).astype(np.int32)
+    for b in range(inputs.B):
+        enc_np2[b, lens2[b]:] = 0.0
+    graph = tbs.Graph.from_synth(graph_np)
+    cap, ref = tbs.Model.from_synth(model_np), tbs.Model.from_synth(model_np)
+    for m in (cap, ref):
+        m.set_schedule("frame")
+    ref.set_graph_capture(False)
+    B, T = inputs.B, inputs.T
+    encs = {"x": (torch.from_numpy(inputs.encoder_out).cuda(), inputs.lengths),
+            "y": (torch.from_numpy(enc_np2).cuda(), lens2)}
+
+    def run(model, which, out):
+        enc, lens = encs[which]
+        tbs.decode_into(model, graph, enc, lens, 4.0, 32, 8, out)
+        torch.cuda.synchronize()
+        return {k: getattr(out, k).cpu().numpy().copy()
+                for k in ("tokens", "num_tokens", "scores", "status", "arcs", "trace")}
+
+    mk = lambda: tbs.allocate_outputs(B, T, 32, status=True, arcs=True, trace=True)
+    want = {k: run(ref, k, mk()) for k in encs}
+    out = mk()
+    for i, which in enumerate(["x", "x", "x", "x", "y", "x", "x", "y", "y", "y"]):
+        got = run(cap, which, out)
+        torch.zeros(1 << 20, device="cuda").add_(1.0)   # eager work between replays
+        for k in got:
+            assert np.array_equal(got[k], want[which][k]), (i, which, k)
+    captures, replays = cap.graph_stats()
+    say(f"  frame-loop graph: {captures} captures, {replays} replays")
+    assert (captures, replays) == (2, 6)   # x: direct, capture, 2 replays; y direct; x 2 replays; y capture, 2 replays
+    assert ref.graph_stats() == (0, 0)
