@@ -2350,31 +2350,44 @@ template <int RG, int NCG, bool RES>
 __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* hl, int hstride,
                                                  float* part, int cg0,
                                                  const float4 (&wres)[kResSlices]) {
+  // v_mfma_f32_4x4x1f32 computes 16 independent 4 x 4 x 1 blocks: lane l = 4 j + c
+  // supplies row c of A block j and column c of B block j, and accumulator element
+  // v of lane l is (row v, column c) of block j.  With A = h[4 g + (l & 3)][k] and
+  // B = W[64 cg + l][k] every block reads the same four rows, so element v of lane l
+  // accumulates z[4 g + v][64 cg + l] over this wave's k values: one instruction is
+  // 4 rows x 64 columns x 1 k, twice the unpacked fp32 FMA rate of the VALU.
   constexpr int NR = 4 * RG;
   constexpr int CH = 8 / NCG;  // k slices per chunk
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Vpad = m.Vpad;
   const int qw = m.Kpad / 16;  // k slices per wave (a multiple of 32)
   const int q0 = wave * qw;
-  const char* hrows = reinterpret_cast<const char*>(hl);
-  const size_t rstride = (size_t)hstride * 4;
-  float acc[NCG][NR];
+  const char* hrows = reinterpret_cast<const char*>(hl) + (size_t)(lane & 3) * hstride * 4;
+  const size_t gstride = (size_t)hstride * 16;  // bytes between row groups of 4
+  f32x4 acc[NCG][RG];
 #pragma unroll
   for (int j = 0; j < NCG; ++j)
 #pragma unroll
-    for (int r = 0; r < NR; ++r) acc[j][r] = 0.f;
-  if (RES) {
+    for (int g = 0; g < RG; ++g) acc[j][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto slice = [&](size_t ko, const float4 (&w)[NCG]) {
+#pragma unroll
+    for (int g = 0; g < RG; ++g) {
+      const float4 a = *reinterpret_cast<const float4*>(hrows + g * gstride + ko);
+#pragma unroll
+      for (int j = 0; j < NCG; ++j) {
+        acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.x, w[j].x, acc[j][g], 0, 0, 0);
+        acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.y, w[j].y, acc[j][g], 0, 0, 0);
+        acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.z, w[j].z, acc[j][g], 0, 0, 0);
+        acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.w, w[j].w, acc[j][g], 0, 0, 0);
+      }
+    }
+  };
+  static_assert(!RES || NCG == 1, "a resident W slice is one column group");
+  if constexpr (RES) {
 #pragma unroll
     for (int u = 0; u < kResSlices; ++u) {
-      const size_t ko = (size_t)(q0 + u) * 16;
-#pragma unroll
-      for (int r = 0; r < NR; ++r) {
-        const float4 a = *reinterpret_cast<const float4*>(hrows + (size_t)r * rstride + ko);
-        acc[0][r] = fmaf(a.x, wres[u].x, acc[0][r]);
-        acc[0][r] = fmaf(a.y, wres[u].y, acc[0][r]);
-        acc[0][r] = fmaf(a.z, wres[u].z, acc[0][r]);
-        acc[0][r] = fmaf(a.w, wres[u].w, acc[0][r]);
-      }
+      const float4 w[1] = {wres[u]};
+      slice((size_t)(q0 + u) * 16, w);
     }
   } else {
     const int steps = qw / CH;   // even
@@ -2389,20 +2402,7 @@ __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* 
     };
     auto compute = [&](int step, const float4 (&w)[CH][NCG]) {
 #pragma unroll
-      for (int u = 0; u < CH; ++u) {
-        const size_t ko = (size_t)(q0 + step * CH + u) * 16;
-#pragma unroll
-        for (int r = 0; r < NR; ++r) {
-          const float4 a = *reinterpret_cast<const float4*>(hrows + (size_t)r * rstride + ko);
-#pragma unroll
-          for (int j = 0; j < NCG; ++j) {
-            acc[j][r] = fmaf(a.x, w[u][j].x, acc[j][r]);
-            acc[j][r] = fmaf(a.y, w[u][j].y, acc[j][r]);
-            acc[j][r] = fmaf(a.z, w[u][j].z, acc[j][r]);
-            acc[j][r] = fmaf(a.w, w[u][j].w, acc[j][r]);
-          }
-        }
-      }
+      for (int u = 0; u < CH; ++u) slice((size_t)(q0 + step * CH + u) * 16, w[u]);
     };
     float4 wa[CH][NCG], wb[CH][NCG];
     load_chunk(0, wa);
@@ -2416,7 +2416,9 @@ __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* 
 #pragma unroll
   for (int j = 0; j < NCG; ++j)
 #pragma unroll
-    for (int r = 0; r < NR; ++r) part[((wave * NCG + j) * NR + r) * 64 + lane] = acc[j][r];
+    for (int g = 0; g < RG; ++g)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) part[((wave * NCG + j) * NR + 4 * g + v) * 64 + lane] = acc[j][g][v];
   __syncthreads();
 }
 
