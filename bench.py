@@ -252,9 +252,11 @@ def decode_roofline(prof, K, work, dtype):
                                   "frac": j_tflops / peak_j,
                                   "algorithmic_search_bytes_per_launch": bytes_per_launch,
                                   "search_gbps": s_gbps})
-        # the fp32 per-stream joiner runs on VALU FMAs (bound "alu", against the fp32
-        # vector peak); the bf16 one on 4x4x4 MFMA blocks
-        roofline = {"kernel": "k_" + sk, "bound": "mfma" if dtype == "bf16" else "alu",
+        # the grouped kernel's joiner runs on 4x4x1 fp32 MFMA blocks and the single-
+        # workgroup kernel's bf16 joiner on 4x4x4 bf16 blocks (bound "mfma"); the single-
+        # workgroup fp32 joiner on VALU FMAs (bound "alu", against the fp32 vector peak)
+        mfma = sk == "stream_group" or dtype == "bf16"
+        roofline = {"kernel": "k_" + sk, "bound": "mfma" if mfma else "alu",
                     "achieved": j_tflops, "peak": peak_j, "unit": "TFLOP/s",
                     "frac": j_tflops / peak_j}
     else:
