@@ -155,8 +155,8 @@ struct tbs_graph {
 
 // Exchange buffers of the grouped per-stream kernel (device memory, accessed with
 // device-scope atomics).  A destroyed model returns its buffer to a per-process free
-// list for later models, which then skip the allocation and the clear.  Words carry a
-// 16-bit decode epoch; when the process-wide epoch wraps, a buffer is cleared before
+// list for later models, which then skip the allocation and the clear.  Words carry an
+// 8-bit decode epoch; when the process-wide epoch wraps, a buffer is cleared before
 // its next use.
 struct XBuf {
   int dev = -1;
@@ -419,10 +419,12 @@ hipError_t ensure_xbuf(tbs_model* m, size_t words, hipStream_t st) {
   return hipSuccess;
 }
 
-// Next 16-bit decode epoch (never 0, so zeroed words never match a tag).
+// Next 8-bit decode epoch of the grouped kernel's exchange tags (never 0, so zeroed
+// words never match a tag); a wrap makes every exchange buffer be cleared before its
+// next use.
 unsigned next_epoch() {
   for (;;) {
-    const unsigned e = (g_epoch.fetch_add(1) + 1) & 0xffffu;
+    const unsigned e = (g_epoch.fetch_add(1) + 1) & 0xffu;
     if (e != 0) return e;
     g_wrap.fetch_add(1);
   }
@@ -515,12 +517,13 @@ tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
   const int G = decode_group(m, gd, splan, per_stream, d, maxlen);
   auto launch = [&](int kernel, auto fn) { return timed ? timed_launch(m, kernel, st, fn) : fn(); };
   if (G > 1) {
+    // the epoch first: a wrap it causes must clear the buffer before this decode
+    const unsigned epoch = next_epoch();
     if (!xbuf) {
       HIP_TRY(ensure_xbuf(m, (size_t)d.B * G * 2 * group_words(d.Nc, d.KT), st),
               "exchange buffer");
       xbuf = m->xbuf.p;
     }
-    const unsigned epoch = next_epoch();
     hipError_t e = launch(TBS_KERNEL_STREAM_GROUP, [&] {
       return launch_stream_group(md, gd, d, beam, trace, splan, xbuf, G, epoch, m->spin_limit,
                                  xerr, st);

@@ -2423,20 +2423,27 @@ __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* 
 }
 
 // The member joiner's partial sums (4 waves x 2 column groups x 16 rows x 64 lanes)
-// live in hk and hv; the exchanged words of all members (8 x 16 rows x 35 words)
+// live in hk and hv; the exchanged words of all members (8 x 16 rows x 19 words)
 // in uk and uv.
 static_assert(offsetof(SearchSmem, hv) == offsetof(SearchSmem, hk) + sizeof(SearchSmem::hk) &&
                   sizeof(SearchSmem::hk) + sizeof(SearchSmem::hv) >= 4 * 2 * 16 * 64 * sizeof(float),
               "member joiner partial sums do not fit hk and hv");
 static_assert(offsetof(SearchSmem, uv) == offsetof(SearchSmem, uk) + sizeof(SearchSmem::uk) &&
-                  sizeof(SearchSmem::uk) + sizeof(SearchSmem::uv) >= 8 * 16 * 35 * sizeof(unsigned),
+                  sizeof(SearchSmem::uk) + sizeof(SearchSmem::uv) >=
+                      8 * 16 * (3 + 16) * sizeof(unsigned long long),
               "exchanged words do not fit uk and uv");
 
-// Exchange slot of (stream b, member g, frame parity): Nc rows of RW words.
+// Exchange slot of (stream b, member g, frame parity): Nc rows of RW words.  A word
+// is tag << 48 | payload: the tag (decode epoch << 8 | frame, both mod 256; the
+// epoch is never 0, so cleared words never match) tells a word of this decode and
+// frame from an older one (the slot of a frame parity is rewritten every other
+// frame, and members never drift a frame apart).  Row payloads: the maximum and the
+// sum of exp(z - maximum) over the member's columns, the blank logit (member 0),
+// then KT candidates label << 32 | logit bits (label 0: none).
 struct GroupX {
   unsigned long long* buf;  // device memory (device-scope atomics only)
   int G, xwords;            // members per stream; words per slot
-  unsigned epoch;           // decode number (16 bits), tags are epoch << 16 | frame
+  unsigned epoch;           // decode number (8 bits, never 0)
   unsigned spin_limit;      // polls before a wait is abandoned (recorded in err)
   unsigned* err;            // [1 + B]: timeouts of any stream (checked by every later
                             // wait, which then gives up at once), then per stream
@@ -2483,7 +2490,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Ns = d.Ns, Nc = d.Nc, V = m.V, C = m.C, Kpad = m.Kpad;
   const int KT = FAST ? 4 : d.KT;  // the fast path runs max_states = 4 (4 labels per row)
-  const int RW = 3 + 2 * KT;  // words per row: max, sum exp, KT x (logit, label), blank logit
+  const int RW = 3 + KT;  // words per row: max, sum exp, blank logit, KT candidates
   const int cg0 = mem * NCG;
   const size_t row0 = (size_t)b * Nc;
   const unsigned stride_tb = (unsigned)g.maxdeg + 1u;
@@ -2565,7 +2572,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     float* part = reinterpret_cast<float*>(s.hk);
     group_joiner_f32<RG, NCG, RES>(m, hl, hstride, part, cg0, wres);
     const int nc = FAST ? nc_r : s.nc;
-    const unsigned tag = (x.epoch << 16) | ((unsigned)t & 0xffffu);
+    const unsigned long long tg = (unsigned long long)((x.epoch << 8) | ((unsigned)t & 0xffu)) << 48;
     // this member's row statistics over its columns (partial sums added in wave
     // order, bias, -inf beyond V) -> tagged words
     {
@@ -2628,47 +2635,45 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
           }
         }
         unsigned long long* w = slot + (size_t)j * RW;
-        const unsigned long long tg = (unsigned long long)tag << 32;
         if (lane == 0) {
           __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           const float z0 = cg0 == 0 ? z[0] : 0.f;  // lane 0 of the first member holds label 0
-          __hip_atomic_store(w + 2 + 2 * KT, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
+          __hip_atomic_store(w + 2, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
         }
         if (lane < KT) {
-          __hip_atomic_store(w + 2 + 2 * lane, tg | __float_as_uint(my_z), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(w + 3 + 2 * lane, tg | (unsigned)my_c, __ATOMIC_RELAXED,
+          const unsigned long long c16 = my_c > 0 ? (unsigned long long)my_c << 32 : 0ull;
+          __hip_atomic_store(w + 3 + lane, tg | c16 | __float_as_uint(my_z), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
         }
       }
     }
     // every member's words for this frame (bounded polls), payloads into LDS
-    unsigned* xs = reinterpret_cast<unsigned*>(s.uk);  // [G][nc][RW]
+    unsigned long long* xs = s.uk;  // [G][nc][RW] payloads
     {
       const int per = nc * RW, total = G * per;
+      const unsigned tag = (unsigned)(tg >> 48);
       for (int idx = tid; idx < total; idx += blockDim.x) {
         const int g2 = idx / per, rest = idx - g2 * per;
         const unsigned long long* w = group_slot(x, b, g2, t) + rest;
         unsigned long long v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         unsigned n = 0;
-        while ((unsigned)(v >> 32) != tag) {
+        while ((unsigned)(v >> 48) != tag) {
           ++n;
           if (n > x.spin_limit ||
               ((n & 255u) == 0 &&
                __hip_atomic_load(x.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
             __hip_atomic_fetch_add(x.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_fetch_add(x.err + 1 + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            // a neutral payload (the word may hold another decode's data): score words
-            // -inf, the exp-sum and label words 0, so nothing stale is selected
-            const int r = rest % RW;
-            v = (r & 1) ? 0ull : 0xff800000ull;
+            // a neutral payload (the word may hold another decode's data): -inf and
+            // label 0 (none), and a zero exp-sum, so nothing stale is selected
+            v = rest % RW == 1 ? 0ull : 0xff800000ull;
             break;
           }
           v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        xs[idx] = (unsigned)v;
+        xs[idx] = v & 0xffffffffffffull;
       }
     }
     if (!FAST && t + 1 < L) {
@@ -2684,13 +2689,13 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     // labels are distinct)
     for (int j = wave; j < nc; j += 4) {
       // (the wave reductions combine in a fixed order, the same in every member)
-      const float Mg = lane < G ? __uint_as_float(xs[(lane * nc + j) * RW]) : -INFINITY;
-      const float Sg = lane < G ? __uint_as_float(xs[(lane * nc + j) * RW + 1]) : 0.f;
+      const float Mg = lane < G ? __uint_as_float((unsigned)xs[(lane * nc + j) * RW]) : -INFINITY;
+      const float Sg = lane < G ? __uint_as_float((unsigned)xs[(lane * nc + j) * RW + 1]) : 0.f;
       const float M = wave_max_f(Mg);
       const float S = wave_sum_f(Sg == 0.f ? 0.f : Sg * __expf(Mg - M));
       if (lane == 0) {
         s.s_lse[j] = lse_of(M, S);
-        s.s_z0[j] = __uint_as_float(xs[j * RW + 2 + 2 * KT]);
+        s.s_z0[j] = __uint_as_float((unsigned)xs[j * RW + 2]);
       }
       const int ne = G * KT;
       if (ne <= 64) {
@@ -2699,10 +2704,10 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         unsigned o = 0u, c = 0xffffffffu;
         if (lane < ne) {
           const int g2 = lane / KT, q = lane - g2 * KT;
-          const unsigned* w = xs + (g2 * nc + j) * RW + 2 + 2 * q;
-          if ((int)w[1] >= 0) {
-            o = f2ord(__uint_as_float(w[0]));
-            c = w[1];
+          const unsigned long long w = xs[(g2 * nc + j) * RW + 3 + q];
+          if ((w >> 32) != 0ull) {
+            o = f2ord(__uint_as_float((unsigned)w));
+            c = (unsigned)(w >> 32);
           }
         }
         for (int q = 0; q < KT; ++q) {
@@ -2733,10 +2738,10 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
           kv[h] = 0ull;
           if (e < ne) {
             const int g2 = e / KT, q = e - g2 * KT;
-            const unsigned* w = xs + (g2 * nc + j) * RW + 2 + 2 * q;
-            const int c = (int)w[1];
-            if (c >= 0)
-              kv[h] = ((unsigned long long)f2ord(__uint_as_float(w[0])) << 32) | (0xffffffffu - (unsigned)c);
+            const unsigned long long w = xs[(g2 * nc + j) * RW + 3 + q];
+            const unsigned c = (unsigned)(w >> 32);
+            if (c != 0u)
+              kv[h] = ((unsigned long long)f2ord(__uint_as_float((unsigned)w)) << 32) | (0xffffffffu - c);
           }
         }
         unsigned long long prev = ~0ull;
@@ -3273,7 +3278,7 @@ hipError_t launch_stream(const ModelDev& m, const GraphDev& g, const DecodeDev& 
               : launch_stream_rg<false, false>(m, g, d, beam, trace, p, st);
 }
 
-int group_words(int Nc, int KT) { return Nc * (3 + 2 * KT); }
+int group_words(int Nc, int KT) { return Nc * (3 + KT); }
 
 template <int RG, int NCG, bool RES, bool FAST>
 hipError_t launch_group_t(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
@@ -3315,7 +3320,7 @@ hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const Decod
   const int ncg = m.Vpad / kJoinerBN;
   if (!p.ok || m.bf16 || d.KT <= 0 || G < 2 || ncg % G != 0 || ncg / G > 2)
     return hipErrorInvalidValue;
-  GroupX x{xbuf, G, group_words(d.Nc, d.KT), epoch & 0xffffu, spin_limit, err};
+  GroupX x{xbuf, G, group_words(d.Nc, d.KT), epoch & 0xffu, spin_limit, err};
   // LDS: the search state, the joiner rows and (fast path) the staged decoder rows
   GroupLds ly{p.hoff, p.hstride, p.hoff + p.RG * 4 * p.hstride * 4};
   // one column group per member and K = 512: the member's W slice stays in registers;
