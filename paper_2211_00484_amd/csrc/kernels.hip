@@ -996,6 +996,7 @@ struct SearchSmem {
   int g_src[4];              // grouped fast path: decoder-row source of each new context row
   int ns, nc, nU, nL, n_gt, n_eq, nK, nC;
   float best;
+  double off_d;              // the stream's fp64 score offset (kept here between frames)
 };
 
 __device__ __forceinline__ uint32_t hash_slot(unsigned long long key) {
@@ -1268,6 +1269,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   if (!FUSED && tid == 0) {
     s.ns = d.nsurv[b];
     s.nc = d.nctx[b];
+    if (writer) s.off_d = d.offset[b];  // read now, updated at the end
   }
   float2* stage = reinterpret_cast<float2*>(s.hk);  // softmax partials, [Nc][nvt]
   const bool staged = Nc * nvt <= kStatStage;
@@ -2084,7 +2086,12 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       s.ns = s.nK;
       s.nc = nC;
     }
-    if (writer) d.offset[b] += (double)best;
+    // the offset stays in LDS across the persistent kernels' frames and is stored
+    // after the stream's (or chunk's) last one
+    if (writer) {
+      s.off_d += (double)best;
+      if (!FUSED || t + 1 == L) d.offset[b] = s.off_d;
+    }
   }
 }
 
@@ -2270,6 +2277,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream(ModelDev m, GraphDev 
   if (tid == 0) {
     s.ns = d.nsurv[b];
     s.nc = d.nctx[b];
+    s.off_d = d.offset[b];
   }
   for (int i = tid; i < Ns; i += blockDim.x) {
     const size_t o = (size_t)b * Ns + i;
@@ -2364,11 +2372,13 @@ __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* 
   const int q0 = wave * qw;
   const char* hrows = reinterpret_cast<const char*>(hl) + (size_t)(lane & 3) * hstride * 4;
   const size_t gstride = (size_t)hstride * 16;  // bytes between row groups of 4
-  f32x4 acc[NCG][RG];
+  // two accumulator chains (even and odd k of each slice), so that consecutive
+  // MFMAs never wait on each other's result
+  f32x4 acc[NCG][RG], acc2[NCG][RG];
 #pragma unroll
   for (int j = 0; j < NCG; ++j)
 #pragma unroll
-    for (int g = 0; g < RG; ++g) acc[j][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < RG; ++g) acc[j][g] = acc2[j][g] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto slice = [&](size_t ko, const float4 (&w)[NCG]) {
 #pragma unroll
     for (int g = 0; g < RG; ++g) {
@@ -2376,9 +2386,9 @@ __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* 
 #pragma unroll
       for (int j = 0; j < NCG; ++j) {
         acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.x, w[j].x, acc[j][g], 0, 0, 0);
-        acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.y, w[j].y, acc[j][g], 0, 0, 0);
+        acc2[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.y, w[j].y, acc2[j][g], 0, 0, 0);
         acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.z, w[j].z, acc[j][g], 0, 0, 0);
-        acc[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.w, w[j].w, acc[j][g], 0, 0, 0);
+        acc2[j][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a.w, w[j].w, acc2[j][g], 0, 0, 0);
       }
     }
   };
@@ -2418,7 +2428,8 @@ __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* 
 #pragma unroll
     for (int g = 0; g < RG; ++g)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) part[((wave * NCG + j) * NR + 4 * g + v) * 64 + lane] = acc[j][g][v];
+      for (int v = 0; v < 4; ++v)
+        part[((wave * NCG + j) * NR + 4 * g + v) * 64 + lane] = acc[j][g][v] + acc2[j][g][v];
   __syncthreads();
 }
 
@@ -2510,6 +2521,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
   if (tid == 0) {
     s.ns = d.nsurv[b];
     s.nc = d.nctx[b];
+    s.off_d = d.offset[b];
   }
   for (int i = tid; i < Ns; i += blockDim.x) {
     const size_t o = (size_t)b * Ns + i;
@@ -2867,7 +2879,8 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         d.nsurv[b] = nk;
         d.nctx[b] = nk;
       }
-      d.offset[b] += (double)best;
+      s.off_d += (double)best;
+      if (t + 1 == L) d.offset[b] = s.off_d;
     }
     sb = nb;
     ns_r = nk;
