@@ -11,8 +11,10 @@ consecutive steps on the decode stream; the mean wall time is reported beside it
 Per-kernel durations come
 from K further steps during which the library records HIP events around each launch
 on the decode stream (tbs_model_set_profiling).  Algorithmic work (joiner FLOP,
-search bytes) is counted from the survivor trace of one untimed decode.
-Prints one JSON line.
+search bytes) is counted from the survivor trace of one untimed decode.  The default
+(standard) run also measures the graph, throughput, large and large-bf16 configurations
+the same way and reports them under `other_workloads` (secondary figures; `value` is the
+standard one).  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -282,6 +284,85 @@ def decode_roofline(prof, K, work, dtype):
                         "peak": PEAK["hbm_gbps"], "unit": "GB/s",
                         "frac": s_gbps / PEAK["hbm_gbps"]}
     return kernels, roofline, schedule, j_tflops, s_gbps, peak_j
+
+
+def measure_decode(w, inputs, model, graph, enc, dtype, K, W, work):
+    """W untimed decodes, then K timed ones (the median of the per-step HIP-event
+    intervals on the decode stream), then K more with per-kernel timing; the roofline
+    of the dominant kernel."""
+    import torch
+    from paper_2211_00484_amd import tbs
+    B, T = inputs.B, inputs.T
+    frames = int(inputs.lengths.sum())
+    out = tbs.allocate_outputs(B, T, w.max_states, status=True)
+    for _ in range(W):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+    torch.cuda.synchronize()
+
+    # the timed steps: nothing but the decodes on the stream, with an event between
+    # consecutive steps (a marker, no host synchronisation) for the per-step median
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record()
+    for i in range(K):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(K)]
+
+    # the same steps again with HIP events around every kernel launch: per-kernel
+    # durations for the roofline (the events add a little time between kernels)
+    model.set_profiling(True)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(K):
+        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+    prof = model.read_profile()
+    model.set_profiling(False)
+
+    ms_step = statistics.median(step_ms)
+    kernels, roofline, schedule, j_tflops, s_gbps, peak_j = decode_roofline(prof, K, work, dtype)
+    tr = measured_traffic(w.name if dtype == w.dtype else f"{w.name}-{dtype}", roofline["kernel"])
+    roofline["traffic"] = None if tr is None else tr["bytes_per_launch"]
+    if tr is not None:
+        roofline["traffic_detail"] = tr
+    return {"value": frames / (ms_step * 1e-3), "ms_step": ms_step,
+            "ms_step_mean_wall": (t1 - t0) * 1e3 / K, "ms_step_events": (t3 - t2) * 1e3 / K,
+            "kernels": kernels, "roofline": roofline, "schedule": schedule,
+            "j_tflops": j_tflops, "s_gbps": s_gbps, "peak_j": peak_j}
+
+
+def other_workload(name, dtype=None):
+    """A secondary configuration of the default run, measured as the main one (no CPU
+    baseline): frames/s, per-frame latency, per-kernel times and the roofline."""
+    import torch
+    from paper_2211_00484_amd import synth, tbs
+    w, inputs, model_np, graph_np = synth.make_workload(name, seed=0)
+    dtype = dtype or w.dtype
+    model = tbs.Model.from_synth(model_np, dtype=dtype)
+    graph = tbs.Graph.from_synth(graph_np)
+    enc = torch.from_numpy(inputs.encoder_out).cuda()
+    tr_out = tbs.decode(model, graph, enc, inputs.lengths, beam=w.beam, max_states=w.max_states,
+                        max_contexts=w.max_contexts, want_trace=True)
+    torch.cuda.synchronize()
+    work = algorithmic_work(tr_out.trace.cpu().numpy(), inputs.lengths, graph_np, w.V, w.C,
+                            (w.V + 63) // 64, w.max_states)
+    del tr_out
+    K = DEFAULT_STEPS[w.name]
+    m = measure_decode(w, inputs, model, graph, enc, dtype, K, 2, work)
+    res = {"description": w.description, "joiner": dtype, "schedule": m["schedule"],
+           "frames": int(inputs.lengths.sum()), "steps": K, "value": m["value"],
+           "unit": "frames/s", "ms_per_step": m["ms_step"],
+           "per_frame_latency_us": 1e3 * m["ms_step"] / max(int(inputs.lengths.max()), 1),
+           "roofline": m["roofline"],
+           "kernels": {k: round(v["avg_us"], 3) for k, v in m["kernels"].items()}}
+    model.close()
+    graph.close()
+    return res
 
 
 def chunked_bench(args, w, inputs, model_np, graph_np, model, graph, enc, dtype, K, W):
@@ -647,6 +728,10 @@ def main():
                     help="frame schedule: launch every frame's kernels from the host instead "
                          "of replaying the captured frame loop")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--other-workloads", action=argparse.BooleanOptionalAction, default=True,
+                    help="with the default (standard) workload, also measure the graph, "
+                         "throughput, large and large-bf16 configurations the same way and "
+                         "report them as secondary figures in the same line")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="threads for the oracle baseline (default: all host threads)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -714,46 +799,11 @@ def main():
         logadd_bench(args, w, inputs, model_np, graph_np, model, graph, enc, dtype, K, W, work)
         return
 
-    out = tbs.allocate_outputs(B, T, w.max_states, status=True)
-    for _ in range(W):
-        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
-    torch.cuda.synchronize()
-
-    # the timed steps: nothing but the decodes on the stream, with an event between
-    # consecutive steps (a marker, no host synchronisation) for the per-step median
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    evs[0].record()
-    for i in range(K):
-        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
-        evs[i + 1].record()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(K)]
-
-    # the same steps again with HIP events around every kernel launch: per-kernel
-    # durations for the roofline (the events add a little time between kernels)
-    model.set_profiling(True)
-    torch.cuda.synchronize()
-    t2 = time.perf_counter()
-    for _ in range(K):
-        tbs.decode_into(model, graph, enc, inputs.lengths, w.beam, w.max_states, w.max_contexts, out)
-    torch.cuda.synchronize()
-    t3 = time.perf_counter()
-    prof = model.read_profile()
-    model.set_profiling(False)
-
-    ms_step = statistics.median(step_ms)
-    ms_step_mean_wall = (t1 - t0) * 1e3 / K
-    ms_step_events = (t3 - t2) * 1e3 / K
-    value = frames / (ms_step * 1e-3)
-
-    kernels, roofline, schedule, j_tflops, s_gbps, peak_j = decode_roofline(prof, K, work, dtype)
-    tr = measured_traffic(w.name if dtype == w.dtype else f"{w.name}-{dtype}", roofline["kernel"])
-    roofline["traffic"] = None if tr is None else tr["bytes_per_launch"]
-    if tr is not None:
-        roofline["traffic_detail"] = tr
+    m = measure_decode(w, inputs, model, graph, enc, dtype, K, W, work)
+    value, ms_step, kernels, roofline, schedule = (m["value"], m["ms_step"], m["kernels"],
+                                                   m["roofline"], m["schedule"])
+    j_tflops, s_gbps, peak_j = m["j_tflops"], m["s_gbps"], m["peak_j"]
+    ms_step_mean_wall, ms_step_events = m["ms_step_mean_wall"], m["ms_step_events"]
 
     line = {
         "metric": METRIC, "value": value, "unit": "frames/s", "n_gpus": 1, "steps": K, "warmup": W,
@@ -780,6 +830,14 @@ def main():
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, inputs, model_np, graph_np, dtype,
                                             threads=args.cpu_threads)
+    if (args.other_workloads and w.name == "standard" and dtype == w.dtype
+            and args.schedule == "auto" and not args.alt_graphs):
+        # the other configurations, measured the same way (secondary figures)
+        line["other_workloads"] = {}
+        for name, odt in (("graph", None), ("throughput", None), ("large", None),
+                          ("large", "bf16")):
+            key = name if odt is None else f"{name}-{odt}"
+            line["other_workloads"][key] = other_workload(name, odt)
     print(json.dumps(line), flush=True)
 
 
