@@ -138,6 +138,32 @@ def test_many_candidate_chunks(schedule):
     _run((inputs, model, graph), 3.0, 16, 8, schedule=schedule)
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_maximum_vocabulary(schedule):
+    # V = 46,340, the largest vocabulary whose contexts a * V + b fit int32: the trivial
+    # graph (725 vocabulary tiles per row) and a small graph whose labels reach V - 1
+    rng = np.random.default_rng(21)
+    V, C = 46340, 16
+    model = synth.make_model(rng, V, C, 0.5)
+    inputs = synth.make_inputs(rng, 2, 4, C)
+    _run((inputs, model, synth.trivial_graph(V)), math.inf, 4, 4, schedule=schedule)
+    graph = synth.random_small_graph(rng, 6, V, max_degree=5, with_final=True)
+    graph.label[:] = np.where(rng.uniform(size=graph.num_arcs) < 0.5, V - 1, graph.label)
+    _run((inputs, model, graph), 5.0, 8, 4, schedule=schedule)
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_maximum_dimension(schedule):
+    # C = 2,048, the largest joiner dimension (four K chunks of 512)
+    rng = np.random.default_rng(22)
+    V, C = 60, 2048
+    model = synth.make_model(rng, V, C, 0.03)
+    inputs = synth.make_inputs(rng, 3, 6, C, length_range=(4, 6))
+    graph = synth.random_small_graph(rng, 8, V, max_degree=6)
+    _run((inputs, model, synth.trivial_graph(V)), math.inf, 4, 4, schedule=schedule)
+    _run((inputs, model, graph), 4.0, 12, 6, schedule=schedule)
+
+
 def test_heavy_tailed_states():
     # one state with 5,000 arcs next to ordinary ones, as in the power-law graph's tail
     rng = np.random.default_rng(6)
