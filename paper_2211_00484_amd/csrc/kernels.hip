@@ -990,7 +990,7 @@ struct SearchSmem {
   float rk_z[kMaxTopK * kMaxTopK];  // trivial graph: each row's best labels over all tiles
   int rk_c[kMaxTopK * kMaxTopK];
   float s_z0[kMaxTopK];
-  unsigned hist[256];
+  alignas(16) unsigned hist[256];  // radix counts; direct path: packed scores
   int wsum[4];
   int misc[8];
   int g_src[4];              // grouped fast path: decoder-row source of each new context row
@@ -998,6 +998,22 @@ struct SearchSmem {
   float best;
   double off_d;              // the stream's fp64 score offset (kept here between frames)
 };
+
+// Copies n dwords from global memory into LDS on the global-load-to-LDS path: no
+// registers held, 64 dwords per wave and instruction, all in flight together.  The
+// caller waits for the vector memory counter before the barrier that publishes them.
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ void lds_stage_dwords(void* dst, const void* src, int n, int tid) {
+  const int lane = tid & 63, wave = tid >> 6;
+  const unsigned* gs = reinterpret_cast<const unsigned*>(src);
+  unsigned* ld = reinterpret_cast<unsigned*>(dst);
+  for (int base = 64 * wave; base < n; base += kSearchThreads)  // wave-uniform LDS base
+    if (base + lane < n)
+      __builtin_amdgcn_global_load_lds((global_void*)(gs + base + lane), (lds_void*)(ld + base), 4, 0, 0);
+}
+// s_waitcnt vmcnt(0) (expcnt and lgkmcnt left free)
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 __device__ __forceinline__ uint32_t hash_slot(unsigned long long key) {
   return (uint32_t)((key * 0x9E3779B97F4A7C15ull) >> (64 - kHashBits));
@@ -1273,8 +1289,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   }
   float2* stage = reinterpret_cast<float2*>(s.hk);  // softmax partials, [Nc][nvt]
   const bool staged = Nc * nvt <= kStatStage;
-  if (!FUSED && staged)
-    for (int i = tid; i < Nc * nvt; i += blockDim.x) stage[i] = d.stats[row0 * nvt + i];
+  if (!FUSED && staged) lds_stage_dwords(stage, d.stats + row0 * nvt, 2 * Nc * nvt, tid);
   if (!FUSED)
     for (int i = tid; i < Ns; i += blockDim.x) {
       const size_t o = (size_t)b * Ns + i;
@@ -1284,8 +1299,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       s.s_score[i] = d.surv_score[o];
     }
   if (t + 1 < L && !enc_ready) {
-    const float* er = d.enc + ((size_t)b * d.T + t + 1) * m.C;
-    for (int k = tid; k < m.C; k += blockDim.x) s.enc_next[k] = er[k];
+    lds_stage_dwords(s.enc_next, d.enc + ((size_t)b * d.T + t + 1) * m.C, m.C, tid);
   }
   // trivial graph: the joiner's per-tile best labels of this stream's rows
   const int E = TRIV ? nvt * (kJoinerBN / 16) * d.KT : 0;
@@ -1300,6 +1314,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       }
     for (int j = tid; j < Nc; j += blockDim.x) s.s_z0[j] = d.z0[row0 + j];
   }
+  wait_vmem();  // the staged partials, encoder frame and label lists have landed in LDS
   __syncthreads();
   const int ns = s.ns, nc = s.nc;
   // general graph: the arc ranges of the survivors' states, requested before the
@@ -1581,7 +1596,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   int Nsel = N;
   bool listed = false;
   unsigned thr_ord = 0u;
-  if (N > kSmallCands && beam < INFINITY && N <= kChunk + kMaxStates) {
+  if (N > kDirectCands && beam < INFINITY && N <= kChunk + kMaxStates) {
     float lmax = -INFINITY;
     __syncthreads();  // trivial graph: uk/uv held the staged tile lists until here
     if (TRIV) {
@@ -1670,13 +1685,18 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     listed = true;
   }
 
-  if (Nsel <= kSmallCands) {
-    // small candidate sets: merge and rank directly.  Loops run over a multiple
-    // of 8 padded entries without early exits so their LDS reads pipeline.
-    const int N = Nsel;
-    const int Np = (N + 7) & ~7;
-    unsigned long long myk = kEmpty, myv = 0;
-    if (tid < N) {
+  if (Nsel <= kDirectCands) {
+    // At most one candidate per thread.  Candidates of one key merge in a small LDS
+    // hash table (the maximum of their packed values); the candidate holding that
+    // maximum represents the key and counts the representatives that rank above it
+    // over their packed 32-bit scores, four per LDS read, comparing keys only where
+    // scores are equal.
+    static_assert(kDirectCands == kSearchThreads && 2 * kSearchThreads <= kHashSlots, "direct path");
+    constexpr int kDirBits = 9, kDirSlots = 1 << kDirBits;  // load <= 1/2
+    static_assert(kDirSlots == 2 * kDirectCands, "direct table");
+    const int n = Nsel;
+    unsigned long long myk = kEmpty, myv = 0ull;
+    if (tid < n) {
       if (listed) {
         myk = s.hk[tid];
         myv = s.hv[tid];
@@ -1686,36 +1706,44 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
         myv = kv.y;
       }
     }
-    __syncthreads();  // trivial graph: uk/uv held the staged tile lists until here
-    if (tid < kSmallCands) {
-      s.uk[tid] = myk;
-      s.uv[tid] = myv;
+    __syncthreads();  // listed entries read; trivial graph: uk/uv held the staged tile lists until here
+    for (int i = tid; i < kDirSlots; i += blockDim.x) {
+      s.hk[i] = kEmpty;
+      s.hv[i] = 0ull;
     }
     __syncthreads();
-    // a candidate represents its key iff no candidate with that key has a larger value
-    bool rep = myk != kEmpty;
-    if (tid < N) {
-      bool dom = false;
-      for (int j0 = 0; j0 < Np; j0 += 8) {
-#pragma unroll
-        for (int u = 0; u < 8; ++u) dom |= (s.uk[j0 + u] == myk) & (s.uv[j0 + u] > myv);
+    int slot = -1;
+    if (myk != kEmpty) {
+      uint32_t h = (uint32_t)((myk * 0x9E3779B97F4A7C15ull) >> (64 - kDirBits));
+      for (;;) {
+        const unsigned long long prev = atomicCAS(&s.hk[h], kEmpty, myk);
+        if (prev == kEmpty || prev == myk) break;
+        h = (h + 1) & (kDirSlots - 1);
       }
-      rep = rep && !dom;
+      atomicMax(&s.hv[h], myv);
+      slot = (int)h;
     }
     __syncthreads();
-    if (tid < kSmallCands && !rep) s.uk[tid] = kEmpty;
+    const bool rep = slot >= 0 && s.hv[slot] == myv;  // values are unique (back-pointers)
+    const unsigned so = (unsigned)(myv >> 32);
+    const int n4 = (n + 3) >> 2;
+    if (tid < 4 * n4) {
+      s.hist[tid] = rep ? so : 0u;  // a represented score is never 0 (order code of a number)
+      s.uk[tid] = rep ? myk : kEmpty;
+    }
     __syncthreads();
     if (rep) {
-      const unsigned so = (unsigned)(myv >> 32);
-      int rank = 0;
-      for (int j0 = 0; j0 < Np; j0 += 8) {
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const unsigned long long kj = s.uk[j0 + u];
-          const unsigned soj = (unsigned)(s.uv[j0 + u] >> 32);
-          rank += (kj != kEmpty) & ((soj > so) | ((soj == so) & (kj < myk)));
-        }
+      const uint4* sc4 = reinterpret_cast<const uint4*>(s.hist);
+      int gt = 0, eq = 0;
+#pragma unroll 4
+      for (int j = 0; j < n4; ++j) {
+        const uint4 q = sc4[j];
+        gt += (int)(q.x > so) + (int)(q.y > so) + (int)(q.z > so) + (int)(q.w > so);
+        eq += (int)(q.x == so) + (int)(q.y == so) + (int)(q.z == so) + (int)(q.w == so);
       }
+      int rank = gt;
+      if (eq > 1)  // another representative with this score: keys ascending break the tie
+        for (int j = 0; j < 4 * n4; ++j) rank += (int)((s.hist[j] == so) & (s.uk[j] < myk));
       if (rank < Ns) {
         s.lk[rank] = myk;
         s.lv[rank] = myv;
@@ -1724,26 +1752,41 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     }
     __syncthreads();
   } else {
+    // Hash merge.  Listed entries (at most kChunk + kMaxStates) merge in one pass:
+    // moved from hk/hv to uk/uv (whose made candidates are no longer needed), then
+    // inserted.  Otherwise the candidates are made and merged kChunk at a time, the
+    // best Ns so far carried into each pass.
     constexpr int CPT = kChunk / kSearchThreads;
+    static_assert(8 * (kChunk + kMaxStates) <= 5 * kHashSlots, "one listed pass");
+    const bool one = listed;
+    if (one)
+      for (int i = tid; i < Nsel; i += blockDim.x) {
+        s.uk[i] = s.hk[i];
+        s.uv[i] = s.hv[i];
+      }
     __syncthreads();
-    for (int base = 0; base < N; base += kChunk) {
+    for (int base = 0; base < (one ? 1 : N); base += kChunk) {
       for (int i = tid; i < kHashSlots; i += blockDim.x) {
         s.hk[i] = kEmpty;
         s.hv[i] = 0ull;
       }
       if (tid == 0) s.nU = 0;
       __syncthreads();
-      const int nL = s.nL;
-      for (int i = tid; i < nL; i += blockDim.x) hash_insert(s, s.lk[i], s.lv[i]);
-      ulonglong2 kv[CPT];
+      if (one) {
+        for (int i = tid; i < Nsel; i += blockDim.x) hash_insert(s, s.uk[i], s.uv[i]);
+      } else {
+        const int nL = s.nL;
+        for (int i = tid; i < nL; i += blockDim.x) hash_insert(s, s.lk[i], s.lv[i]);
+        ulonglong2 kv[CPT];
 #pragma unroll
-      for (int u = 0; u < CPT; ++u) {
-        const int c = base + tid + u * kSearchThreads;
-        kv[u] = c < N ? make_cand(c) : make_ulonglong2(kEmpty, 0ull);
+        for (int u = 0; u < CPT; ++u) {
+          const int c = base + tid + u * kSearchThreads;
+          kv[u] = c < N ? make_cand(c) : make_ulonglong2(kEmpty, 0ull);
+        }
+#pragma unroll
+        for (int u = 0; u < CPT; ++u)
+          if (kv[u].x != kEmpty && (unsigned)(kv[u].y >> 32) >= thr_ord) hash_insert(s, kv[u].x, kv[u].y);
       }
-#pragma unroll
-      for (int u = 0; u < CPT; ++u)
-        if (kv[u].x != kEmpty && (unsigned)(kv[u].y >> 32) >= thr_ord) hash_insert(s, kv[u].x, kv[u].y);
       __syncthreads();
       for (int i = tid; i < kHashSlots; i += blockDim.x) {
         if (s.hk[i] != kEmpty) {
