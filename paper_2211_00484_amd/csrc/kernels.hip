@@ -1875,31 +1875,44 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     }
   } else if (K <= 64) {
     // One wave.  The entries are sorted by (context, state) with a bitonic network
-    // across the lanes, so that each context is a run of lanes: its score is the run
-    // maximum of the in-beam scores, its first tuple the run's first in-beam lane; a
-    // context's rank among the contexts (score desc, context asc) is counted over the
-    // run heads staged in LDS; canonical positions and context rows are prefix counts
-    // of ballots, because the sorted order is the canonical one.
+    // across the lanes (carrying each entry's original lane, whose packed value is
+    // fetched once after the sort), so that each context is a run of lanes: its score
+    // is the run maximum of the in-beam scores, its first tuple the run's first
+    // in-beam lane.  The kept contexts are the run heads at or above the Nc-th largest
+    // context score, found bit by bit on ballots (ties: context ascending, the sorted
+    // order); canonical positions and context rows are prefix counts of ballots,
+    // because the sorted order is the canonical one.
     if (wave == 0) {
       auto xor64 = [](unsigned long long v, int m) {
         const int lo = xor_lane((int)(unsigned)v, m), hi = xor_lane((int)(unsigned)(v >> 32), m);
         return ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo;
       };
       unsigned long long sk = tid < K ? ((unsigned long long)my_ci << 32) | my_st : ~0ull;  // sentinels last
-      unsigned long long sv = tid < K ? my_v : 0ull;
-      // (fully unrolled, so that each stage's exchange distance is a constant)
+      int ol = lane;  // the entry's original lane
+      // (fully unrolled, so that each stage's exchange distance is a constant; keys
+      // are unique but for the sentinels, whose order does not matter, so one compare
+      // decides the exchange)
+      auto stage = [&](int k, int j) {
+        const unsigned long long pk = xor64(sk, j);
+        const int po = xor_lane(ol, j);
+        const bool up = (lane & k) == 0, lower = (lane & j) == 0;
+        // (selects rather than a branch: each stage stays a short dependent chain)
+        const bool take = (pk < sk) == (lower == up);
+        sk = take ? pk : sk;
+        ol = take ? po : ol;
+      };
 #pragma unroll
-      for (int k = 2; k <= 64; k <<= 1)
+      for (int k = 2; k <= 32; k <<= 1)
 #pragma unroll
-        for (int j = k >> 1; j > 0; j >>= 1) {
-          const unsigned long long pk = xor64(sk, j), pv = xor64(sv, j);
-          const bool up = (lane & k) == 0, lower = (lane & j) == 0;
-          // (selects rather than a branch: each stage stays a short dependent chain)
-          const bool lt = pk < sk, gt = pk > sk, asc = lower == up;
-          const bool take = (asc & lt) | (!asc & gt);
-          sk = take ? pk : sk;
-          sv = take ? pv : sv;
-        }
+        for (int j = k >> 1; j > 0; j >>= 1) stage(k, j);
+      // with at most 32 entries the upper half holds sentinels only, and the lower
+      // half is sorted: the last merge would exchange nothing
+      if (K > 32)
+#pragma unroll
+        for (int j = 32; j > 0; j >>= 1) stage(64, j);
+      const unsigned long long sv =
+          ((unsigned long long)(unsigned)__shfl((int)(unsigned)(my_v >> 32), ol) << 32) |
+          (unsigned)__shfl((int)(unsigned)my_v, ol);
       const bool valid = sk != ~0ull;
       const unsigned ci = (unsigned)(sk >> 32), stt = (unsigned)sk;
       const float sc = valid ? ord2f((unsigned)(sv >> 32)) : -INFINITY;
@@ -1922,20 +1935,21 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
         if (lane - dd >= rs) run = fmaxf(run, upv);
       }
       const float cs = __shfl(run, valid ? re : lane);
-      const unsigned co = first ? f2ord(cs) : 0u;
-      s.hist[lane] = co;
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      int rank = 0;
-      for (int q0 = 0; q0 < 64; q0 += 8) {
-        unsigned r[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) r[u] = s.hist[q0 + u];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) rank += (r[u] > co) | ((r[u] == co) & (q0 + u < lane));
+      const unsigned co = first ? f2ord(cs) : 0u;  // a head's code is never 0
+      int fkeep = first;
+      if (__popcll(__ballot(first)) > (unsigned)Nc) {
+        // theta: the largest code with at least Nc heads at or above it, i.e. the
+        // Nc-th largest head code (> 0).  Other lanes hold code 0, so plain compares
+        // count heads only, one ballot per bit.
+        unsigned theta = 0u;
+        for (int bit = 31; bit >= 0; --bit) {
+          const unsigned cand = theta | (1u << bit);
+          if (__popcll(__ballot(co >= cand)) >= (unsigned)Nc) theta = cand;
+        }
+        const int room = Nc - (int)__popcll(__ballot(co > theta));  // >= 1
+        const unsigned long long E = __ballot(co == theta);
+        fkeep = first && (co > theta || (co == theta && (int)__popcll(E & below) < room));
       }
-      const int fkeep = first && rank < Nc;
       const int keep2 = k1 && __shfl(fkeep, fl);
       const unsigned long long K2 = __ballot(keep2), F2 = __ballot(keep2 && first);
       my_pos = __popcll(K2 & below);

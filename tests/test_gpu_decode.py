@@ -378,3 +378,50 @@ def test_frame_loop_graph_replays_match_eager():
     say(f"  frame-loop graph: {captures} captures, {replays} replays")
     assert (captures, replays) == (2, 6)   # x: direct, capture, 2 replays; y direct; x 2 replays; y capture, 2 replays
     assert ref.graph_stats() == (0, 0)
+
+
+def _tied_case(kind, seed=77):
+    # Zero joiner weights and bias and zero arc scores: every label has the same
+    # log-probability, so all candidates of a frame score exactly alike, in fp32 on the
+    # GPU and in fp64 in the oracle, and every selection (merge, max-states, context
+    # ranking, final pick) is decided by the tie-break orders alone.
+    rng = np.random.default_rng(seed)
+    V, C = 12, 16
+    model = synth.make_model(rng, V, C, 0.3)
+    model.w_out[:] = 0.0
+    model.b_out[:] = 0.0
+    inputs = synth.make_inputs(rng, 4, 30, C, length_range=(5, 30))
+    if kind == "graph":
+        graph = synth.random_small_graph(rng, 40, V, max_degree=6)
+        graph.score[:] = 0.0
+    else:
+        graph = synth.trivial_graph(V)
+    return inputs, model, graph
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
+@pytest.mark.parametrize("kind,beam,Ns,Nc", [("graph", math.inf, 8, 3), ("graph", 1.0, 40, 6),
+                                             ("graph", math.inf, 100, 20), ("graph", 0.5, 200, 64),
+                                             ("trivial", math.inf, 8, 3), ("trivial", math.inf, 4, 4)])
+def test_exact_ties_follow_the_canonical_orders(kind, beam, Ns, Nc, schedule):
+    from paper_2211_00484_amd import tbs
+    inputs, model, graph = _tied_case(kind)
+    say(f"tied decode {kind} beam={beam} Ns={Ns} Nc={Nc} {schedule}")
+    try:
+        g = gpu_decode(model, graph, inputs, beam, Ns, Nc, schedule=schedule)
+    except tbs.TbsError as e:
+        if schedule == "stream" and e.status == -5:
+            pytest.skip(f"not supported by the per-stream kernel: {e}")
+        raise
+    streams = list(range(inputs.B))
+    o = oracle.decode(model, graph, inputs.encoder_out, inputs.lengths, beam, Ns, Nc,
+                      streams=streams)
+    assert (o.frame_margins[:, :-1] == 0).any(), "the case has no tied decision"
+    for b in streams:
+        L = int(inputs.lengths[b])
+        assert np.array_equal(g["trace"][: L + 1, b], o.trace[: L + 1, b]), f"stream {b}: trace"
+        n = int(g["ntok"][b])
+        assert g["tokens"][b, :n].tolist() == o.tokens[b, : o.ntok[b]].tolist(), f"stream {b}: tokens"
+        assert int(g["status"][b]) == int(o.status[b])
+        assert np.array_equal(g["arcs"][b, :L], o.arcs[b, :L]), f"stream {b}: arcs"
+        assert abs(float(g["scores"][b]) - float(o.scores[b])) <= 1e-4
