@@ -65,6 +65,7 @@ struct Workspace {
   int* surv_state = nullptr;
   float* surv_score = nullptr;
   int* surv_row = nullptr;
+  int2* surv_rp = nullptr;
   int* nctx = nullptr;
   int* ctx_list = nullptr;
   double* offset = nullptr;
@@ -86,7 +87,7 @@ struct Workspace {
 
   void release() {
     (void)hipFree(len); (void)hipFree(nsurv); (void)hipFree(surv_ctx); (void)hipFree(surv_state); (void)hipFree(surv_score);
-    (void)hipFree(surv_row); (void)hipFree(nctx); (void)hipFree(ctx_list); (void)hipFree(offset); (void)hipFree(h);
+    (void)hipFree(surv_row); (void)hipFree(surv_rp); (void)hipFree(nctx); (void)hipFree(ctx_list); (void)hipFree(offset); (void)hipFree(h);
     (void)hipFree(logits); (void)hipFree(stats); (void)hipFree(tk_z); (void)hipFree(tk_c); (void)hipFree(z0);
     (void)hipFree(hist_pl); (void)hipFree(hist_arc); (void)hipFree(path_lab);
     (void)hipFree(gtab);
@@ -337,6 +338,7 @@ tbs_status alloc_workspace(const tbs_model* m, Workspace& w, int B, int T, int N
   HIP_TRY(dalloc(&w.surv_state, BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.surv_score, BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.surv_row, BN), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.surv_rp, BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.nctx, B), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.ctx_list, BC), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.offset, B), "hipMalloc(workspace)");
@@ -478,6 +480,7 @@ DecodeDev decode_dev(const tbs_model* m, const Workspace& w, int B, int T, int N
   d.surv_state = w.surv_state;
   d.surv_score = w.surv_score;
   d.surv_row = w.surv_row;
+  d.surv_rp = w.surv_rp;
   d.nctx = w.nctx;
   d.ctx_list = w.ctx_list;
   d.offset = w.offset;
@@ -561,7 +564,7 @@ tbs_status enqueue_frames(tbs_model* m, const GraphDev& gd, float beam,
     // model, as bytes (GraphDev and DecodeDev hold no padding; the model's tables and
     // the joiner plan follow from the model and d)
     static_assert(sizeof(GraphDev) == 4 * sizeof(int) + 5 * sizeof(void*) &&
-                      sizeof(DecodeDev) == 6 * sizeof(int) + 21 * sizeof(void*),
+                      sizeof(DecodeDev) == 6 * sizeof(int) + 22 * sizeof(void*),
                   "frame-loop key: GraphDev / DecodeDev must have no padding");
     std::vector<unsigned char> key;
     auto put = [&](const void* p, size_t n) {
@@ -950,6 +953,7 @@ size_t carve_workspace(const tbs_model* m, uintptr_t base, int B, int T, int Ns,
   take(w.surv_state, BN);
   take(w.surv_score, BN);
   take(w.surv_row, BN);
+  take(w.surv_rp, BN);
   take(w.nctx, (size_t)B);
   take(w.ctx_list, BC);
   take(w.offset, (size_t)B);

@@ -80,6 +80,7 @@ struct DecodeDev {
   int* surv_state;          // [B][Ns]
   float* surv_score;        // [B][Ns], relative to the stream's best
   int* surv_row;            // [B][Ns], index of the tuple's context in ctx_list
+  int2* surv_rp;            // [B][Ns], arc range [lo, hi) of the tuple's state (frame kernels)
   int* nctx;                // [B]
   int* ctx_list;            // [B][Nc], ascending
   double* offset;           // [B]

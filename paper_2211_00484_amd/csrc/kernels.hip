@@ -918,6 +918,7 @@ __global__ __launch_bounds__(256) void k_init(ModelDev m, DecodeDev d, GraphDev 
     d.surv_state[(size_t)b * d.Ns] = g.start;
     d.surv_score[(size_t)b * d.Ns] = 0.f;
     d.surv_row[(size_t)b * d.Ns] = 0;
+    d.surv_rp[(size_t)b * d.Ns] = make_int2(g.rp[g.start], g.rp[g.start + 1]);
     d.nctx[b] = 1;
     d.ctx_list[(size_t)b * d.Nc] = 0;
     d.offset[b] = 0.0;
@@ -944,11 +945,13 @@ __global__ __launch_bounds__(256) void k_init(ModelDev m, DecodeDev d, GraphDev 
 __global__ __launch_bounds__(256) void k_resume(ModelDev m, DecodeDev d, GraphDev g,
                                                 int* __restrict__ trace, int rows_needed) {
   __shared__ int2 s_off[kMaxStates];
-  __shared__ int s_nc;
+  __shared__ int s_nc, s_ns;
   const int b = blockIdx.x, tid = threadIdx.x;
   if (d.len[b] == 0) return;
+  if (d.graphs) g = d.graphs[b];  // per-stream graphs
   if (tid == 0) {
     s_nc = d.nctx[b];
+    s_ns = d.nsurv[b];
     if (trace && d.base[b] == 0) {
       int* p = trace + (size_t)b * d.Ns * 4;
       p[0] = d.surv_ctx[(size_t)b * d.Ns];
@@ -958,6 +961,12 @@ __global__ __launch_bounds__(256) void k_resume(ModelDev m, DecodeDev d, GraphDe
     }
   }
   __syncthreads();
+  // the arc ranges of the survivors' states, from the graph this chunk decodes with
+  for (int i = tid; i < s_ns; i += blockDim.x) {
+    const size_t o = (size_t)b * d.Ns + i;
+    const int st = d.surv_state[o];
+    d.surv_rp[o] = make_int2(g.rp[st], g.rp[st + 1]);
+  }
   if (!rows_needed) return;
   const int nc = s_nc;
   for (int j = tid; j < nc; j += blockDim.x) {
@@ -1298,6 +1307,16 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       s.s_row[i] = d.surv_row[o];
       s.s_score[i] = d.surv_score[o];
     }
+  // general graph: the arc ranges of the survivors' states, stored with them by the
+  // previous frame (one survivor per thread; the persistent kernels, whose survivors
+  // stay in LDS, read them from the graph below)
+  static_assert(kMaxStates <= kSearchThreads, "one survivor per thread");
+  int rp_lo = 0, rp_hi = 0;
+  if (!TRIV && !FUSED && tid < Ns) {
+    const int2 r = d.surv_rp[(size_t)b * Ns + tid];
+    rp_lo = r.x;
+    rp_hi = r.y;
+  }
   if (t + 1 < L && !enc_ready) {
     lds_stage_dwords(s.enc_next, d.enc + ((size_t)b * d.T + t + 1) * m.C, m.C, tid);
   }
@@ -1317,11 +1336,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   wait_vmem();  // the staged partials, encoder frame and label lists have landed in LDS
   __syncthreads();
   const int ns = s.ns, nc = s.nc;
-  // general graph: the arc ranges of the survivors' states, requested before the
-  // normalisers so that their round trip overlaps them (one survivor per thread)
-  static_assert(kMaxStates <= kSearchThreads, "one survivor per thread");
-  int rp_lo = 0, rp_hi = 0;
-  if (!TRIV && tid < ns) {
+  if (!TRIV && FUSED && tid < ns) {  // requested before the normalisers, which overlap them
     const int st = s.s_state[tid];
     rp_lo = g.rp[st];
     rp_hi = g.rp[st + 1];
@@ -2061,6 +2076,11 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     s.n_rowoff[tid] = make_int2(a * m.Kpad, (c - a * V) * m.Kpad);
   }
   __syncthreads();
+  const bool store_surv = writer && (!FUSED || t + 1 == L);
+  // general graph: the kept tuples' arc ranges for the next frame, requested before
+  // the next rows so that their round trip overlaps them
+  int2 nrp = make_int2(0, 0);
+  if (!TRIV && store_surv && my_keep2) nrp = make_int2(g.rp[my_st], g.rp[my_st + 1]);
   // global stores: joiner rows of the next frame, survivors, history, trace
   if (t + 1 < L) {
     if (FUSED && dspec) {
@@ -2100,7 +2120,6 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
         write_h_rows<kSearchThreads, 32>(m, s.enc_next, 0, s.n_rowoff, nC, hrows, m.Kpad, tid);
     }
   }
-  const bool store_surv = writer && (!FUSED || t + 1 == L);
   if (my_keep2) {
     const unsigned tb = 0xffffffffu - (unsigned)my_v;
     const int parent = (int)(tb / stride_tb);
@@ -2119,6 +2138,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       d.surv_state[o] = (int)my_st;
       d.surv_score[o] = my_sc - best;
       d.surv_row[o] = my_crow;
+      if (!TRIV) d.surv_rp[o] = nrp;
       if (my_first) d.ctx_list[row0 + my_crow] = (int)my_ci;
     }
     const size_t hbase = ((size_t)(fb + t) * d.B + b) * Ns;
