@@ -1722,10 +1722,12 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       }
     }
     __syncthreads();  // listed entries read; trivial graph: uk/uv held the staged tile lists until here
+    int* tcount = reinterpret_cast<int*>(s.uv);  // representatives per score rank (uv is free now)
     for (int i = tid; i < kDirSlots; i += blockDim.x) {
       s.hk[i] = kEmpty;
       s.hv[i] = 0ull;
     }
+    if (tid < kDirectCands) tcount[tid] = 0;
     __syncthreads();
     int slot = -1;
     if (myk != kEmpty) {
@@ -1747,17 +1749,24 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       s.uk[tid] = rep ? myk : kEmpty;
     }
     __syncthreads();
+    // gt: representatives with a larger score.  Equal scores give equal counts and
+    // different scores different ones, so a count shared with another candidate for
+    // the kept set marks a tie, broken by keys ascending.
+    int gt = 0;
     if (rep) {
       const uint4* sc4 = reinterpret_cast<const uint4*>(s.hist);
-      int gt = 0, eq = 0;
 #pragma unroll 4
       for (int j = 0; j < n4; ++j) {
         const uint4 q = sc4[j];
         gt += (int)(q.x > so) + (int)(q.y > so) + (int)(q.z > so) + (int)(q.w > so);
-        eq += (int)(q.x == so) + (int)(q.y == so) + (int)(q.z == so) + (int)(q.w == so);
       }
+    }
+    const bool contend = rep && gt < Ns;
+    if (contend) atomicAdd(&tcount[gt], 1);
+    __syncthreads();
+    if (contend) {
       int rank = gt;
-      if (eq > 1)  // another representative with this score: keys ascending break the tie
+      if (tcount[gt] > 1)
         for (int j = 0; j < 4 * n4; ++j) rank += (int)((s.hist[j] == so) & (s.uk[j] < myk));
       if (rank < Ns) {
         s.lk[rank] = myk;
