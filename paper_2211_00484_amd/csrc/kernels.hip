@@ -673,6 +673,11 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
   const int act = tid < BM ? (int)joiner_row_active(a, r0 + tid) : 0;
   if (tid < BM) s_act[tid] = act;
   if (!__syncthreads_or(act)) return;  // uniform: no active row in this tile
+  // the epilogue's bias values, requested now so that their round trip is hidden
+  // behind the main loop (clamped: past the vocabulary they are never used)
+  float bias_r[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) bias_r[nb] = m.bias[min(64 * vt + 16 * nb + lr, V - 1)];
 
   // slice loads: UA (h) and UB (W) chunks of 16 bytes per thread (BM and BN rows x 8 chunks)
   const char* hsrc = reinterpret_cast<const char*>(a.h);
@@ -827,7 +832,7 @@ __global__ __launch_bounds__(128 * WN) void k_joiner(ModelDev m, JoinArgs a) {
     for (int nb = 0; nb < 4; ++nb) {
       const int col = 64 * vt + 16 * nb + lr;
       cvalid[nb] = FULL || col < V;
-      bias[nb] = cvalid[nb] ? m.bias[col] : 0.f;
+      bias[nb] = cvalid[nb] ? bias_r[nb] : 0.f;
     }
 #pragma unroll
     for (int mb = 0; mb < MBW; ++mb) {
@@ -2134,7 +2139,8 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     const int parent = (int)(tb / stride_tb);
     const int apos = (int)(tb - (unsigned)parent * stride_tb) - 1;
     const int arc = apos < 0 ? -1 : s.s_base[parent] + apos;
-    const int label = arc < 0 ? 0 : (TRIV ? arc + 1 : g.label[arc]);
+    // (the arc's label is the newer label of the tuple's context: no load)
+    const int label = arc < 0 ? 0 : (int)(my_ci % (unsigned)V);
     const size_t o = (size_t)b * Ns + my_pos;
     if (FUSED) {  // every read of the old survivors precedes the last barrier
       s.s_ctx[my_pos] = (int)my_ci;
