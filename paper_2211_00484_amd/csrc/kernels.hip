@@ -423,21 +423,32 @@ __device__ __forceinline__ void joiner_tile_small(const ModelDev& m, const JoinA
   if (tid < BM) s_act[tid] = joiner_row_active(a, r0 + tid);
   // W fragment of the first K chunk (registers) and the bias: issued before the
   // h staging so that all of the tile's loads are in flight together
-  // (Kpad is a multiple of 512: one chunk of W per lane is 32 float4 or 16 uint4)
+  // (Kpad is a multiple of 512: one chunk of W per lane is 32 float4 or 16 uint4).
+  // W is read from its interleaved copy (16-byte k slices, columns consecutive),
+  // where the 16 lanes of a k slice read 256 contiguous bytes.
   float4 wf[BF16 ? 1 : 32];
   uint4 wb[BF16 ? 16 : 1];
-  if (BF16) {
-    const uint16_t* wrow = m.Wb + (size_t)col * Kpad + 16 * lg;
+  const uint4* __restrict__ wi = reinterpret_cast<const uint4*>(m.Wi);
+  const size_t Vp = (size_t)m.Vpad;
+  auto load_w = [&](int kc) {
+    if (BF16) {
+      const size_t q0 = (size_t)(kc / 8 + 2 * lg);
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      wb[2 * s] = *reinterpret_cast<const uint4*>(wrow + s * 64);
-      wb[2 * s + 1] = *reinterpret_cast<const uint4*>(wrow + s * 64 + 8);
+      for (int s = 0; s < 8; ++s) {
+        wb[2 * s] = wi[(q0 + 8 * s) * Vp + col];
+        wb[2 * s + 1] = wi[(q0 + 8 * s + 1) * Vp + col];
+      }
+    } else {
+      const size_t q0 = (size_t)(kc / 4 + lg);
+#pragma unroll
+      for (int s = 0; s < 32; ++s) {
+        const uint4 v = wi[(q0 + 4 * s) * Vp + col];
+        wf[s] = make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                            __uint_as_float(v.w));
+      }
     }
-  } else {
-    const float* wrow = m.Wf + (size_t)col * Kpad + 4 * lg;
-#pragma unroll
-    for (int s = 0; s < 32; ++s) wf[s] = *reinterpret_cast<const float4*>(wrow + s * 16);
-  }
+  };
+  load_w(0);
   const float bias = cvalid ? m.bias[col] : 0.f;
   __syncthreads();
   int any = 0;
@@ -477,20 +488,7 @@ __device__ __forceinline__ void joiner_tile_small(const ModelDev& m, const JoinA
     for (int c = 0; c < 4; ++c) acc[mb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int kc = 0; kc < Kpad; kc += 512) {
-    if (kc > 0) {  // later K chunks (C > 512)
-      if (BF16) {
-        const uint16_t* wrow = m.Wb + (size_t)col * Kpad + kc + 16 * lg;
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          wb[2 * s] = *reinterpret_cast<const uint4*>(wrow + s * 64);
-          wb[2 * s + 1] = *reinterpret_cast<const uint4*>(wrow + s * 64 + 8);
-        }
-      } else {
-        const float* wrow = m.Wf + (size_t)col * Kpad + kc + 4 * lg;
-#pragma unroll
-        for (int s = 0; s < 32; ++s) wf[s] = *reinterpret_cast<const float4*>(wrow + s * 16);
-      }
-    }
+    if (kc > 0) load_w(kc);  // later K chunks (C > 512)
     __syncthreads();
     if (BF16) {
       const uint16_t* hb = reinterpret_cast<const uint16_t*>(smem) + (size_t)lr * ldk + kc + 16 * lg;
