@@ -1099,18 +1099,11 @@ __device__ unsigned long long kth_largest(SearchSmem& s, int n, int k, Get get) 
   return prefix;
 }
 
-// Top `Ns` of the nU merged entries in uk/uv by (score desc, key asc) into lk/lv.
-__device__ __forceinline__ void select_top(SearchSmem& s, int nU, int Ns) {
+// Top `Ns` of the nU > Ns merged entries in uk/uv by (score desc, key asc) into lk/lv,
+// by an exact 8-bit radix select of the score code (several passes) and of the key
+// among equal scores.
+__device__ __attribute__((noinline)) void select_top_radix(SearchSmem& s, int nU, int Ns) {
   const int tid = threadIdx.x;
-  if (nU <= Ns) {
-    for (int i = tid; i < nU; i += blockDim.x) {
-      s.lk[i] = s.uk[i];
-      s.lv[i] = s.uv[i];
-    }
-    if (tid == 0) s.nL = nU;
-    __syncthreads();
-    return;
-  }
   const unsigned theta = (unsigned)kth_largest<32>(s, nU, Ns, [&](int i, unsigned long long& v) {
     v = s.uv[i] >> 32;
     return true;
@@ -1143,6 +1136,112 @@ __device__ __forceinline__ void select_top(SearchSmem& s, int nU, int Ns) {
       const int p = atomicAdd(&s.nL, 1);
       s.lk[p] = s.uk[i];
       s.lv[p] = s.uv[i];
+    }
+  }
+  __syncthreads();
+}
+
+// Top `Ns` of the nU merged entries in uk/uv by (score desc, key asc) into lk/lv.  One
+// histogram pass over the score codes, binned across their own range (min to max), finds
+// the bin holding the Ns-th entry: entries in higher bins are kept, and the bin's own
+// entries (listed in hk/hv, free after the merge) are ranked exactly among themselves.
+// A bin of more than one entry per thread (a narrow or degenerate range) falls back to
+// the radix select.
+__device__ __forceinline__ void select_top(SearchSmem& s, int nU, int Ns) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (nU <= Ns) {
+    for (int i = tid; i < nU; i += blockDim.x) {
+      s.lk[i] = s.uk[i];
+      s.lv[i] = s.uv[i];
+    }
+    if (tid == 0) s.nL = nU;
+    __syncthreads();
+    return;
+  }
+  unsigned lo = 0xffffffffu, hi = 0u;
+  for (int i = tid; i < nU; i += blockDim.x) {
+    const unsigned c = (unsigned)(s.uv[i] >> 32);
+    lo = min(lo, c);
+    hi = max(hi, c);
+  }
+  lo = wave_min_u32(lo);
+  hi = wave_max_u32(hi);
+  if (lane == 0) {
+    s.misc[wave] = (int)lo;
+    s.misc[4 + wave] = (int)hi;
+  }
+  for (int i = tid; i < 256; i += blockDim.x) s.hist[i] = 0u;
+  if (tid == 0) {
+    s.nL = 0;
+    s.n_eq = 0;
+  }
+  __syncthreads();
+  lo = min(min((unsigned)s.misc[0], (unsigned)s.misc[1]), min((unsigned)s.misc[2], (unsigned)s.misc[3]));
+  hi = max(max((unsigned)s.misc[4], (unsigned)s.misc[5]), max((unsigned)s.misc[6], (unsigned)s.misc[7]));
+  const unsigned range = hi - lo;
+  const int shift = range < 256u ? 0 : 24 - __clz((int)range);  // (range >> shift) < 256
+  auto bin = [&](unsigned c) { return (c - lo) >> shift; };
+  for (int i = tid; i < nU; i += blockDim.x) atomicAdd(&s.hist[bin((unsigned)(s.uv[i] >> 32))], 1u);
+  __syncthreads();
+  if (tid < 64) {
+    // the bin holding the Ns-th largest code, scanning from the top bin
+    unsigned c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = s.hist[255 - 4 * lane - j];
+    const unsigned sum = c[0] + c[1] + c[2] + c[3];
+    unsigned incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const unsigned y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    const int first = __ffsll((long long)__ballot(incl >= (unsigned)Ns)) - 1;
+    if (lane == first) {
+      unsigned cum = incl - sum;
+      int bsel = 255 - 4 * lane - 3;
+      for (int j = 0; j < 4; ++j) {
+        if (cum + c[j] >= (unsigned)Ns) {
+          bsel = 255 - 4 * lane - j;
+          break;
+        }
+        cum += c[j];
+      }
+      s.misc[0] = bsel;
+      s.misc[1] = Ns - (int)cum;  // entries still needed from that bin (>= 1)
+    }
+  }
+  __syncthreads();
+  const unsigned bsel = (unsigned)s.misc[0];
+  const int need = s.misc[1], inb = (int)s.hist[bsel];
+  if (inb > kSearchThreads) {  // uniform
+    select_top_radix(s, nU, Ns);
+    return;
+  }
+  for (int i = tid; i < nU; i += blockDim.x) {
+    const unsigned b = bin((unsigned)(s.uv[i] >> 32));
+    if (b > bsel) {
+      const int p = atomicAdd(&s.nL, 1);
+      s.lk[p] = s.uk[i];
+      s.lv[p] = s.uv[i];
+    } else if (b == bsel) {
+      const int q = atomicAdd(&s.n_eq, 1);
+      s.hk[q] = s.uk[i];
+      s.hv[q] = s.uv[i];
+    }
+  }
+  __syncthreads();
+  if (tid < inb) {
+    const unsigned long long k = s.hk[tid], v = s.hv[tid];
+    const unsigned so = (unsigned)(v >> 32);
+    int r = 0;
+    for (int j = 0; j < inb; ++j) {
+      const unsigned sj = (unsigned)(s.hv[j] >> 32);
+      r += (int)((sj > so) | ((sj == so) & (s.hk[j] < k)));
+    }
+    if (r < need) {
+      const int p = atomicAdd(&s.nL, 1);
+      s.lk[p] = k;
+      s.lv[p] = v;
     }
   }
   __syncthreads();
