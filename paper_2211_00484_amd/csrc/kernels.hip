@@ -1805,9 +1805,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   if (Nsel <= kDirectCands) {
     // At most one candidate per thread.  Candidates of one key merge in a small LDS
     // hash table (the maximum of their packed values); the candidate holding that
-    // maximum represents the key and counts the representatives that rank above it
-    // over their packed 32-bit scores, four per LDS read, comparing keys only where
-    // scores are equal.
+    // maximum represents the key and is listed for the top-Ns selection.
     static_assert(kDirectCands == kSearchThreads && 2 * kSearchThreads <= kHashSlots, "direct path");
     constexpr int kDirBits = 9, kDirSlots = 1 << kDirBits;  // load <= 1/2
     static_assert(kDirSlots == 2 * kDirectCands, "direct table");
@@ -1824,12 +1822,11 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       }
     }
     __syncthreads();  // listed entries read; trivial graph: uk/uv held the staged tile lists until here
-    int* tcount = reinterpret_cast<int*>(s.uv);  // representatives per score rank (uv is free now)
     for (int i = tid; i < kDirSlots; i += blockDim.x) {
       s.hk[i] = kEmpty;
       s.hv[i] = 0ull;
     }
-    if (tid < kDirectCands) tcount[tid] = 0;
+    if (tid == 0) s.nU = 0;
     __syncthreads();
     int slot = -1;
     if (myk != kEmpty) {
@@ -1843,40 +1840,13 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       slot = (int)h;
     }
     __syncthreads();
-    const bool rep = slot >= 0 && s.hv[slot] == myv;  // values are unique (back-pointers)
-    const unsigned so = (unsigned)(myv >> 32);
-    const int n4 = (n + 3) >> 2;
-    if (tid < 4 * n4) {
-      s.hist[tid] = rep ? so : 0u;  // a represented score is never 0 (order code of a number)
-      s.uk[tid] = rep ? myk : kEmpty;
+    if (slot >= 0 && s.hv[slot] == myv) {  // values are unique (back-pointers)
+      const int p = atomicAdd(&s.nU, 1);
+      s.uk[p] = myk;
+      s.uv[p] = myv;
     }
     __syncthreads();
-    // gt: representatives with a larger score.  Equal scores give equal counts and
-    // different scores different ones, so a count shared with another candidate for
-    // the kept set marks a tie, broken by keys ascending.
-    int gt = 0;
-    if (rep) {
-      const uint4* sc4 = reinterpret_cast<const uint4*>(s.hist);
-#pragma unroll 4
-      for (int j = 0; j < n4; ++j) {
-        const uint4 q = sc4[j];
-        gt += (int)(q.x > so) + (int)(q.y > so) + (int)(q.z > so) + (int)(q.w > so);
-      }
-    }
-    const bool contend = rep && gt < Ns;
-    if (contend) atomicAdd(&tcount[gt], 1);
-    __syncthreads();
-    if (contend) {
-      int rank = gt;
-      if (tcount[gt] > 1)
-        for (int j = 0; j < 4 * n4; ++j) rank += (int)((s.hist[j] == so) & (s.uk[j] < myk));
-      if (rank < Ns) {
-        s.lk[rank] = myk;
-        s.lv[rank] = myv;
-        atomicAdd(&s.nL, 1);
-      }
-    }
-    __syncthreads();
+    select_top(s, s.nU, Ns);
   } else {
     // Hash merge.  Listed entries (at most kChunk + kMaxStates) merge in one pass:
     // moved from hk/hv to uk/uv (whose made candidates are no longer needed), then
