@@ -18,7 +18,7 @@ constexpr int kSearchThreads = 256;
 constexpr int kChunk = 1024;         // candidates merged per LDS pass (hash path)
 constexpr int kHashBits = 11;
 constexpr int kHashSlots = 1 << kHashBits;  // LDS open-addressing table (load <= 0.63)
-constexpr int kDirectCands = 256;    // candidate sets up to this size (one per thread) are ranked directly
+constexpr int kDirectCands = 512;    // candidate sets up to this size (two per thread) merge directly
 constexpr int kMaxTopK = 16;         // trivial-graph fast path: max_states limit
 constexpr int kStatStage = kHashSlots;  // softmax partials staged in LDS (in hk) per stream (frame kernels)
 constexpr int kTopkStage = 2 * (kChunk + kMaxStates);  // trivial-graph label lists staged in LDS (in uk)

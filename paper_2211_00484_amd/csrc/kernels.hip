@@ -1803,22 +1803,30 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   }
 
   if (Nsel <= kDirectCands) {
-    // At most one candidate per thread.  Candidates of one key merge in a small LDS
-    // hash table (the maximum of their packed values); the candidate holding that
-    // maximum represents the key and is listed for the top-Ns selection.
-    static_assert(kDirectCands == kSearchThreads && 2 * kSearchThreads <= kHashSlots, "direct path");
-    constexpr int kDirBits = 9, kDirSlots = 1 << kDirBits;  // load <= 1/2
-    static_assert(kDirSlots == 2 * kDirectCands, "direct table");
+    // At most DP candidates per thread.  Candidates of one key merge in an LDS hash
+    // table (the maximum of their packed values); the candidate holding that maximum
+    // represents the key and is listed for the top-Ns selection.
+    constexpr int DP = kDirectCands / kSearchThreads;
+    constexpr int kDirBits = 10, kDirSlots = 1 << kDirBits;  // load <= 1/2
+    static_assert(DP * kSearchThreads == kDirectCands && kDirSlots == 2 * kDirectCands &&
+                      kDirSlots <= kHashSlots && kDirectCands <= kChunk + kMaxStates,
+                  "direct path");
     const int n = Nsel;
-    unsigned long long myk = kEmpty, myv = 0ull;
-    if (tid < n) {
-      if (listed) {
-        myk = s.hk[tid];
-        myv = s.hv[tid];
-      } else {
-        const ulonglong2 kv = make_cand(tid);
-        myk = kv.x;
-        myv = kv.y;
+    unsigned long long myk[DP], myv[DP];
+#pragma unroll
+    for (int u = 0; u < DP; ++u) {
+      const int c = tid + u * kSearchThreads;
+      myk[u] = kEmpty;
+      myv[u] = 0ull;
+      if (c < n) {
+        if (listed) {
+          myk[u] = s.hk[c];
+          myv[u] = s.hv[c];
+        } else {
+          const ulonglong2 kv = make_cand(c);
+          myk[u] = kv.x;
+          myv[u] = kv.y;
+        }
       }
     }
     __syncthreads();  // listed entries read; trivial graph: uk/uv held the staged tile lists until here
@@ -1828,23 +1836,29 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
     }
     if (tid == 0) s.nU = 0;
     __syncthreads();
-    int slot = -1;
-    if (myk != kEmpty) {
-      uint32_t h = (uint32_t)((myk * 0x9E3779B97F4A7C15ull) >> (64 - kDirBits));
-      for (;;) {
-        const unsigned long long prev = atomicCAS(&s.hk[h], kEmpty, myk);
-        if (prev == kEmpty || prev == myk) break;
-        h = (h + 1) & (kDirSlots - 1);
+    int slot[DP];
+#pragma unroll
+    for (int u = 0; u < DP; ++u) {
+      slot[u] = -1;
+      if (myk[u] != kEmpty) {
+        uint32_t h = (uint32_t)((myk[u] * 0x9E3779B97F4A7C15ull) >> (64 - kDirBits));
+        for (;;) {
+          const unsigned long long prev = atomicCAS(&s.hk[h], kEmpty, myk[u]);
+          if (prev == kEmpty || prev == myk[u]) break;
+          h = (h + 1) & (kDirSlots - 1);
+        }
+        atomicMax(&s.hv[h], myv[u]);
+        slot[u] = (int)h;
       }
-      atomicMax(&s.hv[h], myv);
-      slot = (int)h;
     }
     __syncthreads();
-    if (slot >= 0 && s.hv[slot] == myv) {  // values are unique (back-pointers)
-      const int p = atomicAdd(&s.nU, 1);
-      s.uk[p] = myk;
-      s.uv[p] = myv;
-    }
+#pragma unroll
+    for (int u = 0; u < DP; ++u)
+      if (slot[u] >= 0 && s.hv[slot[u]] == myv[u]) {  // values are unique (back-pointers)
+        const int p = atomicAdd(&s.nU, 1);
+        s.uk[p] = myk[u];
+        s.uv[p] = myv[u];
+      }
     __syncthreads();
     select_top(s, s.nU, Ns);
   } else {
