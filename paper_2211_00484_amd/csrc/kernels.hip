@@ -134,13 +134,16 @@ __device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v)
   }
   return r;
 }
+// (row maxima, then the row broadcasts of lane 15 into rows 1 and 3 and of lane 31
+// into rows 2 and 3, so that lane 63 holds the wave maximum: one readlane)
 __device__ __forceinline__ unsigned wave_max_u32(unsigned v) {
   v = max(v, (unsigned)dpp_i<kRor8>((int)v));
   v = max(v, (unsigned)dpp_i<kRor4>((int)v));
   v = max(v, (unsigned)dpp_i<kRor2>((int)v));
   v = max(v, (unsigned)dpp_i<kRor1>((int)v));
-  return max(max((unsigned)__builtin_amdgcn_readlane((int)v, 0), (unsigned)__builtin_amdgcn_readlane((int)v, 16)),
-             max((unsigned)__builtin_amdgcn_readlane((int)v, 32), (unsigned)__builtin_amdgcn_readlane((int)v, 48)));
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x142, 0xa, 0xf, false));  // row_bcast:15
+  v = max(v, (unsigned)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x143, 0xc, 0xf, false));  // row_bcast:31
+  return (unsigned)__builtin_amdgcn_readlane((int)v, 63);
 }
 __device__ __forceinline__ unsigned wave_min_u32(unsigned v) {
   v = min(v, (unsigned)dpp_i<kRor8>((int)v));
