@@ -2610,15 +2610,10 @@ __device__ __forceinline__ void group_joiner_f32(const ModelDev& m, const void* 
 }
 
 // The member joiner's partial sums (4 waves x 2 column groups x 16 rows x 64 lanes)
-// live in hk and hv; the exchanged words of all members (8 x 16 rows x 19 words)
-// in uk and uv.
+// live in hk and hv.
 static_assert(offsetof(SearchSmem, hv) == offsetof(SearchSmem, hk) + sizeof(SearchSmem::hk) &&
                   sizeof(SearchSmem::hk) + sizeof(SearchSmem::hv) >= 4 * 2 * 16 * 64 * sizeof(float),
               "member joiner partial sums do not fit hk and hv");
-static_assert(offsetof(SearchSmem, uv) == offsetof(SearchSmem, uk) + sizeof(SearchSmem::uk) &&
-                  sizeof(SearchSmem::uk) + sizeof(SearchSmem::uv) >=
-                      8 * 16 * (3 + 16) * sizeof(unsigned long long),
-              "exchanged words do not fit uk and uv");
 
 // Exchange slot of (stream b, member g, frame parity): Nc rows of RW words.  A word
 // is tag << 48 | payload: the tag (decode epoch << 8 | frame, both mod 256; the
@@ -2649,8 +2644,9 @@ __device__ __forceinline__ unsigned long long* group_slot(const GroupX& x, int b
 }
 
 // Grouped per-stream kernel.  Per frame: member joiner (partial sums per wave),
-// per-row statistics of the member's columns published as tagged words, the other
-// members' words polled, combined in member order, then the search.
+// per-row statistics of the member's columns published as tagged words, the
+// members' words of each row polled by the row's wave and combined in member order,
+// then the search.
 //
 // FAST (RG = 1, NCG = 1, resident W, Kpad = 512, at most 4 tuples): every wave runs
 // the one-wave selection itself (the results are identical), so that each wave can
@@ -2759,6 +2755,19 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     // the partial sums use the hash table's LDS, idle until the search
     float* part = reinterpret_cast<float*>(s.hk);
     group_joiner_f32<RG, NCG, RES>(m, hl, hstride, part, cg0, wres);
+    // FAST: the P0 rows of the survivors' last labels at this lane's columns (read
+    // after the joiner's barrier, which orders them after wave 0's survivor writes;
+    // the label candidates' decoder rows add P1 rows once the labels are known)
+    float2 p0[4];
+    if (FAST) {
+      const char* P0b = reinterpret_cast<const char*>(m.P0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int a = s.s_bprev[sb + i];  // (absent survivors: anything, mapped into row 0)
+        p0[i] = *reinterpret_cast<const float2*>(
+            P0b + (unsigned)(((unsigned)a < (unsigned)V ? a : 0) * kKStep + k0) * 4u);
+      }
+    }
     const int nc = FAST ? nc_r : s.nc;
     const unsigned long long tg = (unsigned long long)((x.epoch << 8) | ((unsigned)t & 0xffu)) << 48;
     // this member's row statistics over its columns (partial sums added in wave
@@ -2782,6 +2791,16 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
 #pragma unroll
         for (int jj = 0; jj < NCG; ++jj) se += __expf(z[jj] - M);
         const float S = wave_sum_f(se);
+        // the maximum, exp-sum and blank logit go out first: the other members start
+        // their normalisers while the candidates are ranked
+        unsigned long long* w = slot + (size_t)j * RW;
+        if (lane == 0) {
+          __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const float z0 = cg0 == 0 ? z[0] : 0.f;  // lane 0 of the first member holds label 0
+          __hip_atomic_store(w + 2, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        }
         // best KT labels in 1..V-1 by (logit desc, label asc); lane q keeps the q-th
         float my_z = -INFINITY;
         int my_c = -1;
@@ -2822,46 +2841,11 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
             prev = best ? best : 1ull;
           }
         }
-        unsigned long long* w = slot + (size_t)j * RW;
-        if (lane == 0) {
-          __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          const float z0 = cg0 == 0 ? z[0] : 0.f;  // lane 0 of the first member holds label 0
-          __hip_atomic_store(w + 2, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-        }
         if (lane < KT) {
           const unsigned long long c16 = my_c > 0 ? (unsigned long long)my_c << 32 : 0ull;
           __hip_atomic_store(w + 3 + lane, tg | c16 | __float_as_uint(my_z), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
         }
-      }
-    }
-    // every member's words for this frame (bounded polls), payloads into LDS
-    unsigned long long* xs = s.uk;  // [G][nc][RW] payloads
-    {
-      const int per = nc * RW, total = G * per;
-      const unsigned tag = (unsigned)(tg >> 48);
-      for (int idx = tid; idx < total; idx += blockDim.x) {
-        const int g2 = idx / per, rest = idx - g2 * per;
-        const unsigned long long* w = group_slot(x, b, g2, t) + rest;
-        unsigned long long v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        unsigned n = 0;
-        while ((unsigned)(v >> 48) != tag) {
-          ++n;
-          if (n > x.spin_limit ||
-              ((n & 255u) == 0 &&
-               __hip_atomic_load(x.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
-            __hip_atomic_fetch_add(x.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_fetch_add(x.err + 1 + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            // a neutral payload (the word may hold another decode's data): -inf and
-            // label 0 (none), and a zero exp-sum, so nothing stale is selected
-            v = rest % RW == 1 ? 0ull : 0xff800000ull;
-            break;
-          }
-          v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        xs[idx] = v & 0xffffffffffffull;
       }
     }
     if (!FAST && t + 1 < L) {
@@ -2871,78 +2855,117 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         if (k < C) s.enc_next[k] = encp[u];
       }
     }
-    __syncthreads();
-    // combine in member order (identical in every member): normaliser, blank logit,
-    // best KT labels over the G lists (the members' columns are disjoint, so the
-    // labels are distinct)
-    for (int j = wave; j < nc; j += 4) {
-      // (the wave reductions combine in a fixed order, the same in every member)
-      const float Mg = lane < G ? __uint_as_float((unsigned)xs[(lane * nc + j) * RW]) : -INFINITY;
-      const float Sg = lane < G ? __uint_as_float((unsigned)xs[(lane * nc + j) * RW + 1]) : 0.f;
-      const float M = wave_max_f(Mg);
-      const float S = wave_sum_f(Sg == 0.f ? 0.f : Sg * __expf(Mg - M));
-      if (lane == 0) {
-        s.s_lse[j] = lse_of(M, S);
-        s.s_z0[j] = __uint_as_float((unsigned)xs[j * RW + 2]);
-      }
+    // Each wave then takes its rows again: it polls the members' words of the row
+    // (bounded) and combines them in member order, identically in every member.  The
+    // maxima and exp-sums are waited for first and the normaliser computed while the
+    // candidates' words (published later by each member) are still on their way.
+    {
+      const unsigned tag = (unsigned)(tg >> 48);
+      // the payload of word wi of a row once its tag is this frame's; a wait that
+      // runs out (or finds another wait already given up) is recorded and yields a
+      // neutral payload: -inf with label 0 (none), and a zero exp-sum
+      auto settle = [&](const unsigned long long* w, unsigned long long v, int wi) {
+        unsigned n = 0;
+        while ((unsigned)(v >> 48) != tag) {
+          ++n;
+          if (n > x.spin_limit ||
+              ((n & 255u) == 0 &&
+               __hip_atomic_load(x.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)) {
+            __hip_atomic_fetch_add(x.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(x.err + 1 + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return wi == 1 ? 0ull : 0xff800000ull;
+          }
+          v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return v & 0xffffffffffffull;
+      };
+      auto wload = [&](const unsigned long long* w) {
+        return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      };
       const int ne = G * KT;
-      if (ne <= 64) {
-        // one entry per lane: wave maximum of the code; equal codes (rare) go to the
-        // smaller label
-        unsigned o = 0u, c = 0xffffffffu;
-        if (lane < ne) {
-          const int g2 = lane / KT, q = lane - g2 * KT;
-          const unsigned long long w = xs[(g2 * nc + j) * RW + 3 + q];
-          if ((w >> 32) != 0ull) {
-            o = f2ord(__uint_as_float((unsigned)w));
-            c = (unsigned)(w >> 32);
-          }
-        }
-        for (int q = 0; q < KT; ++q) {
-          const unsigned mo = wave_max_u32(o);
-          float zq = -INFINITY;
-          int cq = -1;
-          if (mo != 0u) {
-            unsigned long long bal = __ballot(o == mo);
-            if (__popcll(bal) > 1) {
-              const unsigned cm = wave_min_u32(o == mo ? c : 0xffffffffu);
-              bal = __ballot(o == mo && c == cm);
-            }
-            const int wl = __ffsll((long long)bal) - 1;
-            zq = ord2f(mo);
-            cq = __builtin_amdgcn_readlane((int)c, wl);
-            if (lane == wl) o = 0u;
-          }
-          if (lane == 0) {
-            s.rk_z[j * KT + q] = zq;
-            s.rk_c[j * KT + q] = cq;
-          }
-        }
-      } else {
-        unsigned long long kv[2];
+      for (int j = wave; j < nc; j += 4) {
+        // lanes g < G: member g's maximum; G + g: its exp-sum; 2 G: member 0's blank logit
+        const bool hasA = lane <= 2 * G;
+        const int ga = lane < G ? lane : (lane < 2 * G ? lane - G : 0);
+        const int wa = lane < G ? 0 : (lane < 2 * G ? 1 : 2);
+        const unsigned long long* pa = group_slot(x, b, ga, t) + (size_t)j * RW + wa;
+        // candidate entry e (member e / KT, its (e mod KT)-th): lanes e and e - 64
+        const unsigned long long* pb[2];
+        unsigned long long vb[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int e = lane + 64 * h;
-          kv[h] = 0ull;
-          if (e < ne) {
-            const int g2 = e / KT, q = e - g2 * KT;
-            const unsigned long long w = xs[(g2 * nc + j) * RW + 3 + q];
-            const unsigned c = (unsigned)(w >> 32);
-            if (c != 0u)
-              kv[h] = ((unsigned long long)f2ord(__uint_as_float((unsigned)w)) << 32) | (0xffffffffu - c);
-          }
+          const int e = min(lane + 64 * h, ne - 1), g2 = e / KT;
+          pb[h] = group_slot(x, b, g2, t) + (size_t)j * RW + 3 + (e - g2 * KT);
         }
-        unsigned long long prev = ~0ull;
-        for (int q = 0; q < KT; ++q) {
-          unsigned long long mine = 0ull;
+        unsigned long long va = hasA ? wload(pa) : 0ull;
 #pragma unroll
-          for (int h = 0; h < 2; ++h) mine = (kv[h] < prev && kv[h] > mine) ? kv[h] : mine;
-          const unsigned long long best = wave_max_u64(mine);
-          if (lane == 0) {
-            s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
-            s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+        for (int h = 0; h < 2; ++h) vb[h] = (lane + 64 * h < ne) ? wload(pb[h]) : 0ull;
+        if (hasA) va = settle(pa, va, wa);
+        // (the wave reductions combine in a fixed order, the same in every member)
+        const unsigned vs = (unsigned)__shfl((int)(unsigned)va, min(lane + G, 63));
+        const float Mg = lane < G ? __uint_as_float((unsigned)va) : -INFINITY;
+        const float Sg = lane < G ? __uint_as_float(vs) : 0.f;
+        const float M = wave_max_f(Mg);
+        const float S = wave_sum_f(Sg == 0.f ? 0.f : Sg * __expf(Mg - M));
+        const float z0 = __uint_as_float((unsigned)__builtin_amdgcn_readlane((int)(unsigned)va, 2 * G));
+        if (lane == 0) {
+          s.s_lse[j] = lse_of(M, S);
+          s.s_z0[j] = z0;
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          if (lane + 64 * h < ne) vb[h] = settle(pb[h], vb[h], 3);
+        // best KT labels over the G lists (the members' columns are disjoint, so the
+        // labels are distinct)
+        if (ne <= 64) {
+          // one entry per lane: wave maximum of the code; equal codes (rare) go to the
+          // smaller label
+          unsigned o = 0u, c = 0xffffffffu;
+          if (lane < ne && (vb[0] >> 32) != 0ull) {
+            o = f2ord(__uint_as_float((unsigned)vb[0]));
+            c = (unsigned)(vb[0] >> 32);
           }
-          prev = best ? best : 1ull;
+          for (int q = 0; q < KT; ++q) {
+            const unsigned mo = wave_max_u32(o);
+            float zq = -INFINITY;
+            int cq = -1;
+            if (mo != 0u) {
+              unsigned long long bal = __ballot(o == mo);
+              if (__popcll(bal) > 1) {
+                const unsigned cm = wave_min_u32(o == mo ? c : 0xffffffffu);
+                bal = __ballot(o == mo && c == cm);
+              }
+              const int wl = __ffsll((long long)bal) - 1;
+              zq = ord2f(mo);
+              cq = __builtin_amdgcn_readlane((int)c, wl);
+              if (lane == wl) o = 0u;
+            }
+            if (lane == 0) {
+              s.rk_z[j * KT + q] = zq;
+              s.rk_c[j * KT + q] = cq;
+            }
+          }
+        } else {
+          unsigned long long kv[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const unsigned c = (unsigned)(vb[h] >> 32);
+            kv[h] = (lane + 64 * h < ne && c != 0u)
+                        ? ((unsigned long long)f2ord(__uint_as_float((unsigned)vb[h])) << 32) | (0xffffffffu - c)
+                        : 0ull;
+          }
+          unsigned long long prev = ~0ull;
+          for (int q = 0; q < KT; ++q) {
+            unsigned long long mine = 0ull;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) mine = (kv[h] < prev && kv[h] > mine) ? kv[h] : mine;
+            const unsigned long long best = wave_max_u64(mine);
+            if (lane == 0) {
+              s.rk_z[j * KT + q] = best ? ord2f((unsigned)(best >> 32)) : -INFINITY;
+              s.rk_c[j * KT + q] = best ? (int)(0xffffffffu - (unsigned)best) : -1;
+            }
+            prev = best ? best : 1ull;
+          }
         }
       }
     }
@@ -2959,25 +2982,23 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     // (on this path every context holds one tuple, so survivor i sits on context row
     // i.  The LDS reads are unconditional and issued together; entries of absent
     // survivors or labels may hold anything and are mapped into row 0, never used)
-    int pa[4], pb[4][4];
+    // (P0 rows of the survivors were requested at the start of the frame; 32-bit
+    // byte offsets from the uniform base: P1 stays below 4 GiB)
+    int pb[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int a = s.s_bprev[sb + i];
-      pa[i] = (unsigned)a < (unsigned)V ? a : 0;
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int c = s.rk_c[i * 4 + q];
         pb[i][q] = (unsigned)c < (unsigned)V ? c : 0;
       }
-    }
-    float2 p0[4], p1[4][4];
+    float2 p1[4][4];
+    const char* P1b = reinterpret_cast<const char*>(m.P1);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      p0[i] = *reinterpret_cast<const float2*>(m.P0 + (size_t)pa[i] * kKStep + k0);
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        p1[i][q] = *reinterpret_cast<const float2*>(m.P1 + (size_t)pb[i][q] * kKStep + k0);
-    }
+        p1[i][q] = *reinterpret_cast<const float2*>(P1b + (unsigned)(pb[i][q] * kKStep + k0) * 4u);
     const WaveSel sel =
         trivial_select_wave<4>(s, ns_r, 4, V, Ns, Nc, beam, stride_tb, lane, sb, false);
     const int nk = sel.nk;
