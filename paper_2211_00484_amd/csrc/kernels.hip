@@ -108,14 +108,21 @@ __device__ __forceinline__ unsigned long long row16_max_u64(unsigned long long v
 __device__ __forceinline__ float rdlane_f(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
-// whole-wave reductions (all 64 lanes active); uniform result
+// whole-wave reductions (all 64 lanes active); uniform result.  After the row
+// reductions, two DPP row broadcasts fold the rows into the last one (lane 15 into
+// rows 1 and 3, then lane 31 into rows 2 and 3; rows outside the mask keep their
+// value, or add 0) and one readlane of lane 63 returns ((r3 + r2) + (r1 + r0)).
 __device__ __forceinline__ float wave_max_f(float v) {
   v = row16_max(v);
-  return fmaxf(fmaxf(rdlane_f(v, 0), rdlane_f(v, 16)), fmaxf(rdlane_f(v, 32), rdlane_f(v, 48)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x142, 0xa, 0xf, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), 0x143, 0xc, 0xf, false)));
+  return rdlane_f(v, 63);
 }
 __device__ __forceinline__ float wave_sum_f(float v) {
   v = row16_sum(v);
-  return (rdlane_f(v, 0) + rdlane_f(v, 16)) + (rdlane_f(v, 32) + rdlane_f(v, 48));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xa, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xc, 0xf, false));
+  return rdlane_f(v, 63);
 }
 __device__ __forceinline__ unsigned long long umin64(unsigned long long a, unsigned long long b) {
   return a < b ? a : b;
