@@ -314,21 +314,30 @@ __device__ void write_h_rows_pairs(const ModelDev& m, const float* __restrict__ 
         ++r;
       }
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (ro[u] >= nrows) continue;
+    // (one fully unrolled loop per store type: a rolled loop would load every item
+    // again, one round trip each, instead of indexing the registers above)
+    auto hpair = [&](int u) {
       const int k = ko[u];
-      float h0 = 0.f, h1 = 0.f;
+      float2 h = make_float2(0.f, 0.f);
       if (k < C) {
-        h0 = tanh_fast(enc[k] + fmaxf(p0[u].x + p1[u].x, 0.f));
-        h1 = tanh_fast(enc[k + 1] + fmaxf(p0[u].y + p1[u].y, 0.f));
+        h.x = tanh_fast(enc[k] + fmaxf(p0[u].x + p1[u].x, 0.f));
+        h.y = tanh_fast(enc[k + 1] + fmaxf(p0[u].y + p1[u].y, 0.f));
       }
-      const size_t o = (size_t)ro[u] * hstride + k;
-      if (m.bf16)
-        *reinterpret_cast<unsigned*>(reinterpret_cast<uint16_t*>(hbase) + o) =
-            (unsigned)f32_to_bf16_rne(h0) | ((unsigned)f32_to_bf16_rne(h1) << 16);
-      else
-        *reinterpret_cast<float2*>(reinterpret_cast<float*>(hbase) + o) = make_float2(h0, h1);
+      return h;
+    };
+    if (m.bf16) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (ro[u] < nrows) {
+          const float2 h = hpair(u);
+          *reinterpret_cast<unsigned*>(reinterpret_cast<uint16_t*>(hbase) + (size_t)ro[u] * hstride + ko[u]) =
+              (unsigned)f32_to_bf16_rne(h.x) | ((unsigned)f32_to_bf16_rne(h.y) << 16);
+        }
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (ro[u] < nrows)
+          *reinterpret_cast<float2*>(reinterpret_cast<float*>(hbase) + (size_t)ro[u] * hstride + ko[u]) = hpair(u);
     }
   }
 }
