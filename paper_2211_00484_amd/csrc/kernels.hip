@@ -253,20 +253,25 @@ __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_ro
     int ro[U], ko[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = tid + j * NT;
       ro[u] = r;
-      ko[u] = k;
-      // past the last row or column: load a valid element and drop the result, so
-      // that no branch separates the loads (all of them in flight at once)
-      const int rc = min(r, nrows - 1), kc = min(k, C - 1);
-      const int2 off = rowoff[rc];
-      e[u] = enc_rows[(size_t)rc * enc_stride + kc];
-      p0[u] = P0[(size_t)off.x + kc];
-      p1[u] = P1[(size_t)off.y + kc];
+      ko[u] = tid + j * NT;
       if (++j == cols) {
         j = 0;
         ++r;
       }
+    }
+    // the elements' table rows (LDS reads issued together), then every load; past
+    // the last row or column an element loads a valid one and drops it, so that no
+    // branch separates the loads (all of them in flight at once)
+    int2 off[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) off[u] = rowoff[min(ro[u], nrows - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int rc = min(ro[u], nrows - 1), kc = min(ko[u], C - 1);
+      e[u] = enc_rows[(size_t)rc * enc_stride + kc];
+      p0[u] = P0[(size_t)off[u].x + kc];
+      p1[u] = P1[(size_t)off[u].y + kc];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -291,8 +296,9 @@ __device__ void write_h_rows_pairs(const ModelDev& m, const float* __restrict__ 
                                    const int2* rowoff, int nrows, void* __restrict__ hbase,
                                    int hstride, int tid) {
   const int C = m.C, Kpad = m.Kpad;
-  const float* __restrict__ P0 = m.P0;
-  const float* __restrict__ P1 = m.P1;
+  // (32-bit byte offsets from the uniform table bases: P0 and P1 stay below 4 GiB)
+  const char* P0b = reinterpret_cast<const char*>(m.P0);
+  const char* P1b = reinterpret_cast<const char*>(m.P1);
   const int cols = Kpad / (2 * NT);  // column pairs per thread per row
   int r = 0, j = 0;                  // (row, pair slot) of the next item
   while (r < nrows) {
@@ -300,19 +306,24 @@ __device__ void write_h_rows_pairs(const ModelDev& m, const float* __restrict__ 
     int ro[U], ko[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = 2 * (tid + j * NT);
       ro[u] = r;
-      ko[u] = k;
-      // past the last row or column: load a valid pair and drop the result (no
-      // branch separates the loads)
-      const int rc = min(r, nrows - 1), kc = min(k, C - 2);
-      const int2 off = rowoff[rc];
-      p0[u] = *reinterpret_cast<const float2*>(P0 + (size_t)off.x + kc);
-      p1[u] = *reinterpret_cast<const float2*>(P1 + (size_t)off.y + kc);
+      ko[u] = 2 * (tid + j * NT);
       if (++j == cols) {
         j = 0;
         ++r;
       }
+    }
+    // the items' table rows (LDS reads issued together), then every load; past the
+    // last row or column an item loads a valid pair and drops it (no branch
+    // separates the loads)
+    int2 off[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) off[u] = rowoff[min(ro[u], nrows - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const unsigned kc = (unsigned)min(ko[u], C - 2);
+      p0[u] = *reinterpret_cast<const float2*>(P0b + ((unsigned)off[u].x + kc) * 4u);
+      p1[u] = *reinterpret_cast<const float2*>(P1b + ((unsigned)off[u].y + kc) * 4u);
     }
     // (one fully unrolled loop per store type: a rolled loop would load every item
     // again, one round trip each, instead of indexing the registers above)
@@ -2228,7 +2239,11 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       // (the gathers of up to 16 rows of K = 512 in one batch)
       const size_t esz = m.bf16 ? 2 : 4;
       char* hrows = reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz;
-      if ((m.C & 1) == 0)
+      // (a batch of 8 items when at most 8 rows: a row per item at K = 512, so no
+      // batch loads rows it drops)
+      if ((m.C & 1) == 0 && nC <= 8)
+        write_h_rows_pairs<kSearchThreads, 8>(m, s.enc_next, s.n_rowoff, nC, hrows, m.Kpad, tid);
+      else if ((m.C & 1) == 0)
         write_h_rows_pairs<kSearchThreads, 16>(m, s.enc_next, s.n_rowoff, nC, hrows, m.Kpad, tid);
       else
         write_h_rows<kSearchThreads, 32>(m, s.enc_next, 0, s.n_rowoff, nC, hrows, m.Kpad, tid);
