@@ -172,6 +172,19 @@ __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v)
   return r;
 }
 
+// Inclusive prefix sum over the wave's 64 lanes on DPP: shifts by 1, 2, 4 and 8 within
+// each row of 16 (lanes before the shift's source add 0), then the row broadcasts of
+// lane 15 (into rows 1 and 3) and lane 31 (into rows 2 and 3); no LDS round trip.
+__device__ __forceinline__ unsigned wave_incl_scan_u32(unsigned v) {
+  v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, true);  // row_shr:1
+  v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, true);  // row_shr:2
+  v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, true);  // row_shr:4
+  v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, true);  // row_shr:8
+  v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
 // log-sum-exp of one joiner row from its per-tile (max, sum exp) partials.  The
 // logarithm is taken in double: the device logf is biased low by a fraction of
 // an ulp, which would otherwise accumulate over the frames of a stream.
@@ -1095,12 +1108,7 @@ __device__ unsigned long long kth_largest(SearchSmem& s, int n, int k, Get get) 
 #pragma unroll
       for (int j = 0; j < 4; ++j) c[j] = s.hist[255 - 4 * lane - j];
       const unsigned sum = c[0] + c[1] + c[2] + c[3];
-      unsigned incl = sum;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const unsigned y = __shfl_up(incl, o);
-        if (lane >= o) incl += y;
-      }
+      const unsigned incl = wave_incl_scan_u32(sum);
       const unsigned long long bal = __ballot(incl >= (unsigned)k);
       const int first = __ffsll((long long)bal) - 1;
       if (lane == first) {
@@ -1219,12 +1227,7 @@ __device__ __forceinline__ void select_top(SearchSmem& s, int nU, int Ns) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) c[j] = s.hist[255 - 4 * lane - j];
     const unsigned sum = c[0] + c[1] + c[2] + c[3];
-    unsigned incl = sum;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const unsigned y = __shfl_up(incl, o);
-      if (lane >= o) incl += y;
-    }
+    const unsigned incl = wave_incl_scan_u32(sum);
     const int first = __ffsll((long long)__ballot(incl >= (unsigned)Ns)) - 1;
     if (lane == first) {
       unsigned cum = incl - sum;
@@ -1665,13 +1668,8 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
   // exclusive offsets of each survivor's candidates (block scan over <= 256 entries)
   {
     const int per = TRIV ? d.KT : 0;
-    int v = tid < ns ? (TRIV ? per : s.s_off[tid + 1]) : 0;
-    int incl = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(incl, o);
-      if (lane >= o) incl += y;
-    }
+    const int v = tid < ns ? (TRIV ? per : s.s_off[tid + 1]) : 0;
+    const int incl = (int)wave_incl_scan_u32((unsigned)v);
     if (lane == 63) s.wsum[wave] = incl;
     __syncthreads();
     int woff = 0;
