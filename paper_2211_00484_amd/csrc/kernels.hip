@@ -2055,7 +2055,7 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       const unsigned ci = (unsigned)(sk >> 32), stt = (unsigned)sk;
       const float sc = valid ? ord2f((unsigned)(sv >> 32)) : -INFINITY;
       const bool k1 = valid && sc >= thr;
-      const unsigned prev = (unsigned)__shfl_up((int)ci, 1);
+      const unsigned prev = (unsigned)__builtin_amdgcn_update_dpp(0, (int)ci, 0x138, 0xf, 0xf, false);  // wave_shr:1
       const bool head = valid && (lane == 0 || prev != ci);
       const unsigned long long H = __ballot(head), K1 = __ballot(k1);
       const unsigned long long below = lane ? ~0ull >> (64 - lane) : 0ull;  // lanes < this one
@@ -2066,11 +2066,25 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       const unsigned long long k1run = K1 & (~0ull << rs);
       const int fl = k1run ? __ffsll((long long)k1run) - 1 : 63;             // run's first in-beam lane
       const bool first = k1 && lane == fl;
-      float run = k1 ? sc : -INFINITY;  // run maxima by a segmented inclusive scan
-#pragma unroll
-      for (int dd = 1; dd < 64; dd <<= 1) {
-        const float upv = __shfl_up(run, dd);
-        if (lane - dd >= rs) run = fmaxf(run, upv);
+      // run maxima by a segmented inclusive scan on DPP: shifts by 1, 2, 4 and 8
+      // within each row of 16 (a source outside the row reads -inf), each taken only
+      // from a lane of the same run; then the row broadcasts of lane 15 (into rows 1
+      // and 3) and lane 31 (into rows 2 and 3), taken when that lane is in the run
+      float run = k1 ? sc : -INFINITY;
+      {
+        const int ninf = __float_as_int(-INFINITY);
+        const float u1 = __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(run), 0x111, 0xf, 0xf, false));
+        if (lane - 1 >= rs) run = fmaxf(run, u1);
+        const float u2 = __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(run), 0x112, 0xf, 0xf, false));
+        if (lane - 2 >= rs) run = fmaxf(run, u2);
+        const float u4 = __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(run), 0x114, 0xf, 0xf, false));
+        if (lane - 4 >= rs) run = fmaxf(run, u4);
+        const float u8 = __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(run), 0x118, 0xf, 0xf, false));
+        if (lane - 8 >= rs) run = fmaxf(run, u8);
+        const float b15 = __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(run), 0x142, 0xa, 0xf, false));
+        if ((lane & 16) && (lane & ~15) - 1 >= rs) run = fmaxf(run, b15);
+        const float b31 = __int_as_float(__builtin_amdgcn_update_dpp(ninf, __float_as_int(run), 0x143, 0xc, 0xf, false));
+        if (lane >= 32 && 31 >= rs) run = fmaxf(run, b31);
       }
       const float cs = __shfl(run, valid ? re : lane);
       const unsigned co = first ? f2ord(cs) : 0u;  // a head's code is never 0
