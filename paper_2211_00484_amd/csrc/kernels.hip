@@ -300,6 +300,66 @@ __device__ void write_h_rows(const ModelDev& m, const float* __restrict__ enc_ro
   }
 }
 
+// The same rows for C a multiple of 4, four adjacent columns per item: item i of the
+// nrows x Kpad / 4 (row, column quad) items is thread i mod NT's; a batch of U items per
+// thread issues U 16-byte loads of P0 and of P1 (all in flight at once), then U 16-byte
+// (fp32) or 8-byte (bf16) stores.  enc is one frame shared by every row.
+template <int NT, int U>
+__device__ void write_h_rows_quads(const ModelDev& m, const float* __restrict__ enc,
+                                   const int2* rowoff, int nrows, void* __restrict__ hbase,
+                                   int hstride, int tid) {
+  const int C = m.C, qpr = m.Kpad / 4;  // column quads per row
+  // (32-bit byte offsets from the uniform table bases: P0 and P1 stay below 4 GiB)
+  const char* P0b = reinterpret_cast<const char*>(m.P0);
+  const char* P1b = reinterpret_cast<const char*>(m.P1);
+  const int total = nrows * qpr;
+  for (int i0 = 0; i0 < total; i0 += U * NT) {
+    int ro[U], ko[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int it = min(i0 + tid + u * NT, total - 1);  // past the end: a valid item, dropped
+      ro[u] = it / qpr;
+      ko[u] = 4 * (it - ro[u] * qpr);
+    }
+    // the items' table rows (LDS reads together), then every load
+    int2 off[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) off[u] = rowoff[ro[u]];
+    float4 p0[U], p1[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const unsigned kc = (unsigned)min(ko[u], C - 4);
+      p0[u] = *reinterpret_cast<const float4*>(P0b + ((unsigned)off[u].x + kc) * 4u);
+      p1[u] = *reinterpret_cast<const float4*>(P1b + ((unsigned)off[u].y + kc) * 4u);
+    }
+    // every value first, then the stores (fully unrolled: see write_h_rows)
+    float4 h[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = ko[u];
+      const float4 e = *reinterpret_cast<const float4*>(enc + k);
+      h[u] = k < C ? make_float4(tanh_fast(e.x + fmaxf(p0[u].x + p1[u].x, 0.f)),
+                                 tanh_fast(e.y + fmaxf(p0[u].y + p1[u].y, 0.f)),
+                                 tanh_fast(e.z + fmaxf(p0[u].z + p1[u].z, 0.f)),
+                                 tanh_fast(e.w + fmaxf(p0[u].w + p1[u].w, 0.f)))
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    if (m.bf16) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (i0 + tid + u * NT < total)
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(hbase) + (size_t)ro[u] * hstride + ko[u]) =
+              make_uint2((unsigned)f32_to_bf16_rne(h[u].x) | ((unsigned)f32_to_bf16_rne(h[u].y) << 16),
+                         (unsigned)f32_to_bf16_rne(h[u].z) | ((unsigned)f32_to_bf16_rne(h[u].w) << 16));
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (i0 + tid + u * NT < total)
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(hbase) + (size_t)ro[u] * hstride + ko[u]) = h[u];
+    }
+  }
+}
+
 // The same rows for an even C, two adjacent columns per item: thread tid owns the
 // column pairs (2 tid, 2 tid + 1), (2 tid + 2 NT, ...), ... of every row, so a batch
 // of U items issues U 8-byte loads of P0 and of P1 (all in flight at once) and U
@@ -2251,9 +2311,14 @@ __device__ __forceinline__ void search_frame(const ModelDev& m, const GraphDev& 
       // (the gathers of up to 16 rows of K = 512 in one batch)
       const size_t esz = m.bf16 ? 2 : 4;
       char* hrows = reinterpret_cast<char*>(d.h) + row0 * m.Kpad * esz;
-      // (a batch of 8 items when at most 8 rows: a row per item at K = 512, so no
-      // batch loads rows it drops)
-      if ((m.C & 1) == 0 && nC <= 8)
+      // (C a multiple of 4: 16-byte column quads, 4 items per thread and batch for at
+      // most 8 rows, else 8; otherwise column pairs, a batch of 8 items when at most 8
+      // rows: a row per item at K = 512, so no batch loads rows it drops)
+      if ((m.C & 3) == 0 && nC <= 8)
+        write_h_rows_quads<kSearchThreads, 4>(m, s.enc_next, s.n_rowoff, nC, hrows, m.Kpad, tid);
+      else if ((m.C & 3) == 0)
+        write_h_rows_quads<kSearchThreads, 8>(m, s.enc_next, s.n_rowoff, nC, hrows, m.Kpad, tid);
+      else if ((m.C & 1) == 0 && nC <= 8)
         write_h_rows_pairs<kSearchThreads, 8>(m, s.enc_next, s.n_rowoff, nC, hrows, m.Kpad, tid);
       else if ((m.C & 1) == 0)
         write_h_rows_pairs<kSearchThreads, 16>(m, s.enc_next, s.n_rowoff, nC, hrows, m.Kpad, tid);
