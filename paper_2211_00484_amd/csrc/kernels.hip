@@ -332,7 +332,9 @@ __device__ void write_h_rows_quads(const ModelDev& m, const float* __restrict__ 
       p0[u] = *reinterpret_cast<const float4*>(P0b + ((unsigned)off[u].x + kc) * 4u);
       p1[u] = *reinterpret_cast<const float4*>(P1b + ((unsigned)off[u].y + kc) * 4u);
     }
-    // every value first, then the stores (fully unrolled: see write_h_rows)
+    // every value first, then the stores (fully unrolled: a rolled loop would load
+    // every item again, one round trip each, and stores between the uses would make
+    // each use wait for all of them)
     float4 h[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -3090,8 +3092,8 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
     // (on this path every context holds one tuple, so survivor i sits on context row
     // i.  The LDS reads are unconditional and issued together; entries of absent
     // survivors or labels may hold anything and are mapped into row 0, never used)
-    // (P0 rows of the survivors were requested at the start of the frame; 32-bit
-    // byte offsets from the uniform base: P1 stays below 4 GiB)
+    // (the survivors' P0 rows were requested after the joiner; 32-bit byte offsets
+    // from the uniform base: P1 stays below 4 GiB)
     int pb[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
