@@ -1100,7 +1100,6 @@ struct SearchSmem {
   double s_lse[kMaxStates];
   uint4 fent[kMaxStates];    // final stage: (ctx, state, score bits, context-score bits)
   int fflg[kMaxStates];      // bit 0 in beam, bit 1 first tuple of its context, bit 2 kept
-  alignas(16) float enc_next[kMaxDim];  // encoder frame t+1 of this stream (next frame's joiner rows)
   float wmax[4];
   int n_ctx_list[kMaxStates];
   int2 n_rowoff[kMaxStates];  // (a * Kpad, b * Kpad) of each next-frame context (a, b)
@@ -1114,6 +1113,10 @@ struct SearchSmem {
   int ns, nc, nU, nL, n_gt, n_eq, nK, nC;
   float best;
   double off_d;              // the stream's fp64 score offset (kept here between frames)
+  // encoder frame t+1 of this stream (next frame's joiner rows).  Last member: the
+  // frame search kernel allocates only its first Kpad entries, which keeps two of its
+  // workgroups within one CU's LDS
+  alignas(16) float enc_next[kMaxDim];
 };
 
 // Copies n dwords from global memory into LDS on the global-load-to-LDS path: no
@@ -3515,12 +3518,14 @@ hipError_t launch_joiner_frame(const ModelDev& m, const DecodeDev& d, const Join
 
 hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const DecodeDev& d,
                                float beam, int t, int* trace, hipStream_t st) {
-  const size_t lds = sizeof(SearchSmem);
+  // (the attribute admits the whole layout; a launch allocates enc_next up to Kpad)
+  const size_t lds = offsetof(SearchSmem, enc_next) + (size_t)m.Kpad * sizeof(float);
+  const int lds_max = (int)sizeof(SearchSmem);
   if (d.KT > 0) {
     static bool attr = false;
     if (!attr) {
       hipError_t e = hipFuncSetAttribute((const void*)k_search<true>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
       if (e != hipSuccess) return e;
       attr = true;
     }
@@ -3530,7 +3535,7 @@ hipError_t launch_search_frame(const ModelDev& m, const GraphDev& g, const Decod
     static bool attr = false;
     if (!attr) {
       hipError_t e = hipFuncSetAttribute((const void*)k_search<false>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
       if (e != hipSuccess) return e;
       attr = true;
     }
