@@ -1378,7 +1378,9 @@ struct WaveSel {
 // own.  Survivors are read at offset sb of the survivor arrays, with the row
 // normalisers and each row's best labels (rk_z, rk_c, s_z0).  publish: also write
 // n_ctx_list, nK, nC and best.
-// KTC > 0: the number of labels per row is the compile-time KTC (KT is ignored).
+// KTC > 0: the number of labels per row is the compile-time KTC (KT is ignored), and
+// survivor i sits on context row i (every context holds one tuple), so that every LDS
+// read of a lane is issued at once.
 template <int KTC = 0>
 __device__ __forceinline__ WaveSel trivial_select_wave(SearchSmem& s, int ns, int KT_, int V, int Ns,
                                                        int Nc, float beam, unsigned stride_tb,
@@ -1387,7 +1389,31 @@ __device__ __forceinline__ WaveSel trivial_select_wave(SearchSmem& s, int ns, in
   const int P = 1 + KT, n = ns * P;
   unsigned long long myk = kEmpty, myv = 0ull;
   int src = 0;
-  if (lane < n) {
+  if (KTC > 0) {
+    if (lane < n) {
+      const int i = lane / P, q = lane - i * P - 1;
+      const int e = i * KT + max(q, 0);
+      const double lse = s.s_lse[i];
+      const float sc0 = s.s_score[sb + i];
+      const int lab = s.rk_c[e];
+      const float zl = s.rk_z[e], z0 = s.s_z0[i];
+      const int st = s.s_state[sb + i], ctx = s.s_ctx[sb + i], bp = s.s_bprev[sb + i];
+      if (q < 0) {
+        const float sc = sc0 + logp_of(z0, lse);
+        myk = ((unsigned long long)(unsigned)st << 32) | (unsigned)ctx;
+        myv = ((unsigned long long)f2ord(sc) << 32) | (0xffffffffu - (unsigned)i * stride_tb);
+        src = -(1 + i);
+      } else {
+        if (lab >= 0) {
+          const float sc = sc0 + logp_of(zl, lse);
+          myk = (unsigned)bp * (unsigned)V + (unsigned)lab;
+          myv = ((unsigned long long)f2ord(sc) << 32) |
+                (0xffffffffu - ((unsigned)i * stride_tb + (unsigned)lab));
+        }
+        src = e;
+      }
+    }
+  } else if (lane < n) {
     const int i = lane / P, q = lane - i * P - 1;
     const int row = s.s_row[sb + i];
     const double lse = s.s_lse[row];
