@@ -227,6 +227,21 @@ def test_trivial_wide_frame_joiner(dtype, B):
          streams=range(0, B, B // 8), schedule="frame")
 
 
+def test_general_graph_wide_batch():
+    # general graph on the frame schedule with B = 1,024 streams: four search workgroups
+    # per CU over the batch, two of them resident on a CU at a time (each allocates the
+    # next encoder frame up to Kpad only), up to 32 x 40 candidates per stream (the hash
+    # merge beyond 512); 64 streams spread over the batch checked
+    rng = np.random.default_rng(21)
+    V, C = 200, 64
+    model = synth.make_model(rng, V, C, 0.4)
+    inputs = synth.make_inputs(rng, 1024, 6, C, length_range=(0, 6))
+    graph = synth.random_small_graph(rng, 40, V, max_degree=40, with_final=True)
+    _, _, rep = _run((inputs, model, graph), 4.0, 32, 8, streams=range(0, 1024, 16),
+                     schedule="frame")
+    assert rep.streams == 64
+
+
 LARGE_STREAMS = list(range(0, 128, 8))
 # oracle margins on these streams: fp32 99.6% of frames above 1e-4 (58% prefix, 5 clean
 # streams); bf16 91.9% above 2e-3 (4% prefix, no clean stream: the replay carries it)
