@@ -79,7 +79,8 @@ struct Workspace {
   int* hist_arc = nullptr;
   int* path_lab = nullptr;
   int* len_host = nullptr;  // pinned staging for lengths (and frame bases), [2B]
-  unsigned* xerr = nullptr;  // [1 + B] exchange timeouts of the grouped kernel: any, per stream
+  unsigned* xerr = nullptr;  // [1 + B] exchange timeouts of the grouped kernel: any, per stream;
+                             // then its [kXTickets] per-XCD arrival counters
   GraphDev* gtab = nullptr;       // [B] per-stream graph table (decodes with one graph per stream)
   GraphDev* gtab_host = nullptr;  // pinned staging for it
   hipEvent_t done = nullptr;
@@ -355,7 +356,7 @@ tbs_status alloc_workspace(const tbs_model* m, Workspace& w, int B, int T, int N
   HIP_TRY(dalloc(&w.hist_arc, (size_t)T * BN), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.path_lab, (size_t)B * T), "hipMalloc(workspace)");
   HIP_TRY(dalloc(&w.gtab, B), "hipMalloc(workspace)");
-  HIP_TRY(dalloc(&w.xerr, 1 + (size_t)B), "hipMalloc(workspace)");
+  HIP_TRY(dalloc(&w.xerr, 1 + (size_t)B + kXTickets), "hipMalloc(workspace)");
   HIP_TRY(hipHostMalloc((void**)&w.len_host, (size_t)(B > 0 ? 2 * B : 1) * 4, hipHostMallocDefault),
           "hipHostMalloc(workspace)");
   HIP_TRY(hipHostMalloc((void**)&w.gtab_host, (size_t)(B > 0 ? B : 1) * sizeof(GraphDev),
@@ -914,7 +915,7 @@ tbs_status decode_impl(const tbs_model* model, const tbs_graph* graph,
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
-  HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B, 0, st), "fill(exchange errors)");
+  HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B + kXTickets, 0, st), "fill(exchange errors)");
   bool grouped = false;
   s = enqueue_frames(m, gd, beam, splan, per_stream, d, maxlen, trace, w.xerr, nullptr, true,
                      m->graphs, st, &grouped);
@@ -971,7 +972,7 @@ size_t carve_workspace(const tbs_model* m, uintptr_t base, int B, int T, int Ns,
   take(w.hist_pl, (size_t)T * BN);
   take(w.hist_arc, (size_t)T * BN);
   take(w.path_lab, (size_t)B * T);
-  take(w.xerr, 1 + (size_t)B);
+  take(w.xerr, 1 + (size_t)B + kXTickets);
   *xbuf = nullptr;
   if (xwords) take(*xbuf, xwords);
   w.B = B;
@@ -1013,7 +1014,7 @@ tbs_status state_create_impl(const tbs_model* model, const tbs_graph* graph,
   if (s == TBS_OK) s = alloc_workspace(m, S->w, B, max_frames, S->Ns, S->Nc, S->KT, S->KT == 0);
   hipError_t e = hipSuccess;
   if (s == TBS_OK) {
-    e = launch_fill_i32((int*)S->w.xerr, 1 + (long long)B, 0, st);
+    e = launch_fill_i32((int*)S->w.xerr, 1 + (long long)B + kXTickets, 0, st);
     // the initial tuple of every stream (k_init with zero lengths writes no joiner row)
     if (e == hipSuccess) e = launch_fill_i32(S->w.len, 2 * (long long)B, 0, st);
     // the graph table stays for the state's lifetime
@@ -1369,7 +1370,7 @@ tbs_status tbs_decode_noalloc(const tbs_model* model, const tbs_graph* graph,
   if (trace)
     HIP_TRY(launch_fill_i32(trace, (long long)(T + 1) * B * Ns * 4, -1, st), "fill(trace)");
   HIP_TRY(launch_init(md, d, gd, trace, st), "launch(init)");
-  HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B, 0, st), "fill(exchange errors)");
+  HIP_TRY(launch_fill_i32((int*)w.xerr, 1 + (long long)B + kXTickets, 0, st), "fill(exchange errors)");
   // the array keeps the last call's contents: the exchange words start at zero
   if (xbuf) HIP_TRY(launch_fill_i32((int*)xbuf, 2 * (long long)xwords, 0, st), "fill(exchange)");
   bool grouped = false;

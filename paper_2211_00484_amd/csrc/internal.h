@@ -10,6 +10,7 @@ namespace tbs {
 constexpr int kMaxStates = 256;      // max_states limit (canonical ranking is O(Ns^2) per stream)
 constexpr int kMaxDim = 2048;        // joiner dimension limit
 constexpr unsigned kDefaultSpinLimit = 1u << 22;  // grouped kernel: polls per exchange wait
+constexpr int kXTickets = 8 * 64;   // grouped kernel: per-XCD arrival counters after its [1 + B] timeouts
 constexpr int kMaxVocab = 46340;     // contexts a * V + b are int32: V * V < 2^31
 constexpr int kJoinerBN = 64;        // joiner vocabulary columns per tile (4 waves x 16)
 constexpr int kKStep = 512;          // K padding granule of the packed weights and h rows (one

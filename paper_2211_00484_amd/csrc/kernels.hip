@@ -2762,13 +2762,36 @@ static_assert(offsetof(SearchSmem, hv) == offsetof(SearchSmem, hk) + sizeof(Sear
 // sum of exp(z - maximum) over the member's columns, the blank logit (member 0),
 // then KT candidates label << 32 | logit bits (label 0: none).
 struct GroupX {
-  unsigned long long* buf;  // device memory (device-scope atomics only)
+  unsigned long long* buf;  // device memory (exchange words only)
   int G, xwords;            // members per stream; words per slot
   unsigned epoch;           // decode number (8 bits, never 0)
   unsigned spin_limit;      // polls before a wait is abandoned (recorded in err)
   unsigned* err;            // [1 + B]: timeouts of any stream (checked by every later
                             // wait, which then gives up at once), then per stream
+  unsigned* tickets;        // [8][64] (zeroed): per-XCD arrival counters (xlocal)
+  int xlocal;               // one workgroup per CU on every CU of 8 XCDs: each stream's
+                            // members are placed on one XCD by arrival order there, and
+                            // their words pass through that XCD's L2 (stores sc0, loads
+                            // sc0 sc1) instead of device-scope atomics
 };
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+// Exchange word access of the grouped kernel (off: byte offset in the buffer r covers).
+__device__ __forceinline__ unsigned long long xw_load(const GroupX& x, __amdgpu_buffer_rsrc_t r,
+                                                      const unsigned long long* w) {
+  if (x.xlocal)
+    return __builtin_bit_cast(unsigned long long,
+                              __builtin_amdgcn_raw_buffer_load_b64(
+                                  r, (unsigned)((const char*)w - (const char*)x.buf), 0, 17));
+  return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void xw_store(const GroupX& x, __amdgpu_buffer_rsrc_t r,
+                                         unsigned long long* w, unsigned long long v) {
+  if (x.xlocal)
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, v), r,
+                                          (unsigned)((char*)w - (char*)x.buf), 0, 1);
+  else
+    __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // LDS layout of the grouped kernel beyond SearchSmem.
 struct GroupLds {
@@ -2802,11 +2825,32 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
                                                                  GroupLds ly, GroupX x) {
   static_assert(!FAST || (RG == 1 && NCG == 1 && RES), "the fast path is for 4 rows, resident W");
   const int G = x.G;
-  const int b = blockIdx.x / G, mem = blockIdx.x - b * G;
-  const int L = d.len[b];
-  if (L == 0) return;  // every member of the stream returns here
   extern __shared__ __align__(16) unsigned char smem[];
   SearchSmem& s = *reinterpret_cast<SearchSmem*>(smem);
+  int b = blockIdx.x / G, mem = blockIdx.x - b * G;
+  if (x.xlocal) {
+    // (XCC_ID, the XCD this workgroup runs on; every XCD holds gridDim.x / 8 of them)
+    if (threadIdx.x == 0) {
+      const unsigned xcc = __builtin_amdgcn_s_getreg((3 << 11) | 20) & 0xfu;
+      const unsigned per = gridDim.x / 8;
+      const unsigned tk = xcc < 8 ? __hip_atomic_fetch_add(x.tickets + 64 * xcc, 1u, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT)
+                                  : per;
+      s.misc[0] = tk < per ? (int)(xcc * per + tk) : -1;
+    }
+    __syncthreads();
+    const int slot = s.misc[0];
+    if (slot < 0) {  // placement not as assumed: the other members' waits time out
+      if (threadIdx.x == 0) __hip_atomic_fetch_add(x.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    b = slot / G;
+    mem = slot - b * G;
+  }
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      x.buf, (short)0, (int)(gridDim.x * 2u * (unsigned)x.xwords * 8u), 0x00020000);
+  const int L = d.len[b];
+  if (L == 0) return;  // every member of the stream returns here
   unsigned char* hl = smem + ly.hoff;
   const int hstride = ly.hstride;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -2934,11 +2978,10 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         // their normalisers while the candidates are ranked
         unsigned long long* w = slot + (size_t)j * RW;
         if (lane == 0) {
-          __hip_atomic_store(w, tg | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(w + 1, tg | __float_as_uint(S), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          xw_store(x, xr, w, tg | __float_as_uint(M));
+          xw_store(x, xr, w + 1, tg | __float_as_uint(S));
           const float z0 = cg0 == 0 ? z[0] : 0.f;  // lane 0 of the first member holds label 0
-          __hip_atomic_store(w + 2, tg | __float_as_uint(z0), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
+          xw_store(x, xr, w + 2, tg | __float_as_uint(z0));
         }
         // best KT labels in 1..V-1 by (logit desc, label asc); lane q keeps the q-th
         float my_z = -INFINITY;
@@ -2982,8 +3025,7 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
         }
         if (lane < KT) {
           const unsigned long long c16 = my_c > 0 ? (unsigned long long)my_c << 32 : 0ull;
-          __hip_atomic_store(w + 3 + lane, tg | c16 | __float_as_uint(my_z), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
+          xw_store(x, xr, w + 3 + lane, tg | c16 | __float_as_uint(my_z));
         }
       }
     }
@@ -3014,13 +3056,11 @@ __global__ __launch_bounds__(kSearchThreads) void k_stream_group(ModelDev m, Gra
             __hip_atomic_fetch_add(x.err + 1 + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             return wi == 1 ? 0ull : 0xff800000ull;
           }
-          v = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          v = xw_load(x, xr, w);
         }
         return v & 0xffffffffffffull;
       };
-      auto wload = [&](const unsigned long long* w) {
-        return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      };
+      auto wload = [&](const unsigned long long* w) { return xw_load(x, xr, w); };
       const int ne = G * KT;
       for (int j = wave; j < nc; j += 4) {
         // lanes g < G: member g's maximum; G + g: its exp-sum; 2 G: member 0's blank logit
@@ -3664,6 +3704,19 @@ hipError_t launch_group_rg(int RG, const ModelDev& m, const GraphDev& g, const D
   }
 }
 
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const DecodeDev& d, float beam,
                                int* trace, const StreamPlan& p, unsigned long long* xbuf, int G,
                                unsigned epoch, unsigned spin_limit, unsigned* err,
@@ -3671,7 +3724,15 @@ hipError_t launch_stream_group(const ModelDev& m, const GraphDev& g, const Decod
   const int ncg = m.Vpad / kJoinerBN;
   if (!p.ok || m.bf16 || d.KT <= 0 || G < 2 || ncg % G != 0 || ncg / G > 2)
     return hipErrorInvalidValue;
-  GroupX x{xbuf, G, group_words(d.Nc, d.KT), epoch & 0xffu, spin_limit, err};
+  // one workgroup per CU (the LDS holds one) on all 256 CUs of the 8 XCDs
+  const int ncu = device_cus();
+  const bool xlocal = ncu == 256 && d.B * G == ncu && (ncu / 8) % G == 0;
+  GroupX x{xbuf, G, group_words(d.Nc, d.KT), epoch & 0xffu, spin_limit, err,
+           err + 1 + d.B, xlocal ? 1 : 0};
+  if (xlocal) {  // the arrival counters start at zero for every launch
+    const hipError_t e = launch_fill_i32(reinterpret_cast<int*>(x.tickets), kXTickets, 0, st);
+    if (e != hipSuccess) return e;
+  }
   // LDS: the search state, the joiner rows and (fast path) the staged decoder rows
   GroupLds ly{p.hoff, p.hstride, p.hoff + p.RG * 4 * p.hstride * 4};
   // one column group per member and K = 512: the member's W slice stays in registers;
