@@ -26,6 +26,10 @@ CASES = [
     (500, 300, 48, 16, 12, 6.0, True),       # G = 4, two column groups each, 12 rows
     (500, 700, 7, 4, 2, 3.0, True),          # K = 1024, G = 8
     (448, 512, 20, 16, 16, math.inf, False),  # 7 column groups: no grouping
+    # B x G = 256, one workgroup on every CU: a stream's members share one XCD and pass
+    # their words through its L2
+    (256, 512, 64, 8, 8, math.inf, True),    # G = 4, 8 rows
+    (128, 64, 128, 4, 4, 2.0, True),         # G = 2, the per-wave fast path
 ]
 
 
