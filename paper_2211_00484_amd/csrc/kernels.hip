@@ -2775,7 +2775,9 @@ struct GroupX {
                             // sc0 sc1) instead of device-scope atomics
 };
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
-// Exchange word access of the grouped kernel (off: byte offset in the buffer r covers).
+// Exchange word access of the grouped kernel.  r is a buffer resource over x.buf; the
+// L2 path addresses a word by its byte offset there, with cache policy 17 (sc0 sc1) on
+// loads and 1 (sc0) on stores.
 __device__ __forceinline__ unsigned long long xw_load(const GroupX& x, __amdgpu_buffer_rsrc_t r,
                                                       const unsigned long long* w) {
   if (x.xlocal)
